@@ -1,0 +1,123 @@
+"""Seeded synthetic inputs for the GDN chunk forward.
+
+This module is shared by the tests, the benchmark and the smoke check.  It
+holds no part of the method's arithmetic: it only draws random tensors of the
+shapes and value distributions of the five workloads below, and rounds them to
+the storage type.  Both the HIP path and the fp64 oracle read the very same
+stored arrays.
+
+Recipe (PCG64 via ``numpy.random.default_rng(seed)``, seed = 1000 * workload
++ call index, draws in this order):
+  q, k ~ N(0, 1) in fp32, each (b, t, h) row L2-normalised over D in fp32,
+  v ~ N(0, 1), the alpha noise, the beta noise, then state_in; bf16 workloads
+  round q, k, v to bf16 with round-to-nearest-even after normalising.
+
+The tokens stand in for DiT activations of 1280x704 video: a latent frame is a
+44 x 80 token grid (3520 tokens), a streaming chunk is 3 frames.  The decay
+alpha follows the Mamba-2 style exp(-softplus(.)) shape of the paper's decay
+gate (equation appendix_gdn_alpha) and beta the sigmoid of its write gate
+(equation appendix_gdn_beta); the weights producing them are not part of this
+path, so their pre-activations are drawn as Gaussians.
+"""
+from dataclasses import dataclass
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    T: int
+    H: int
+    Dk: int
+    Dv: int
+    dtype: str          # "f32" or "bf16" for q, k, v and out
+    alpha: str          # "softplus0", "softplus2" or "uniform0.5"
+    beta: str           # "sigmoid" or "uniform"
+    state: str          # "zero" or "normal0.02"
+    calls: int = 1
+    chunk: int = 64
+
+
+WORKLOADS = (
+    Workload("tiny-f32 B1 T256 H2 D64", 1, 256, 2, 64, 64, "f32",
+             "softplus0", "sigmoid", "zero"),
+    Workload("frame-1280x704 B1 T3520 H16 D128", 1, 3520, 16, 128, 128, "bf16",
+             "softplus0", "sigmoid", "normal0.02"),
+    Workload("stream-3frame x20 B1 T10560 H16 D128", 1, 10560, 16, 128, 128, "bf16",
+             "softplus0", "sigmoid", "zero", calls=20),
+    Workload("cfg-batch B4 T10560 H20 D64 fast-forget", 4, 10560, 20, 64, 64, "bf16",
+             "softplus2", "sigmoid", "normal0.02"),
+    Workload("long-12frame B1 T42240 H32 D128", 1, 42240, 32, 128, 128, "bf16",
+             "uniform0.5", "uniform", "normal0.02"),
+)
+
+
+def f32_to_bf16_bits(x):
+    """Round fp32 values to bf16 (round-to-nearest-even); returns uint16 bit patterns."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounding = ((u >> 16) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + rounding) >> 16).astype(np.uint16)
+
+
+def bf16_bits_to_f32(b):
+    """Widen bf16 bit patterns to fp32 exactly."""
+    return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def _unit_rows(x):
+    n = np.sqrt(np.sum(x * x, axis=-1, keepdims=True, dtype=np.float32))
+    return (x / n).astype(np.float32)
+
+
+def make_inputs(workload, call=0, *, B=None, T=None, H=None, Dk=None, Dv=None,
+                dtype=None, state=None, seed=None):
+    """Draw one call's inputs for ``workload`` (an index into WORKLOADS or a Workload).
+
+    Keyword overrides change the shape (e.g. a ragged T) while keeping the value
+    distributions.  Returns a dict with numpy arrays:
+      q, k [B,T,H,Dk] and v [B,T,H,Dv]: float32, or uint16 bf16 bit patterns;
+      alpha, beta [B,T,H] float32; state_in [B,H,Dk,Dv] float32 or None;
+    plus "dtype" ("f32"/"bf16").
+    """
+    w = WORKLOADS[workload] if isinstance(workload, int) else workload
+    idx = WORKLOADS.index(w) if w in WORKLOADS else 99
+    B = w.B if B is None else B
+    T = w.T if T is None else T
+    H = w.H if H is None else H
+    Dk = w.Dk if Dk is None else Dk
+    Dv = w.Dv if Dv is None else Dv
+    dtype = w.dtype if dtype is None else dtype
+    state = w.state if state is None else state
+    rng = np.random.default_rng(1000 * idx + call if seed is None else seed)
+
+    q = _unit_rows(rng.standard_normal((B, T, H, Dk), dtype=np.float32))
+    k = _unit_rows(rng.standard_normal((B, T, H, Dk), dtype=np.float32))
+    v = rng.standard_normal((B, T, H, Dv), dtype=np.float32)
+    if w.alpha.startswith("softplus"):
+        mu = float(w.alpha[len("softplus"):])
+        z = rng.standard_normal((B, T, H)).astype(np.float64) + mu
+        alpha = np.exp(-np.logaddexp(0.0, z)).astype(np.float32)
+    elif w.alpha == "uniform0.5":
+        alpha = rng.uniform(0.5, 1.0, (B, T, H)).astype(np.float32)
+    else:
+        raise ValueError(w.alpha)
+    if w.beta == "sigmoid":
+        z = rng.standard_normal((B, T, H)).astype(np.float64)
+        beta = (1.0 / (1.0 + np.exp(-z))).astype(np.float32)
+    elif w.beta == "uniform":
+        beta = rng.uniform(0.0, 1.0, (B, T, H)).astype(np.float32)
+    else:
+        raise ValueError(w.beta)
+    if state == "zero":
+        state_in = None
+    elif state == "normal0.02":
+        state_in = (0.02 * rng.standard_normal((B, H, Dk, Dv), dtype=np.float32)).astype(np.float32)
+    else:
+        raise ValueError(state)
+    if dtype == "bf16":
+        q, k, v = f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
+    elif dtype != "f32":
+        raise ValueError(dtype)
+    return dict(q=q, k=k, v=v, alpha=alpha, beta=beta, state_in=state_in, dtype=dtype)

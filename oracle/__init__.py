@@ -1,0 +1,86 @@
+"""fp64 CPU oracle for the gated delta-rule forward -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  It shares no code with the HIP library
+and the product path never calls it.
+
+* :func:`gdn_forward` -- the token-by-token recurrence in fp64 (C library,
+  ``gdn_oracle.c``), the reference every GPU result is compared with.
+* :mod:`oracle.chunked` -- the chunked (WY / UT) rewrite in fp64 numpy, used
+  only to pin the recurrence against an independent algebraic form.
+* :mod:`oracle.framewise` -- the paper's frame-wise compact update written as
+  printed, used to tie the recurrence to the paper's own equation.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+_LIB = None
+_DT_QKV = {np.dtype(np.float32): 0, np.dtype(np.uint16): 1, np.dtype(np.float64): 2}
+_DT_GATE = {np.dtype(np.float32): 0, np.dtype(np.float64): 2}
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        lib = ctypes.CDLL(_build.LIB)
+        vp, i = ctypes.c_void_p, ctypes.c_int
+        lib.gdn_oracle_forward.restype = ctypes.c_int
+        lib.gdn_oracle_forward.argtypes = [vp, vp, vp, i, vp, vp, i, vp, i, vp, vp,
+                                           i, i, i, i, i, i]
+        _LIB = lib
+    return _LIB
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def gdn_forward(q, k, v, alpha, beta, state_in=None, nthreads=None,
+                want_state=True):
+    """Run the fp64 token recurrence.
+
+    q, k: [B, T, H, Dk]; v: [B, T, H, Dv] -- all float32, float64, or uint16
+    holding bf16 bit patterns (widened exactly).  alpha, beta: [B, T, H]
+    float32/float64.  state_in: [B, H, Dk, Dv] float32/float64 or None (zero).
+    Returns (out [B, T, H, Dv] float64, state_out [B, H, Dk, Dv] float64 or None).
+    """
+    q, k, v = (np.ascontiguousarray(x) for x in (q, k, v))
+    if not (q.dtype == k.dtype == v.dtype) or q.dtype not in _DT_QKV:
+        raise TypeError(f"q/k/v must share one of {list(_DT_QKV)}; got "
+                        f"{q.dtype}, {k.dtype}, {v.dtype}")
+    alpha = np.ascontiguousarray(alpha)
+    beta = np.ascontiguousarray(beta, dtype=alpha.dtype)
+    if alpha.dtype not in _DT_GATE:
+        raise TypeError(f"alpha/beta dtype {alpha.dtype} unsupported")
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if k.shape != (B, T, H, Dk) or v.shape != (B, T, H, Dv):
+        raise ValueError("q/k/v shape mismatch")
+    if alpha.shape != (B, T, H) or beta.shape != (B, T, H):
+        raise ValueError("alpha/beta must be [B, T, H]")
+    sdt = 0
+    if state_in is not None:
+        state_in = np.ascontiguousarray(state_in)
+        if state_in.dtype not in _DT_GATE:
+            raise TypeError(f"state_in dtype {state_in.dtype} unsupported")
+        if state_in.shape != (B, H, Dk, Dv):
+            raise ValueError("state_in must be [B, H, Dk, Dv]")
+        sdt = _DT_GATE[state_in.dtype]
+    out = np.empty((B, T, H, Dv), dtype=np.float64)
+    state_out = np.empty((B, H, Dk, Dv), dtype=np.float64) if want_state else None
+    if nthreads is None:
+        nthreads = os.cpu_count() or 1
+    rc = _lib().gdn_oracle_forward(
+        _ptr(q), _ptr(k), _ptr(v), _DT_QKV[q.dtype],
+        _ptr(alpha), _ptr(beta), _DT_GATE[alpha.dtype],
+        _ptr(state_in), sdt, _ptr(out), _ptr(state_out),
+        B, H, T, Dk, Dv, int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"gdn_oracle_forward failed with {rc}")
+    return out, state_out

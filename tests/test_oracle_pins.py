@@ -1,0 +1,272 @@
+"""Pins of the fp64 oracle against what the paper and the mathematics fix.
+
+Each test names the mistake in the oracle it would catch.  None of them
+re-types the oracle's loop: they use closed forms, invariants, the paper's own
+printed (compact, frame-wise) equation, an independent chunked rewrite, and a
+hand-worked example.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import gdn_inputs
+import oracle
+from oracle.chunked import gdn_chunked
+from oracle.framewise import framewise_forward
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+rng = np.random.default_rng
+
+
+def unit_rows(x):
+    return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+
+def rand_case(seed, B=1, T=40, H=2, Dk=8, Dv=6, state=True):
+    r = rng(seed)
+    q = r.standard_normal((B, T, H, Dk))
+    k = unit_rows(r.standard_normal((B, T, H, Dk)))
+    v = r.standard_normal((B, T, H, Dv))
+    a = r.uniform(0.2, 1.0, (B, T, H))
+    b = r.uniform(0.0, 1.0, (B, T, H))
+    s = r.standard_normal((B, H, Dk, Dv)) if state else None
+    return q, k, v, a, b, s
+
+
+def rel(x, y):
+    return np.abs(x - y).max() / max(np.abs(y).max(), 1e-300)
+
+
+# P1 -- beta = 0, alpha = 1 leaves the state unchanged (spec invariant).
+# Catches: a write that does not scale by beta, a decay applied when alpha = 1.
+def test_p1_beta0_alpha1_state_unchanged():
+    q, k, v, a, b, s = rand_case(1)
+    a[:] = 1.0
+    b[:] = 0.0
+    out, st = oracle.gdn_forward(q, k, v, a, b, s)
+    assert np.array_equal(st, s)
+    ref = np.einsum("bthi,bhij->bthj", q, s)
+    assert rel(out, ref) < 1e-14
+
+
+# P2 -- beta = 1, alpha = 1 and a unit key: the state maps k_t to v_t exactly
+# (spec invariant).  With q_t = k_t the output is v_t.
+# Catches: a sign error in the residual, reading the output before the update,
+# a transposed state (Dk != Dv here), a missing k k^T projection.
+def test_p2_beta1_alpha1_writes_v():
+    q, k, v, a, b, s = rand_case(2, Dk=8, Dv=5)
+    a[:] = 1.0
+    b[:] = 1.0
+    out, st = oracle.gdn_forward(k, k, v, a, b, s)
+    assert rel(out, v) < 1e-12
+    last = np.einsum("bhij,bhi->bhj", st, k[:, -1])
+    assert rel(last, v[:, -1]) < 1e-12
+
+
+# P3 -- alpha_t* = 0 resets: H_t* = beta k v^T and nothing before t* (state or
+# tokens) reaches later outputs (spec invariant).
+# Catches: a decay that misses the prediction term (v - p instead of v - alpha p).
+def test_p3_alpha0_resets():
+    q, k, v, a, b, s = rand_case(3, T=30)
+    ts = 17
+    a[:, ts] = 0.0
+    out1, st1 = oracle.gdn_forward(q[:, :ts + 1], k[:, :ts + 1], v[:, :ts + 1],
+                                   a[:, :ts + 1], b[:, :ts + 1], s)
+    outer = b[:, ts, :, None, None] * k[:, ts, :, :, None] * v[:, ts, :, None, :]
+    assert rel(st1, outer) < 1e-15
+    q2, k2, v2, _, b2, s2 = rand_case(33, T=30)
+    q2[:, ts:], k2[:, ts:], v2[:, ts:], b2[:, ts:] = q[:, ts:], k[:, ts:], v[:, ts:], b[:, ts:]
+    out_a, st_a = oracle.gdn_forward(q, k, v, a, b, s)
+    out_b, st_b = oracle.gdn_forward(q2, k2, v2, a, b2, s2)
+    assert np.array_equal(out_a[:, ts:], out_b[:, ts:])
+    assert np.array_equal(st_a, st_b)
+
+
+# P4 -- the chunked (WY/UT) rewrite equals the recurrence for every chunk size,
+# including a ragged last chunk (spec invariant).
+# Catches: any error that the independent chunked algebra does not share.
+@pytest.mark.parametrize("chunk", [1, 7, 16, 64, 203])
+def test_p4_chunked_equals_recurrence(chunk):
+    q, k, v, a, b, s = rand_case(4, B=2, T=203, H=2, Dk=16, Dv=12)
+    out, st = oracle.gdn_forward(q, k, v, a, b, s)
+    oc, sc = gdn_chunked(q, k, v, a, b, s, chunk=chunk)
+    assert rel(oc, out) < 1e-12
+    assert rel(sc, st) < 1e-12
+
+
+def test_p4_chunked_equals_recurrence_workload0():
+    inp = gdn_inputs.make_inputs(0)
+    out, st = oracle.gdn_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"])
+    oc, sc = gdn_chunked(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], chunk=64)
+    assert rel(oc, out) < 1e-12 and rel(sc, st) < 1e-12
+
+
+# P5 -- linearity in (state_in, v) for fixed q, k, alpha, beta.
+# Catches: a term that mixes v and the state non-linearly or drops one of them.
+def test_p5_linearity():
+    q, k, v, a, b, s = rand_case(5)
+    o1, s1 = oracle.gdn_forward(q, k, v, a, b, s)
+    o2, s2 = oracle.gdn_forward(q, k, np.zeros_like(v), a, b, s)
+    o3, s3 = oracle.gdn_forward(q, k, v, a, b, None)
+    assert rel(o2 + o3, o1) < 1e-12
+    assert rel(s2 + s3, s1) < 1e-12
+
+
+# P6 -- streaming split: two calls with the state threaded equal one call
+# (the streaming cache carries only the terminal state).
+# Catches: a state written before the last token, or state_in ignored.
+@pytest.mark.parametrize("m", [1, 13, 39])
+def test_p6_streaming_split(m):
+    q, k, v, a, b, s = rand_case(6)
+    o, st = oracle.gdn_forward(q, k, v, a, b, s)
+    oa, sa = oracle.gdn_forward(q[:, :m], k[:, :m], v[:, :m], a[:, :m], b[:, :m], s)
+    ob, sb = oracle.gdn_forward(q[:, m:], k[:, m:], v[:, m:], a[:, m:], b[:, m:], sa)
+    assert np.array_equal(np.concatenate([oa, ob], axis=1), o)
+    assert np.array_equal(sb, st)
+
+
+# P7 -- alpha = 1, beta = 2, v = 0 and unit keys make each step a Householder
+# reflection I - 2 k k^T, which preserves the Frobenius norm.
+# Catches: a wrong factor on the k k^T term (beta/2, beta^2, ...).
+def test_p7_reflection_preserves_norm():
+    q, k, v, a, b, s = rand_case(7, T=60)
+    a[:] = 1.0
+    b[:] = 2.0
+    _, st = oracle.gdn_forward(q, k, np.zeros_like(v), a, b, s)
+    n0 = np.linalg.norm(s.reshape(s.shape[0], s.shape[1], -1), axis=-1)
+    n1 = np.linalg.norm(st.reshape(st.shape[0], st.shape[1], -1), axis=-1)
+    assert rel(n1, n0) < 1e-12
+    assert rel(st, s) > 1e-3  # the state did move
+
+
+# P8 -- keys drawn from an orthonormal basis R: in that basis the state rows
+# c_j = H^T R[:, j] evolve independently: every row decays by alpha_t and the
+# written row becomes alpha_t (1 - beta_t) c_j + beta_t v_t.
+# Catches: alpha applied to the write only, beta misplaced, transposed state.
+def test_p8_orthonormal_keys_closed_form():
+    r = rng(8)
+    Dk, Dv, T = 6, 4, 50
+    R, _ = np.linalg.qr(r.standard_normal((Dk, Dk)))
+    js = r.integers(0, Dk, T)
+    k = R[:, js].T[None, :, None, :].copy()
+    q = r.standard_normal((1, T, 1, Dk))
+    v = r.standard_normal((1, T, 1, Dv))
+    a = r.uniform(0.3, 1.0, (1, T, 1))
+    b = r.uniform(0.0, 1.0, (1, T, 1))
+    H0 = r.standard_normal((1, 1, Dk, Dv))
+    out, st = oracle.gdn_forward(q, k, v, a, b, H0)
+    C = R.T @ H0[0, 0]
+    exp_out = np.zeros((T, Dv))
+    for t in range(T):
+        j = js[t]
+        C = a[0, t, 0] * C
+        C[j] = (1.0 - b[0, t, 0]) * C[j] + b[0, t, 0] * v[0, t, 0]
+        exp_out[t] = C.T @ (R.T @ q[0, t, 0])
+    assert rel(out[0, :, 0], exp_out) < 1e-12
+    assert rel(st[0, 0], R @ C) < 1e-12
+
+
+# P9 -- Dk = Dv = 1: h_T = prod(m) h_0 + sum_t prod_{u>t}(m_u) beta_t k_t v_t with
+# m_t = alpha_t (1 - beta_t k_t^2), summed in closed form rather than stepped.
+# Catches: a misplaced alpha or beta in the scalar gain / write terms.
+def test_p9_scalar_closed_form():
+    r = rng(9)
+    T = 50
+    q = r.standard_normal((1, T, 1, 1))
+    k = r.uniform(-1.2, 1.2, (1, T, 1, 1))
+    v = r.standard_normal((1, T, 1, 1))
+    a = r.uniform(0.5, 1.0, (1, T, 1))
+    b = r.uniform(0.0, 1.0, (1, T, 1))
+    h0 = r.standard_normal((1, 1, 1, 1))
+    out, st = oracle.gdn_forward(q, k, v, a, b, h0)
+    m = a[0, :, 0] * (1.0 - b[0, :, 0] * k[0, :, 0, 0] ** 2)
+    w = b[0, :, 0] * k[0, :, 0, 0] * v[0, :, 0, 0]
+    for t in (0, 1, 24, T - 1):
+        h = np.prod(m[:t + 1]) * h0[0, 0, 0, 0] + sum(np.prod(m[s + 1:t + 1]) * w[s] for s in range(t + 1))
+        assert abs(out[0, t, 0, 0] - h * q[0, t, 0, 0]) < 1e-12 * max(1.0, abs(h))
+        if t == T - 1:
+            assert abs(st[0, 0, 0, 0] - h) < 1e-12 * max(1.0, abs(h))
+
+
+# P10 -- T = 1: H_1 = alpha (I - beta k k^T) H_0 + beta k v^T, as one matrix expression.
+def test_p10_single_token():
+    q, k, v, a, b, s = rand_case(10, T=1, H=1)
+    out, st = oracle.gdn_forward(q, k, v, a, b, s)
+    kk, vv, qq = k[0, 0, 0], v[0, 0, 0], q[0, 0, 0]
+    H1 = a[0, 0, 0] * (np.eye(len(kk)) - b[0, 0, 0] * np.outer(kk, kk)) @ s[0, 0] + b[0, 0, 0] * np.outer(kk, vv)
+    assert rel(st[0, 0], H1) < 1e-14
+    assert rel(out[0, 0, 0], H1.T @ qq) < 1e-14
+
+
+# P11 -- the paper's compact frame-wise equation with one token per frame equals
+# the oracle (ties the oracle to the printed equation and orientation S = H^T).
+def test_p11_paper_compact_equation_n1():
+    q, k, v, a, b, s = rand_case(11, H=1, Dk=7, Dv=5)
+    out, st = oracle.gdn_forward(q, k, v, a, b, s)
+    Y, S = framewise_forward(q[0, :, 0], k[0, :, 0], v[0, :, 0], a[0, :, 0], b[0, :, 0],
+                             S0=s[0, 0].T, N=1)
+    assert rel(out[0, :, 0], Y) < 1e-12
+    assert rel(st[0, 0], S.T) < 1e-12
+
+
+# P12 -- a hand-worked two-token example (tests/golden/hand_T2_D2.json).
+def test_p12_hand_worked_example():
+    g = json.load(open(os.path.join(GOLDEN, "hand_T2_D2.json")))
+    shp = lambda x, *d: np.asarray(x, dtype=np.float64).reshape(*d)
+    B, T, H, Dk, Dv = g["B"], g["T"], g["H"], g["Dk"], g["Dv"]
+    out, st = oracle.gdn_forward(shp(g["q"], B, T, H, Dk), shp(g["k"], B, T, H, Dk),
+                                 shp(g["v"], B, T, H, Dv), shp(g["alpha"], B, T, H),
+                                 shp(g["beta"], B, T, H), shp(g["state_in"], B, H, Dk, Dv))
+    assert np.allclose(out.reshape(T, Dv), g["expected_out"], rtol=0, atol=1e-14)
+    assert np.allclose(st.reshape(Dk, Dv), g["expected_state"], rtol=0, atol=1e-14)
+
+
+# Regression record written by tests/golden/make_golden.py from the oracle itself.
+def test_oracle_regression_record():
+    g = json.load(open(os.path.join(GOLDEN, "oracle_small.json")))
+    inp = gdn_inputs.make_inputs(0, seed=g["seed"], state="normal0.02", **g["shape"])
+    out, st = oracle.gdn_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
+                                 inp["state_in"], nthreads=1)
+    exp_out = np.array([float.fromhex(x) for x in g["out"]])
+    exp_st = np.array([float.fromhex(x) for x in g["state"]])
+    assert rel(out.ravel(), exp_out) < 1e-14
+    assert rel(st.ravel(), exp_st) < 1e-14
+
+
+# The bf16 reader widens exactly, and threading does not change any bit.
+def test_bf16_widening_and_threads_bitwise():
+    inp = gdn_inputs.make_inputs(1, T=70, H=3)
+    q, k, v = inp["q"], inp["k"], inp["v"]
+    assert q.dtype == np.uint16
+    w = lambda x: gdn_inputs.bf16_bits_to_f32(x).astype(np.float64)
+    o1, s1 = oracle.gdn_forward(q, k, v, inp["alpha"], inp["beta"], inp["state_in"], nthreads=1)
+    o2, s2 = oracle.gdn_forward(w(q), w(k), w(v), inp["alpha"].astype(np.float64),
+                                inp["beta"].astype(np.float64),
+                                inp["state_in"].astype(np.float64), nthreads=3)
+    assert np.array_equal(o1, o2) and np.array_equal(s1, s2)
+
+
+def test_oracle_rejects_bad_arguments():
+    q, k, v, a, b, s = rand_case(12)
+    with pytest.raises(ValueError):
+        oracle.gdn_forward(q, k, v[:, :-1], a, b, s)
+    with pytest.raises(TypeError):
+        oracle.gdn_forward(q.astype(np.float32), k, v, a, b, s)
+
+
+def test_inputs_recipe():
+    inp = gdn_inputs.make_inputs(3, T=128, B=2)
+    a, b = inp["alpha"], inp["beta"]
+    assert a.shape == (2, 128, 20) and inp["q"].shape == (2, 128, 20, 64)
+    assert 0.0 < a.min() and a.max() < 1.0 and np.median(a) < 0.2   # fast-forget heads
+    assert 0.0 < b.min() and b.max() < 1.0
+    qf = gdn_inputs.bf16_bits_to_f32(inp["q"]).astype(np.float64)
+    assert np.allclose(np.linalg.norm(qf, axis=-1), 1.0, atol=1e-2)
+    a4 = gdn_inputs.make_inputs(4, T=64)["alpha"]
+    assert a4.min() >= 0.5 and a4.max() <= 1.0
+    assert gdn_inputs.make_inputs(2, T=64)["state_in"] is None
+    x = np.array([1.0, 1.00390625, 1.01171875, -3.0e-3], dtype=np.float32)
+    # RNE ties: 1+2^-8 rounds to 1 (even), 1+3*2^-8 rounds up to 1+2^-6
+    assert list(gdn_inputs.bf16_bits_to_f32(gdn_inputs.f32_to_bf16_bits(x))[:3]) == [1.0, 1.0, 1.015625]

@@ -1,0 +1,208 @@
+"""Benchmark of the GDN chunk forward on one MI355X.
+
+A step is one full pass of the hot path (WY transform, state scan, output) over
+one 1280x704 latent frame: B=1, T=3520 tokens (44x80), H=16 heads,
+Dk=Dv=128, chunk 64, bf16 q/k/v with an fp32 state carried in and out.  The
+inputs are seeded synthetic tensors already resident in HBM; the workspace is
+preallocated, so the timed region only enqueues the three kernels per step.
+
+Prints ONE JSON line.  Besides throughput it reports the roofline of the
+dominant kernel (per-stage durations from HIP events recorded on the stream
+the kernels run on) and, on rank 0, the fp64 CPU oracle timed on the host
+cores as a reported baseline.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import gdn_inputs  # noqa: E402
+
+METRIC = "GDN fwd tokens/sec and TFLOP/s at T=3520,H=16,D=128 bf16; % of MFMA peak"
+WORKLOAD = 1                 # one 1280x704 frame
+PEAK_BF16_TFLOPS = 2516.6    # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
+STAGES = ("gdn_wy_kernel", "gdn_scan_kernel", "gdn_output_kernel")
+
+
+def algorithmic_counts(B, T, H, Dk, Dv, C=64):
+    """Per-stage algorithmic flops and the path's algorithmic bytes (no workspace traffic)."""
+    n = B * T * H  # token-heads
+    f_wy = n * ((C - 1) * (2 * Dk + Dv) + C * C / 3.0)
+    f_scan = n * 4.0 * Dk * Dv
+    f_out = n * (2.0 * Dk * Dv + (C + 1) * (Dk + Dv))
+    io_bytes = n * ((2 * Dk + Dv) * 2 + 8 + Dv * 2) + 2 * B * H * Dk * Dv * 4
+    # bytes each stage must move at minimum (its own inputs/outputs, workspace included)
+    nch = B * H * -(-T // C)
+    b_wy = n * ((Dk + Dv) * 2 + 8) + nch * C * (4 + 2 * (2 * Dk + Dv))
+    return dict(flops=dict(wy=f_wy, scan=f_scan, out=f_out, total=f_wy + f_scan + f_out),
+                bytes=io_bytes, bytes_wy=b_wy)
+
+
+def host_threads():
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(n, 16))
+
+
+def cpu_baseline(inp, B, T, min_seconds=10.0):
+    """Time the fp64 oracle (as it stands) on whole workload calls for ~10 s."""
+    import oracle
+    threads = host_threads()
+    reps, elapsed = 0, 0.0
+    while elapsed < min_seconds and reps < 50:
+        t0 = time.perf_counter()
+        oracle.gdn_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
+                           inp["state_in"], nthreads=threads)
+        elapsed += time.perf_counter() - t0
+        reps += 1
+    return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H=16, D=128), "
+                      f"fp64 token recurrence, {elapsed:.1f} s"}
+
+
+def load_traffic(kernel):
+    """HBM traffic per launch for `kernel` from the committed counter summary, or None
+    when the summary is missing or was taken on different kernel source."""
+    path = os.path.join(ROOT, "profiles", "traffic_frame1280x704.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        import hashlib
+        h = hashlib.sha256()
+        for f in rec["sources"]:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+        if h.hexdigest() != rec["source_sha256"]:
+            return None
+        k = rec["kernels"].get(kernel)
+        return None if k is None else float(k["hbm_bytes_per_launch"])
+    except Exception:
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
+    ap.add_argument("--cold-steps", type=int, default=20,
+                    help="extra steps each preceded by a 1 GiB write that evicts the caches")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the (b, h) streams shard across GPUs with no communication, so the one-GPU "
+              "number is the per-GPU figure).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2605_30409_amd as gdn
+
+    w = gdn_inputs.WORKLOADS[WORKLOAD]
+    B, T, H, Dk, Dv, C = w.B, w.T, w.H, w.Dk, w.Dv, w.chunk
+    inp = gdn_inputs.make_inputs(WORKLOAD)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+
+    def to_dev(a):
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(a).to(dev)
+
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
+    out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
+    s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
+    ws = gdn.workspace(q, v)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        gdn.gdn_chunk_forward_ws(q, k, v, alpha, beta, s_in, out, s_out, ws, chunk=C, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+
+    # Per-stage durations: HIP events recorded by the library on the same stream.
+    stage_ms = gdn.gdn_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws,
+                                      reps=args.steps, chunk=C, stream=stream)
+    torch.cuda.synchronize()
+
+    # Cold-cache steps: a 1 GiB write before each (outside the events) evicts L2 and MALL.
+    cold_ms = None
+    if args.cold_steps > 0:
+        scratch = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        times = []
+        for i in range(args.cold_steps):
+            scratch.fill_(float(i))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            step()
+            b.record(stream)
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        cold_ms = float(np.median(times))
+        del scratch
+
+    cnt = algorithmic_counts(B, T, H, Dk, Dv, C)
+    sec = ms_per_step / 1e3
+    tflops = cnt["flops"]["total"] / sec / 1e12
+    names = dict(zip(STAGES, stage_ms))
+    dom = max(names, key=names.get)
+    dom_flops = {"gdn_wy_kernel": cnt["flops"]["wy"], "gdn_scan_kernel": cnt["flops"]["scan"],
+                 "gdn_output_kernel": cnt["flops"]["out"]}[dom]
+    achieved = dom_flops / (names[dom] / 1e3) / 1e12
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": load_traffic(dom),
+                "duration_ms": round(names[dom], 5),
+                "algorithmic_flops_per_launch": dom_flops}
+
+    rec = {
+        "metric": METRIC,
+        "value": round(B * T / sec, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "one 1280x704 latent frame: B=1 T=3520 (44x80) H=16 Dk=Dv=128 "
+                               "chunk=64, bf16 q/k/v, fp32 state in/out",
+                   "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C},
+        "tflops": round(tflops, 2),
+        "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "hbm_frac_algorithmic": round(cnt["bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
+        "ms_per_step_cold": None if cold_ms is None else round(cold_ms, 5),
+        "stage_ms": {k_: round(v_, 5) for k_, v_ in names.items()},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(inp, B, T)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

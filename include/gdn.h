@@ -1,0 +1,135 @@
+/*
+ * gdn.h -- C ABI of the MI355X (gfx950) gated delta-rule chunk forward.
+ *
+ * Operation (paper: Section "Hybrid Architecture", equation gdn_combined, and
+ * Section "Frame-wise Gated DeltaNet", equations appendix_gdn_kv_update /
+ * appendix_gdn_kv_compact, applied with one token per update; readout as in
+ * equation appendix_gdn_readout without the normalizer, gate or projection):
+ *
+ *   for each batch b and head h independently, for t = 0 .. T-1:
+ *     S_t = alpha_t S_{t-1} (I - beta_t k_t k_t^T) + beta_t v_t k_t^T
+ *     o_t = S_t q_t
+ *
+ * S_{-1} is state_in, and the terminal S_{T-1} is written to state_out: only
+ * that terminal state is carried from one streaming call to the next
+ * (subsection "Streaming cache").  The state is stored transposed, as
+ * H = S^T with shape [Dk][Dv] per (b, h), the orientation in which the paper's
+ * kernel section writes the scan (S_f = alpha_f P_f S_{f-1} + A_f).
+ *
+ * The work is evaluated chunk by chunk (chunks of `chunk` tokens): a per-chunk
+ * WY/UT transform, a sequential scan of the state across chunks, and a
+ * per-chunk output pass.  This is an exact rewrite of the recurrence; results
+ * differ from it only by rounding.
+ *
+ * Layouts (all contiguous, row-major, 64-bit indexed):
+ *   q, k      [B][T][H][Dk]      bf16 (gdn_chunk_forward*) or fp32 (*_f32*)
+ *   v, out    [B][T][H][Dv]      same element type as q
+ *   alpha     [B][T][H]          fp32, decay gate, expected in [0, 1]
+ *   beta      [B][T][H]          fp32, write gate, expected in [0, 1] (any finite value works)
+ *   state_in  [B][H][Dk][Dv]     fp32, or NULL for a zero initial state
+ *   state_out [B][H][Dk][Dv]     fp32, or NULL to drop the terminal state
+ *
+ * Pointers q .. state_out are DEVICE pointers on the current HIP device,
+ * owned by the caller and 16-byte aligned.  state_in == state_out (in-place
+ * streaming) is allowed; `out` and `state_out` must not overlap any input
+ * otherwise.  Supported shapes: B, H, T >= 1; Dk, Dv in {64, 128};
+ * chunk == 64.  T need not be a multiple of the chunk: the tail is processed
+ * as if padded with alpha = 1, beta = 0, q = k = v = 0, which is an exact
+ * no-op on the state.
+ *
+ * Calls are asynchronous on `stream` (a hipStream_t, NULL = the default
+ * stream): they validate the arguments on the host, enqueue three kernels and
+ * return.  On a validation failure nothing is enqueued and a negative status
+ * is returned.  Values are not checked: non-finite alpha or beta propagate,
+ * and alpha < 0 is outside the supported domain (the scan works with
+ * log alpha; log alpha is clamped below at -87.3, i.e. alpha < 1.2e-38 acts
+ * as that value).
+ */
+#ifndef GDN_H
+#define GDN_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    GDN_OK = 0,
+    GDN_ERR_NULL = -1,        /* a required pointer is NULL */
+    GDN_ERR_SHAPE = -2,       /* B, H or T < 1, or an index would overflow */
+    GDN_ERR_UNSUPPORTED = -3, /* Dk/Dv not in {64,128} or chunk != 64 */
+    GDN_ERR_WORKSPACE = -4,   /* workspace missing, too small or misaligned */
+    GDN_ERR_HIP = -5,         /* a HIP runtime call or kernel launch failed */
+    GDN_ERR_ALIGN = -6,       /* a pointer is not 16-byte aligned */
+    GDN_ERR_ALIAS = -7        /* out/state_out overlaps an input it may not */
+} gdn_status;
+
+/*
+ * bf16 path: q, k, v and out hold bf16; alpha, beta and the state are fp32.
+ * Products run on bf16 MFMA with fp32 accumulation; the recurrent state stays
+ * fp32 across the whole scan.  Uses a workspace cached by the library per
+ * device (allocated with hipMalloc on first use and grown when a larger call
+ * needs it; a growing call synchronizes the device).  Not safe to call
+ * concurrently from several host threads or on several streams at once: use
+ * gdn_chunk_forward_ws for that.
+ */
+int gdn_chunk_forward(const void *q, const void *k, const void *v,
+                      const float *alpha, const float *beta, const float *state_in,
+                      void *out, float *state_out,
+                      int B, int H, int T, int Dk, int Dv, int chunk, void *stream);
+
+/* fp32 path: same contract, q, k, v and out hold fp32 (fp32 MFMA throughout). */
+int gdn_chunk_forward_f32(const float *q, const float *k, const float *v,
+                          const float *alpha, const float *beta, const float *state_in,
+                          float *out, float *state_out,
+                          int B, int H, int T, int Dk, int Dv, int chunk, void *stream);
+
+/*
+ * Bytes of device workspace the *_ws variants need for this shape
+ * (is_bf16 = 1 for the bf16 path, 0 for fp32).  Returns 0 for unsupported
+ * or invalid shapes.
+ */
+size_t gdn_workspace_bytes(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16);
+
+/*
+ * Explicit-workspace variants: identical to the calls above, but use the
+ * caller-owned device buffer `ws` (256-byte aligned, at least
+ * gdn_workspace_bytes(...) bytes) and allocate nothing.  Concurrent calls
+ * are safe when each uses its own workspace.  The workspace holds only
+ * intermediate results; its contents on entry do not matter.
+ */
+int gdn_chunk_forward_ws(const void *q, const void *k, const void *v,
+                         const float *alpha, const float *beta, const float *state_in,
+                         void *out, float *state_out,
+                         int B, int H, int T, int Dk, int Dv, int chunk,
+                         void *ws, size_t ws_bytes, void *stream);
+
+int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v,
+                             const float *alpha, const float *beta, const float *state_in,
+                             float *out, float *state_out,
+                             int B, int H, int T, int Dk, int Dv, int chunk,
+                             void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Per-stage timing (measurement aid, same arguments as gdn_chunk_forward_ws
+ * plus is_bf16): runs the whole path `reps` times on `stream`, recording HIP
+ * events on that stream around each of the three stages (WY transform, state
+ * scan, output), then synchronizes the stream and writes the mean duration of
+ * each stage in milliseconds to stage_ms[0..2] (host memory).  Creates and
+ * destroys its own events.
+ */
+int gdn_profile_stages(const void *q, const void *k, const void *v,
+                       const float *alpha, const float *beta, const float *state_in,
+                       void *out, float *state_out,
+                       int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
+                       void *ws, size_t ws_bytes, int reps, float *stage_ms, void *stream);
+
+/* Static, human-readable text for a status code. */
+const char *gdn_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_H */

@@ -1,0 +1,305 @@
+// Host side of libgdn: argument validation, workspace layout and caching,
+// kernel launches, and the extern "C" entry points declared in gdn.h.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <mutex>
+#include <unordered_map>
+#include <vector>
+
+#include "gdn.h"
+#include "gdn_kernels.h"
+
+namespace {
+
+using gdn::kChunk;
+
+struct WsLayout {
+    size_t g, W, Kt, Ut, Hs, Us, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz) {
+    const size_t nch = (size_t)B * H * (((size_t)T + kChunk - 1) / kChunk);
+    WsLayout L;
+    size_t off = 0;
+    L.g = off;  off = align256(off + nch * kChunk * 8);
+    L.W = off;  off = align256(off + nch * kChunk * Dk * esz);
+    L.Kt = off; off = align256(off + nch * Dk * kChunk * esz);
+    L.Ut = off; off = align256(off + nch * Dv * kChunk * esz);
+    L.Hs = off; off = align256(off + nch * Dv * Dk * esz);
+    L.Us = off; off = align256(off + nch * Dv * kChunk * esz);
+    L.total = off;
+    return L;
+}
+
+bool shape_ok(int B, int H, int T) {
+    if (B < 1 || H < 1 || T < 1) return false;
+    // gridDim.y carries B*H
+    if ((long long)B * H > 65535) return false;
+    return true;
+}
+
+bool dims_ok(int Dk, int Dv, int chunk) {
+    return (Dk == 64 || Dk == 128) && (Dv == 64 || Dv == 128) && chunk == kChunk;
+}
+
+bool misaligned(const void *p) { return p && ((uintptr_t)p & 15u); }
+
+struct Range {
+    uintptr_t lo, hi;
+    bool valid() const { return lo != 0; }
+    bool overlaps(const Range &o) const { return valid() && o.valid() && lo < o.hi && o.lo < hi; }
+};
+Range range(const void *p, size_t bytes) { return Range{(uintptr_t)p, (uintptr_t)p + bytes}; }
+
+int validate(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+             const float *state_in, const void *out, const float *state_out, int B, int H, int T,
+             int Dk, int Dv, int chunk, size_t esz) {
+    if (!q || !k || !v || !alpha || !beta || !out) return GDN_ERR_NULL;
+    if (!shape_ok(B, H, T)) return GDN_ERR_SHAPE;
+    if (!dims_ok(Dk, Dv, chunk)) return GDN_ERR_UNSUPPORTED;
+    if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(alpha) || misaligned(beta) ||
+        misaligned(state_in) || misaligned(out) || misaligned(state_out))
+        return GDN_ERR_ALIGN;
+    const size_t ntok = (size_t)B * T * H;
+    const Range rq = range(q, ntok * Dk * esz), rk = range(k, ntok * Dk * esz),
+                rv = range(v, ntok * Dv * esz), ra = range(alpha, ntok * 4), rb = range(beta, ntok * 4),
+                ro = range(out, ntok * Dv * esz);
+    const size_t sbytes = (size_t)B * H * Dk * Dv * 4;
+    const Range rsi = range(state_in, sbytes), rso = range(state_out, sbytes);
+    const Range ins[] = {rq, rk, rv, ra, rb, rsi};
+    for (const Range &r : ins)
+        if (ro.overlaps(r)) return GDN_ERR_ALIAS;
+    if (rso.valid()) {
+        for (int i = 0; i < 5; ++i)
+            if (rso.overlaps(ins[i])) return GDN_ERR_ALIAS;
+        if (rso.overlaps(ro)) return GDN_ERR_ALIAS;
+        if (rsi.valid() && rso.overlaps(rsi) && rso.lo != rsi.lo) return GDN_ERR_ALIAS;
+    }
+    return GDN_OK;
+}
+
+template <class E>
+gdn::Params<E> make_params(const void *q, const void *k, const void *v, const float *alpha,
+                           const float *beta, const float *state_in, void *out, float *state_out,
+                           int B, int H, int T, int Dk, int Dv, void *ws) {
+    gdn::Params<E> p;
+    p.q = (const E *)q;
+    p.k = (const E *)k;
+    p.v = (const E *)v;
+    p.alpha = alpha;
+    p.beta = beta;
+    p.state_in = state_in;
+    p.out = (E *)out;
+    p.state_out = state_out;
+    p.B = B;
+    p.H = H;
+    p.T = T;
+    p.NC = (T + kChunk - 1) / kChunk;
+    const WsLayout L = ws_layout(B, H, T, Dk, Dv, sizeof(E));
+    unsigned char *base = (unsigned char *)ws;
+    p.g = (double *)(base + L.g);
+    p.W = (E *)(base + L.W);
+    p.Kt = (E *)(base + L.Kt);
+    p.Ut = (E *)(base + L.Ut);
+    p.Hs = (E *)(base + L.Hs);
+    p.Us = (E *)(base + L.Us);
+    return p;
+}
+
+template <class E, int DK, int DV>
+hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, hipEvent_t *ev) {
+    static std::once_flag attr_once;
+    static hipError_t attr_err = hipSuccess;
+    const size_t lds1 = gdn::WyLds<E, DK, DV>::bytes;
+    const size_t lds3 = gdn::OutLds<E, DK, DV>::bytes;
+    std::call_once(attr_once, [&] {
+        hipError_t e1 = hipFuncSetAttribute((const void *)gdn::gdn_wy_kernel<E, DK, DV>,
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds1);
+        hipError_t e3 = hipFuncSetAttribute((const void *)gdn::gdn_output_kernel<E, DK, DV>,
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds3);
+        attr_err = (e1 != hipSuccess) ? e1 : e3;
+    });
+    if (attr_err != hipSuccess) return attr_err;
+    const unsigned BH = (unsigned)(p.B * p.H);
+    hipError_t er = hipSuccess;
+    auto mark = [&](int i) {
+        if (ev && er == hipSuccess) er = hipEventRecord(ev[i], s);
+    };
+    mark(0);
+    hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds1, s, p);
+    mark(1);
+    hipLaunchKernelGGL((gdn::gdn_scan_kernel<E, DK, DV>), dim3(DV / 16, BH), dim3(DK * 2), 0, s, p);
+    mark(2);
+    hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
+    mark(3);
+    const hipError_t le = hipGetLastError();
+    return le != hipSuccess ? le : er;
+}
+
+template <class E>
+hipError_t dispatch(const gdn::Params<E> &p, int Dk, int Dv, hipStream_t s, hipEvent_t *ev) {
+    if (Dk == 128 && Dv == 128) return launch_path<E, 128, 128>(p, s, ev);
+    if (Dk == 64 && Dv == 64) return launch_path<E, 64, 64>(p, s, ev);
+    if (Dk == 128 && Dv == 64) return launch_path<E, 128, 64>(p, s, ev);
+    return launch_path<E, 64, 128>(p, s, ev);
+}
+
+int run(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+        const float *state_in, void *out, float *state_out, int B, int H, int T, int Dk, int Dv,
+        int chunk, bool bf16, void *ws, size_t ws_bytes, void *stream, hipEvent_t *ev) {
+    const size_t esz = bf16 ? 2 : 4;
+    int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
+    if (st != GDN_OK) return st;
+    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz).total)
+        return GDN_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (bf16) {
+        e = dispatch(make_params<uint16_t>(q, k, v, alpha, beta, state_in, out, state_out, B, H, T,
+                                           Dk, Dv, ws),
+                     Dk, Dv, s, ev);
+    } else {
+        e = dispatch(make_params<float>(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk,
+                                        Dv, ws),
+                     Dk, Dv, s, ev);
+    }
+    return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+// Library-cached workspace, one buffer per device, grown on demand.
+std::mutex g_ws_mu;
+std::unordered_map<int, std::pair<void *, size_t>> g_ws;
+
+int cached_workspace(size_t need, void **ws) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return GDN_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_ws_mu);
+    auto &slot = g_ws[dev];
+    if (slot.second < need) {
+        if (slot.first) {
+            if (hipDeviceSynchronize() != hipSuccess) return GDN_ERR_HIP;
+            if (hipFree(slot.first) != hipSuccess) return GDN_ERR_HIP;
+            slot = {nullptr, 0};
+        }
+        void *ptr = nullptr;
+        if (hipMalloc(&ptr, need) != hipSuccess) return GDN_ERR_HIP;
+        slot = {ptr, need};
+    }
+    *ws = slot.first;
+    return GDN_OK;
+}
+
+int run_cached(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+               const float *state_in, void *out, float *state_out, int B, int H, int T, int Dk,
+               int Dv, int chunk, bool bf16, void *stream) {
+    const size_t esz = bf16 ? 2 : 4;
+    int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
+    if (st != GDN_OK) return st;
+    const size_t need = ws_layout(B, H, T, Dk, Dv, esz).total;
+    void *ws = nullptr;
+    st = cached_workspace(need, &ws);
+    if (st != GDN_OK) return st;
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, bf16, ws,
+               need, stream, nullptr);
+}
+
+}  // namespace
+
+extern "C" {
+
+int gdn_chunk_forward(const void *q, const void *k, const void *v, const float *alpha,
+                      const float *beta, const float *state_in, void *out, float *state_out, int B,
+                      int H, int T, int Dk, int Dv, int chunk, void *stream) {
+    return run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, true,
+                      stream);
+}
+
+int gdn_chunk_forward_f32(const float *q, const float *k, const float *v, const float *alpha,
+                          const float *beta, const float *state_in, float *out, float *state_out,
+                          int B, int H, int T, int Dk, int Dv, int chunk, void *stream) {
+    return run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, false,
+                      stream);
+}
+
+size_t gdn_workspace_bytes(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16) {
+    if (!shape_ok(B, H, T) || !dims_ok(Dk, Dv, chunk)) return 0;
+    return ws_layout(B, H, T, Dk, Dv, is_bf16 ? 2 : 4).total;
+}
+
+int gdn_chunk_forward_ws(const void *q, const void *k, const void *v, const float *alpha,
+                         const float *beta, const float *state_in, void *out, float *state_out,
+                         int B, int H, int T, int Dk, int Dv, int chunk, void *ws, size_t ws_bytes,
+                         void *stream) {
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, true, ws,
+               ws_bytes, stream, nullptr);
+}
+
+int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v, const float *alpha,
+                             const float *beta, const float *state_in, float *out, float *state_out,
+                             int B, int H, int T, int Dk, int Dv, int chunk, void *ws,
+                             size_t ws_bytes, void *stream) {
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, false, ws,
+               ws_bytes, stream, nullptr);
+}
+
+int gdn_profile_stages(const void *q, const void *k, const void *v, const float *alpha,
+                       const float *beta, const float *state_in, void *out, float *state_out,
+                       int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, void *ws,
+                       size_t ws_bytes, int reps, float *stage_ms, void *stream) {
+    if (!stage_ms || reps < 1) return GDN_ERR_NULL;
+    const bool bf16 = is_bf16 != 0;
+    const size_t esz = bf16 ? 2 : 4;
+    int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
+    if (st != GDN_OK) return st;
+    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz).total)
+        return GDN_ERR_WORKSPACE;
+    std::vector<hipEvent_t> ev((size_t)reps * 4, nullptr);
+    int status = GDN_OK;
+    for (auto &e : ev)
+        if (hipEventCreate(&e) != hipSuccess) {
+            e = nullptr;
+            status = GDN_ERR_HIP;
+        }
+    for (int r = 0; r < reps && status == GDN_OK; ++r)
+        status = run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, bf16,
+                     ws, ws_bytes, stream, &ev[(size_t)r * 4]);
+    if (status == GDN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
+        status = GDN_ERR_HIP;
+    if (status == GDN_OK) {
+        double sum[3] = {0.0, 0.0, 0.0};
+        for (int r = 0; r < reps && status == GDN_OK; ++r) {
+            for (int s = 0; s < 3; ++s) {
+                float ms = 0.f;
+                if (hipEventElapsedTime(&ms, ev[(size_t)r * 4 + s], ev[(size_t)r * 4 + s + 1]) !=
+                    hipSuccess) {
+                    status = GDN_ERR_HIP;
+                    break;
+                }
+                sum[s] += ms;
+            }
+        }
+        for (int s = 0; s < 3; ++s) stage_ms[s] = (float)(sum[s] / reps);
+    }
+    for (auto &e : ev)
+        if (e) (void)hipEventDestroy(e);
+    return status;
+}
+
+const char *gdn_status_string(int status) {
+    switch (status) {
+    case GDN_OK: return "ok";
+    case GDN_ERR_NULL: return "a required pointer is NULL";
+    case GDN_ERR_SHAPE: return "invalid shape (B, H, T must be >= 1 and B*H <= 65535)";
+    case GDN_ERR_UNSUPPORTED: return "unsupported configuration (Dk, Dv in {64,128}; chunk == 64)";
+    case GDN_ERR_WORKSPACE: return "workspace missing, too small or not 256-byte aligned";
+    case GDN_ERR_HIP: return "HIP runtime error or kernel launch failure";
+    case GDN_ERR_ALIGN: return "a pointer is not 16-byte aligned";
+    case GDN_ERR_ALIAS: return "an output overlaps an input";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,176 @@
+"""Thin ctypes binding of libgdn.so (the C ABI declared in include/gdn.h).
+
+Argument marshalling only: every step of the GDN chunk forward runs in the HIP
+kernels behind the C ABI.  PyTorch supplies device memory and the current
+stream.  There is no fallback: if libgdn.so is missing or a call fails, this
+module raises.
+"""
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgdn.so")
+CHUNK = 64
+
+GDN_OK = 0
+_lib = None
+
+
+class GdnError(RuntimeError):
+    """A libgdn call returned a negative status."""
+
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} failed: {gdn_status_string(status)} (status {status})")
+
+
+def lib():
+    """Load libgdn.so (built in-tree by paper_2605_30409_amd/build.py)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
+                              "or python paper_2605_30409_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i, sz, f_p = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
+        core = [vp, vp, vp, f_p, f_p, f_p, vp, f_p, i, i, i, i, i, i]
+        for name in ("gdn_chunk_forward", "gdn_chunk_forward_f32"):
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = i, core + [vp]
+        for name in ("gdn_chunk_forward_ws", "gdn_chunk_forward_f32_ws"):
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = i, core + [vp, sz, vp]
+        L.gdn_workspace_bytes.restype = sz
+        L.gdn_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
+        L.gdn_profile_stages.restype = i
+        L.gdn_profile_stages.argtypes = core + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        L.gdn_status_string.restype = ctypes.c_char_p
+        L.gdn_status_string.argtypes = [i]
+        _lib = L
+    return _lib
+
+
+def gdn_status_string(status):
+    return lib().gdn_status_string(int(status)).decode()
+
+
+def gdn_workspace_bytes(B, H, T, Dk, Dv, chunk=CHUNK, is_bf16=True):
+    return int(lib().gdn_workspace_bytes(B, H, T, Dk, Dv, chunk, 1 if is_bf16 else 0))
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check(q, k, v, alpha, beta, state_in, out, state_out):
+    """Shape/dtype/device/contiguity checks; returns (B, H, T, Dk, Dv, is_bf16)."""
+    if q.dtype not in (torch.bfloat16, torch.float32):
+        raise TypeError(f"q must be bfloat16 or float32, got {q.dtype}")
+    for name, t in (("k", k), ("v", v), ("out", out)):
+        if t is not None and t.dtype != q.dtype:
+            raise TypeError(f"{name} must have dtype {q.dtype}, got {t.dtype}")
+    for name, t in (("alpha", alpha), ("beta", beta), ("state_in", state_in), ("state_out", state_out)):
+        if t is not None and t.dtype != torch.float32:
+            raise TypeError(f"{name} must be float32, got {t.dtype}")
+    dev = q.device
+    tensors = dict(q=q, k=k, v=v, alpha=alpha, beta=beta, state_in=state_in, out=out, state_out=state_out)
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if t.device != dev or dev.type != "cuda":
+            raise ValueError(f"{name} must be on the same GPU as q ({dev}), got {t.device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if q.dim() != 4:
+        raise ValueError("q must be [B, T, H, Dk]")
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if tuple(k.shape) != (B, T, H, Dk) or tuple(v.shape) != (B, T, H, Dv):
+        raise ValueError("k must be [B, T, H, Dk] and v [B, T, H, Dv]")
+    if tuple(alpha.shape) != (B, T, H) or tuple(beta.shape) != (B, T, H):
+        raise ValueError("alpha and beta must be [B, T, H]")
+    for name, t in (("state_in", state_in), ("state_out", state_out)):
+        if t is not None and tuple(t.shape) != (B, H, Dk, Dv):
+            raise ValueError(f"{name} must be [B, H, Dk, Dv]")
+    if out is not None and tuple(out.shape) != (B, T, H, Dv):
+        raise ValueError("out must be [B, T, H, Dv]")
+    return B, H, T, Dk, Dv, q.dtype == torch.bfloat16
+
+
+def _stream(dev, stream):
+    s = torch.cuda.current_stream(dev) if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _call(name, q, k, v, alpha, beta, state_in, out, state_out, chunk, extra, stream):
+    B, H, T, Dk, Dv, is_bf16 = _check(q, k, v, alpha, beta, state_in, out, state_out)
+    with torch.cuda.device(q.device):
+        rc = getattr(lib(), name)(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(beta), _ptr(state_in),
+                                  _ptr(out), _ptr(state_out), B, H, T, Dk, Dv, int(chunk), *extra,
+                                  _stream(q.device, stream))
+    if rc != GDN_OK:
+        raise GdnError(name, rc)
+
+
+def gdn_chunk_forward(q, k, v, alpha, beta, state_in, out, state_out, chunk=CHUNK, stream=None):
+    """bf16 path with the library-cached workspace (asynchronous on the current stream)."""
+    _call("gdn_chunk_forward", q, k, v, alpha, beta, state_in, out, state_out, chunk, (), stream)
+
+
+def gdn_chunk_forward_f32(q, k, v, alpha, beta, state_in, out, state_out, chunk=CHUNK, stream=None):
+    """fp32 path with the library-cached workspace."""
+    _call("gdn_chunk_forward_f32", q, k, v, alpha, beta, state_in, out, state_out, chunk, (), stream)
+
+
+def gdn_chunk_forward_ws(q, k, v, alpha, beta, state_in, out, state_out, ws, chunk=CHUNK, stream=None):
+    """bf16 path with a caller-owned workspace (a uint8 device tensor)."""
+    _call("gdn_chunk_forward_ws", q, k, v, alpha, beta, state_in, out, state_out, chunk,
+          (_ptr(ws), ws.numel()), stream)
+
+
+def gdn_chunk_forward_f32_ws(q, k, v, alpha, beta, state_in, out, state_out, ws, chunk=CHUNK,
+                             stream=None):
+    """fp32 path with a caller-owned workspace."""
+    _call("gdn_chunk_forward_f32_ws", q, k, v, alpha, beta, state_in, out, state_out, chunk,
+          (_ptr(ws), ws.numel()), stream)
+
+
+def gdn_profile_stages(q, k, v, alpha, beta, state_in, out, state_out, ws, reps=20, chunk=CHUNK,
+                       stream=None):
+    """Mean per-stage durations in ms (WY transform, state scan, output) over `reps` runs."""
+    is_bf16 = q.dtype == torch.bfloat16
+    ms = (ctypes.c_float * 3)()
+    _call("gdn_profile_stages", q, k, v, alpha, beta, state_in, out, state_out, chunk,
+          (1 if is_bf16 else 0, _ptr(ws), ws.numel(), int(reps), ms), stream)
+    return [float(x) for x in ms]
+
+
+def workspace(q, v, chunk=CHUNK):
+    """Allocate a workspace tensor sized for inputs shaped like q [B,T,H,Dk] and v [.., Dv]."""
+    B, T, H, Dk = q.shape
+    n = gdn_workspace_bytes(B, H, T, Dk, v.shape[-1], chunk, q.dtype == torch.bfloat16)
+    if n == 0:
+        raise ValueError("unsupported shape for the GDN chunk forward")
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def forward(q, k, v, alpha, beta, state_in=None, *, out=None, state_out=None, want_state=True,
+            ws=None, chunk=CHUNK, stream=None):
+    """GDN chunk forward.  q, k [B,T,H,Dk] and v [B,T,H,Dv] in bf16 or fp32 (on the GPU);
+    alpha, beta [B,T,H] fp32; state_in [B,H,Dk,Dv] fp32 or None (zero).
+    Returns (out [B,T,H,Dv] like v, state_out [B,H,Dk,Dv] fp32 or None)."""
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if out is None:
+        out = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    if state_out is None and want_state:
+        state_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+    bf = q.dtype == torch.bfloat16
+    if ws is None:
+        fn = gdn_chunk_forward if bf else gdn_chunk_forward_f32
+        fn(q, k, v, alpha, beta, state_in, out, state_out, chunk=chunk, stream=stream)
+    else:
+        fn = gdn_chunk_forward_ws if bf else gdn_chunk_forward_f32_ws
+        fn(q, k, v, alpha, beta, state_in, out, state_out, ws, chunk=chunk, stream=stream)
+    return out, state_out

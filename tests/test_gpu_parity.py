@@ -1,0 +1,234 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Error metric (per tensor): max|x - x_ref| / max|x_ref|, for `out` and for the
+terminal state.  Bounds: 1e-4 for the fp32 path and 2e-2 for bf16 q/k/v with
+an fp32 state.  The oracle reads the very same stored (bf16-rounded) inputs,
+so the error measures the kernels, not input quantization.
+"""
+import numpy as np
+import pytest
+
+import gdn_inputs
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def torch_mod():
+    import torch
+    return torch
+
+
+def dev_tensor(a):
+    torch = torch_mod()
+    if a is None:
+        return None
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host_f64(t):
+    torch = torch_mod()
+    if t.dtype == torch.bfloat16:
+        return gdn_inputs.bf16_bits_to_f32(t.view(torch.int16).cpu().numpy().view(np.uint16)).astype(np.float64)
+    return t.cpu().numpy().astype(np.float64)
+
+
+def rel_err(x, ref):
+    return float(np.abs(x - ref).max() / max(np.abs(ref).max(), 1e-30))
+
+
+def run_gpu(gdn, inp, state_in="input", ws=False):
+    t = {k: dev_tensor(inp[k]) for k in ("q", "k", "v", "alpha", "beta")}
+    si = dev_tensor(inp["state_in"]) if state_in == "input" else state_in
+    kw = {}
+    if ws:
+        kw["ws"] = gdn.workspace(t["q"], t["v"])
+    out, st = gdn.forward(t["q"], t["k"], t["v"], t["alpha"], t["beta"], si, **kw)
+    torch_mod().cuda.synchronize()
+    return out, st
+
+
+def check(gdn, inp, label, heads=None):
+    """Full comparison (or on a sampled subset of heads) against the oracle."""
+    out, st = run_gpu(gdn, inp)
+    o, s = host_f64(out), host_f64(st)
+    sl = slice(None) if heads is None else list(heads)
+    ref_o, ref_s = oracle.gdn_forward(inp["q"][:, :, sl], inp["k"][:, :, sl], inp["v"][:, :, sl],
+                                      inp["alpha"][:, :, sl], inp["beta"][:, :, sl],
+                                      None if inp["state_in"] is None else inp["state_in"][:, sl])
+    eo, es = rel_err(o[:, :, sl], ref_o), rel_err(s[:, sl], ref_s)
+    tol = TOL[inp["dtype"]]
+    print(f"[parity] {label}: out err {eo:.3e}, state err {es:.3e} (tol {tol:g})", flush=True)
+    assert np.isfinite(o).all() and np.isfinite(s).all()
+    assert eo < tol, (label, eo)
+    assert es < tol, (label, es)
+    return eo, es
+
+
+# ---- small shapes: several chunks, ragged tails, every (Dk, Dv) pair, both dtypes ----
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("Dk,Dv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+@pytest.mark.parametrize("T", [1, 63, 64, 65, 200, 457])
+def test_small_shapes(gdn, dtype, Dk, Dv, T):
+    inp = gdn_inputs.make_inputs(1, B=2, T=T, H=3, Dk=Dk, Dv=Dv, dtype=dtype,
+                                 seed=7000 + T + Dk + 2 * Dv)
+    check(gdn, inp, f"B2 T{T} H3 Dk{Dk} Dv{Dv} {dtype}")
+
+
+def test_workload0_tiny_f32(gdn):
+    check(gdn, gdn_inputs.make_inputs(0), "workload 0 (tiny fp32)")
+
+
+def test_workload1_frame(gdn):
+    check(gdn, gdn_inputs.make_inputs(1), "workload 1 (one 1280x704 frame)")
+
+
+def test_workload1_ragged(gdn):
+    check(gdn, gdn_inputs.make_inputs(1, T=3520 + 37), "workload 1 shape, T=3557 ragged")
+
+
+def test_workload3_batched_fast_forget(gdn):
+    check(gdn, gdn_inputs.make_inputs(3), "workload 3 (B4 H20 D64, fast-forget alpha)")
+
+
+def test_workload4_long_context(gdn):
+    # The oracle runs on 4 of the 32 heads (independent streams), every token.
+    check(gdn, gdn_inputs.make_inputs(4), "workload 4 (T42240 H32), heads 0,9,22,31",
+          heads=[0, 9, 22, 31])
+
+
+def test_workload2_streaming_20_calls(gdn):
+    """20 calls with the fp32 state threaded on the device; oracle on 2 heads."""
+    torch = torch_mod()
+    heads = [0, 11]
+    st_dev = None
+    ref_state = None
+    worst_o = worst_s = 0.0
+    for call in range(20):
+        inp = gdn_inputs.make_inputs(2, call)
+        out, st_dev = run_gpu(gdn, inp, state_in=st_dev)
+        ref_o, ref_state = oracle.gdn_forward(inp["q"][:, :, heads], inp["k"][:, :, heads],
+                                              inp["v"][:, :, heads], inp["alpha"][:, :, heads],
+                                              inp["beta"][:, :, heads], ref_state)
+        o = host_f64(out)[:, :, heads]
+        s = host_f64(st_dev)[:, heads]
+        worst_o = max(worst_o, rel_err(o, ref_o))
+        worst_s = max(worst_s, rel_err(s, ref_state))
+    print(f"[parity] workload 2 (20 streaming calls): out err {worst_o:.3e}, state err {worst_s:.3e}",
+          flush=True)
+    assert worst_o < TOL["bf16"] and worst_s < TOL["bf16"]
+    assert torch.isfinite(st_dev).all()
+
+
+# ---- semantics and edge cases ----
+def test_zero_state_in_equals_none(gdn):
+    torch = torch_mod()
+    inp = gdn_inputs.make_inputs(1, T=300, H=2, state="zero")
+    o1, s1 = run_gpu(gdn, inp, state_in=None)
+    z = torch.zeros(1, 2, 128, 128, device="cuda")
+    o2, s2 = run_gpu(gdn, inp, state_in=z)
+    assert torch.equal(o1, o2) and torch.equal(s1, s2)
+
+
+def test_state_out_none_and_inplace_state(gdn):
+    torch = torch_mod()
+    inp = gdn_inputs.make_inputs(1, T=300, H=2)
+    t = {k: dev_tensor(inp[k]) for k in ("q", "k", "v", "alpha", "beta")}
+    si = dev_tensor(inp["state_in"])
+    o_ref, s_ref = gdn.forward(t["q"], t["k"], t["v"], t["alpha"], t["beta"], si)
+    o_none, s_none = gdn.forward(t["q"], t["k"], t["v"], t["alpha"], t["beta"], si, want_state=False)
+    assert s_none is None
+    buf = si.clone()
+    o_inp, s_inp = gdn.forward(t["q"], t["k"], t["v"], t["alpha"], t["beta"], buf, state_out=buf)
+    torch.cuda.synchronize()
+    assert torch.equal(o_none, o_ref) and torch.equal(o_inp, o_ref)
+    assert torch.equal(buf, s_ref)
+
+
+def test_workspace_variant_matches_cached(gdn):
+    torch = torch_mod()
+    for dtype in ("bf16", "f32"):
+        inp = gdn_inputs.make_inputs(1, T=333, H=3, dtype=dtype)
+        o1, s1 = run_gpu(gdn, inp)
+        o2, s2 = run_gpu(gdn, inp, ws=True)
+        assert torch.equal(o1, o2) and torch.equal(s1, s2)
+
+
+def test_deterministic(gdn):
+    torch = torch_mod()
+    inp = gdn_inputs.make_inputs(1, T=1000, H=4)
+    o1, s1 = run_gpu(gdn, inp)
+    o2, s2 = run_gpu(gdn, inp)
+    assert torch.equal(o1, o2) and torch.equal(s1, s2)
+
+
+@pytest.mark.parametrize("m", [128, 1024, 100])
+def test_streaming_split(gdn, m):
+    """One call on x equals two calls (x[:m], then x[m:] with the carried state).
+    At a chunk-aligned split the chunking is identical, so the match is exact."""
+    torch = torch_mod()
+    inp = gdn_inputs.make_inputs(1, T=1500, H=2)
+    o, s = run_gpu(gdn, inp)
+    a = {k: (inp[k][:, :m] if k in ("q", "k", "v", "alpha", "beta") else inp[k]) for k in inp}
+    b = {k: (inp[k][:, m:] if k in ("q", "k", "v", "alpha", "beta") else inp[k]) for k in inp}
+    oa, sa = run_gpu(gdn, a)
+    ob, sb = run_gpu(gdn, b, state_in=sa)
+    o2 = torch.cat([oa, ob], dim=1)
+    if m % 64 == 0:
+        assert torch.equal(o2, o) and torch.equal(sb, s)
+    else:
+        assert rel_err(host_f64(o2), host_f64(o)) < 1e-2
+        assert rel_err(host_f64(sb), host_f64(s)) < 1e-2
+
+
+def test_invariant_beta0_alpha1_keeps_state(gdn):
+    torch = torch_mod()
+    inp = gdn_inputs.make_inputs(1, T=500, H=2)
+    inp["alpha"][:] = 1.0
+    inp["beta"][:] = 0.0
+    out, st = run_gpu(gdn, inp)
+    assert torch.equal(st.cpu(), torch.from_numpy(inp["state_in"]))
+    check(gdn, inp, "beta=0 alpha=1")
+
+
+def test_invariant_beta1_alpha1_unit_key_writes_v(gdn):
+    inp = gdn_inputs.make_inputs(1, T=200, H=2, dtype="f32")
+    inp["alpha"][:] = 1.0
+    inp["beta"][:] = 1.0
+    inp["q"] = inp["k"].copy()
+    out, _ = run_gpu(gdn, inp)
+    assert rel_err(host_f64(out), inp["v"].astype(np.float64)) < 1e-4
+
+
+def test_invariant_alpha0_resets(gdn):
+    """alpha = 0 at token t*: outputs from t* on do not depend on the past.  Earlier
+    tokens of the same chunk still enter the chunked algebra with weights of
+    order 1e-38 (log alpha is clamped at -87.3), and the bf16 rounding of the
+    outputs can flip by one unit in the last place, hence a 1e-3 bound."""
+    torch = torch_mod()
+    ts = 150
+    inp = gdn_inputs.make_inputs(1, T=300, H=2)
+    inp["alpha"][:, ts] = 0.0
+    other = gdn_inputs.make_inputs(1, T=300, H=2, seed=999)
+    for key in ("q", "k", "v", "alpha", "beta"):
+        other[key][:, ts:] = inp[key][:, ts:]
+    o1, s1 = run_gpu(gdn, inp)
+    o2, s2 = run_gpu(gdn, other)
+    d_o = rel_err(host_f64(o1)[:, ts:], host_f64(o2)[:, ts:])
+    d_s = rel_err(host_f64(s1), host_f64(s2))
+    assert d_o < 1e-3 and d_s < 1e-6, (d_o, d_s)
+    check(gdn, inp, "alpha=0 at t=150")
+
+
+def test_extreme_gates(gdn):
+    """alpha in {0, tiny, 1} and beta in {0, 1} mixed: no NaN, parity holds."""
+    inp = gdn_inputs.make_inputs(1, T=400, H=2, dtype="f32", seed=31)
+    r = np.random.default_rng(5)
+    choice = r.integers(0, 3, inp["alpha"].shape)
+    inp["alpha"] = np.where(choice == 0, 0.0, np.where(choice == 1, 1e-30, 1.0)).astype(np.float32)
+    inp["beta"] = r.integers(0, 2, inp["beta"].shape).astype(np.float32)
+    check(gdn, inp, "extreme gates")

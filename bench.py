@@ -98,6 +98,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps each preceded by a 1 GiB write that evicts the caches")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (a known-size "
+                         "reference for hardware traffic counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -125,6 +128,14 @@ def main():
     s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
     ws = gdn.workspace(q, v)
     stream = torch.cuda.current_stream(dev)
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 18  # float32 elements
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step():
         gdn.gdn_chunk_forward_ws(q, k, v, alpha, beta, s_in, out, s_out, ws, chunk=C, stream=stream)

@@ -276,13 +276,15 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
 }
 
 // --------------------------------------------------------------------------
-// Stage 2: sequential state scan across chunks.  Grid (Dv/16, B*H); one
-// workgroup owns 16 state columns of one (b, h) and carries them through all
+// Stage 2: sequential state scan across chunks.  1-D grid of
+// (Dv/16) * 8 * ceil(B*H / 8) workgroups; one workgroup owns 16 state columns
+// of one (b, h) and carries them through all
 // chunks in fp32 accumulators.  Its DK/32 waves split the Dk rows (32 each),
 // so every chunk costs one cross-wave reduction of the partial W H products.
 // --------------------------------------------------------------------------
 template <class E, int DK, int DV>
-__global__ __launch_bounds__(DK * 2) void gdn_scan_kernel(Params<E> p) {
+__global__ __launch_bounds__(DK * 2) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gdn_scan_kernel(Params<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
     using quad = typename TR::quad;
@@ -292,7 +294,14 @@ __global__ __launch_bounds__(DK * 2) void gdn_scan_kernel(Params<E> p) {
     __shared__ f32x4 sP[NW][4][64];    // partial (W H) tiles
     __shared__ quad sU[4][64];         // U tiles, already rounded to E
 
-    const int jt = blockIdx.x, bh = blockIdx.y;
+    // XCD-aware placement: workgroups are dealt round-robin to the 8 XCDs, so
+    // id = 8 slot + x runs on XCD x.  The NJ column blocks of one (b, h) are
+    // given consecutive slots of the same XCD and share its L2 for the
+    // chunk operands W and Kt that all of them read.
+    constexpr int NJ = DV / 16;
+    const int id = blockIdx.x, x = id & 7, slot = id >> 3;
+    const int bh = (slot / NJ) * 8 + x, jt = slot % NJ;
+    if (bh >= p.B * p.H) return;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
     const int j0 = 16 * jt, d0 = 32 * w;
     const int j = j0 + li;  // this lane's state column
@@ -344,16 +353,23 @@ __global__ __launch_bounds__(DK * 2) void gdn_scan_kernel(Params<E> p) {
         // H_{c-1} rounded to E: B operand over this wave's 32 rows, and saved for stage 3.
         const frag hb = TR::cat(TR::from_f32(Hacc[0]), TR::from_f32(Hacc[1]));
         TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)j * DK + d0 + 8 * lg, hb);
+        // Partial W H over this wave's rows: four independent MFMAs, then the LDS exchange.
+        f32x4 part[4];
 #pragma unroll
-        for (int st = 0; st < 4; ++st) sP[w][st][l] = TR::mma(f.wf[st], hb, f32x4{0.f, 0.f, 0.f, 0.f});
+        for (int st = 0; st < 4; ++st) part[st] = TR::mma(f.wf[st], hb, f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+        for (int st = 0; st < 4; ++st) sP[w][st][l] = part[st];
         lds_barrier();
         E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)j * kChunk + 8 * lg;
 #pragma unroll
         for (int o = 0; o < NOWN; ++o) {
             const int st = w + NW * o;
+            f32x4 pr[NW];
+#pragma unroll
+            for (int ww = 0; ww < NW; ++ww) pr[ww] = sP[ww][st][l];
             f32x4 u = TR::to_f32(f.uq[o]);
 #pragma unroll
-            for (int ww = 0; ww < NW; ++ww) u -= sP[ww][st][l];
+            for (int ww = 0; ww < NW; ++ww) u -= pr[ww];
             const quad uqr = TR::from_f32(u);
             TR::store(Us + 32 * (st >> 1) + 4 * (st & 1), uqr);
             sU[st][l] = uqr;

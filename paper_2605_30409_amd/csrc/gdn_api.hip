@@ -132,7 +132,7 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, hipEvent_t *ev) {
     hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds1, s, p);
     mark(1);
     const unsigned scan_groups = (DV / 16) * 8u * ((BH + 7u) / 8u);
-    hipLaunchKernelGGL((gdn::gdn_scan_kernel<E, DK, DV>), dim3(scan_groups), dim3(DK * 2), 0, s, p);
+    hipLaunchKernelGGL((gdn::gdn_scan_kernel<E, DK, DV>), dim3(scan_groups), dim3(DK), 0, s, p);
     mark(2);
     hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
     mark(3);

@@ -66,6 +66,10 @@ template <> struct Tr<uint16_t> {
     static __device__ __forceinline__ frag cat(quad lo, quad hi) {
         return frag{lo[0], lo[1], hi[0], hi[1]};
     }
+    static __device__ __forceinline__ quad lo(frag f) { return quad{f[0], f[1]}; }
+    // all bits kept (m = ~0) or the quad zeroed (m = 0)
+    static __device__ __forceinline__ quad mask(quad v, uint32_t m) { return quad{v[0] & m, v[1] & m}; }
+    static __device__ __forceinline__ quad hi(frag f) { return quad{f[2], f[3]}; }
     static __device__ __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
         return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                         __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
@@ -89,6 +93,12 @@ template <> struct Tr<float> {
     static __device__ __forceinline__ frag cat(quad lo, quad hi) {
         return frag{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     }
+    static __device__ __forceinline__ quad lo(frag f) { return quad{f[0], f[1], f[2], f[3]}; }
+    static __device__ __forceinline__ quad mask(quad v, uint32_t m) {
+        return quad{__uint_as_float(__float_as_uint(v[0]) & m), __uint_as_float(__float_as_uint(v[1]) & m),
+                    __uint_as_float(__float_as_uint(v[2]) & m), __uint_as_float(__float_as_uint(v[3]) & m)};
+    }
+    static __device__ __forceinline__ quad hi(frag f) { return quad{f[4], f[5], f[6], f[7]}; }
     static __device__ __forceinline__ f32x4 mma(frag a, frag b, f32x4 c) {
 #pragma unroll
         for (int s = 0; s < 8; ++s) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], c, 0, 0, 0);
@@ -101,6 +111,37 @@ template <> struct Tr<float> {
 template <class E>
 __device__ __forceinline__ typename Tr<E>::frag load_frag(const E *row_base, int lg) {
     return Tr<E>::load8(row_base + 8 * lg);
+}
+
+// Operand fragment whose k index runs down the rows of a row-major LDS tile
+// M (row stride ld elements): lane (li, lg) receives M[row0 + 8 lg + q'][col]
+// for q' = 0..7, with col = colbase + li, or, for tile a of a P32 pair,
+// col = colbase + p32_row(a, li).  bf16 uses the gfx950 transposing LDS read
+// ds_read_b64_tr_b16 (inside each 16-lane group, lane i slot q receives element
+// i % 4 of the 8 bytes that lane 4 q + i / 4 addressed); fp32 gathers.
+template <class E>
+__device__ __forceinline__ typename Tr<E>::frag tr_frag(const E *M, int ld, int row0, int colbase,
+                                                        bool p32, int a, int li, int lg);
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+template <>
+__device__ __forceinline__ Tr<uint16_t>::frag tr_frag<uint16_t>(const uint16_t *M, int ld, int row0,
+                                                                int colbase, bool p32, int a, int li,
+                                                                int lg) {
+    const int row = row0 + 8 * lg + (li >> 2);
+    const int col = p32 ? colbase + 8 * (li & 3) + 4 * a : colbase + 4 * (li & 3);
+    typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(M + row * ld + col));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(M + (row + 4) * ld + col));
+    return Tr<uint16_t>::cat(__builtin_bit_cast(u32x2, lo), __builtin_bit_cast(u32x2, hi));
+}
+template <>
+__device__ __forceinline__ Tr<float>::frag tr_frag<float>(const float *M, int ld, int row0, int colbase,
+                                                          bool p32, int a, int li, int lg) {
+    const int col = p32 ? colbase + p32_row(a, li) : colbase + li;
+    Tr<float>::frag f;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) f[q] = M[(row0 + 8 * lg + q) * ld + col];
+    return f;
 }
 
 // Workgroup barrier that orders LDS only: outstanding global loads and stores

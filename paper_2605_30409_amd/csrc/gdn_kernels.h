@@ -20,11 +20,19 @@
 // Workspace per (b*H + h, chunk) -- see gdn_api.hip for the byte layout:
 //   g  [64]       fp64   cumulative log decay (fp64 so that g_r - g_s keeps
 //                        its precision when the decay over a chunk is huge)
-//   W  [64][Dk]   E      WY factor, token-major
-//   Kt [Dk][64]   E      (diag(e^{g_C - g}) K)^T
-//   Ut [Dv][64]   E      Ut^T
+//   W  64*Dk      E      -W (the WY factor, negated), fragment-major for the scan
+//   Kt Dk*64      E      Kt = (diag(e^{g_C - g}) K)^T, fragment-major
+//   Ut Dv*64      E      Ut, fragment-major
 //   Hs [Dv][Dk]   E      H_{c-1}^T, the state entering the chunk
 //   Us [Dv][64]   E      U^T
+// "Fragment-major" means the exact per-lane order in which the scan's MFMAs
+// consume the operand, so every scan load is one contiguous wave access:
+//   W  [Dk/64 wave][4 token tile][2 k block][64 lane][8]
+//        = -W[32 m + p32_row(a, li)][64 wave + 32 kb + 8 lg + e]    (tile 2 m + a)
+//   Kt [Dk/64 wave][4 row tile][2 token block][64 lane][8]
+//        = Kt[64 wave + 32 (t / 2) + p32_row(t % 2, li)][32 m + 8 lg + e]
+//   Ut [Dv/16 column tile][4 token tile][64 lane][4]
+//        = Ut[32 m + 8 lg + 4 a + e][16 jt + li]                      (tile 2 m + a)
 #pragma once
 
 #include "gdn_device.h"
@@ -48,15 +56,16 @@ constexpr float kLogAlphaMin = -87.3f;  // ~ log(FLT_MIN): alpha below this acts
 // --------------------------------------------------------------------------
 template <class E, int DK, int DV> struct WyLds {
     static constexpr int PAD = 16 / (int)sizeof(E);
-    static constexpr int LDK = DK + PAD;      // K (row-major), later the W staging tile
-    static constexpr int LDT = kChunk + PAD;  // K^T and V^T (token-contiguous rows)
+    static constexpr int LDK = DK + PAD;      // K, row-major (token rows)
+    static constexpr int LDV = DV + PAD;      // V, row-major
     static constexpr int LDA = kChunk + 4;    // A and T (fp32)
+    static constexpr int LDB = kChunk + PAD;  // T diag(beta e^g) and T diag(beta) (E)
     static constexpr size_t szA = 4 * kChunk * LDA;
-    static constexpr size_t szVt = sizeof(E) * DV * LDT;
+    static constexpr size_t szB = 2 * sizeof(E) * kChunk * LDB;
     static constexpr size_t oK = 0;
-    static constexpr size_t oKt = oK + sizeof(E) * kChunk * LDK;
-    static constexpr size_t oA = oKt + sizeof(E) * DK * LDT;     // A, then V^T once A is dead
-    static constexpr size_t oT = oA + (szA > szVt ? szA : szVt);
+    static constexpr size_t oV = oK + sizeof(E) * kChunk * LDK;
+    static constexpr size_t oA = oV + sizeof(E) * kChunk * LDV;  // A, then the scaled T pair
+    static constexpr size_t oT = oA + (szA > szB ? szA : szB);
     static constexpr size_t oG = oT + szA;
     static constexpr size_t bytes = oG + 8 * kChunk + 4 * 3 * kChunk;
 };
@@ -65,18 +74,23 @@ template <class E, int DK, int DV>
 __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     using L = WyLds<E, DK, DV>;
     using TR = Tr<E>;
-    constexpr int VE = 16 / (int)sizeof(E);   // elements per 16-byte vector
-    constexpr int NVV = kChunk * (DV / VE) / 256;
+    using frag = typename TR::frag;
+    constexpr int VE = 16 / (int)sizeof(E);       // elements per 16-byte vector
+    constexpr int NKV = kChunk * (DK / VE) / 256;  // K vectors per thread
+    constexpr int NVV = kChunk * (DV / VE) / 256;  // V vectors per thread
+    constexpr int NFR = (DK / 64) * 8;             // W (and Kt) fragments per chunk
+    constexpr double kLog2e = 1.4426950408889634;
     extern __shared__ __align__(16) unsigned char smem[];
     E *sK = (E *)(smem + L::oK);
-    E *sKt = (E *)(smem + L::oKt);
+    E *sV = (E *)(smem + L::oV);
     float *sA = (float *)(smem + L::oA);
-    E *sVt = (E *)(smem + L::oA);
+    E *sTw = (E *)(smem + L::oA);                 // T diag(beta e^g), once A is dead
+    E *sTu = sTw + kChunk * L::LDB;               // T diag(beta)
     float *sT = (float *)(smem + L::oT);
-    double *sg = (double *)(smem + L::oG);     // g_r
-    float *sb = (float *)(sg + kChunk);        // beta_r
-    float *sw = sb + kChunk;                   // beta_r e^{g_r}
-    float *sd = sw + kChunk;                   // e^{g_C - g_r}
+    double *sg = (double *)(smem + L::oG);        // g_r
+    float *sb = (float *)(sg + kChunk);           // beta_r
+    float *sw = sb + kChunk;                      // beta_r e^{g_r}
+    float *sd = sw + kChunk;                      // e^{g_C - g_r}
 
     const int c = blockIdx.x, bh = blockIdx.y;
     const int b = bh / p.H, h = bh - b * p.H;
@@ -87,13 +101,19 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     const size_t row0 = ((size_t)b * p.T + t0) * p.H + h;  // token-row index of token t0
     const size_t rstride = (size_t)p.H;                    // token-row stride
 
-    // V is only needed after the solve; its loads are issued now (lane = token row).
-    uint4 vreg[NVV];
+    // K and V rows, 16-byte coalesced loads (padding rows are zero).
+    uint4 kreg[NKV], vreg[NVV];
+#pragma unroll
+    for (int n = 0; n < NKV; ++n) {
+        const int idx = tid + 256 * n, r = idx / (DK / VE), cv = idx % (DK / VE);
+        kreg[n] = make_uint4(0u, 0u, 0u, 0u);
+        if (r < nvalid) kreg[n] = *(const uint4 *)(p.k + (row0 + r * rstride) * DK + cv * VE);
+    }
 #pragma unroll
     for (int n = 0; n < NVV; ++n) {
-        const int cv = w + 4 * n;
+        const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
         vreg[n] = make_uint4(0u, 0u, 0u, 0u);
-        if (l < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + l * rstride) * DV + cv * VE);
+        if (r < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + r * rstride) * DV + cv * VE);
     }
     // Gates: wave-wide inclusive prefix sum of clamped log alpha in fp64
     // (padding tokens: alpha = 1, beta = 0).
@@ -111,21 +131,22 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
             const double o = __shfl_up(g, d);
             if (l >= d) g += o;
         }
+        const double gC = __shfl(g, kChunk - 1);
         sg[l] = g;
         sb[l] = be;
-        sw[l] = be * expf((float)g);
+        sw[l] = be * __builtin_amdgcn_exp2f((float)(g * kLog2e));
+        sd[l] = __builtin_amdgcn_exp2f((float)((gC - g) * kLog2e));
         p.g[cidx * kChunk + l] = g;
     }
-    // K into LDS row-major and transposed (lane = token row; padded rows are zero).
 #pragma unroll
-    for (int n = 0; n < DK / VE / 4; ++n) {
-        const int cv = w + 4 * n;
-        uint4 val = make_uint4(0u, 0u, 0u, 0u);
-        if (l < nvalid) val = *(const uint4 *)(p.k + (row0 + l * rstride) * DK + cv * VE);
-        *(uint4 *)(sK + l * L::LDK + cv * VE) = val;
-        const E *e = (const E *)&val;
+    for (int n = 0; n < NKV; ++n) {
+        const int idx = tid + 256 * n, r = idx / (DK / VE), cv = idx % (DK / VE);
+        *(uint4 *)(sK + r * L::LDK + cv * VE) = kreg[n];
+    }
 #pragma unroll
-        for (int u = 0; u < VE; ++u) sKt[(cv * VE + u) * L::LDT + l] = e[u];
+    for (int n = 0; n < NVV; ++n) {
+        const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
+        *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
     }
     // Upper block-triangle of T is zero.
     for (int idx = tid; idx < kChunk * kChunk; idx += 256) {
@@ -133,7 +154,6 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         if ((s2 >> 4) > (r >> 4)) sT[r * L::LDA + s2] = 0.f;
     }
     lds_barrier();
-    if (w == 0) sd[l] = expf((float)(sg[kChunk - 1] - sg[l]));
 
     // A = strict_lower(beta_r e^{g_r - g_s} K K^T): the 10 lower 16x16 blocks.
     for (int t = w; t < 10; t += 4) {
@@ -141,37 +161,59 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         const int bj = t - bi * (bi + 1) / 2;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb) {
-            auto fa = load_frag<E>(sK + (16 * bi + li) * L::LDK + 32 * kb, lg);
-            auto fb = load_frag<E>(sK + (16 * bj + li) * L::LDK + 32 * kb, lg);
-            acc = TR::mma(fa, fb, acc);
-        }
+        for (int kb = 0; kb < DK / 32; ++kb)
+            acc = TR::mma(load_frag<E>(sK + (16 * bi + li) * L::LDK + 32 * kb, lg),
+                          load_frag<E>(sK + (16 * bj + li) * L::LDK + 32 * kb, lg), acc);
         const int s2 = 16 * bj + li;
         const double gs = sg[s2];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int r = 16 * bi + 4 * lg + q;
             float val = 0.f;
-            if (s2 < r) val = sb[r] * expf((float)(sg[r] - gs)) * acc[q];
+            if (s2 < r) val = sb[r] * __builtin_amdgcn_exp2f((float)((sg[r] - gs) * kLog2e)) * acc[q];
             sA[r * L::LDA + s2] = val;
         }
     }
     lds_barrier();
 
-    // T = (I + A)^{-1}, fp32.  Diagonal 16x16 blocks by forward substitution,
-    // one block per wave, one column per lane.
-    if (l < 16) {
-        const int base = 16 * w, j = l;
+    // T = (I + A)^{-1} in fp32.  Wave 0 inverts the four diagonal 16x16 blocks
+    // by forward substitution (lane = block * 16 + column) while the other
+    // waves emit the Kt fragments, which need only K and the gates.
+    if (w == 0) {
+        const int base = 16 * (l >> 4), j = l & 15;
         float x[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
+            const float *arow = sA + (base + r) * L::LDA + base;
             float acc = (r == j) ? 1.f : 0.f;
 #pragma unroll
-            for (int s2 = 0; s2 < r; ++s2) acc -= sA[(base + r) * L::LDA + base + s2] * x[s2];
+            for (int s4 = 0; s4 < (r + 3) / 4; ++s4) {
+                const f32x4 av = *(const f32x4 *)(arow + 4 * s4);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (4 * s4 + e < r) acc -= av[e] * x[4 * s4 + e];
+            }
             x[r] = acc;
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(base + r) * L::LDA + base + j] = x[r];
+    } else {
+        // Kt fragment f = (wave * 4 + t) * 2 + m holds, for lane (li, lg),
+        // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
+        E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
+        for (int f = w - 1; f < NFR; f += 3) {
+            const int wv = f >> 3, t = (f >> 1) & 3, m = f & 1;
+            const frag kv = tr_frag<E>(sK, L::LDK, 32 * m, 64 * wv + 32 * (t >> 1), true, t & 1, li, lg);
+            const f32x4 k0 = TR::to_f32(TR::lo(kv)), k1 = TR::to_f32(TR::hi(kv));
+            const int s0 = 32 * m + 8 * lg;
+            f32x4 o0, o1;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                o0[q] = k0[q] * sd[s0 + q];
+                o1[q] = k1[q] * sd[s0 + 4 + q];
+            }
+            TR::store8(Kf + f * 512, TR::cat(TR::from_f32(o0), TR::from_f32(o1)));
+        }
     }
     lds_barrier();
     // Off-diagonal blocks by block distance: T_ij = -T_ii sum_{m=j}^{i-1} A_im T_mj.
@@ -194,105 +236,77 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         }
         lds_barrier();
     }
-    // A is dead: V^T takes its place.
+    // A is dead: T diag(beta e^g) and T diag(beta), rounded to E, take its place.
+    for (int idx = tid; idx < kChunk * kChunk / 8; idx += 256) {
+        const int r = idx >> 3, s0 = (idx & 7) * 8;
+        const f32x4 t0v = *(const f32x4 *)(sT + r * L::LDA + s0);
+        const f32x4 t1v = *(const f32x4 *)(sT + r * L::LDA + s0 + 4);
+        f32x4 w0, w1, u0, u1;
 #pragma unroll
-    for (int n = 0; n < NVV; ++n) {
-        const int cv = w + 4 * n;
-        const E *e = (const E *)&vreg[n];
-#pragma unroll
-        for (int u = 0; u < VE; ++u) sVt[(cv * VE + u) * L::LDT + l] = e[u];
-    }
-
-    // A operands of W = T diag(beta e^g) K and Ut = T diag(beta) V.
-    typename TR::frag aw[4][2], au[4][2];
-#pragma unroll
-    for (int bi = 0; bi < 4; ++bi) {
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
-            const int s0 = 32 * m + 8 * lg, s1 = s0 + 4;
-            const float *trow = sT + (16 * bi + li) * L::LDA + s0;
-            const f32x4 tlo = *(const f32x4 *)trow;
-            const f32x4 thi = *(const f32x4 *)(trow + 4);
-            f32x4 wl, wh, ul, uh;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                wl[q] = tlo[q] * sw[s0 + q];
-                wh[q] = thi[q] * sw[s1 + q];
-                ul[q] = tlo[q] * sb[s0 + q];
-                uh[q] = thi[q] * sb[s1 + q];
-            }
-            aw[bi][m] = TR::cat(TR::from_f32(wl), TR::from_f32(wh));
-            au[bi][m] = TR::cat(TR::from_f32(ul), TR::from_f32(uh));
+        for (int q = 0; q < 4; ++q) {
+            w0[q] = t0v[q] * sw[s0 + q];
+            w1[q] = t1v[q] * sw[s0 + 4 + q];
+            u0[q] = t0v[q] * sb[s0 + q];
+            u1[q] = t1v[q] * sb[s0 + 4 + q];
         }
-    }
-    // W tiles, staged in LDS over the dead K buffer.
-    E *sW = sK;
-    for (int dt = w; dt < DK / 16; dt += 4) {
-        auto b0 = load_frag<E>(sKt + (16 * dt + li) * L::LDT, lg);
-        auto b1 = load_frag<E>(sKt + (16 * dt + li) * L::LDT + 32, lg);
-#pragma unroll
-        for (int bi = 0; bi < 4; ++bi) {
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            acc = TR::mma(aw[bi][0], b0, acc);
-            if (bi >= 2) acc = TR::mma(aw[bi][1], b1, acc);
-            const auto qv = TR::from_f32(acc);
-            const E *e = (const E *)&qv;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) sW[(16 * bi + 4 * lg + q) * L::LDK + 16 * dt + li] = e[q];
-        }
-    }
-    // Kt = (diag(e^{g_C - g}) K)^T, token-contiguous rows.
-    E *Kt = p.Kt + cidx * (size_t)DK * kChunk;
-    for (int idx = tid; idx < DK * (kChunk / 4); idx += 256) {
-        const int d = idx >> 4, s2 = (idx & 15) * 4;
-        const f32x4 kv = TR::to_f32(TR::load(sKt + d * L::LDT + s2));
-        f32x4 o;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) o[q] = kv[q] * sd[s2 + q];
-        TR::store(Kt + d * kChunk + s2, TR::from_f32(o));
+        TR::store8(sTw + r * L::LDB + s0, TR::cat(TR::from_f32(w0), TR::from_f32(w1)));
+        TR::store8(sTu + r * L::LDB + s0, TR::cat(TR::from_f32(u0), TR::from_f32(u1)));
     }
     lds_barrier();
-    // Ut tiles, written straight out transposed (4 consecutive tokens per lane).
-    E *Ut = p.Ut + cidx * (size_t)DV * kChunk;
-    for (int jt = w; jt < DV / 16; jt += 4) {
-        auto b0 = load_frag<E>(sVt + (16 * jt + li) * L::LDT, lg);
-        auto b1 = load_frag<E>(sVt + (16 * jt + li) * L::LDT + 32, lg);
+
+    // -W fragments, computed transposed (W^T = K^T (T diag(beta e^g))^T) so that
+    // each lane ends up holding the 8 consecutive Dk entries the scan consumes:
+    // fragment f = (wave * 4 + st) * 2 + kb, lane (li, lg) =
+    // -W[32 m + p32_row(a_s, li)][64 wave + 32 kb + 8 lg + e]  (st = 2 m + a_s).
+    E *Wf = p.W + cidx * (size_t)kChunk * DK + l * 8;
+    for (int f = w; f < NFR; f += 4) {
+        const int wv = f >> 3, st = (f >> 1) & 3, kb = f & 1, m = st >> 1, as = st & 1;
+        const int d0 = 64 * wv + 32 * kb;
+        const E *trow = sTw + (32 * m + p32_row(as, li)) * L::LDB;
+        f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-        for (int bi = 0; bi < 4; ++bi) {
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-            acc = TR::mma(au[bi][0], b0, acc);
-            if (bi >= 2) acc = TR::mma(au[bi][1], b1, acc);
-            TR::store(Ut + (16 * jt + li) * kChunk + 16 * bi + 4 * lg, TR::from_f32(acc));
+        for (int sk = 0; sk < 2; ++sk) {
+            if (sk > m) break;
+            const frag bt = load_frag<E>(trow + 32 * sk, lg);
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+                acc[a] = TR::mma(tr_frag<E>(sK, L::LDK, 32 * sk, d0, true, a, li, lg), bt, acc[a]);
         }
+        TR::store8(Wf + f * 512, TR::cat(TR::from_f32(-acc[0]), TR::from_f32(-acc[1])));
     }
-    // W staging -> global, 16-byte coalesced.
-    {
-        E *Wg = p.W + cidx * (size_t)kChunk * DK;
-        for (int idx = tid; idx < kChunk * (DK / VE); idx += 256) {
-            const int r = idx / (DK / VE), cv = idx - r * (DK / VE);
-            *(uint4 *)(Wg + r * DK + cv * VE) = *(const uint4 *)(sW + r * L::LDK + cv * VE);
+    // Ut tiles (jt, st) in P32 row order, written as fragment-major quads:
+    // lane (li, lg) = Ut[32 m + 8 lg + 4 a_s + q][16 jt + li].
+    E *Uf = p.Ut + cidx * (size_t)DV * kChunk + l * 4;
+    for (int u = w; u < (DV / 16) * 4; u += 4) {
+        const int jt = u >> 2, st = u & 3, m = st >> 1, as = st & 1;
+        const E *trow = sTu + (32 * m + p32_row(as, li)) * L::LDB;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int sk = 0; sk < 2; ++sk) {
+            if (sk > m) break;
+            acc = TR::mma(load_frag<E>(trow + 32 * sk, lg),
+                          tr_frag<E>(sV, L::LDV, 32 * sk, 16 * jt, false, 0, li, lg), acc);
         }
+        TR::store(Uf + u * 256, TR::from_f32(acc));
     }
 }
 
 // --------------------------------------------------------------------------
 // Stage 2: sequential state scan across chunks.  1-D grid of
 // (Dv/16) * 8 * ceil(B*H / 8) workgroups; one workgroup owns 16 state columns
-// of one (b, h) and carries them through all
-// chunks in fp32 accumulators.  Its DK/32 waves split the Dk rows (32 each),
-// so every chunk costs one cross-wave reduction of the partial W H products.
+// of one (b, h) and carries them through all chunks in fp32 accumulators.
+// Its Dk/64 waves split the state rows (64 each); with two waves every chunk
+// costs one exchange of the partial W H products through LDS (double-buffered,
+// one barrier), after which both waves hold the whole U.
 // --------------------------------------------------------------------------
 template <class E, int DK, int DV>
-__global__ __launch_bounds__(DK * 2) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(DK) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gdn_scan_kernel(Params<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
     using quad = typename TR::quad;
-    constexpr int NW = DK / 32;        // waves; wave w owns state rows [32w, 32w+32)
-    constexpr int NOWN = 4 / NW;       // token tiles each wave reduces
-    constexpr int PF = sizeof(E) == 2 ? 4 : 2;  // chunks of operands kept in flight
-    __shared__ f32x4 sP[NW][4][64];    // partial (W H) tiles
-    __shared__ quad sU[4][64];         // U tiles, already rounded to E
+    constexpr int NW = DK / 64;                 // waves; wave w owns rows [64w, 64w+64)
+    __shared__ f32x4 sP[2][NW][4][64];          // partial (W H) tiles, double-buffered
 
     // XCD-aware placement: workgroups are dealt round-robin to the 8 XCDs, so
     // id = 8 slot + x runs on XCD x.  The NJ column blocks of one (b, h) are
@@ -303,114 +317,103 @@ void gdn_scan_kernel(Params<E> p) {
     const int bh = (slot / NJ) * 8 + x, jt = slot % NJ;
     if (bh >= p.B * p.H) return;
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
-    const int j0 = 16 * jt, d0 = 32 * w;
-    const int j = j0 + li;  // this lane's state column
+    const int d0 = 64 * w;
+    const int j = 16 * jt + li;  // this lane's state column
 
-    // H rows d0 + [0, 32) as two accumulator tiles in P32 order:
-    // Hacc[a][q] = H[d0 + 8 lg + 4 a + q][j].
-    f32x4 Hacc[2];
+    // H rows d0 + [0, 64) as four accumulator tiles t = 2 pp + a in P32 order:
+    // Hacc[t][q] = H[d0 + 32 pp + 8 lg + 4 a + q][j].
+    f32x4 Hacc[4];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            Hacc[a][q] = p.state_in
-                             ? p.state_in[((size_t)bh * DK + d0 + 8 * lg + 4 * a + q) * DV + j]
-                             : 0.f;
+            Hacc[t][q] = p.state_in ? p.state_in[((size_t)bh * DK + d0 + 32 * (t >> 1) + 8 * lg +
+                                                  4 * (t & 1) + q) * DV + j]
+                                    : 0.f;
 
-    // Token tile st = 2 m + a of a chunk is produced in P32 order inside the
-    // 32-token block m: its tile row i is token 32 m + p32_row(a, i).
-    struct Pre {
-        frag wf[4];      // A operand: W[32 m + p32_row(a, li)][d0 + k]
-        frag kf[2][2];   // A operand: Kt[d0 + p32_row(a, li)][32 m + k]
-        quad uq[NOWN];   // Ut^T[j][32 m + 8 lg + 4 a + q] of the owned token tiles
-        double gC;       // g at the chunk's last token
-    };
-    auto fetch = [&](int c, Pre &f) {
+    // Operands are prefetched one chunk ahead in two staggered groups, so only
+    // one copy of each is live: W and Ut for chunk c+1 are requested as soon as
+    // the W H products of chunk c have consumed W(c); Kt and g for chunk c+1 as
+    // soon as the state update of chunk c has consumed Kt(c).
+    frag wf[4][2];   // -W, token tile st, k block kb (this wave's rows)
+    frag kf[4][2];   // Kt, row tile t, token block m
+    quad uq[4];      // Ut quads of token tile st, this workgroup's columns
+    double gC;       // g at the chunk's last token
+    auto fetch_w = [&](int c) {
         const size_t cidx = (size_t)bh * p.NC + c;
-        const E *Wc = p.W + cidx * (size_t)kChunk * DK;
-        const E *Kc = p.Kt + cidx * (size_t)DK * kChunk;
-        const E *Uc = p.Ut + cidx * (size_t)DV * kChunk + (size_t)j * kChunk + 8 * lg;
+        const E *Wc = p.W + cidx * (size_t)kChunk * DK + (size_t)w * 4096 + l * 8;
+        const E *Uc = p.Ut + cidx * (size_t)DV * kChunk + (size_t)jt * 1024 + l * 4;
 #pragma unroll
         for (int st = 0; st < 4; ++st)
-            f.wf[st] = load_frag<E>(Wc + (32 * (st >> 1) + p32_row(st & 1, li)) * DK + d0, lg);
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+            for (int kb = 0; kb < 2; ++kb) wf[st][kb] = TR::load8(Wc + (st * 2 + kb) * 512);
 #pragma unroll
-            for (int m = 0; m < 2; ++m)
-                f.kf[a][m] = load_frag<E>(Kc + (d0 + p32_row(a, li)) * kChunk + 32 * m, lg);
-#pragma unroll
-        for (int o = 0; o < NOWN; ++o) {
-            const int st = w + NW * o;
-            f.uq[o] = TR::load(Uc + 32 * (st >> 1) + 4 * (st & 1));
-        }
-        f.gC = p.g[cidx * kChunk + kChunk - 1];
-        // Keep the whole fetch group together: a load scheduled into a later step
-        // looks younger than the next slots' loads and forces an early full wait.
-        __builtin_amdgcn_sched_barrier(0);
+        for (int st = 0; st < 4; ++st) uq[st] = TR::load(Uc + st * 256);
     };
-    auto step = [&](int c, const Pre &f) {
+    auto fetch_k = [&](int c) {
         const size_t cidx = (size_t)bh * p.NC + c;
-        // H_{c-1} rounded to E: B operand over this wave's 32 rows, and saved for stage 3.
-        const frag hb = TR::cat(TR::from_f32(Hacc[0]), TR::from_f32(Hacc[1]));
-        TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)j * DK + d0 + 8 * lg, hb);
-        // Partial W H over this wave's rows: four independent MFMAs, then the LDS exchange.
-        f32x4 part[4];
+        const E *Kc = p.Kt + cidx * (size_t)DK * kChunk + (size_t)w * 4096 + l * 8;
 #pragma unroll
-        for (int st = 0; st < 4; ++st) part[st] = TR::mma(f.wf[st], hb, f32x4{0.f, 0.f, 0.f, 0.f});
+        for (int t = 0; t < 4; ++t)
 #pragma unroll
-        for (int st = 0; st < 4; ++st) sP[w][st][l] = part[st];
-        lds_barrier();
-        E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)j * kChunk + 8 * lg;
-#pragma unroll
-        for (int o = 0; o < NOWN; ++o) {
-            const int st = w + NW * o;
-            f32x4 pr[NW];
-#pragma unroll
-            for (int ww = 0; ww < NW; ++ww) pr[ww] = sP[ww][st][l];
-            f32x4 u = TR::to_f32(f.uq[o]);
-#pragma unroll
-            for (int ww = 0; ww < NW; ++ww) u -= pr[ww];
-            const quad uqr = TR::from_f32(u);
-            TR::store(Us + 32 * (st >> 1) + 4 * (st & 1), uqr);
-            sU[st][l] = uqr;
-        }
-        lds_barrier();
-        const frag u0 = TR::cat(sU[0][l], sU[1][l]);
-        const frag u1 = TR::cat(sU[2][l], sU[3][l]);
-        const float gam = expf((float)f.gC);
-#pragma unroll
-        for (int a = 0; a < 2; ++a) {
-            Hacc[a] *= gam;
-            Hacc[a] = TR::mma(f.kf[a][0], u0, Hacc[a]);
-            Hacc[a] = TR::mma(f.kf[a][1], u1, Hacc[a]);
-        }
+            for (int m = 0; m < 2; ++m) kf[t][m] = TR::load8(Kc + (t * 2 + m) * 512);
+        gC = p.g[cidx * kChunk + kChunk - 1];
     };
 
-    // Operands for chunk c live in ring slot c % PF and are fetched PF chunks
-    // ahead.  The main loop is branch-free (fetches past the end re-read the
-    // last chunk and are never used) so the compiler can keep every slot's
-    // loads in flight across iterations.
-    Pre ring[PF];
+    fetch_w(0);
+    fetch_k(0);
+    for (int c = 0; c < p.NC; ++c) {
+        const size_t cidx = (size_t)bh * p.NC + c;
+        const int cn = min(c + 1, p.NC - 1);  // the last prefetch re-reads the last chunk
+        // H_{c-1} rounded to E: B operands over this wave's two 32-row blocks,
+        // also saved for stage 3.
+        frag hb[2];
 #pragma unroll
-    for (int i = 0; i < PF; ++i) fetch(min(i, p.NC - 1), ring[i]);
-    int c0 = 0;
-    for (; c0 + PF <= p.NC; c0 += PF) {
-#pragma unroll
-        for (int i = 0; i < PF; ++i) {
-            step(c0 + i, ring[i]);
-            fetch(min(c0 + i + PF, p.NC - 1), ring[i]);
+        for (int pp = 0; pp < 2; ++pp) {
+            hb[pp] = TR::cat(TR::from_f32(Hacc[2 * pp]), TR::from_f32(Hacc[2 * pp + 1]));
+            TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)j * DK + d0 + 32 * pp + 8 * lg, hb[pp]);
         }
-    }
+        // U = Ut - W H accumulated by the MFMAs (the workspace holds -W): wave 0
+        // seeds its accumulators with Ut, wave 1 with zero, and the two partial
+        // sums over their row halves are exchanged through LDS.
+        const uint32_t keep = (w == 0) ? 0xffffffffu : 0u;
+        f32x4 part[4];
 #pragma unroll
-    for (int i = 0; i < PF; ++i)
-        if (c0 + i < p.NC) step(c0 + i, ring[i]);
+        for (int st = 0; st < 4; ++st) part[st] = TR::mma(wf[st][0], hb[0], TR::to_f32(TR::mask(uq[st], keep)));
+#pragma unroll
+        for (int st = 0; st < 4; ++st) part[st] = TR::mma(wf[st][1], hb[1], part[st]);
+        fetch_w(cn);
+        if constexpr (NW > 1) {
+            const int buf = c & 1;
+#pragma unroll
+            for (int st = 0; st < 4; ++st) sP[buf][w][st][l] = part[st];
+            lds_barrier();
+#pragma unroll
+            for (int st = 0; st < 4; ++st) part[st] += sP[buf][1 - w][st][l];
+        }
+        quad uqr[4];
+#pragma unroll
+        for (int st = 0; st < 4; ++st) uqr[st] = TR::from_f32(part[st]);
+        const frag u0 = TR::cat(uqr[0], uqr[1]);
+        const frag u1 = TR::cat(uqr[2], uqr[3]);
+        E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)j * kChunk + 8 * lg;
+        if (NW == 1 || w == 0) TR::store8(Us, u0);
+        if (NW == 1 || w == 1) TR::store8(Us + 32, u1);
+        const float gam = expf((float)gC);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) Hacc[t] = TR::mma(kf[t][0], u0, Hacc[t] * gam);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) Hacc[t] = TR::mma(kf[t][1], u1, Hacc[t]);
+        fetch_k(cn);
+    }
 
     if (p.state_out) {
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int t = 0; t < 4; ++t)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                p.state_out[((size_t)bh * DK + d0 + 8 * lg + 4 * a + q) * DV + j] = Hacc[a][q];
+                p.state_out[((size_t)bh * DK + d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1) + q) * DV + j] =
+                    Hacc[t][q];
     }
 }
 

@@ -1,10 +1,10 @@
 """Benchmark of the GDN chunk forward on one MI355X.
 
-A step is one full pass of the hot path (WY transform, state scan, output) over
-one 1280x704 latent frame: B=1, T=3520 tokens (44x80), H=16 heads,
-Dk=Dv=128, chunk 64, bf16 q/k/v with an fp32 state carried in and out.  The
-inputs are seeded synthetic tensors already resident in HBM; the workspace is
-preallocated, so the timed region only enqueues the three kernels per step.
+A step is one full pass of the hot path (WY transform, grouped state scan,
+output) over one 1280x704 latent frame: B=1, T=3520 tokens (44x80), H=16
+heads, Dk=Dv=128, chunk 64, bf16 q/k/v with an fp32 state carried in and out.
+The inputs are seeded synthetic tensors already resident in HBM; the workspace
+is preallocated, so the timed region only enqueues the five kernels per step.
 
 Prints ONE JSON line.  Besides throughput it reports the roofline of the
 dominant kernel (per-stage durations from HIP events recorded on the stream
@@ -29,21 +29,49 @@ METRIC = "GDN fwd tokens/sec and TFLOP/s at T=3520,H=16,D=128 bf16; % of MFMA pe
 WORKLOAD = 1                 # one 1280x704 frame
 PEAK_BF16_TFLOPS = 2516.6    # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
-STAGES = ("gdn_wy_kernel", "gdn_scan_kernel", "gdn_output_kernel")
+# stage name (as the library reports stages) -> kernel
+KERNELS = {"wy": "gdn_wy_kernel", "group_transfer": "gdn_chunkscan_kernel<SCAN_TRANS>",
+           "group_scan": "gdn_groupscan_kernel", "chunk_states": "gdn_chunkscan_kernel<SCAN_STATES>",
+           "output": "gdn_output_kernel"}
 
 
-def algorithmic_counts(B, T, H, Dk, Dv, C=64):
-    """Per-stage algorithmic flops and the path's algorithmic bytes (no workspace traffic)."""
-    n = B * T * H  # token-heads
-    f_wy = n * ((C - 1) * (2 * Dk + Dv) + C * C / 3.0)
-    f_scan = n * 4.0 * Dk * Dv
-    f_out = n * (2.0 * Dk * Dv + (C + 1) * (Dk + Dv))
-    io_bytes = n * ((2 * Dk + Dv) * 2 + 8 + Dv * 2) + 2 * B * H * Dk * Dv * 4
-    # bytes each stage must move at minimum (its own inputs/outputs, workspace included)
-    nch = B * H * -(-T // C)
-    b_wy = n * ((Dk + Dv) * 2 + 8) + nch * C * (4 + 2 * (2 * Dk + Dv))
-    return dict(flops=dict(wy=f_wy, scan=f_scan, out=f_out, total=f_wy + f_scan + f_out),
-                bytes=io_bytes, bytes_wy=b_wy)
+def algorithmic_counts(B, T, H, Dk, Dv, G, C=64, esz=2):
+    """Per-stage algorithmic flops and bytes (each stage's own inputs and outputs,
+    workspace included, every byte once), and the path's external I/O bytes."""
+    n = B * T * H                       # token-heads
+    NC = -(-T // C)
+    NG = -(-NC // G)
+    nch = B * H * NC                    # chunks (the ragged tail counts as a whole chunk)
+    ngr = B * H * NG if NG > 1 else 0   # scan groups (none with a single group)
+    st = B * H * Dk * Dv * 4            # one fp32 state per (b, h)
+    wy_out = nch * C * (8 + (2 * Dk + Dv) * esz)      # g, -W, Kt, Ut
+    f = {"wy": n * ((C - 1) * (2 * Dk + Dv) + C * C / 3.0),
+         "group_transfer": nch * C * 4.0 * Dk * (Dk + Dv) if ngr else 0.0,
+         "group_scan": ngr * (2.0 * Dk * Dk * Dv + 2.0 * Dk * Dv),
+         "chunk_states": nch * C * 4.0 * Dk * Dv,
+         "output": n * (2.0 * Dk * Dv + (C + 1) * (Dk + Dv))}
+    b = {"wy": n * ((Dk + Dv) * esz + 8) + wy_out,
+         "group_transfer": (wy_out + ngr * (Dk * Dk * esz + Dv * Dk * 4 + 8)) if ngr else 0,
+         "group_scan": (ngr * (Dk * Dk * esz + 2 * Dv * Dk * 4 + 8) + 2 * st) if ngr else 0,
+         "chunk_states": wy_out + (ngr * Dv * Dk * 4 if ngr else 2 * st) + nch * Dv * (Dk + C) * esz,
+         "output": n * (2 * Dk + Dv) * esz + nch * (C * 8 + Dv * (Dk + C) * esz)}
+    io_bytes = n * ((2 * Dk + Dv) * esz + 8 + Dv * esz) + 2 * st
+    return dict(flops=f, bytes=b, io_bytes=io_bytes, groups=NG, group_size=G)
+
+
+def binding_roof(flops, nbytes, ms):
+    """The roof (MFMA or HBM) whose lower bound on the duration is larger, and the
+    achieved rate against it."""
+    t_mfma = flops / (PEAK_BF16_TFLOPS * 1e12)
+    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
+    sec = ms / 1e3
+    if t_mfma >= t_hbm:
+        a = flops / sec / 1e12
+        return {"bound": "mfma", "achieved": round(a, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(a / PEAK_BF16_TFLOPS, 4)}
+    a = nbytes / sec / 1e9
+    return {"bound": "hbm", "achieved": round(a, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(a / PEAK_HBM_GBS, 4)}
 
 
 def host_threads():
@@ -154,6 +182,7 @@ def main():
     # Per-stage durations: HIP events recorded by the library on the same stream.
     stage_ms = gdn.gdn_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws,
                                       reps=args.steps, chunk=C, stream=stream)
+    names = dict(zip(gdn.STAGE_NAMES, stage_ms))
     torch.cuda.synchronize()
 
     # Cold-cache steps: a 1 GiB write before each (outside the events) evicts L2 and MALL.
@@ -172,20 +201,18 @@ def main():
         cold_ms = float(np.median(times))
         del scratch
 
-    cnt = algorithmic_counts(B, T, H, Dk, Dv, C)
+    G = gdn.gdn_scan_group_size(B, H, T, Dk, Dv, C)
+    cnt = algorithmic_counts(B, T, H, Dk, Dv, G, C)
     sec = ms_per_step / 1e3
-    tflops = cnt["flops"]["total"] / sec / 1e12
-    names = dict(zip(STAGES, stage_ms))
+    tflops = sum(cnt["flops"].values()) / sec / 1e12
     dom = max(names, key=names.get)
-    dom_flops = {"gdn_wy_kernel": cnt["flops"]["wy"], "gdn_scan_kernel": cnt["flops"]["scan"],
-                 "gdn_output_kernel": cnt["flops"]["out"]}[dom]
-    achieved = dom_flops / (names[dom] / 1e3) / 1e12
-    roofline = {"kernel": dom, "bound": "mfma", "achieved": round(achieved, 2),
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                "traffic": load_traffic(dom),
-                "duration_ms": round(names[dom], 5),
-                "algorithmic_flops_per_launch": dom_flops}
+    roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
+    roofline.update({"traffic": load_traffic(KERNELS[dom]), "kernel": KERNELS[dom],
+                     "duration_ms": round(names[dom], 5),
+                     "algorithmic_flops_per_launch": cnt["flops"][dom],
+                     "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
+    stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_)
+                   for k_, v_ in names.items() if v_ > 0 and (cnt["flops"][k_] or cnt["bytes"][k_])}
 
     rec = {
         "metric": METRIC,
@@ -202,12 +229,14 @@ def main():
         "data": "synthetic",
         "config": {"workload": "one 1280x704 latent frame: B=1 T=3520 (44x80) H=16 Dk=Dv=128 "
                                "chunk=64, bf16 q/k/v, fp32 state in/out",
-                   "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C},
+                   "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C,
+                   "scan_group": G, "scan_groups": cnt["groups"]},
         "tflops": round(tflops, 2),
         "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-        "hbm_frac_algorithmic": round(cnt["bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
+        "hbm_frac_io": round(cnt["io_bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
         "ms_per_step_cold": None if cold_ms is None else round(cold_ms, 5),
         "stage_ms": {k_: round(v_, 5) for k_, v_ in names.items()},
+        "stage_roofline": {k_: (v_["bound"], v_["frac"]) for k_, v_ in stage_roofs.items()},
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:

@@ -17,9 +17,14 @@
  * kernel section writes the scan (S_f = alpha_f P_f S_{f-1} + A_f).
  *
  * The work is evaluated chunk by chunk (chunks of `chunk` tokens): a per-chunk
- * WY/UT transform, a sequential scan of the state across chunks, and a
- * per-chunk output pass.  This is an exact rewrite of the recurrence; results
- * differ from it only by rounding.
+ * WY/UT transform, a scan of the state across chunks, and a per-chunk output
+ * pass.  Long sequences split the scan into groups of consecutive chunks: the
+ * transfer map of every group (its product of per-chunk transitions and its
+ * zero-start state) is formed in parallel, a short sequential scan over the
+ * groups yields each group's entry state, and the chunk states inside all
+ * groups then follow in parallel.  This is an exact rewrite of the
+ * recurrence; results differ from it only by rounding (and, slightly, with
+ * the group size).
  *
  * Layouts (all contiguous, row-major, 64-bit indexed):
  *   q, k      [B][T][H][Dk]      bf16 (gdn_chunk_forward*) or fp32 (*_f32*)
@@ -38,7 +43,7 @@
  * no-op on the state.
  *
  * Calls are asynchronous on `stream` (a hipStream_t, NULL = the default
- * stream): they validate the arguments on the host, enqueue three kernels and
+ * stream): they validate the arguments on the host, enqueue the kernels and
  * return.  On a validation failure nothing is enqueued and a negative status
  * is returned.  Values are not checked: non-finite alpha or beta propagate,
  * and alpha < 0 is outside the supported domain (the scan works with
@@ -112,18 +117,44 @@ int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v,
                              void *ws, size_t ws_bytes, void *stream);
 
 /*
- * Per-stage timing (measurement aid, same arguments as gdn_chunk_forward_ws
- * plus is_bf16): runs the whole path `reps` times on `stream`, recording HIP
- * events on that stream around each of the three stages (WY transform, state
- * scan, output), then synchronizes the stream and writes the mean duration of
- * each stage in milliseconds to stage_ms[0..2] (host memory).  Creates and
- * destroys its own events.
+ * Scan-group control.  scan_group = chunks per scan group: 0 picks the
+ * library's choice (one group when T is at most 64 chunks or when
+ * B*H*Dv/16 >= 512, else about sqrt(chunks)), a value >= the number of
+ * chunks gives a single sequential scan, and any value in between is used as
+ * given (negative counts as 0).  The two calls
+ * below take it explicitly: gdn_workspace_bytes_ex sizes the workspace for
+ * it (the workspace differs between group sizes), and gdn_chunk_forward_ex
+ * is gdn_chunk_forward_ws / gdn_chunk_forward_f32_ws (is_bf16 selects) run
+ * with it.  gdn_workspace_bytes(...) equals gdn_workspace_bytes_ex(..., 0).
+ */
+size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
+                              int scan_group);
+
+/* Chunks per scan group the calls above use for this shape and scan_group
+ * (0 for unsupported arguments). */
+int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int scan_group);
+
+int gdn_chunk_forward_ex(const void *q, const void *k, const void *v,
+                         const float *alpha, const float *beta, const float *state_in,
+                         void *out, float *state_out,
+                         int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
+                         int scan_group, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Per-stage timing (measurement aid, same arguments as gdn_chunk_forward_ex):
+ * runs the whole path `reps` times on `stream`, recording HIP events on that
+ * stream between its five stages, then synchronizes the stream and writes the
+ * mean duration of each stage in milliseconds to stage_ms[0..4] (host
+ * memory): [0] WY transform, [1] group transfer maps, [2] scan over groups,
+ * [3] chunk states, [4] output.  Stages 1 and 2 take ~0 ms when the scan runs
+ * as one group.  Creates and destroys its own events.
  */
 int gdn_profile_stages(const void *q, const void *k, const void *v,
                        const float *alpha, const float *beta, const float *state_in,
                        void *out, float *state_out,
                        int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
-                       void *ws, size_t ws_bytes, int reps, float *stage_ms, void *stream);
+                       int scan_group, void *ws, size_t ws_bytes, int reps, float *stage_ms,
+                       void *stream);
 
 /* Static, human-readable text for a status code. */
 const char *gdn_status_string(int status);

@@ -15,21 +15,47 @@ namespace {
 using gdn::kChunk;
 
 struct WsLayout {
-    size_t g, W, Kt, Ut, Hs, Us, total;
+    size_t g, W, Kt, Ut, Hs, Us, Nf, PsiT, lgam, HgT, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz) {
-    const size_t nch = (size_t)B * H * (((size_t)T + kChunk - 1) / kChunk);
+int num_chunks(int T) { return (T + kChunk - 1) / kChunk; }
+
+// Chunks per scan group.  A single group (one sequential scan per (b, h),
+// spread over Dv/16 workgroups) when the sequence is short or when the
+// (b, h) streams alone fill the chip; otherwise about sqrt(NC) chunks per
+// group, which balances the group-parallel passes (two passes over G chunks)
+// against the sequential scan over NC / G groups.
+int auto_group(int NC, long long BH, int Dv) {
+    if (NC <= 64 || BH * (Dv / 16) >= 512) return NC;
+    int G = (int)(__builtin_sqrt((double)NC) + 0.5);
+    return G < 2 ? 2 : G;
+}
+
+int resolve_group(int NC, long long BH, int Dv, int group) {
+    if (group <= 0) group = auto_group(NC, BH, Dv);
+    return group > NC ? NC : group;
+}
+
+WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
+    const int NC = num_chunks(T);
+    const int NG = (NC + G - 1) / G;
+    const size_t bh = (size_t)B * H;
+    const size_t nch = bh * NC;
+    const size_t ngr = NG > 1 ? bh * NG : 0;
     WsLayout L;
     size_t off = 0;
-    L.g = off;  off = align256(off + nch * kChunk * 8);
-    L.W = off;  off = align256(off + nch * kChunk * Dk * esz);
-    L.Kt = off; off = align256(off + nch * Dk * kChunk * esz);
-    L.Ut = off; off = align256(off + nch * Dv * kChunk * esz);
-    L.Hs = off; off = align256(off + nch * Dv * Dk * esz);
-    L.Us = off; off = align256(off + nch * Dv * kChunk * esz);
+    L.g = off;    off = align256(off + nch * kChunk * 8);
+    L.W = off;    off = align256(off + nch * kChunk * Dk * esz);
+    L.Kt = off;   off = align256(off + nch * Dk * kChunk * esz);
+    L.Ut = off;   off = align256(off + nch * Dv * kChunk * esz);
+    L.Hs = off;   off = align256(off + nch * Dv * Dk * esz);
+    L.Us = off;   off = align256(off + nch * Dv * kChunk * esz);
+    L.Nf = off;   off = align256(off + ngr * Dk * Dk * esz);
+    L.PsiT = off; off = align256(off + ngr * Dv * Dk * 4);
+    L.lgam = off; off = align256(off + ngr * 8);
+    L.HgT = off;  off = align256(off + ngr * Dv * Dk * 4);
     L.total = off;
     return L;
 }
@@ -84,7 +110,7 @@ int validate(const void *q, const void *k, const void *v, const float *alpha, co
 template <class E>
 gdn::Params<E> make_params(const void *q, const void *k, const void *v, const float *alpha,
                            const float *beta, const float *state_in, void *out, float *state_out,
-                           int B, int H, int T, int Dk, int Dv, void *ws) {
+                           int B, int H, int T, int Dk, int Dv, int G, void *ws) {
     gdn::Params<E> p;
     p.q = (const E *)q;
     p.k = (const E *)k;
@@ -97,8 +123,10 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
     p.B = B;
     p.H = H;
     p.T = T;
-    p.NC = (T + kChunk - 1) / kChunk;
-    const WsLayout L = ws_layout(B, H, T, Dk, Dv, sizeof(E));
+    p.NC = num_chunks(T);
+    p.G = G;
+    p.NG = (p.NC + G - 1) / G;
+    const WsLayout L = ws_layout(B, H, T, Dk, Dv, sizeof(E), G);
     unsigned char *base = (unsigned char *)ws;
     p.g = (double *)(base + L.g);
     p.W = (E *)(base + L.W);
@@ -106,8 +134,14 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
     p.Ut = (E *)(base + L.Ut);
     p.Hs = (E *)(base + L.Hs);
     p.Us = (E *)(base + L.Us);
+    p.Nf = (E *)(base + L.Nf);
+    p.PsiT = (float *)(base + L.PsiT);
+    p.lgam = (double *)(base + L.lgam);
+    p.HgT = (float *)(base + L.HgT);
     return p;
 }
+
+constexpr int kStages = 5;  // WY transform, group transfers, group scan, chunk states, output
 
 template <class E, int DK, int DV>
 hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, hipEvent_t *ev) {
@@ -124,18 +158,37 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, hipEvent_t *ev) {
     });
     if (attr_err != hipSuccess) return attr_err;
     const unsigned BH = (unsigned)(p.B * p.H);
+    constexpr unsigned CT = gdn::ScanCT<E>::value;
     hipError_t er = hipSuccess;
     auto mark = [&](int i) {
         if (ev && er == hipSuccess) er = hipEventRecord(ev[i], s);
     };
+    // workgroup counts: column blocks x 8 x ceil(units / 8) (see the XCD placement)
+    auto groups = [](unsigned nblocks, unsigned units) { return nblocks * 8u * ((units + 7u) / 8u); };
     mark(0);
     hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds1, s, p);
     mark(1);
-    const unsigned scan_groups = (DV / 16) * 8u * ((BH + 7u) / 8u);
-    hipLaunchKernelGGL((gdn::gdn_scan_kernel<E, DK, DV>), dim3(scan_groups), dim3(DK), 0, s, p);
+    if (p.NG > 1) {
+        hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT>),
+                           dim3(groups((DK + DV) / (16 * CT), BH * p.NG)), dim3(DK), 0, s, p);
+    }
     mark(2);
-    hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
+    if (p.NG > 1) {
+        hipLaunchKernelGGL((gdn::gdn_groupscan_kernel<E, DK, DV>), dim3(groups(DV / 16, BH)), dim3(DK),
+                           0, s, p);
+    }
     mark(3);
+    if (p.NG > 1) {
+        hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT>),
+                           dim3(groups(DV / (16 * CT), BH * p.NG)), dim3(DK), 0, s, p);
+    } else {
+        // one sequential scan per (b, h): 16-column workgroups for parallelism
+        hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1>),
+                           dim3(groups(DV / 16, BH)), dim3(DK), 0, s, p);
+    }
+    mark(4);
+    hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
+    mark(5);
     const hipError_t le = hipGetLastError();
     return le != hipSuccess ? le : er;
 }
@@ -150,21 +203,22 @@ hipError_t dispatch(const gdn::Params<E> &p, int Dk, int Dv, hipStream_t s, hipE
 
 int run(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
         const float *state_in, void *out, float *state_out, int B, int H, int T, int Dk, int Dv,
-        int chunk, bool bf16, void *ws, size_t ws_bytes, void *stream, hipEvent_t *ev) {
+        int chunk, bool bf16, int group, void *ws, size_t ws_bytes, void *stream, hipEvent_t *ev) {
     const size_t esz = bf16 ? 2 : 4;
     int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
     if (st != GDN_OK) return st;
-    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz).total)
+    const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, group);
+    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz, G).total)
         return GDN_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     hipError_t e;
     if (bf16) {
         e = dispatch(make_params<uint16_t>(q, k, v, alpha, beta, state_in, out, state_out, B, H, T,
-                                           Dk, Dv, ws),
+                                           Dk, Dv, G, ws),
                      Dk, Dv, s, ev);
     } else {
         e = dispatch(make_params<float>(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk,
-                                        Dv, ws),
+                                        Dv, G, ws),
                      Dk, Dv, s, ev);
     }
     return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
@@ -199,11 +253,12 @@ int run_cached(const void *q, const void *k, const void *v, const float *alpha, 
     const size_t esz = bf16 ? 2 : 4;
     int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
     if (st != GDN_OK) return st;
-    const size_t need = ws_layout(B, H, T, Dk, Dv, esz).total;
+    const size_t need =
+        ws_layout(B, H, T, Dk, Dv, esz, resolve_group(num_chunks(T), (long long)B * H, Dv, 0)).total;
     void *ws = nullptr;
     st = cached_workspace(need, &ws);
     if (st != GDN_OK) return st;
-    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, bf16, ws,
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, bf16, 0, ws,
                need, stream, nullptr);
 }
 
@@ -226,15 +281,27 @@ int gdn_chunk_forward_f32(const float *q, const float *k, const float *v, const 
 }
 
 size_t gdn_workspace_bytes(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16) {
+    return gdn_workspace_bytes_ex(B, H, T, Dk, Dv, chunk, is_bf16, 0);
+}
+
+int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int scan_group) {
     if (!shape_ok(B, H, T) || !dims_ok(Dk, Dv, chunk)) return 0;
-    return ws_layout(B, H, T, Dk, Dv, is_bf16 ? 2 : 4).total;
+    return resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group);
+}
+
+size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
+                              int scan_group) {
+    if (!shape_ok(B, H, T) || !dims_ok(Dk, Dv, chunk)) return 0;
+    return ws_layout(B, H, T, Dk, Dv, is_bf16 ? 2 : 4,
+                     resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group))
+        .total;
 }
 
 int gdn_chunk_forward_ws(const void *q, const void *k, const void *v, const float *alpha,
                          const float *beta, const float *state_in, void *out, float *state_out,
                          int B, int H, int T, int Dk, int Dv, int chunk, void *ws, size_t ws_bytes,
                          void *stream) {
-    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, true, ws,
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, true, 0, ws,
                ws_bytes, stream, nullptr);
 }
 
@@ -242,22 +309,32 @@ int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v, con
                              const float *beta, const float *state_in, float *out, float *state_out,
                              int B, int H, int T, int Dk, int Dv, int chunk, void *ws,
                              size_t ws_bytes, void *stream) {
-    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, false, ws,
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, false, 0, ws,
                ws_bytes, stream, nullptr);
+}
+
+int gdn_chunk_forward_ex(const void *q, const void *k, const void *v, const float *alpha,
+                         const float *beta, const float *state_in, void *out, float *state_out,
+                         int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group,
+                         void *ws, size_t ws_bytes, void *stream) {
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, is_bf16 != 0,
+               scan_group, ws, ws_bytes, stream, nullptr);
 }
 
 int gdn_profile_stages(const void *q, const void *k, const void *v, const float *alpha,
                        const float *beta, const float *state_in, void *out, float *state_out,
-                       int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, void *ws,
-                       size_t ws_bytes, int reps, float *stage_ms, void *stream) {
+                       int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group,
+                       void *ws, size_t ws_bytes, int reps, float *stage_ms, void *stream) {
     if (!stage_ms || reps < 1) return GDN_ERR_NULL;
     const bool bf16 = is_bf16 != 0;
     const size_t esz = bf16 ? 2 : 4;
     int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
     if (st != GDN_OK) return st;
-    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz).total)
+    const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group);
+    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz, G).total)
         return GDN_ERR_WORKSPACE;
-    std::vector<hipEvent_t> ev((size_t)reps * 4, nullptr);
+    constexpr int NE = kStages + 1;
+    std::vector<hipEvent_t> ev((size_t)reps * NE, nullptr);
     int status = GDN_OK;
     for (auto &e : ev)
         if (hipEventCreate(&e) != hipSuccess) {
@@ -266,15 +343,15 @@ int gdn_profile_stages(const void *q, const void *k, const void *v, const float 
         }
     for (int r = 0; r < reps && status == GDN_OK; ++r)
         status = run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, bf16,
-                     ws, ws_bytes, stream, &ev[(size_t)r * 4]);
+                     scan_group, ws, ws_bytes, stream, &ev[(size_t)r * NE]);
     if (status == GDN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
         status = GDN_ERR_HIP;
     if (status == GDN_OK) {
-        double sum[3] = {0.0, 0.0, 0.0};
+        double sum[kStages] = {};
         for (int r = 0; r < reps && status == GDN_OK; ++r) {
-            for (int s = 0; s < 3; ++s) {
+            for (int s = 0; s < kStages; ++s) {
                 float ms = 0.f;
-                if (hipEventElapsedTime(&ms, ev[(size_t)r * 4 + s], ev[(size_t)r * 4 + s + 1]) !=
+                if (hipEventElapsedTime(&ms, ev[(size_t)r * NE + s], ev[(size_t)r * NE + s + 1]) !=
                     hipSuccess) {
                     status = GDN_ERR_HIP;
                     break;
@@ -282,7 +359,7 @@ int gdn_profile_stages(const void *q, const void *k, const void *v, const float 
                 sum[s] += ms;
             }
         }
-        for (int s = 0; s < 3; ++s) stage_ms[s] = (float)(sum[s] / reps);
+        for (int s = 0; s < kStages; ++s) stage_ms[s] = (float)(sum[s] / reps);
     }
     for (auto &e : ev)
         if (e) (void)hipEventDestroy(e);

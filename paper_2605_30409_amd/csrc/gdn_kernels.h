@@ -45,8 +45,13 @@ template <class E> struct Params {
     E *out;
     float *state_out;
     int B, H, T, NC;
+    int G, NG;        // chunks per scan group, number of groups
     double *g;
     E *W, *Kt, *Ut, *Hs, *Us;
+    E *Nf;            // per (b*H + h, group): N_g = Phi_g - Gamma_g I, fragment-major
+    float *PsiT;      // per (b*H + h, group): Psi_g^T [Dv][Dk]
+    double *lgam;     // per (b*H + h, group): log Gamma_g
+    float *HgT;       // per (b*H + h, group): entry state H^T [Dv][Dk]
 };
 
 constexpr float kLogAlphaMin = -87.3f;  // ~ log(FLT_MIN): alpha below this acts as 1.2e-38
@@ -292,63 +297,112 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
 }
 
 // --------------------------------------------------------------------------
-// Stage 2: sequential state scan across chunks.  1-D grid of
-// (Dv/16) * 8 * ceil(B*H / 8) workgroups; one workgroup owns 16 state columns
-// of one (b, h) and carries them through all chunks in fp32 accumulators.
-// Its Dk/64 waves split the state rows (64 each); with two waves every chunk
-// costs one exchange of the partial W H products through LDS (double-buffered,
-// one barrier), after which both waves hold the whole U.
+// Stage 2: the state recurrence across chunks, H_c = gamma_c H_{c-1} + Kt_c^T U_c
+// with U_c = Ut_c - W_c H_{c-1}, i.e. H_c = A_c H_{c-1} + B_c with the affine
+// chunk transfer A_c = gamma_c I - Kt_c^T W_c, B_c = Kt_c^T Ut_c (the token-wise
+// counterpart of the paper's S_f = alpha_f P_f S_{f-1} + A_f).  The chunks are
+// cut into groups of G; the sequential dependency is reduced to one step per
+// group:
+//   (T) gdn_chunkscan_kernel<.., SCAN_TRANS>: for every group in parallel, run
+//       the recurrence over its chunks from [Phi | Psi] = [I | 0], giving the
+//       group transfer Phi_g = prod A_c and the zero-start state Psi_g;
+//   (S) gdn_groupscan_kernel: H <- Phi_g H + Psi_g over the groups, recording
+//       every group's entry state (and the final state);
+//   (O) gdn_chunkscan_kernel<.., SCAN_STATES>: for every group in parallel, run
+//       the recurrence from the group's true entry state and write the
+//       per-chunk state H_{c-1} and pseudo-values U_c the output stage needs.
+// With a single group only (O) runs, from state_in, and writes state_out.
+//
+// gdn_chunkscan_kernel: one workgroup owns 16 * CT state columns of one
+// (b, h, group) and carries them through the group's chunks in fp32
+// accumulators.  Its Dk/64 waves split the state rows (64 each); with two
+// waves every chunk costs one exchange of the partial W H products through LDS
+// (double-buffered, one barrier), after which both waves hold the whole U.
+// Several column tiles per workgroup reuse each chunk operand fragment CT
+// times, which keeps the operand traffic through the CU's L1 in check.
 // --------------------------------------------------------------------------
-template <class E, int DK, int DV>
+enum { SCAN_TRANS = 0, SCAN_STATES = 1 };
+
+// Column tiles per workgroup for the grouped passes (wide: operand reuse) and
+// for a single-group scan (narrow: as many workgroups as possible).
+template <class E> struct ScanCT { static constexpr int value = sizeof(E) == 2 ? 4 : 2; };
+
+template <class E, int DK, int DV, int PHASE, int CT>
 __global__ __launch_bounds__(DK) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gdn_scan_kernel(Params<E> p) {
+void gdn_chunkscan_kernel(Params<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
     using quad = typename TR::quad;
-    constexpr int NW = DK / 64;                 // waves; wave w owns rows [64w, 64w+64)
-    __shared__ f32x4 sP[2][NW][4][64];          // partial (W H) tiles, double-buffered
+    constexpr int NW = DK / 64;                          // waves; wave w owns rows [64w, 64w+64)
+    constexpr int WCOLS = PHASE == SCAN_TRANS ? DK + DV : DV;
+    constexpr int NJB = WCOLS / (16 * CT);               // column blocks per (b, h, group)
+    constexpr int NLDN = 16 * CT;                        // rows of the N^T staging tile
+    constexpr int LDN = DK + 16 / (int)sizeof(E);
+    __shared__ f32x4 sP[2][NW][4][CT][64];               // partial (W H) tiles, double-buffered
+    static_assert(sizeof(E) * NLDN * LDN <= sizeof(f32x4) * 2 * NW * 4 * CT * 64, "N^T staging");
 
     // XCD-aware placement: workgroups are dealt round-robin to the 8 XCDs, so
-    // id = 8 slot + x runs on XCD x.  The NJ column blocks of one (b, h) are
-    // given consecutive slots of the same XCD and share its L2 for the
-    // chunk operands W and Kt that all of them read.
-    constexpr int NJ = DV / 16;
+    // id = 8 slot + x runs on XCD x.  The NJB column blocks of one (b, h, group)
+    // get consecutive slots of the same XCD and share its L2 for the chunk
+    // operands W, Kt that all of them read.
     const int id = blockIdx.x, x = id & 7, slot = id >> 3;
-    const int bh = (slot / NJ) * 8 + x, jt = slot % NJ;
-    if (bh >= p.B * p.H) return;
+    const int unit = (slot / NJB) * 8 + x, jb = slot % NJB;
+    if (unit >= p.B * p.H * p.NG) return;
+    const int bh = unit / p.NG, grp = unit - bh * p.NG;
+    const int c_begin = grp * p.G, c_end = min(p.NC, c_begin + p.G);
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
     const int d0 = 64 * w;
-    const int j = 16 * jt + li;  // this lane's state column
+    const int col0 = 16 * CT * jb;
+    const bool is_phi = PHASE == SCAN_TRANS && col0 < DK;
+    // columns of this workgroup within the state (Phi columns or Psi / H columns)
+    const int jbase = (PHASE == SCAN_TRANS && !is_phi) ? col0 - DK : col0;
 
-    // H rows d0 + [0, 64) as four accumulator tiles t = 2 pp + a in P32 order:
-    // Hacc[t][q] = H[d0 + 32 pp + 8 lg + 4 a + q][j].
-    f32x4 Hacc[4];
+    // State rows d0 + [0, 64) as four accumulator tiles t = 2 pp + a in P32
+    // order, for each column tile ct: Hacc[t][ct][q] = H[d0 + 32 pp + 8 lg + 4 a + q][jbase + 16 ct + li].
+    f32x4 Hacc[4][CT];
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+    for (int ct = 0; ct < CT; ++ct) {
+        const int j = jbase + 16 * ct + li;
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            Hacc[t][q] = p.state_in ? p.state_in[((size_t)bh * DK + d0 + 32 * (t >> 1) + 8 * lg +
-                                                  4 * (t & 1) + q) * DV + j]
-                                    : 0.f;
+        for (int t = 0; t < 4; ++t) {
+            const int r0 = d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
+            if (PHASE == SCAN_TRANS) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) Hacc[t][ct][q] = (is_phi && r0 + q == j) ? 1.f : 0.f;
+            } else if (p.NG > 1) {
+                Hacc[t][ct] = *(const f32x4 *)(p.HgT + ((size_t)unit * DV + j) * DK + r0);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    Hacc[t][ct][q] = p.state_in ? p.state_in[((size_t)bh * DK + r0 + q) * DV + j] : 0.f;
+            }
+        }
+    }
 
     // Operands are prefetched one chunk ahead in two staggered groups, so only
     // one copy of each is live: W and Ut for chunk c+1 are requested as soon as
     // the W H products of chunk c have consumed W(c); Kt and g for chunk c+1 as
     // soon as the state update of chunk c has consumed Kt(c).
-    frag wf[4][2];   // -W, token tile st, k block kb (this wave's rows)
-    frag kf[4][2];   // Kt, row tile t, token block m
-    quad uq[4];      // Ut quads of token tile st, this workgroup's columns
-    double gC;       // g at the chunk's last token
+    frag wf[4][2];      // -W, token tile st, k block kb (this wave's rows)
+    frag kf[4][2];      // Kt, row tile t, token block m
+    quad uq[4][CT];     // Ut quads of token tile st, column tile ct
+    double gC;          // g at the chunk's last token
+    double lgam = 0.0;  // sum of gC over the group
+    const bool seed_ut = PHASE == SCAN_STATES || !is_phi;
     auto fetch_w = [&](int c) {
         const size_t cidx = (size_t)bh * p.NC + c;
         const E *Wc = p.W + cidx * (size_t)kChunk * DK + (size_t)w * 4096 + l * 8;
-        const E *Uc = p.Ut + cidx * (size_t)DV * kChunk + (size_t)jt * 1024 + l * 4;
 #pragma unroll
         for (int st = 0; st < 4; ++st)
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) wf[st][kb] = TR::load8(Wc + (st * 2 + kb) * 512);
+        if (seed_ut) {
+            const E *Uc = p.Ut + cidx * (size_t)DV * kChunk + (size_t)(jbase / 16) * 1024 + l * 4;
 #pragma unroll
-        for (int st = 0; st < 4; ++st) uq[st] = TR::load(Uc + st * 256);
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int st = 0; st < 4; ++st) uq[st][ct] = TR::load(Uc + ct * 1024 + st * 256);
+        }
     };
     auto fetch_k = [&](int c) {
         const size_t cidx = (size_t)bh * p.NC + c;
@@ -360,53 +414,213 @@ void gdn_scan_kernel(Params<E> p) {
         gC = p.g[cidx * kChunk + kChunk - 1];
     };
 
-    fetch_w(0);
-    fetch_k(0);
-    for (int c = 0; c < p.NC; ++c) {
+    fetch_w(c_begin);
+    fetch_k(c_begin);
+    for (int c = c_begin; c < c_end; ++c) {
         const size_t cidx = (size_t)bh * p.NC + c;
-        const int cn = min(c + 1, p.NC - 1);  // the last prefetch re-reads the last chunk
-        // H_{c-1} rounded to E: B operands over this wave's two 32-row blocks,
-        // also saved for stage 3.
-        frag hb[2];
+        const int cn = min(c + 1, c_end - 1);  // the last prefetch re-reads the last chunk
+        // H_{c-1} rounded to E: B operands over this wave's two 32-row blocks.
+        frag hb[2][CT];
 #pragma unroll
-        for (int pp = 0; pp < 2; ++pp) {
-            hb[pp] = TR::cat(TR::from_f32(Hacc[2 * pp]), TR::from_f32(Hacc[2 * pp + 1]));
-            TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)j * DK + d0 + 32 * pp + 8 * lg, hb[pp]);
-        }
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int pp = 0; pp < 2; ++pp) {
+                hb[pp][ct] = TR::cat(TR::from_f32(Hacc[2 * pp][ct]), TR::from_f32(Hacc[2 * pp + 1][ct]));
+                if (PHASE == SCAN_STATES)
+                    TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)(jbase + 16 * ct + li) * DK + d0 +
+                                   32 * pp + 8 * lg,
+                               hb[pp][ct]);
+            }
         // U = Ut - W H accumulated by the MFMAs (the workspace holds -W): wave 0
-        // seeds its accumulators with Ut, wave 1 with zero, and the two partial
-        // sums over their row halves are exchanged through LDS.
-        const uint32_t keep = (w == 0) ? 0xffffffffu : 0u;
-        f32x4 part[4];
+        // seeds its accumulators with Ut (zero for Phi columns), wave 1 with
+        // zero, and the two partial sums over their row halves are exchanged.
+        const uint32_t keep = (w == 0 && seed_ut) ? 0xffffffffu : 0u;
+        f32x4 part[4][CT];
 #pragma unroll
-        for (int st = 0; st < 4; ++st) part[st] = TR::mma(wf[st][0], hb[0], TR::to_f32(TR::mask(uq[st], keep)));
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-        for (int st = 0; st < 4; ++st) part[st] = TR::mma(wf[st][1], hb[1], part[st]);
+            for (int st = 0; st < 4; ++st)
+                part[st][ct] = TR::mma(wf[st][0], hb[0][ct],
+                                       seed_ut ? TR::to_f32(TR::mask(uq[st][ct], keep))
+                                               : f32x4{0.f, 0.f, 0.f, 0.f});
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int st = 0; st < 4; ++st) part[st][ct] = TR::mma(wf[st][1], hb[1][ct], part[st][ct]);
         fetch_w(cn);
         if constexpr (NW > 1) {
             const int buf = c & 1;
 #pragma unroll
-            for (int st = 0; st < 4; ++st) sP[buf][w][st][l] = part[st];
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int st = 0; st < 4; ++st) sP[buf][w][st][ct][l] = part[st][ct];
             lds_barrier();
 #pragma unroll
-            for (int st = 0; st < 4; ++st) part[st] += sP[buf][1 - w][st][l];
-        }
-        quad uqr[4];
+            for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-        for (int st = 0; st < 4; ++st) uqr[st] = TR::from_f32(part[st]);
-        const frag u0 = TR::cat(uqr[0], uqr[1]);
-        const frag u1 = TR::cat(uqr[2], uqr[3]);
-        E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)j * kChunk + 8 * lg;
-        if (NW == 1 || w == 0) TR::store8(Us, u0);
-        if (NW == 1 || w == 1) TR::store8(Us + 32, u1);
+                for (int st = 0; st < 4; ++st) part[st][ct] += sP[buf][1 - w][st][ct][l];
+        }
+        frag ub[2][CT];
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            ub[0][ct] = TR::cat(TR::from_f32(part[0][ct]), TR::from_f32(part[1][ct]));
+            ub[1][ct] = TR::cat(TR::from_f32(part[2][ct]), TR::from_f32(part[3][ct]));
+            if (PHASE == SCAN_STATES) {
+                E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)(jbase + 16 * ct + li) * kChunk + 8 * lg;
+                if (NW == 1 || w == 0) TR::store8(Us, ub[0][ct]);
+                if (NW == 1 || w == 1) TR::store8(Us + 32, ub[1][ct]);
+            }
+        }
+        lgam += gC;
         const float gam = expf((float)gC);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) Hacc[t] = TR::mma(kf[t][0], u0, Hacc[t] * gam);
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) Hacc[t] = TR::mma(kf[t][1], u1, Hacc[t]);
+            for (int t = 0; t < 4; ++t) Hacc[t][ct] = TR::mma(kf[t][0], ub[0][ct], Hacc[t][ct] * gam);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) Hacc[t][ct] = TR::mma(kf[t][1], ub[1][ct], Hacc[t][ct]);
         fetch_k(cn);
     }
 
+    const size_t gidx = (size_t)bh * p.NG + grp;
+    if constexpr (PHASE == SCAN_STATES) {
+        if (p.NG == 1 && p.state_out) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int t = 0; t < 4; ++t)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        p.state_out[((size_t)bh * DK + d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1) + q) * DV +
+                                    jbase + 16 * ct + li] = Hacc[t][ct][q];
+        }
+    } else if (!is_phi) {  // SCAN_TRANS from here on
+        // Psi_g^T [Dv][Dk], fp32
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                *(f32x4 *)(p.PsiT + (gidx * DV + jbase + 16 * ct + li) * DK + d0 + 32 * (t >> 1) + 8 * lg +
+                           4 * (t & 1)) = Hacc[t][ct];
+    } else {
+        if (jb == 0 && tid == 0) p.lgam[gidx] = lgam;
+        // N_g = Phi_g - Gamma_g I, rounded to E, staged in LDS as N^T (row e =
+        // state column, token-contiguous rows d) and re-read with the transposing
+        // LDS read into the group scan's A-operand fragments: fragment
+        // (wave v, row tile t, k block kb), lane (li, lg) =
+        //   N[64 v + 32 (t / 2) + p32_row(t % 2, li)][32 kb + 8 lg + e].
+        const float Gam = expf((float)lgam);
+        E *sN = (E *)&sP[0][0][0][0][0];
+        lds_barrier();  // every wave is done with the exchange buffer
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) {
+            const int e = 16 * ct + li;  // staging row = state column - col0
+#pragma unroll
+            for (int pp = 0; pp < 2; ++pp) {
+                f32x4 lo = Hacc[2 * pp][ct], hi = Hacc[2 * pp + 1][ct];
+                const int r0 = d0 + 32 * pp + 8 * lg;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (r0 + q == col0 + e) lo[q] -= Gam;
+                    if (r0 + 4 + q == col0 + e) hi[q] -= Gam;
+                }
+                TR::store8(sN + e * LDN + r0, TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
+            }
+        }
+        lds_barrier();
+        static_assert(CT % 2 == 0, "the transfer pass writes whole 32-column k blocks");
+        const int kb0 = col0 / 32;
+        constexpr int NKB = (16 * CT) / 32;                      // k blocks in this workgroup
+        constexpr int NFRAG = (DK / 64) * 4 * NKB;
+        E *Nf = p.Nf + gidx * (size_t)DK * DK + l * 8;
+        for (int f = w; f < NFRAG; f += NW) {
+            const int v = f / (4 * NKB), t = (f / NKB) % 4, kk = f % NKB;
+            const frag nf = tr_frag<E>(sN, LDN, 32 * kk, 64 * v + 32 * (t >> 1), true, t & 1, li, lg);
+            TR::store8(Nf + (size_t)((v * 4 + t) * (DK / 32) + kb0 + kk) * 512, nf);
+        }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Group scan: H <- Gamma_g H + N_g H + Psi_g over the groups of one (b, h), in
+// 16-column blocks (one workgroup each, Dk/64 waves splitting the rows, which
+// exchange their halves of H each step through LDS).  Records every group's
+// entry state H^T for the state stage and writes the final state.
+// --------------------------------------------------------------------------
+template <class E, int DK, int DV>
+__global__ __launch_bounds__(DK) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gdn_groupscan_kernel(Params<E> p) {
+    using TR = Tr<E>;
+    using frag = typename TR::frag;
+    constexpr int NW = DK / 64;
+    constexpr int NJ = DV / 16;
+    constexpr int KB = DK / 32;
+    __shared__ frag sH[2][NW][2][64];  // bf16 halves of H, double-buffered
+
+    const int id = blockIdx.x, x = id & 7, slot = id >> 3;
+    const int bh = (slot / NJ) * 8 + x, jt = slot % NJ;
+    if (bh >= p.B * p.H) return;
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
+    const int d0 = 64 * w;
+    const int j = 16 * jt + li;
+
+    f32x4 Hacc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            Hacc[t][q] = p.state_in ? p.state_in[((size_t)bh * DK + d0 + 32 * (t >> 1) + 8 * lg +
+                                                  4 * (t & 1) + q) * DV + j]
+                                    : 0.f;
+    frag nf[4][KB];
+    f32x4 ps[4];
+    double lg_g;
+    auto fetch = [&](int g) {
+        const size_t gidx = (size_t)bh * p.NG + g;
+        const E *Nc = p.Nf + gidx * (size_t)DK * DK + (size_t)w * 4 * KB * 512 + l * 8;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) nf[t][kb] = TR::load8(Nc + (t * KB + kb) * 512);
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            ps[t] = *(const f32x4 *)(p.PsiT + (gidx * DV + j) * DK + d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1));
+        lg_g = p.lgam[gidx];
+    };
+    fetch(0);
+    for (int g = 0; g < p.NG; ++g) {
+        const size_t gidx = (size_t)bh * p.NG + g;
+        // entry state of group g
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+            *(f32x4 *)(p.HgT + (gidx * DV + j) * DK + d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1)) = Hacc[t];
+        frag hb[KB];
+        const frag own0 = TR::cat(TR::from_f32(Hacc[0]), TR::from_f32(Hacc[1]));
+        const frag own1 = TR::cat(TR::from_f32(Hacc[2]), TR::from_f32(Hacc[3]));
+        if constexpr (NW > 1) {
+            const int buf = g & 1;
+            sH[buf][w][0][l] = own0;
+            sH[buf][w][1][l] = own1;
+            lds_barrier();
+            hb[2 * w] = own0;
+            hb[2 * w + 1] = own1;
+            hb[2 * (1 - w)] = sH[buf][1 - w][0][l];
+            hb[2 * (1 - w) + 1] = sH[buf][1 - w][1][l];
+        } else {
+            hb[0] = own0;
+            hb[1] = own1;
+        }
+        const float Gam = expf((float)lg_g);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) Hacc[t] = Hacc[t] * Gam + ps[t];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) Hacc[t] = TR::mma(nf[t][kb], hb[kb], Hacc[t]);
+        fetch(min(g + 1, p.NG - 1));
+    }
     if (p.state_out) {
 #pragma unroll
         for (int t = 0; t < 4; ++t)

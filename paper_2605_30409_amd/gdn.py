@@ -43,8 +43,14 @@ def lib():
             fn.restype, fn.argtypes = i, core + [vp, sz, vp]
         L.gdn_workspace_bytes.restype = sz
         L.gdn_workspace_bytes.argtypes = [i, i, i, i, i, i, i]
+        L.gdn_workspace_bytes_ex.restype = sz
+        L.gdn_workspace_bytes_ex.argtypes = [i, i, i, i, i, i, i, i]
+        L.gdn_scan_group_size.restype = i
+        L.gdn_scan_group_size.argtypes = [i, i, i, i, i, i, i]
+        L.gdn_chunk_forward_ex.restype = i
+        L.gdn_chunk_forward_ex.argtypes = core + [i, i, vp, sz, vp]
         L.gdn_profile_stages.restype = i
-        L.gdn_profile_stages.argtypes = core + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        L.gdn_profile_stages.argtypes = core + [i, i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
         L.gdn_status_string.restype = ctypes.c_char_p
         L.gdn_status_string.argtypes = [i]
         _lib = L
@@ -57,6 +63,11 @@ def gdn_status_string(status):
 
 def gdn_workspace_bytes(B, H, T, Dk, Dv, chunk=CHUNK, is_bf16=True):
     return int(lib().gdn_workspace_bytes(B, H, T, Dk, Dv, chunk, 1 if is_bf16 else 0))
+
+
+def gdn_workspace_bytes_ex(B, H, T, Dk, Dv, chunk=CHUNK, is_bf16=True, scan_group=0):
+    return int(lib().gdn_workspace_bytes_ex(B, H, T, Dk, Dv, chunk, 1 if is_bf16 else 0,
+                                            int(scan_group)))
 
 
 def _ptr(t):
@@ -136,29 +147,46 @@ def gdn_chunk_forward_f32_ws(q, k, v, alpha, beta, state_in, out, state_out, ws,
           (_ptr(ws), ws.numel()), stream)
 
 
-def gdn_profile_stages(q, k, v, alpha, beta, state_in, out, state_out, ws, reps=20, chunk=CHUNK,
-                       stream=None):
-    """Mean per-stage durations in ms (WY transform, state scan, output) over `reps` runs."""
+def gdn_scan_group_size(B, H, T, Dk, Dv, chunk=CHUNK, scan_group=0):
+    return int(lib().gdn_scan_group_size(B, H, T, Dk, Dv, chunk, int(scan_group)))
+
+
+def gdn_chunk_forward_ex(q, k, v, alpha, beta, state_in, out, state_out, ws, scan_group=0,
+                         chunk=CHUNK, stream=None):
+    """Either path (selected by q's dtype) with an explicit scan-group size and workspace."""
     is_bf16 = q.dtype == torch.bfloat16
-    ms = (ctypes.c_float * 3)()
+    _call("gdn_chunk_forward_ex", q, k, v, alpha, beta, state_in, out, state_out, chunk,
+          (1 if is_bf16 else 0, int(scan_group), _ptr(ws), ws.numel()), stream)
+
+
+STAGE_NAMES = ("wy", "group_transfer", "group_scan", "chunk_states", "output")
+
+
+def gdn_profile_stages(q, k, v, alpha, beta, state_in, out, state_out, ws, reps=20, chunk=CHUNK,
+                       scan_group=0, stream=None):
+    """Mean per-stage durations in ms over `reps` runs, in the order of STAGE_NAMES."""
+    is_bf16 = q.dtype == torch.bfloat16
+    ms = (ctypes.c_float * len(STAGE_NAMES))()
     _call("gdn_profile_stages", q, k, v, alpha, beta, state_in, out, state_out, chunk,
-          (1 if is_bf16 else 0, _ptr(ws), ws.numel(), int(reps), ms), stream)
+          (1 if is_bf16 else 0, int(scan_group), _ptr(ws), ws.numel(), int(reps), ms), stream)
     return [float(x) for x in ms]
 
 
-def workspace(q, v, chunk=CHUNK):
+def workspace(q, v, chunk=CHUNK, scan_group=0):
     """Allocate a workspace tensor sized for inputs shaped like q [B,T,H,Dk] and v [.., Dv]."""
     B, T, H, Dk = q.shape
-    n = gdn_workspace_bytes(B, H, T, Dk, v.shape[-1], chunk, q.dtype == torch.bfloat16)
+    n = gdn_workspace_bytes_ex(B, H, T, Dk, v.shape[-1], chunk, q.dtype == torch.bfloat16,
+                               scan_group)
     if n == 0:
         raise ValueError("unsupported shape for the GDN chunk forward")
     return torch.empty(n, dtype=torch.uint8, device=q.device)
 
 
 def forward(q, k, v, alpha, beta, state_in=None, *, out=None, state_out=None, want_state=True,
-            ws=None, chunk=CHUNK, stream=None):
+            ws=None, chunk=CHUNK, scan_group=None, stream=None):
     """GDN chunk forward.  q, k [B,T,H,Dk] and v [B,T,H,Dv] in bf16 or fp32 (on the GPU);
-    alpha, beta [B,T,H] fp32; state_in [B,H,Dk,Dv] fp32 or None (zero).
+    alpha, beta [B,T,H] fp32; state_in [B,H,Dk,Dv] fp32 or None (zero).  scan_group
+    (chunks per scan group, 0 = the library's choice) selects gdn_chunk_forward_ex.
     Returns (out [B,T,H,Dv] like v, state_out [B,H,Dk,Dv] fp32 or None)."""
     B, T, H, Dk = q.shape
     Dv = v.shape[-1]
@@ -167,7 +195,12 @@ def forward(q, k, v, alpha, beta, state_in=None, *, out=None, state_out=None, wa
     if state_out is None and want_state:
         state_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
     bf = q.dtype == torch.bfloat16
-    if ws is None:
+    if scan_group is not None:
+        if ws is None:
+            ws = workspace(q, v, chunk, scan_group)
+        gdn_chunk_forward_ex(q, k, v, alpha, beta, state_in, out, state_out, ws, scan_group,
+                             chunk=chunk, stream=stream)
+    elif ws is None:
         fn = gdn_chunk_forward if bf else gdn_chunk_forward_f32
         fn(q, k, v, alpha, beta, state_in, out, state_out, chunk=chunk, stream=stream)
     else:

@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 7 and "gdn_workspace_bytes" in names, names
+    assert len(names) == 10 and "gdn_workspace_bytes" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -34,12 +34,34 @@ def test_status_strings():
     assert gdn.gdn_status_string(-99) == "unknown status"
 
 
+def test_scan_group_size():
+    sg = gdn.gdn_scan_group_size
+    assert sg(1, 16, 3520, 128, 128) == 55               # 55 chunks: one group
+    assert sg(1, 16, 4097, 128, 128) == 8                # 65 chunks: round(sqrt(65))
+    assert sg(1, 16, 10560, 128, 128) == 13              # 165 chunks
+    assert sg(1, 32, 42240, 128, 128) == 26              # 660 chunks
+    assert sg(4, 20, 10560, 64, 64) == 13                # 80 streams x 4 column tiles
+    assert sg(8, 16, 10560, 128, 128) == 165             # 128 streams x 8 column tiles fill the chip
+    assert sg(1, 2, 1, 64, 64) == 1
+    assert sg(1, 16, 3520, 128, 128, scan_group=7) == 7
+    assert sg(1, 16, 3520, 128, 128, scan_group=1000) == 55
+    assert sg(1, 16, 10560, 128, 128, scan_group=-3) == 13
+    assert sg(1, 16, 0, 128, 128) == 0
+    assert sg(1, 16, 64, 128, 128, chunk=32) == 0
+    assert sg(1, 16, 64, 96, 128) == 0
+
+
 def test_workspace_bytes():
-    n = gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 64, True)
     nch = 16 * 55
-    # g + W + Kt + Ut + Hs + Us (each region 256-byte aligned)
-    expect = nch * 64 * 8 + nch * 2 * (64 * 128 * 4 + 128 * 128)
-    assert expect <= n < expect + 6 * 256
+    base = nch * 64 * 8 + nch * 2 * (64 * 128 * 4 + 128 * 128)   # g, -W, Kt, Ut, Hs, Us
+    n = gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 64, True)    # one scan group
+    assert base <= n < base + 10 * 256
+    assert n == gdn.gdn_workspace_bytes_ex(1, 16, 3520, 128, 128, 64, True, 0)
+    # 11 groups of 5 chunks add N (bf16), Psi^T, log Gamma and entry states (fp32)
+    ngr = 16 * 11
+    grouped = gdn.gdn_workspace_bytes_ex(1, 16, 3520, 128, 128, 64, True, 5)
+    expect = base + ngr * (128 * 128 * 2 + 128 * 128 * 4 * 2 + 8)
+    assert expect <= grouped < expect + 10 * 256
     assert gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 64, False) > n
     assert gdn.gdn_workspace_bytes(1, 16, 3520, 96, 128, 64, True) == 0
     assert gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 32, True) == 0
@@ -59,13 +81,16 @@ def call(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, a=BASE + 192 * MB, b=B
          ws_bytes=0):
     L = gdn.lib()
     args = [q, k, v, a, b, si, o, so, B, H, T, Dk, Dv, chunk]
-    if fn.endswith("_ws"):
+    if fn.endswith("_ex"):
+        args += [1, 0]                                   # bf16, library group size
+    if fn.endswith("_ws") or fn.endswith("_ex"):
         args += [ws, ws_bytes]
     return getattr(L, fn)(*args, None)
 
 
 @pytest.mark.parametrize("fn", ["gdn_chunk_forward", "gdn_chunk_forward_f32",
-                                "gdn_chunk_forward_ws", "gdn_chunk_forward_f32_ws"])
+                                "gdn_chunk_forward_ws", "gdn_chunk_forward_f32_ws",
+                                "gdn_chunk_forward_ex"])
 def test_validation_errors(fn):
     assert call(fn, q=None) == -1
     assert call(fn, o=None) == -1
@@ -80,7 +105,7 @@ def test_validation_errors(fn):
     assert call(fn, o=BASE + 4096) == -7                 # out overlaps q
     assert call(fn, so=BASE + 64 * MB) == -7             # state_out overlaps k
     assert call(fn, si=BASE + 300 * MB, so=BASE + 300 * MB + 4096) == -7  # partial state overlap
-    if fn.endswith("_ws"):
+    if fn.endswith("_ws") or fn.endswith("_ex"):
         assert call(fn) == -4                            # no workspace
         assert call(fn, ws=BASE + 512 * MB, ws_bytes=100) == -4
         assert call(fn, ws=BASE + 512 * MB + 16, ws_bytes=1 << 30) == -4   # misaligned

@@ -41,20 +41,22 @@ def rel_err(x, ref):
     return float(np.abs(x - ref).max() / max(np.abs(ref).max(), 1e-30))
 
 
-def run_gpu(gdn, inp, state_in="input", ws=False):
+def run_gpu(gdn, inp, state_in="input", ws=False, scan_group=None):
     t = {k: dev_tensor(inp[k]) for k in ("q", "k", "v", "alpha", "beta")}
     si = dev_tensor(inp["state_in"]) if state_in == "input" else state_in
     kw = {}
     if ws:
         kw["ws"] = gdn.workspace(t["q"], t["v"])
+    if scan_group is not None:
+        kw["scan_group"] = scan_group
     out, st = gdn.forward(t["q"], t["k"], t["v"], t["alpha"], t["beta"], si, **kw)
     torch_mod().cuda.synchronize()
     return out, st
 
 
-def check(gdn, inp, label, heads=None):
+def check(gdn, inp, label, heads=None, scan_group=None):
     """Full comparison (or on a sampled subset of heads) against the oracle."""
-    out, st = run_gpu(gdn, inp)
+    out, st = run_gpu(gdn, inp, scan_group=scan_group)
     o, s = host_f64(out), host_f64(st)
     sl = slice(None) if heads is None else list(heads)
     ref_o, ref_s = oracle.gdn_forward(inp["q"][:, :, sl], inp["k"][:, :, sl], inp["v"][:, :, sl],
@@ -77,6 +79,27 @@ def test_small_shapes(gdn, dtype, Dk, Dv, T):
     inp = gdn_inputs.make_inputs(1, B=2, T=T, H=3, Dk=Dk, Dv=Dv, dtype=dtype,
                                  seed=7000 + T + Dk + 2 * Dv)
     check(gdn, inp, f"B2 T{T} H3 Dk{Dk} Dv{Dv} {dtype}")
+
+
+# ---- grouped scan: every group size from one chunk per group to a single group ----
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("Dk,Dv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+@pytest.mark.parametrize("G", [1, 2, 7, 24])
+def test_scan_groups(gdn, dtype, Dk, Dv, G):
+    """T = 1500 is 24 chunks (the last ragged): G = 7 leaves a short last group,
+    G = 24 is the single sequential scan."""
+    inp = gdn_inputs.make_inputs(1, B=1, T=1500, H=3, Dk=Dk, Dv=Dv, dtype=dtype,
+                                 seed=8100 + G + Dk + 2 * Dv)
+    check(gdn, inp, f"T1500 H3 Dk{Dk} Dv{Dv} {dtype} scan groups of {G}", scan_group=G)
+
+
+def test_scan_groups_agree(gdn):
+    """The grouped and the single-group scans agree to rounding on a long sequence."""
+    inp = gdn_inputs.make_inputs(1, T=6000, H=4)
+    o1, s1 = run_gpu(gdn, inp, scan_group=0)
+    o2, s2 = run_gpu(gdn, inp, scan_group=10 ** 6)
+    assert rel_err(host_f64(o1), host_f64(o2)) < 1e-2
+    assert rel_err(host_f64(s1), host_f64(s2)) < 1e-2
 
 
 def test_workload0_tiny_f32(gdn):
@@ -134,9 +157,11 @@ def test_zero_state_in_equals_none(gdn):
     assert torch.equal(o1, o2) and torch.equal(s1, s2)
 
 
-def test_state_out_none_and_inplace_state(gdn):
+@pytest.mark.parametrize("T", [300, 1500])
+def test_state_out_none_and_inplace_state(gdn, T):
+    """T = 300 runs one scan group, T = 1500 the grouped scan."""
     torch = torch_mod()
-    inp = gdn_inputs.make_inputs(1, T=300, H=2)
+    inp = gdn_inputs.make_inputs(1, T=T, H=2)
     t = {k: dev_tensor(inp[k]) for k in ("q", "k", "v", "alpha", "beta")}
     si = dev_tensor(inp["state_in"])
     o_ref, s_ref = gdn.forward(t["q"], t["k"], t["v"], t["alpha"], t["beta"], si)
@@ -166,33 +191,38 @@ def test_deterministic(gdn):
     assert torch.equal(o1, o2) and torch.equal(s1, s2)
 
 
+@pytest.mark.parametrize("group", [10 ** 6, 0])
 @pytest.mark.parametrize("m", [128, 1024, 100])
-def test_streaming_split(gdn, m):
+def test_streaming_split(gdn, m, group):
     """One call on x equals two calls (x[:m], then x[m:] with the carried state).
-    At a chunk-aligned split the chunking is identical, so the match is exact."""
+    With a single scan group and a chunk-aligned split the chunking is identical,
+    so the match is exact; otherwise it holds to rounding."""
     torch = torch_mod()
     inp = gdn_inputs.make_inputs(1, T=1500, H=2)
-    o, s = run_gpu(gdn, inp)
+    o, s = run_gpu(gdn, inp, scan_group=group)
     a = {k: (inp[k][:, :m] if k in ("q", "k", "v", "alpha", "beta") else inp[k]) for k in inp}
     b = {k: (inp[k][:, m:] if k in ("q", "k", "v", "alpha", "beta") else inp[k]) for k in inp}
-    oa, sa = run_gpu(gdn, a)
-    ob, sb = run_gpu(gdn, b, state_in=sa)
+    oa, sa = run_gpu(gdn, a, scan_group=group)
+    ob, sb = run_gpu(gdn, b, state_in=sa, scan_group=group)
     o2 = torch.cat([oa, ob], dim=1)
-    if m % 64 == 0:
+    if m % 64 == 0 and group > 0:
         assert torch.equal(o2, o) and torch.equal(sb, s)
     else:
         assert rel_err(host_f64(o2), host_f64(o)) < 1e-2
         assert rel_err(host_f64(sb), host_f64(s)) < 1e-2
 
 
-def test_invariant_beta0_alpha1_keeps_state(gdn):
+@pytest.mark.parametrize("T", [500, 3000])
+def test_invariant_beta0_alpha1_keeps_state(gdn, T):
+    """No write and no decay keeps the state bit for bit, also through the
+    grouped scan (T = 3000): every group transfer is exactly the identity."""
     torch = torch_mod()
-    inp = gdn_inputs.make_inputs(1, T=500, H=2)
+    inp = gdn_inputs.make_inputs(1, T=T, H=2)
     inp["alpha"][:] = 1.0
     inp["beta"][:] = 0.0
     out, st = run_gpu(gdn, inp)
     assert torch.equal(st.cpu(), torch.from_numpy(inp["state_in"]))
-    check(gdn, inp, "beta=0 alpha=1")
+    check(gdn, inp, f"beta=0 alpha=1 T={T}")
 
 
 def test_invariant_beta1_alpha1_unit_key_writes_v(gdn):

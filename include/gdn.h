@@ -142,12 +142,16 @@ int gdn_chunk_forward_ex(const void *q, const void *k, const void *v,
 
 /*
  * Per-stage timing (measurement aid, same arguments as gdn_chunk_forward_ex):
- * runs the whole path `reps` times on `stream`, recording HIP events on that
- * stream between its five stages, then synchronizes the stream and writes the
- * mean duration of each stage in milliseconds to stage_ms[0..4] (host
- * memory): [0] WY transform, [1] group transfer maps, [2] scan over groups,
- * [3] chunk states, [4] output.  Stages 1 and 2 take ~0 ms when the scan runs
- * as one group.  Creates and destroys its own events.
+ * enqueues the path once on `stream`, with every stage launched `reps` times
+ * back to back between two HIP events recorded on that stream (a stage's
+ * launches are identical re-runs, since a stage only reads the inputs and the
+ * previous stages' results), then synchronizes the stream and writes the mean
+ * duration of one launch of each stage in milliseconds to stage_ms[0..4]
+ * (host memory): [0] WY transform, [1] group transfer maps, [2] scan over
+ * groups, [3] chunk states, [4] output.  Stages that do not run for this
+ * shape (1 and 2 with a single scan group) report 0.  state_in ==
+ * state_out is rejected with GDN_ERR_ALIAS.  The outputs are those of one
+ * ordinary call.  Creates and destroys its own events.
  */
 int gdn_profile_stages(const void *q, const void *k, const void *v,
                        const float *alpha, const float *beta, const float *state_in,

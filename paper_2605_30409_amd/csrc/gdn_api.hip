@@ -15,7 +15,7 @@ namespace {
 using gdn::kChunk;
 
 struct WsLayout {
-    size_t g, W, Kt, Ut, Hs, Us, Nf, PsiT, lgam, HgT, total;
+    size_t g, gc, W, Kt, Ut, Hs, Us, Nf, PsiT, lgam, HgT, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -47,6 +47,7 @@ WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
     WsLayout L;
     size_t off = 0;
     L.g = off;    off = align256(off + nch * kChunk * 8);
+    L.gc = off;   off = align256(off + nch * 8);
     L.W = off;    off = align256(off + nch * kChunk * Dk * esz);
     L.Kt = off;   off = align256(off + nch * Dk * kChunk * esz);
     L.Ut = off;   off = align256(off + nch * Dv * kChunk * esz);
@@ -129,6 +130,7 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
     const WsLayout L = ws_layout(B, H, T, Dk, Dv, sizeof(E), G);
     unsigned char *base = (unsigned char *)ws;
     p.g = (double *)(base + L.g);
+    p.gc = (double *)(base + L.gc);
     p.W = (E *)(base + L.W);
     p.Kt = (E *)(base + L.Kt);
     p.Ut = (E *)(base + L.Ut);
@@ -143,67 +145,103 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
 
 constexpr int kStages = 5;  // WY transform, group transfers, group scan, chunk states, output
 
+// Stage timing (measurement aid): every stage that launches is enqueued `reps`
+// times back to back between the events ev[2 s] and ev[2 s + 1].
+struct StageTiming {
+    int reps;
+    hipEvent_t ev[2 * kStages];
+    bool ran[kStages];
+};
+
 template <class E, int DK, int DV>
-hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, hipEvent_t *ev) {
+hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) {
+    constexpr int CT = gdn::ScanCT<E>::value;
+    constexpr int NCW = gdn::kScanNCW;
+    using LT = gdn::ScanLds<E, DK, CT, NCW>;  // grouped passes
+    using L1 = gdn::ScanLds<E, DK, 1, 1>;     // single-group scan
+    constexpr unsigned scan_threads = (NCW + 2) * 64, scan_threads1 = 3 * 64;
     static std::once_flag attr_once;
     static hipError_t attr_err = hipSuccess;
     const size_t lds1 = gdn::WyLds<E, DK, DV>::bytes;
     const size_t lds3 = gdn::OutLds<E, DK, DV>::bytes;
     std::call_once(attr_once, [&] {
-        hipError_t e1 = hipFuncSetAttribute((const void *)gdn::gdn_wy_kernel<E, DK, DV>,
-                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds1);
-        hipError_t e3 = hipFuncSetAttribute((const void *)gdn::gdn_output_kernel<E, DK, DV>,
-                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds3);
-        attr_err = (e1 != hipSuccess) ? e1 : e3;
+        const struct {
+            const void *fn;
+            size_t bytes;
+        } dyn[] = {
+            {(const void *)gdn::gdn_wy_kernel<E, DK, DV>, lds1},
+            {(const void *)gdn::gdn_output_kernel<E, DK, DV>, lds3},
+            {(const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT, NCW>, LT::bytes},
+            {(const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT, NCW>, LT::bytes},
+            {(const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1>, L1::bytes},
+        };
+        for (const auto &d : dyn) {
+            const hipError_t e =
+                hipFuncSetAttribute(d.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)d.bytes);
+            if (e != hipSuccess && attr_err == hipSuccess) attr_err = e;
+        }
     });
     if (attr_err != hipSuccess) return attr_err;
     const unsigned BH = (unsigned)(p.B * p.H);
-    constexpr unsigned CT = gdn::ScanCT<E>::value;
-    hipError_t er = hipSuccess;
-    auto mark = [&](int i) {
-        if (ev && er == hipSuccess) er = hipEventRecord(ev[i], s);
-    };
     // workgroup counts: column blocks x 8 x ceil(units / 8) (see the XCD placement)
     auto groups = [](unsigned nblocks, unsigned units) { return nblocks * 8u * ((units + 7u) / 8u); };
-    mark(0);
-    hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds1, s, p);
-    mark(1);
-    if (p.NG > 1) {
-        hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT>),
-                           dim3(groups((DK + DV) / (16 * CT), BH * p.NG)), dim3(DK), 0, s, p);
+    auto stage = [&](int i) {
+        switch (i) {
+        case 0:
+            hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds1, s, p);
+            break;
+        case 1:
+            hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT, NCW>),
+                               dim3(groups((DK + DV) / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads),
+                               LT::bytes, s, p);
+            break;
+        case 2:
+            hipLaunchKernelGGL((gdn::gdn_groupscan_kernel<E, DK, DV>), dim3(groups(DV / 16, BH)),
+                               dim3(DK), 0, s, p);
+            break;
+        case 3:
+            if (p.NG > 1) {
+                hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT, NCW>),
+                                   dim3(groups(DV / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads),
+                                   LT::bytes, s, p);
+            } else {
+                // one sequential scan per (b, h): one column tile per compute wave
+                hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1>),
+                                   dim3(groups(DV / 16, BH)), dim3(scan_threads1), L1::bytes, s, p);
+            }
+            break;
+        default:
+            hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
+        }
+    };
+    hipError_t er = hipSuccess;
+    for (int i = 0; i < kStages && er == hipSuccess; ++i) {
+        const bool runs = (i != 1 && i != 2) || p.NG > 1;
+        if (tm) tm->ran[i] = runs;
+        if (!runs) continue;
+        if (!tm) {
+            stage(i);
+            continue;
+        }
+        er = hipEventRecord(tm->ev[2 * i], s);
+        for (int r = 0; r < tm->reps && er == hipSuccess; ++r) stage(i);
+        if (er == hipSuccess) er = hipEventRecord(tm->ev[2 * i + 1], s);
     }
-    mark(2);
-    if (p.NG > 1) {
-        hipLaunchKernelGGL((gdn::gdn_groupscan_kernel<E, DK, DV>), dim3(groups(DV / 16, BH)), dim3(DK),
-                           0, s, p);
-    }
-    mark(3);
-    if (p.NG > 1) {
-        hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT>),
-                           dim3(groups(DV / (16 * CT), BH * p.NG)), dim3(DK), 0, s, p);
-    } else {
-        // one sequential scan per (b, h): 16-column workgroups for parallelism
-        hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1>),
-                           dim3(groups(DV / 16, BH)), dim3(DK), 0, s, p);
-    }
-    mark(4);
-    hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
-    mark(5);
     const hipError_t le = hipGetLastError();
     return le != hipSuccess ? le : er;
 }
 
 template <class E>
-hipError_t dispatch(const gdn::Params<E> &p, int Dk, int Dv, hipStream_t s, hipEvent_t *ev) {
-    if (Dk == 128 && Dv == 128) return launch_path<E, 128, 128>(p, s, ev);
-    if (Dk == 64 && Dv == 64) return launch_path<E, 64, 64>(p, s, ev);
-    if (Dk == 128 && Dv == 64) return launch_path<E, 128, 64>(p, s, ev);
-    return launch_path<E, 64, 128>(p, s, ev);
+hipError_t dispatch(const gdn::Params<E> &p, int Dk, int Dv, hipStream_t s, StageTiming *tm) {
+    if (Dk == 128 && Dv == 128) return launch_path<E, 128, 128>(p, s, tm);
+    if (Dk == 64 && Dv == 64) return launch_path<E, 64, 64>(p, s, tm);
+    if (Dk == 128 && Dv == 64) return launch_path<E, 128, 64>(p, s, tm);
+    return launch_path<E, 64, 128>(p, s, tm);
 }
 
 int run(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
         const float *state_in, void *out, float *state_out, int B, int H, int T, int Dk, int Dv,
-        int chunk, bool bf16, int group, void *ws, size_t ws_bytes, void *stream, hipEvent_t *ev) {
+        int chunk, bool bf16, int group, void *ws, size_t ws_bytes, void *stream, StageTiming *tm) {
     const size_t esz = bf16 ? 2 : 4;
     int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
     if (st != GDN_OK) return st;
@@ -215,11 +253,11 @@ int run(const void *q, const void *k, const void *v, const float *alpha, const f
     if (bf16) {
         e = dispatch(make_params<uint16_t>(q, k, v, alpha, beta, state_in, out, state_out, B, H, T,
                                            Dk, Dv, G, ws),
-                     Dk, Dv, s, ev);
+                     Dk, Dv, s, tm);
     } else {
         e = dispatch(make_params<float>(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk,
                                         Dv, G, ws),
-                     Dk, Dv, s, ev);
+                     Dk, Dv, s, tm);
     }
     return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
@@ -326,42 +364,28 @@ int gdn_profile_stages(const void *q, const void *k, const void *v, const float 
                        int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group,
                        void *ws, size_t ws_bytes, int reps, float *stage_ms, void *stream) {
     if (!stage_ms || reps < 1) return GDN_ERR_NULL;
-    const bool bf16 = is_bf16 != 0;
-    const size_t esz = bf16 ? 2 : 4;
-    int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
-    if (st != GDN_OK) return st;
-    const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group);
-    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz, G).total)
-        return GDN_ERR_WORKSPACE;
-    constexpr int NE = kStages + 1;
-    std::vector<hipEvent_t> ev((size_t)reps * NE, nullptr);
+    // Stages are re-run in place, so the state may not be updated in place.
+    if (state_in && state_in == state_out) return GDN_ERR_ALIAS;
+    StageTiming tm{};
+    tm.reps = reps;
     int status = GDN_OK;
-    for (auto &e : ev)
-        if (hipEventCreate(&e) != hipSuccess) {
+    for (auto &e : tm.ev)
+        if (status == GDN_OK && hipEventCreate(&e) != hipSuccess) {
             e = nullptr;
             status = GDN_ERR_HIP;
         }
-    for (int r = 0; r < reps && status == GDN_OK; ++r)
-        status = run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, bf16,
-                     scan_group, ws, ws_bytes, stream, &ev[(size_t)r * NE]);
+    if (status == GDN_OK)
+        status = run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk,
+                     is_bf16 != 0, scan_group, ws, ws_bytes, stream, &tm);
     if (status == GDN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess)
         status = GDN_ERR_HIP;
-    if (status == GDN_OK) {
-        double sum[kStages] = {};
-        for (int r = 0; r < reps && status == GDN_OK; ++r) {
-            for (int s = 0; s < kStages; ++s) {
-                float ms = 0.f;
-                if (hipEventElapsedTime(&ms, ev[(size_t)r * NE + s], ev[(size_t)r * NE + s + 1]) !=
-                    hipSuccess) {
-                    status = GDN_ERR_HIP;
-                    break;
-                }
-                sum[s] += ms;
-            }
-        }
-        for (int s = 0; s < kStages; ++s) stage_ms[s] = (float)(sum[s] / reps);
+    for (int i = 0; i < kStages && status == GDN_OK; ++i) {
+        float ms = 0.f;
+        if (tm.ran[i] && hipEventElapsedTime(&ms, tm.ev[2 * i], tm.ev[2 * i + 1]) != hipSuccess)
+            status = GDN_ERR_HIP;
+        stage_ms[i] = tm.ran[i] ? ms / reps : 0.f;
     }
-    for (auto &e : ev)
+    for (auto &e : tm.ev)
         if (e) (void)hipEventDestroy(e);
     return status;
 }

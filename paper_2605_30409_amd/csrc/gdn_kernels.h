@@ -20,6 +20,7 @@
 // Workspace per (b*H + h, chunk) -- see gdn_api.hip for the byte layout:
 //   g  [64]       fp64   cumulative log decay (fp64 so that g_r - g_s keeps
 //                        its precision when the decay over a chunk is huge)
+//   gc            fp64   g at the chunk's last token (compact, for the scan)
 //   W  64*Dk      E      -W (the WY factor, negated), fragment-major for the scan
 //   Kt Dk*64      E      Kt = (diag(e^{g_C - g}) K)^T, fragment-major
 //   Ut Dv*64      E      Ut, fragment-major
@@ -47,6 +48,7 @@ template <class E> struct Params {
     int B, H, T, NC;
     int G, NG;        // chunks per scan group, number of groups
     double *g;
+    double *gc;       // per (b*H + h, chunk): g at the chunk's last token
     E *W, *Kt, *Ut, *Hs, *Us;
     E *Nf;            // per (b*H + h, group): N_g = Phi_g - Gamma_g I, fragment-major
     float *PsiT;      // per (b*H + h, group): Psi_g^T [Dv][Dk]
@@ -142,6 +144,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         sw[l] = be * __builtin_amdgcn_exp2f((float)(g * kLog2e));
         sd[l] = __builtin_amdgcn_exp2f((float)((gC - g) * kLog2e));
         p.g[cidx * kChunk + l] = g;
+        if (l == 0) p.gc[cidx] = gC;
     }
 #pragma unroll
     for (int n = 0; n < NKV; ++n) {
@@ -313,33 +316,86 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
 //       per-chunk state H_{c-1} and pseudo-values U_c the output stage needs.
 // With a single group only (O) runs, from state_in, and writes state_out.
 //
-// gdn_chunkscan_kernel: one workgroup owns 16 * CT state columns of one
-// (b, h, group) and carries them through the group's chunks in fp32
-// accumulators.  Its Dk/64 waves split the state rows (64 each); with two
-// waves every chunk costs one exchange of the partial W H products through LDS
-// (double-buffered, one barrier), after which both waves hold the whole U.
-// Several column tiles per workgroup reuse each chunk operand fragment CT
-// times, which keeps the operand traffic through the CU's L1 in check.
+// gdn_chunkscan_kernel: a workgroup owns NCW * 16 * CT state columns of one
+// (b, h, group).  It has NCW compute waves, each carrying 16 * CT columns over
+// all Dk rows through the group's chunks in fp32 accumulators (so U = Ut - W H
+// needs no exchange between waves), and two loader waves that stream the chunk
+// operands (-W, Kt, and the workgroup's Ut columns) into an LDS ring of DEPTH
+// slots with asynchronous global->LDS copies (1 KB per instruction, lane i's
+// 16 bytes landing at +16 i, so the fragment-major workspace layout is kept).
+// One workgroup barrier per chunk hands a slot over: before barrier c the
+// loaders have waited (vmcnt) for chunk c's copies; after it they refill the
+// slot of chunk c - 1, which every compute wave has finished reading.  The
+// copies for chunk c are thus issued DEPTH - 1 chunks ahead, and neither the
+// copy issue nor its latency sits on the compute waves' chain.
 // --------------------------------------------------------------------------
 enum { SCAN_TRANS = 0, SCAN_STATES = 1 };
 
-// Column tiles per workgroup for the grouped passes (wide: operand reuse) and
-// for a single-group scan (narrow: as many workgroups as possible).
-template <class E> struct ScanCT { static constexpr int value = sizeof(E) == 2 ? 4 : 2; };
+// Column tiles per compute wave and compute waves per workgroup for the
+// grouped passes; a single-group scan uses one column tile and one compute
+// wave per workgroup (every workgroup loads all of W and Kt each chunk, so
+// narrow workgroups spread that traffic over more CUs).
+template <class E> struct ScanCT { static constexpr int value = sizeof(E) == 2 ? 2 : 1; };
+constexpr int kScanNCW = 2;
 
-template <class E, int DK, int DV, int PHASE, int CT>
-__global__ __launch_bounds__(DK) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <class E, int DK, int CT, int NCW> struct ScanLds {
+    static constexpr int KB = DK / 32;                     // 32-row blocks of the state
+    static constexpr int NT = DK / 16;                     // 16-row tiles of the state
+    static constexpr int WK = kChunk * DK;                 // elements of -W (and of Kt) per chunk
+    static constexpr int UT = NCW * CT * 1024;             // elements of the workgroup's Ut per chunk
+    static constexpr int SLOT = 2 * WK + UT;               // ring slot: -W, Kt, Ut
+    static constexpr int SLOT_BYTES = SLOT * (int)sizeof(E);
+    static constexpr int NC_W = WK * (int)sizeof(E) / 1024;   // 1 KB copies of -W (and of Kt)
+    static constexpr int NC_U = UT * (int)sizeof(E) / 1024;
+    // loader 0 copies -W and the first half of Ut, loader 1 Kt and the rest
+    static constexpr int NC_U0 = NC_U / 2, NC_U1 = NC_U - NC_U0;
+    static constexpr int NCOPY0 = NC_W + NC_U0, NCOPY1 = NC_W + NC_U1;
+    static constexpr int LDS_CAP = 152 * 1024;
+    static constexpr int DL = LDS_CAP / SLOT_BYTES;
+    // the loader waits with D - 2 younger chunks in flight: vmcnt <= 63
+    static constexpr int DV_ = 2 + 63 / (NCOPY0 > NCOPY1 ? NCOPY0 : NCOPY1);
+    static constexpr int DEPTH = (DL < 4 ? DL : 4) < DV_ ? (DL < 4 ? DL : 4) : DV_;
+    static constexpr size_t bytes = (size_t)DEPTH * SLOT_BYTES;
+    static_assert(DEPTH >= 2, "scan ring needs two slots");
+    static_assert((WK * sizeof(E)) % 1024 == 0 && (UT * sizeof(E)) % 2048 == 0, "whole 1 KB copies");
+};
+
+template <int N> __device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// Workgroup barrier for waves that communicate through LDS while asynchronous
+// global->LDS copies are in flight: waits for this wave's LDS accesses only
+// (a workgroup fence would also wait for the copies).
+__device__ __forceinline__ void lds_only_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Copy N whole KB from global to LDS: instruction i moves bytes
+// [1024 i, 1024 i + 1024), lane l its 16 bytes at 1024 i + 16 l.
+template <int N> __device__ __forceinline__ void copy_kb(const void *src, void *dst, int l) {
+#pragma unroll
+    for (int i = 0; i < N; ++i)
+        __builtin_amdgcn_global_load_lds((const void *)((const char *)src + 1024 * i + 16 * l),
+                                         (__attribute__((address_space(3))) void *)((char *)dst + 1024 * i),
+                                         16, 0, 0);
+}
+
+template <class E, int DK, int DV, int PHASE, int CT, int NCW>
+__global__ __launch_bounds__((NCW + 2) * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gdn_chunkscan_kernel(Params<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
-    using quad = typename TR::quad;
-    constexpr int NW = DK / 64;                          // waves; wave w owns rows [64w, 64w+64)
+    using L = ScanLds<E, DK, CT, NCW>;
+    constexpr int D = L::DEPTH;
+    constexpr int KB = L::KB, NT = L::NT;
+    constexpr int WGC = NCW * 16 * CT;                   // columns per workgroup
     constexpr int WCOLS = PHASE == SCAN_TRANS ? DK + DV : DV;
-    constexpr int NJB = WCOLS / (16 * CT);               // column blocks per (b, h, group)
-    constexpr int NLDN = 16 * CT;                        // rows of the N^T staging tile
-    constexpr int LDN = DK + 16 / (int)sizeof(E);
-    __shared__ f32x4 sP[2][NW][4][CT][64];               // partial (W H) tiles, double-buffered
-    static_assert(sizeof(E) * NLDN * LDN <= sizeof(f32x4) * 2 * NW * 4 * CT * 64, "N^T staging");
+    constexpr int NJB = WCOLS / WGC;                     // column blocks per (b, h, group)
+    static_assert(WCOLS % WGC == 0 && DK % WGC == 0, "column blocks do not straddle Phi and Psi");
+    extern __shared__ __align__(16) unsigned char scan_lds[];
+    E *ring = (E *)scan_lds;
 
     // XCD-aware placement: workgroups are dealt round-robin to the 8 XCDs, so
     // id = 8 slot + x runs on XCD x.  The NJB column blocks of one (b, h, group)
@@ -350,139 +406,182 @@ void gdn_chunkscan_kernel(Params<E> p) {
     if (unit >= p.B * p.H * p.NG) return;
     const int bh = unit / p.NG, grp = unit - bh * p.NG;
     const int c_begin = grp * p.G, c_end = min(p.NC, c_begin + p.G);
-    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
-    const int d0 = 64 * w;
-    const int col0 = 16 * CT * jb;
+    // w is wave-uniform: scalar branches and addresses
+    const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63, li = l & 15,
+              lg = l >> 4;
+    const int col0 = WGC * jb;
     const bool is_phi = PHASE == SCAN_TRANS && col0 < DK;
-    // columns of this workgroup within the state (Phi columns or Psi / H columns)
-    const int jbase = (PHASE == SCAN_TRANS && !is_phi) ? col0 - DK : col0;
+    // first column of this workgroup within the state (Phi columns or Psi / H columns)
+    const int wbase = (PHASE == SCAN_TRANS && !is_phi) ? col0 - DK : col0;
+    const bool has_ut = PHASE == SCAN_STATES || !is_phi;
+    auto slot_of = [&](int c) { return ring + (size_t)((c - c_begin) % D) * L::SLOT; };
 
-    // State rows d0 + [0, 64) as four accumulator tiles t = 2 pp + a in P32
-    // order, for each column tile ct: Hacc[t][ct][q] = H[d0 + 32 pp + 8 lg + 4 a + q][jbase + 16 ct + li].
-    f32x4 Hacc[4][CT];
-#pragma unroll
-    for (int ct = 0; ct < CT; ++ct) {
-        const int j = jbase + 16 * ct + li;
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            const int r0 = d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
-            if (PHASE == SCAN_TRANS) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) Hacc[t][ct][q] = (is_phi && r0 + q == j) ? 1.f : 0.f;
-            } else if (p.NG > 1) {
-                Hacc[t][ct] = *(const f32x4 *)(p.HgT + ((size_t)unit * DV + j) * DK + r0);
+    if (w >= NCW) {
+        // ---------------- loader waves ----------------
+        const int ld = w - NCW;
+        auto issue = [&](int c) {
+            const size_t cidx = (size_t)bh * p.NC + c;
+            E *sl = slot_of(c);
+            const E *ut = p.Ut + cidx * (size_t)DV * kChunk + (size_t)(wbase / 16) * 1024;
+            if (ld == 0) {
+                copy_kb<L::NC_W>(p.W + cidx * (size_t)L::WK, sl, l);
+                if (has_ut) copy_kb<L::NC_U0>(ut, sl + 2 * L::WK, l);
             } else {
+                copy_kb<L::NC_W>(p.Kt + cidx * (size_t)L::WK, sl + L::WK, l);
+                if (has_ut)
+                    copy_kb<L::NC_U1>((const char *)ut + 1024 * L::NC_U0,
+                                      (char *)(sl + 2 * L::WK) + 1024 * L::NC_U0, l);
+            }
+        };
+        // Chunk c's copies have landed once at most D - 2 younger chunks' are
+        // in flight (every chunk issues the same number of copies).
+        auto wait_oldest = [&]() {
+            if (ld == 0) {
+                if (has_ut) wait_vmcnt<(D - 2) * L::NCOPY0>();
+                else wait_vmcnt<(D - 2) * L::NC_W>();
+            } else {
+                if (has_ut) wait_vmcnt<(D - 2) * L::NCOPY1>();
+                else wait_vmcnt<(D - 2) * L::NC_W>();
+            }
+        };
+        // prologue: chunks c_begin .. c_begin + D - 2 (past the end: the last
+        // chunk again, into its own slot, so the count per chunk is constant)
+#pragma unroll
+        for (int i = 0; i < D - 1; ++i) issue(min(c_begin + i, c_end - 1));
+        for (int c = c_begin; c < c_end; ++c) {
+            wait_oldest();
+            lds_only_barrier();                 // chunk c handed to the compute waves
+            issue(min(c + D - 1, c_end - 1));   // refills the slot of chunk c - 1
+        }
+        wait_vmcnt<0>();
+        lds_only_barrier();                     // ring quiet: the compute waves may reuse it
+        if (PHASE == SCAN_TRANS && is_phi) lds_only_barrier();  // matches the N staging barrier
+        return;
+    }
+
+    // ---------------- compute waves ----------------
+    const int jw = wbase + 16 * CT * w;          // this wave's first column
+    // State H[:, jw + 16 ct + li] as NT accumulator tiles in P32 order:
+    // Hacc[t][ct][q] = H[32 (t / 2) + 8 lg + 4 (t % 2) + q][jw + 16 ct + li].
+    f32x4 Hacc[NT][CT];
+    auto row0 = [&](int t) { return 32 * (t >> 1) + 8 * lg + 4 * (t & 1); };
+    if constexpr (PHASE == SCAN_TRANS) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    Hacc[t][ct][q] = p.state_in ? p.state_in[((size_t)bh * DK + r0 + q) * DV + j] : 0.f;
-            }
-        }
+                    Hacc[t][ct][q] = (is_phi && row0(t) + q == jw + 16 * ct + li) ? 1.f : 0.f;
+    } else if (p.NG > 1) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                Hacc[t][ct] = *(const f32x4 *)(p.HgT + ((size_t)unit * DV + jw + 16 * ct + li) * DK + row0(t));
+    } else if (p.state_in) {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    Hacc[t][ct][q] = p.state_in[((size_t)bh * DK + row0(t) + q) * DV + jw + 16 * ct + li];
+    } else {
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int t = 0; t < NT; ++t) Hacc[t][ct] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-
-    // Operands are prefetched one chunk ahead in two staggered groups, so only
-    // one copy of each is live: W and Ut for chunk c+1 are requested as soon as
-    // the W H products of chunk c have consumed W(c); Kt and g for chunk c+1 as
-    // soon as the state update of chunk c has consumed Kt(c).
-    frag wf[4][2];      // -W, token tile st, k block kb (this wave's rows)
-    frag kf[4][2];      // Kt, row tile t, token block m
-    quad uq[4][CT];     // Ut quads of token tile st, column tile ct
-    double gC;          // g at the chunk's last token
     double lgam = 0.0;  // sum of gC over the group
-    const bool seed_ut = PHASE == SCAN_STATES || !is_phi;
-    auto fetch_w = [&](int c) {
-        const size_t cidx = (size_t)bh * p.NC + c;
-        const E *Wc = p.W + cidx * (size_t)kChunk * DK + (size_t)w * 4096 + l * 8;
-#pragma unroll
-        for (int st = 0; st < 4; ++st)
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) wf[st][kb] = TR::load8(Wc + (st * 2 + kb) * 512);
-        if (seed_ut) {
-            const E *Uc = p.Ut + cidx * (size_t)DV * kChunk + (size_t)(jbase / 16) * 1024 + l * 4;
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int st = 0; st < 4; ++st) uq[st][ct] = TR::load(Uc + ct * 1024 + st * 256);
-        }
-    };
-    auto fetch_k = [&](int c) {
-        const size_t cidx = (size_t)bh * p.NC + c;
-        const E *Kc = p.Kt + cidx * (size_t)DK * kChunk + (size_t)w * 4096 + l * 8;
-#pragma unroll
-        for (int t = 0; t < 4; ++t)
-#pragma unroll
-            for (int m = 0; m < 2; ++m) kf[t][m] = TR::load8(Kc + (t * 2 + m) * 512);
-        gC = p.g[cidx * kChunk + kChunk - 1];
-    };
 
-    fetch_w(c_begin);
-    fetch_k(c_begin);
-    for (int c = c_begin; c < c_end; ++c) {
-        const size_t cidx = (size_t)bh * p.NC + c;
-        const int cn = min(c + 1, c_end - 1);  // the last prefetch re-reads the last chunk
-        // H_{c-1} rounded to E: B operands over this wave's two 32-row blocks.
-        frag hb[2][CT];
+    // Blocks of 64 chunks: gC of chunk cblk + i sits in lane i of gcl.
+    for (int cblk = c_begin; cblk < c_end; cblk += 64) {
+        const double gcl = (cblk + l < c_end) ? p.gc[(size_t)bh * p.NC + cblk + l] : 0.0;
+        const int cstop = min(c_end, cblk + 64);
+        for (int c = cblk; c < cstop; ++c) {
+            const size_t cidx = (size_t)bh * p.NC + c;
+            const unsigned long long gbits = __builtin_bit_cast(unsigned long long, gcl);
+            const double gC = __builtin_bit_cast(
+                double, ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)(gbits >> 32), c - cblk)
+                         << 32) |
+                            (unsigned)__builtin_amdgcn_readlane((int)gbits, c - cblk));
+            lds_only_barrier();  // chunk c's operands are in its slot
+            const E *sl = slot_of(c);
+            const E *Wl = sl + l * 8;
+            const E *Kl = sl + L::WK + l * 8;
+            const E *Ul = sl + 2 * L::WK + (size_t)w * CT * 1024 + l * 4;
+
+            // All operand fragments of the chunk, read up front so the LDS
+            // latency overlaps the MFMA chain:
+            //   -W fragment (wave kb / 2, token tile st, k block kb % 2),
+            //   Kt fragment (row tile t = 4 v + t', token block m) at (2 t + m).
+            frag wf[KB][4], kf[NT][2];
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
+            for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-            for (int pp = 0; pp < 2; ++pp) {
-                hb[pp][ct] = TR::cat(TR::from_f32(Hacc[2 * pp][ct]), TR::from_f32(Hacc[2 * pp + 1][ct]));
-                if (PHASE == SCAN_STATES)
-                    TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)(jbase + 16 * ct + li) * DK + d0 +
-                                   32 * pp + 8 * lg,
-                               hb[pp][ct]);
-            }
-        // U = Ut - W H accumulated by the MFMAs (the workspace holds -W): wave 0
-        // seeds its accumulators with Ut (zero for Phi columns), wave 1 with
-        // zero, and the two partial sums over their row halves are exchanged.
-        const uint32_t keep = (w == 0 && seed_ut) ? 0xffffffffu : 0u;
-        f32x4 part[4][CT];
+                for (int st = 0; st < 4; ++st)
+                    wf[kb][st] = TR::load8(Wl + (((kb >> 1) * 4 + st) * 2 + (kb & 1)) * 512);
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
-            for (int st = 0; st < 4; ++st)
-                part[st][ct] = TR::mma(wf[st][0], hb[0][ct],
-                                       seed_ut ? TR::to_f32(TR::mask(uq[st][ct], keep))
-                                               : f32x4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int st = 0; st < 4; ++st) part[st][ct] = TR::mma(wf[st][1], hb[1][ct], part[st][ct]);
-        fetch_w(cn);
-        if constexpr (NW > 1) {
-            const int buf = c & 1;
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int st = 0; st < 4; ++st) sP[buf][w][st][ct][l] = part[st][ct];
-            lds_barrier();
+                for (int m = 0; m < 2; ++m) kf[t][m] = TR::load8(Kl + (t * 2 + m) * 512);
+            // U = Ut - W H (the workspace holds -W); the MFMAs start from Ut
+            // (zero for Phi columns).  Token tile st = 2 m + a holds tokens
+            // 32 m + 8 lg + 4 a + q.
+            f32x4 part[4][CT];
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-                for (int st = 0; st < 4; ++st) part[st][ct] += sP[buf][1 - w][st][ct][l];
-        }
-        frag ub[2][CT];
+                for (int st = 0; st < 4; ++st)
+                    part[st][ct] = has_ut ? TR::to_f32(TR::load(Ul + ct * 1024 + st * 256)) : f32x4{0.f, 0.f, 0.f, 0.f};
+            // H_{c-1} rounded to E: B operands over the KB 32-row blocks.
+            frag hb[KB][CT];
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) {
-            ub[0][ct] = TR::cat(TR::from_f32(part[0][ct]), TR::from_f32(part[1][ct]));
-            ub[1][ct] = TR::cat(TR::from_f32(part[2][ct]), TR::from_f32(part[3][ct]));
+            for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+                    hb[kb][ct] = TR::cat(TR::from_f32(Hacc[2 * kb][ct]), TR::from_f32(Hacc[2 * kb + 1][ct]));
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct) part[st][ct] = TR::mma(wf[kb][st], hb[kb][ct], part[st][ct]);
             if (PHASE == SCAN_STATES) {
-                E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)(jbase + 16 * ct + li) * kChunk + 8 * lg;
-                if (NW == 1 || w == 0) TR::store8(Us, ub[0][ct]);
-                if (NW == 1 || w == 1) TR::store8(Us + 32, ub[1][ct]);
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+                    for (int kb = 0; kb < KB; ++kb)
+                        TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)(jw + 16 * ct + li) * DK + 32 * kb + 8 * lg,
+                                   hb[kb][ct]);
+            }
+            frag ub[2][CT];
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                ub[0][ct] = TR::cat(TR::from_f32(part[0][ct]), TR::from_f32(part[1][ct]));
+                ub[1][ct] = TR::cat(TR::from_f32(part[2][ct]), TR::from_f32(part[3][ct]));
+            }
+            lgam += gC;
+            const float gam = expf((float)gC);
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct)
+                        Hacc[t][ct] = TR::mma(kf[t][m], ub[m][ct], m == 0 ? Hacc[t][ct] * gam : Hacc[t][ct]);
+            if (PHASE == SCAN_STATES) {
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
+                    E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)(jw + 16 * ct + li) * kChunk + 8 * lg;
+                    TR::store8(Us, ub[0][ct]);
+                    TR::store8(Us + 32, ub[1][ct]);
+                }
             }
         }
-        lgam += gC;
-        const float gam = expf((float)gC);
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) Hacc[t][ct] = TR::mma(kf[t][0], ub[0][ct], Hacc[t][ct] * gam);
-#pragma unroll
-        for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) Hacc[t][ct] = TR::mma(kf[t][1], ub[1][ct], Hacc[t][ct]);
-        fetch_k(cn);
     }
+    lds_only_barrier();  // the loaders have drained: the ring is free
 
     const size_t gidx = (size_t)bh * p.NG + grp;
     if constexpr (PHASE == SCAN_STATES) {
@@ -490,37 +589,37 @@ void gdn_chunkscan_kernel(Params<E> p) {
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
+                for (int t = 0; t < NT; ++t)
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
-                        p.state_out[((size_t)bh * DK + d0 + 32 * (t >> 1) + 8 * lg + 4 * (t & 1) + q) * DV +
-                                    jbase + 16 * ct + li] = Hacc[t][ct][q];
+                        p.state_out[((size_t)bh * DK + row0(t) + q) * DV + jw + 16 * ct + li] = Hacc[t][ct][q];
         }
     } else if (!is_phi) {  // SCAN_TRANS from here on
         // Psi_g^T [Dv][Dk], fp32
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-            for (int t = 0; t < 4; ++t)
-                *(f32x4 *)(p.PsiT + (gidx * DV + jbase + 16 * ct + li) * DK + d0 + 32 * (t >> 1) + 8 * lg +
-                           4 * (t & 1)) = Hacc[t][ct];
+            for (int t = 0; t < NT; ++t)
+                *(f32x4 *)(p.PsiT + (gidx * DV + jw + 16 * ct + li) * DK + row0(t)) = Hacc[t][ct];
     } else {
-        if (jb == 0 && tid == 0) p.lgam[gidx] = lgam;
-        // N_g = Phi_g - Gamma_g I, rounded to E, staged in LDS as N^T (row e =
-        // state column, token-contiguous rows d) and re-read with the transposing
-        // LDS read into the group scan's A-operand fragments: fragment
-        // (wave v, row tile t, k block kb), lane (li, lg) =
+        if (jb == 0 && w == 0 && l == 0) p.lgam[gidx] = lgam;
+        // N_g = Phi_g - Gamma_g I, rounded to E, staged in LDS (in the ring
+        // memory) as N^T (row e = state column - col0, rows d contiguous) and
+        // re-read with the transposing LDS read into the group scan's A-operand
+        // fragments: fragment (wave v, row tile t, k block kb), lane (li, lg) =
         //   N[64 v + 32 (t / 2) + p32_row(t % 2, li)][32 kb + 8 lg + e].
+        static_assert(WGC % 32 == 0, "the transfer pass writes whole 32-column k blocks");
+        constexpr int LDN = DK + 16 / (int)sizeof(E);
+        static_assert(sizeof(E) * WGC * LDN <= L::bytes, "N^T staging");
         const float Gam = expf((float)lgam);
-        E *sN = (E *)&sP[0][0][0][0][0];
-        lds_barrier();  // every wave is done with the exchange buffer
+        E *sN = ring;
 #pragma unroll
         for (int ct = 0; ct < CT; ++ct) {
-            const int e = 16 * ct + li;  // staging row = state column - col0
+            const int e = 16 * CT * w + 16 * ct + li;  // staging row
 #pragma unroll
-            for (int pp = 0; pp < 2; ++pp) {
-                f32x4 lo = Hacc[2 * pp][ct], hi = Hacc[2 * pp + 1][ct];
-                const int r0 = d0 + 32 * pp + 8 * lg;
+            for (int kb = 0; kb < KB; ++kb) {
+                f32x4 lo = Hacc[2 * kb][ct], hi = Hacc[2 * kb + 1][ct];
+                const int r0 = 32 * kb + 8 * lg;
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     if (r0 + q == col0 + e) lo[q] -= Gam;
@@ -529,13 +628,12 @@ void gdn_chunkscan_kernel(Params<E> p) {
                 TR::store8(sN + e * LDN + r0, TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
             }
         }
-        lds_barrier();
-        static_assert(CT % 2 == 0, "the transfer pass writes whole 32-column k blocks");
+        lds_only_barrier();  // staging written (the loaders take this barrier too)
         const int kb0 = col0 / 32;
-        constexpr int NKB = (16 * CT) / 32;                      // k blocks in this workgroup
+        constexpr int NKB = WGC / 32;                       // k blocks in this workgroup
         constexpr int NFRAG = (DK / 64) * 4 * NKB;
         E *Nf = p.Nf + gidx * (size_t)DK * DK + l * 8;
-        for (int f = w; f < NFRAG; f += NW) {
+        for (int f = w; f < NFRAG; f += NCW) {
             const int v = f / (4 * NKB), t = (f / NKB) % 4, kk = f % NKB;
             const frag nf = tr_frag<E>(sN, LDN, 32 * kk, 64 * v + 32 * (t >> 1), true, t & 1, li, lg);
             TR::store8(Nf + (size_t)((v * 4 + t) * (DK / 32) + kb0 + kk) * 512, nf);

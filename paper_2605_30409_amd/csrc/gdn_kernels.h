@@ -156,11 +156,6 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
         *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
     }
-    // Upper block-triangle of T is zero.
-    for (int idx = tid; idx < kChunk * kChunk; idx += 256) {
-        const int r = idx >> 6, s2 = idx & 63;
-        if ((s2 >> 4) > (r >> 4)) sT[r * L::LDA + s2] = 0.f;
-    }
     lds_barrier();
 
     // A = strict_lower(beta_r e^{g_r - g_s} K K^T): the 10 lower 16x16 blocks.
@@ -245,10 +240,13 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         lds_barrier();
     }
     // A is dead: T diag(beta e^g) and T diag(beta), rounded to E, take its place.
+    // (Only the lower block-triangle of sT was written; the upper blocks of T
+    // are zero.)
     for (int idx = tid; idx < kChunk * kChunk / 8; idx += 256) {
         const int r = idx >> 3, s0 = (idx & 7) * 8;
-        const f32x4 t0v = *(const f32x4 *)(sT + r * L::LDA + s0);
-        const f32x4 t1v = *(const f32x4 *)(sT + r * L::LDA + s0 + 4);
+        const bool upper = (s0 >> 4) > (r >> 4);
+        const f32x4 t0v = upper ? f32x4{0.f, 0.f, 0.f, 0.f} : *(const f32x4 *)(sT + r * L::LDA + s0);
+        const f32x4 t1v = upper ? f32x4{0.f, 0.f, 0.f, 0.f} : *(const f32x4 *)(sT + r * L::LDA + s0 + 4);
         f32x4 w0, w1, u0, u1;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {

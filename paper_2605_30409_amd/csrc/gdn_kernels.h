@@ -750,6 +750,10 @@ __global__ __launch_bounds__(256) void gdn_output_kernel(Params<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
     using quad = typename TR::quad;
+    constexpr int VE = 16 / (int)sizeof(E);            // elements per 16-byte vector
+    constexpr int NH = DV * DK / VE / 256;             // H^T vectors per thread
+    constexpr int NU = DV * kChunk / VE / 256;         // U^T vectors per thread
+    constexpr int NK = kChunk * DK / VE / 256;         // K vectors per thread
     extern __shared__ __align__(16) unsigned char smem[];
     E *sH = (E *)(smem + L::oH);
     E *sU = (E *)(smem + L::oU);
@@ -765,22 +769,43 @@ __global__ __launch_bounds__(256) void gdn_output_kernel(Params<E> p) {
     const size_t row0 = ((size_t)b * p.T + t0) * p.H + h;
     const size_t rstride = (size_t)p.H;
 
-    stage_rows<E, DK, 256>(sH, L::LDH, p.Hs + cidx * (size_t)DV * DK, DK, DV, DV, tid);
-    stage_rows<E, kChunk, 256>(sU, L::LDU, p.Us + cidx * (size_t)DV * kChunk, kChunk, DV, DV, tid);
-    stage_rows<E, DK, 256>(sK, L::LDK, p.k + row0 * DK, rstride * DK, kChunk, nvalid, tid);
-    if (tid < kChunk) sg[tid] = p.g[cidx * kChunk + tid];
-
-    // Q rows of this wave's tokens as B operands (B[k=d][n=r] = Q[r][d]); padded tokens are 0.
+    // Every global load is issued before the first LDS store, so their
+    // latencies overlap: Q rows of this wave's tokens as B operands
+    // (B[k=d][n=r] = Q[r][d]; padded tokens are 0), then H^T, U^T and K
+    // rows with 16-byte coalesced loads.
     const int r = 16 * w + li;  // token within the chunk
     const bool rvalid = r < nvalid;
     frag qf[DK / 32];
 #pragma unroll
-    for (int kb = 0; kb < DK / 32; ++kb) {
-        if (rvalid) {
-            qf[kb] = load_frag<E>(p.q + (row0 + r * rstride) * DK + 32 * kb, lg);
-        } else {
-            qf[kb] = TR::cat(TR::zero(), TR::zero());
-        }
+    for (int kb = 0; kb < DK / 32; ++kb)
+        qf[kb] = rvalid ? load_frag<E>(p.q + (row0 + r * rstride) * DK + 32 * kb, lg) : TR::cat(TR::zero(), TR::zero());
+    uint4 hreg[NH], ureg[NU], kreg[NK];
+    const E *Hs = p.Hs + cidx * (size_t)DV * DK;
+    const E *Us = p.Us + cidx * (size_t)DV * kChunk;
+#pragma unroll
+    for (int n = 0; n < NH; ++n) hreg[n] = *(const uint4 *)(Hs + (size_t)(tid + 256 * n) * VE);
+#pragma unroll
+    for (int n = 0; n < NU; ++n) ureg[n] = *(const uint4 *)(Us + (size_t)(tid + 256 * n) * VE);
+#pragma unroll
+    for (int n = 0; n < NK; ++n) {
+        const int idx = tid + 256 * n, kr = idx / (DK / VE), kc = idx % (DK / VE);
+        kreg[n] = kr < nvalid ? *(const uint4 *)(p.k + (row0 + kr * rstride) * DK + kc * VE) : make_uint4(0u, 0u, 0u, 0u);
+    }
+    if (tid < kChunk) sg[tid] = p.g[cidx * kChunk + tid];
+#pragma unroll
+    for (int n = 0; n < NH; ++n) {
+        const int idx = tid + 256 * n;
+        *(uint4 *)(sH + (idx / (DK / VE)) * L::LDH + (idx % (DK / VE)) * VE) = hreg[n];
+    }
+#pragma unroll
+    for (int n = 0; n < NU; ++n) {
+        const int idx = tid + 256 * n;
+        *(uint4 *)(sU + (idx / (kChunk / VE)) * L::LDU + (idx % (kChunk / VE)) * VE) = ureg[n];
+    }
+#pragma unroll
+    for (int n = 0; n < NK; ++n) {
+        const int idx = tid + 256 * n;
+        *(uint4 *)(sK + (idx / (DK / VE)) * L::LDK + (idx % (DK / VE)) * VE) = kreg[n];
     }
     lds_barrier();
 
@@ -810,17 +835,27 @@ __global__ __launch_bounds__(256) void gdn_output_kernel(Params<E> p) {
     const frag pf1 = TR::cat(pq[2], pq[3]);
     const float er = expf((float)gr);
 
+    // O^T = H^T Q^T e^{g_r} + U^T P^T in 32-column blocks J; the two tiles a of
+    // a block take A rows (output columns) 32 J + p32_row(a, i), so lane
+    // (li, lg) ends up with the 8 consecutive columns 32 J + 8 lg + [0, 8) of
+    // token r and writes them with one 16-byte store.
     E *orow = p.out + (row0 + r * rstride) * DV;
 #pragma unroll 2
-    for (int jt = 0; jt < DV / 16; ++jt) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int J = 0; J < DV / 32; ++J) {
+        f32x4 acc[2];
 #pragma unroll
-        for (int kb = 0; kb < DK / 32; ++kb)
-            acc = TR::mma(load_frag<E>(sH + (16 * jt + li) * L::LDH + 32 * kb, lg), qf[kb], acc);
-        acc *= er;
-        acc = TR::mma(load_frag<E>(sU + (16 * jt + li) * L::LDU, lg), pf0, acc);
-        if (w >= 2) acc = TR::mma(load_frag<E>(sU + (16 * jt + li) * L::LDU + 32, lg), pf1, acc);
-        if (rvalid) TR::store(orow + 16 * jt + 4 * lg, TR::from_f32(acc));
+        for (int a = 0; a < 2; ++a) {
+            const int col = 32 * J + p32_row(a, li);
+            f32x4 x = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < DK / 32; ++kb)
+                x = TR::mma(load_frag<E>(sH + col * L::LDH + 32 * kb, lg), qf[kb], x);
+            x *= er;
+            x = TR::mma(load_frag<E>(sU + col * L::LDU, lg), pf0, x);
+            if (w >= 2) x = TR::mma(load_frag<E>(sU + col * L::LDU + 32, lg), pf1, x);
+            acc[a] = x;
+        }
+        if (rvalid) TR::store8(orow + 32 * J + 8 * lg, TR::cat(TR::from_f32(acc[0]), TR::from_f32(acc[1])));
     }
 }
 

@@ -98,9 +98,9 @@ def cpu_baseline(inp, B, T, min_seconds=10.0):
                       f"fp64 token recurrence, {elapsed:.1f} s"}
 
 
-def load_traffic(kernel):
-    """HBM traffic per launch for `kernel` from the committed counter summary, or None
-    when the summary is missing or was taken on different kernel source."""
+def load_traffic(stage):
+    """HBM traffic per launch of `stage`'s kernel from the committed counter summary,
+    or None when the summary is missing or was taken on different kernel source."""
     path = os.path.join(ROOT, "profiles", "traffic_frame1280x704.json")
     if not os.path.exists(path):
         return None
@@ -112,7 +112,7 @@ def load_traffic(kernel):
             h.update(open(os.path.join(ROOT, f), "rb").read())
         if h.hexdigest() != rec["source_sha256"]:
             return None
-        k = rec["kernels"].get(kernel)
+        k = rec["stages"].get(stage)
         return None if k is None else float(k["hbm_bytes_per_launch"])
     except Exception:
         return None
@@ -207,7 +207,7 @@ def main():
     tflops = sum(cnt["flops"].values()) / sec / 1e12
     dom = max(names, key=names.get)
     roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
-    roofline.update({"traffic": load_traffic(KERNELS[dom]), "kernel": KERNELS[dom],
+    roofline.update({"traffic": load_traffic(dom), "kernel": KERNELS[dom],
                      "duration_ms": round(names[dom], 5),
                      "algorithmic_flops_per_launch": cnt["flops"][dom],
                      "algorithmic_bytes_per_launch": cnt["bytes"][dom]})

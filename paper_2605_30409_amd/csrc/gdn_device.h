@@ -158,19 +158,4 @@ __device__ __forceinline__ f32x4 mma_f32_k4(float a, float b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// Copy `rows` rows of COLS elements (global row stride g_stride) into LDS
-// (row stride l_stride) with 16-byte accesses; rows >= valid become zero.
-template <class E, int COLS, int NT>
-__device__ __forceinline__ void stage_rows(E *dst, int l_stride, const E *src, size_t g_stride,
-                                           int rows, int valid, int tid) {
-    constexpr int VE = 16 / (int)sizeof(E);
-    constexpr int VPR = COLS / VE;
-    for (int idx = tid; idx < rows * VPR; idx += NT) {
-        const int r = idx / VPR, cv = idx - r * VPR;
-        uint4 val = make_uint4(0u, 0u, 0u, 0u);
-        if (r < valid) val = *(const uint4 *)(src + (size_t)r * g_stride + cv * VE);
-        *(uint4 *)(dst + r * l_stride + cv * VE) = val;
-    }
-}
-
 }  // namespace gdn

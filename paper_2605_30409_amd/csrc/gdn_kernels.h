@@ -1,4 +1,4 @@
-// The three gfx950 kernels of the GDN chunk forward.
+// The gfx950 kernels of the GDN chunk forward.
 //
 // Notation (per batch b, head h; state H = S^T of shape [Dk][Dv]).  Inside a
 // chunk of C = 64 tokens r = 0..63 with entry state H_0:

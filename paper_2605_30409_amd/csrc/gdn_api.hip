@@ -136,11 +136,24 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
     p.Ut = (E *)(base + L.Ut);
     p.Hs = (E *)(base + L.Hs);
     p.Us = (E *)(base + L.Us);
+    // The output is fused into the scan on the bf16 path with one scan group;
+    // its Q and P fragments then live in the (unused) Hs and Us regions.
+    p.fused = (sizeof(E) == 2 && p.NG == 1) ? 1 : 0;
+    p.Qf = p.Hs;
+    p.Pf = p.Us;
     p.Nf = (E *)(base + L.Nf);
     p.PsiT = (float *)(base + L.PsiT);
     p.lgam = (double *)(base + L.lgam);
     p.HgT = (float *)(base + L.HgT);
     return p;
+}
+
+// The scan kernel with the output fused (bf16 only; nullptr for fp32).
+template <class E, int DK, int DV> const void *fused_scan_fn() {
+    if constexpr (sizeof(E) == 2)
+        return (const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1, true>;
+    else
+        return nullptr;
 }
 
 constexpr int kStages = 5;  // WY transform, group transfers, group scan, chunk states, output
@@ -159,7 +172,8 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
     constexpr int NCW = gdn::kScanNCW;
     using LT = gdn::ScanLds<E, DK, CT, NCW>;  // grouped passes
     using L1 = gdn::ScanLds<E, DK, 1, 1>;     // single-group scan
-    constexpr unsigned scan_threads = (NCW + 2) * 64, scan_threads1 = 3 * 64;
+    using LF = gdn::ScanLds<E, DK, 1, 1, sizeof(E) == 2>;  // single-group scan with the output fused
+    constexpr unsigned scan_threads = (NCW + 2) * 64, scan_threads1 = 3 * 64, scan_threadsF = 4 * 64;
     static std::once_flag attr_once;
     static hipError_t attr_err = hipSuccess;
     const size_t lds1 = gdn::WyLds<E, DK, DV>::bytes;
@@ -174,8 +188,10 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
             {(const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT, NCW>, LT::bytes},
             {(const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT, NCW>, LT::bytes},
             {(const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1>, L1::bytes},
+            {fused_scan_fn<E, DK, DV>(), LF::bytes},
         };
         for (const auto &d : dyn) {
+            if (!d.fn) continue;
             const hipError_t e =
                 hipFuncSetAttribute(d.fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)d.bytes);
             if (e != hipSuccess && attr_err == hipSuccess) attr_err = e;
@@ -204,6 +220,12 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
                 hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT, NCW>),
                                    dim3(groups(DV / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads),
                                    LT::bytes, s, p);
+            } else if (p.fused) {
+                // one sequential scan per (b, h), one column tile per workgroup,
+                // which also computes the output of its columns
+                if constexpr (sizeof(E) == 2)
+                    hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1, true>),
+                                       dim3(groups(DV / 16, BH)), dim3(scan_threadsF), LF::bytes, s, p);
             } else {
                 // one sequential scan per (b, h): one column tile per compute wave
                 hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1>),
@@ -216,7 +238,7 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
     };
     hipError_t er = hipSuccess;
     for (int i = 0; i < kStages && er == hipSuccess; ++i) {
-        const bool runs = (i != 1 && i != 2) || p.NG > 1;
+        const bool runs = (i == 1 || i == 2) ? p.NG > 1 : (i == 4 ? !p.fused : true);
         if (tm) tm->ran[i] = runs;
         if (!runs) continue;
         if (!tm) {

@@ -50,6 +50,11 @@ template <class E> struct Params {
     double *g;
     double *gc;       // per (b*H + h, chunk): g at the chunk's last token
     E *W, *Kt, *Ut, *Hs, *Us;
+    // Fused output (bf16, one scan group): the scan computes the output, from
+    // Qf = diag(e^g) Q and Pf = (Q K^T o M) row fragments written by the WY
+    // kernel (they reuse the Hs / Us workspace regions, which are then unused).
+    int fused;
+    E *Qf, *Pf;
     E *Nf;            // per (b*H + h, group): N_g = Phi_g - Gamma_g I, fragment-major
     float *PsiT;      // per (b*H + h, group): Psi_g^T [Dv][Dk]
     double *lgam;     // per (b*H + h, group): log Gamma_g
@@ -122,6 +127,18 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         vreg[n] = make_uint4(0u, 0u, 0u, 0u);
         if (r < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + r * rstride) * DV + cv * VE);
     }
+    // Fused output: Q rows of this wave's 16 tokens as row fragments
+    // (Q[r][32 kb + 8 lg + e], r = 16 w + li; padded tokens are 0).
+    const int rq = 16 * w + li;
+    frag qf[DK / 32];
+    if constexpr (sizeof(E) == 2) {
+        if (p.fused) {
+#pragma unroll
+            for (int kb = 0; kb < DK / 32; ++kb)
+                qf[kb] = rq < nvalid ? load_frag<E>(p.q + (row0 + rq * rstride) * DK + 32 * kb, lg)
+                                     : TR::cat(TR::zero(), TR::zero());
+        }
+    }
     // Gates: wave-wide inclusive prefix sum of clamped log alpha in fp64
     // (padding tokens: alpha = 1, beta = 0).
     if (w == 0) {
@@ -157,6 +174,45 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
     }
     lds_barrier();
+
+    // Fused output: wave w writes, for its token tile rt = w,
+    //   Qf[rt][kb][lane][e] = e^{g_r} Q[r][32 kb + 8 lg + e]
+    //   Pf[rt][m][lane][e]  = e^{g_r - g_s} q_r . k_s (s <= r, else 0), s = 32 m + 8 lg + e,
+    // the row fragments (B operands over d, resp. s) of the fused output.  P^T
+    // tiles take their s rows in P32 order, so a tile pair is one fragment;
+    // block m = 1 only matters for r >= 32.
+    if constexpr (sizeof(E) == 2) {
+        if (p.fused) {
+            const double gr = sg[rq];
+            const float er = expf((float)gr);
+            E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
+#pragma unroll
+            for (int kb = 0; kb < DK / 32; ++kb) {
+                const f32x4 lo = TR::to_f32(TR::lo(qf[kb])) * er, hi = TR::to_f32(TR::hi(qf[kb])) * er;
+                TR::store8(Qf + (size_t)(w * (DK / 32) + kb) * 512, TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
+            }
+            E *Pf = p.Pf + cidx * (size_t)kChunk * kChunk + l * 8;
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+                if (m == 1 && w < 2) break;
+                typename TR::quad pq[2];
+#pragma unroll
+                for (int a = 0; a < 2; ++a) {
+                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int kb = 0; kb < DK / 32; ++kb)
+                        acc = TR::mma(load_frag<E>(sK + (32 * m + p32_row(a, li)) * L::LDK + 32 * kb, lg), qf[kb], acc);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int s2 = 32 * m + 8 * lg + 4 * a + q;
+                        acc[q] = (s2 <= rq) ? __builtin_amdgcn_exp2f((float)((gr - sg[s2]) * kLog2e)) * acc[q] : 0.f;
+                    }
+                    pq[a] = TR::from_f32(acc);
+                }
+                TR::store8(Pf + (size_t)(w * 2 + m) * 512, TR::cat(pq[0], pq[1]));
+            }
+        }
+    }
 
     // A = strict_lower(beta_r e^{g_r - g_s} K K^T): the 10 lower 16x16 blocks.
     for (int t = w; t < 10; t += 4) {
@@ -336,7 +392,7 @@ enum { SCAN_TRANS = 0, SCAN_STATES = 1 };
 template <class E> struct ScanCT { static constexpr int value = sizeof(E) == 2 ? 2 : 1; };
 constexpr int kScanNCW = 2;
 
-template <class E, int DK, int CT, int NCW> struct ScanLds {
+template <class E, int DK, int CT, int NCW, bool FUSE = false> struct ScanLds {
     static constexpr int KB = DK / 32;                     // 32-row blocks of the state
     static constexpr int NT = DK / 16;                     // 16-row tiles of the state
     static constexpr int WK = kChunk * DK;                 // elements of -W (and of Kt) per chunk
@@ -349,11 +405,16 @@ template <class E, int DK, int CT, int NCW> struct ScanLds {
     static constexpr int NC_U0 = NC_U / 2, NC_U1 = NC_U - NC_U0;
     static constexpr int NCOPY0 = NC_W + NC_U0, NCOPY1 = NC_W + NC_U1;
     static constexpr int LDS_CAP = 152 * 1024;
-    static constexpr int DL = LDS_CAP / SLOT_BYTES;
+    // fused output: H_{c-1} (KB fragments) and U (2) per column tile handed
+    // from each compute wave to its output wave, double-buffered
+    static constexpr int HOFF_FRAGS = CT * (KB + 2);
+    static constexpr int HOFF_BYTES = FUSE ? 2 * NCW * HOFF_FRAGS * 64 * (int)sizeof(typename Tr<E>::frag) : 0;
+    static constexpr int DL = (LDS_CAP - HOFF_BYTES) / SLOT_BYTES;
     // the loader waits with D - 2 younger chunks in flight: vmcnt <= 63
     static constexpr int DV_ = 2 + 63 / (NCOPY0 > NCOPY1 ? NCOPY0 : NCOPY1);
     static constexpr int DEPTH = (DL < 4 ? DL : 4) < DV_ ? (DL < 4 ? DL : 4) : DV_;
-    static constexpr size_t bytes = (size_t)DEPTH * SLOT_BYTES;
+    static constexpr size_t oHOFF = (size_t)DEPTH * SLOT_BYTES;
+    static constexpr size_t bytes = oHOFF + HOFF_BYTES;
     static_assert(DEPTH >= 2, "scan ring needs two slots");
     static_assert((WK * sizeof(E)) % 1024 == 0 && (UT * sizeof(E)) % 2048 == 0, "whole 1 KB copies");
 };
@@ -380,12 +441,14 @@ template <int N> __device__ __forceinline__ void copy_kb(const void *src, void *
                                          16, 0, 0);
 }
 
-template <class E, int DK, int DV, int PHASE, int CT, int NCW>
-__global__ __launch_bounds__((NCW + 2) * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <class E, int DK, int DV, int PHASE, int CT, int NCW, bool FUSE = false>
+__global__ __launch_bounds__((NCW * (FUSE ? 2 : 1) + 2) * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gdn_chunkscan_kernel(Params<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
-    using L = ScanLds<E, DK, CT, NCW>;
+    using L = ScanLds<E, DK, CT, NCW, FUSE>;
+    static_assert(!FUSE || PHASE == SCAN_STATES, "the output is fused into the state pass only");
+    constexpr int NOW = FUSE ? NCW : 0;                  // output waves
     constexpr int D = L::DEPTH;
     constexpr int KB = L::KB, NT = L::NT;
     constexpr int WGC = NCW * 16 * CT;                   // columns per workgroup
@@ -414,9 +477,15 @@ void gdn_chunkscan_kernel(Params<E> p) {
     const bool has_ut = PHASE == SCAN_STATES || !is_phi;
     auto slot_of = [&](int c) { return ring + (size_t)((c - c_begin) % D) * L::SLOT; };
 
-    if (w >= NCW) {
+    // fused output hand-off: buffer i, compute wave wc, fragment f of column tile ct
+    frag *hoff = (frag *)(scan_lds + L::oHOFF);
+    auto hoff_at = [&](int i, int wc, int ct, int f) {
+        return hoff + ((size_t)((i * NCW + wc) * CT + ct) * (KB + 2) + f) * 64 + l;
+    };
+
+    if (w >= NCW + NOW) {
         // ---------------- loader waves ----------------
-        const int ld = w - NCW;
+        const int ld = w - NCW - NOW;
         auto issue = [&](int c) {
             const size_t cidx = (size_t)bh * p.NC + c;
             E *sl = slot_of(c);
@@ -455,6 +524,80 @@ void gdn_chunkscan_kernel(Params<E> p) {
         lds_only_barrier();                     // ring quiet: the compute waves may reuse it
         if (PHASE == SCAN_TRANS && is_phi) lds_only_barrier();  // matches the N staging barrier
         return;
+    }
+
+    if constexpr (FUSE) {
+        if (w >= NCW) {
+            // ---------------- output waves ----------------
+            // Output wave wo finishes chunk c - 1 after barrier c (and the
+            // last chunk after the final barrier) for the columns of compute
+            // wave wo:  O^T = H_{c-1}^T Qf^T + U^T Pf^T, per token tile rt
+            //   A operands: the handed-off H_{c-1} and U fragments (B-operand
+            //   layout over d, resp. s, which is also the A layout),
+            //   B operands: the Qf / Pf row fragments of the chunk.
+            // Lane (li, lg) gets O[16 rt + li][jw + 16 ct + 4 lg + q].
+            const int wo = w - NCW;
+            const int jw = wbase + 16 * CT * wo;
+            const int b = bh / p.H, h = bh - b * p.H;
+            // Operands of chunk c live in register set (c - c_begin) & 1: at
+            // barrier c the wave requests chunk c's and finishes chunk c - 1
+            // from the other set, so a load is consumed one chunk later.
+            frag q0[4][KB], p0[4][2], q1[4][KB], p1[4][2];
+            auto load_ops = [&](int c, frag (&q)[4][KB], frag (&pf)[4][2]) {
+                const size_t cidx = (size_t)bh * p.NC + c;
+                const E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
+                const E *Pf = p.Pf + cidx * (size_t)kChunk * kChunk + l * 8;
+#pragma unroll
+                for (int rt = 0; rt < 4; ++rt) {
+#pragma unroll
+                    for (int kb = 0; kb < KB; ++kb) q[rt][kb] = TR::load8(Qf + (size_t)(rt * KB + kb) * 512);
+#pragma unroll
+                    for (int m = 0; m < 2; ++m)
+                        if (m == 0 || rt >= 2) pf[rt][m] = TR::load8(Pf + (size_t)(rt * 2 + m) * 512);
+                }
+            };
+            auto finish = [&](int c, const frag (&cq)[4][KB], const frag (&cp)[4][2]) {
+                const int i = (c - c_begin) & 1;
+                const int nvalid = min(kChunk, p.T - c * kChunk);
+                const size_t row0 = ((size_t)b * p.T + (size_t)c * kChunk) * p.H + h;
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
+                    frag hbf[KB], ubf[2];
+#pragma unroll
+                    for (int f = 0; f < KB; ++f) hbf[f] = *hoff_at(i, wo, ct, f);
+#pragma unroll
+                    for (int m = 0; m < 2; ++m) ubf[m] = *hoff_at(i, wo, ct, KB + m);
+#pragma unroll
+                    for (int rt = 0; rt < 4; ++rt) {
+                        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int kb = 0; kb < KB; ++kb) acc = TR::mma(hbf[kb], cq[rt][kb], acc);
+#pragma unroll
+                        for (int m = 0; m < 2; ++m)
+                            if (m == 0 || rt >= 2) acc = TR::mma(ubf[m], cp[rt][m], acc);
+                        const int r = 16 * rt + li;
+                        if (r < nvalid)
+                            TR::store(p.out + (row0 + (size_t)r * p.H) * DV + jw + 16 * ct + 4 * lg, TR::from_f32(acc));
+                    }
+                }
+            };
+            for (int c = c_begin; c < c_end; c += 2) {
+                lds_only_barrier();  // barrier c
+                load_ops(c, q0, p0);
+                if (c > c_begin) finish(c - 1, q1, p1);
+                if (c + 1 < c_end) {
+                    lds_only_barrier();  // barrier c + 1
+                    load_ops(c + 1, q1, p1);
+                    finish(c, q0, p0);
+                }
+            }
+            lds_only_barrier();  // the compute waves have handed off the last chunk
+            if ((c_end - 1 - c_begin) & 1)
+                finish(c_end - 1, q1, p1);
+            else
+                finish(c_end - 1, q0, p0);
+            return;
+        }
     }
 
     // ---------------- compute waves ----------------
@@ -511,28 +654,34 @@ void gdn_chunkscan_kernel(Params<E> p) {
             const E *Ul = sl + 2 * L::WK + (size_t)w * CT * 1024 + l * 4;
 
             // All operand fragments of the chunk, read up front so the LDS
-            // latency overlaps the MFMA chain:
+            // latency overlaps the MFMA chain (the U~t seeds first: the first
+            // MFMAs need them):
             //   -W fragment (wave kb / 2, token tile st, k block kb % 2),
             //   Kt fragment (row tile t = 4 v + t', token block m) at (2 t + m).
-            frag wf[KB][4], kf[NT][2];
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                for (int st = 0; st < 4; ++st)
-                    wf[kb][st] = TR::load8(Wl + (((kb >> 1) * 4 + st) * 2 + (kb & 1)) * 512);
-#pragma unroll
-            for (int t = 0; t < NT; ++t)
-#pragma unroll
-                for (int m = 0; m < 2; ++m) kf[t][m] = TR::load8(Kl + (t * 2 + m) * 512);
-            // U = Ut - W H (the workspace holds -W); the MFMAs start from Ut
-            // (zero for Phi columns).  Token tile st = 2 m + a holds tokens
-            // 32 m + 8 lg + 4 a + q.
+            // U = U~t - W H (the workspace holds -W): token tile st = 2 m + a
+            // holds tokens 32 m + 8 lg + 4 a + q; the MFMAs start from U~t
+            // (zero for Phi columns).
             f32x4 part[4][CT];
 #pragma unroll
             for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
                 for (int st = 0; st < 4; ++st)
                     part[st][ct] = has_ut ? TR::to_f32(TR::load(Ul + ct * 1024 + st * 256)) : f32x4{0.f, 0.f, 0.f, 0.f};
+            frag wf[KB][4], kf[NT][2];
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) {
+                        const int st = 2 * m + a;
+                        wf[kb][st] = TR::load8(Wl + (((kb >> 1) * 4 + st) * 2 + (kb & 1)) * 512);
+                    }
+#pragma unroll
+            for (int m = 0; m < 2; ++m)
+#pragma unroll
+                for (int t = 0; t < NT; ++t) kf[t][m] = TR::load8(Kl + (t * 2 + m) * 512);
+
             // H_{c-1} rounded to E: B operands over the KB 32-row blocks.
             frag hb[KB][CT];
 #pragma unroll
@@ -540,38 +689,61 @@ void gdn_chunkscan_kernel(Params<E> p) {
 #pragma unroll
                 for (int kb = 0; kb < KB; ++kb)
                     hb[kb][ct] = TR::cat(TR::from_f32(Hacc[2 * kb][ct]), TR::from_f32(Hacc[2 * kb + 1][ct]));
+            // The chain per token half m: its W H MFMAs, the conversion of its
+            // U half, then that half's Kt^T U update.  Half 0 is finished
+            // first, so its conversion and the decay of H overlap the MFMAs
+            // of half 1, and half 1's conversion those of the first update.
+            frag ub[2][CT];
+            auto wh_half = [&](int m) {
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
+                for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-                for (int st = 0; st < 4; ++st)
+                    for (int a = 0; a < 2; ++a)
 #pragma unroll
-                    for (int ct = 0; ct < CT; ++ct) part[st][ct] = TR::mma(wf[kb][st], hb[kb][ct], part[st][ct]);
-            if (PHASE == SCAN_STATES) {
+                        for (int ct = 0; ct < CT; ++ct)
+                            part[2 * m + a][ct] = TR::mma(wf[kb][2 * m + a], hb[kb][ct], part[2 * m + a][ct]);
+            };
+            auto cvt_half = [&](int m) {
 #pragma unroll
                 for (int ct = 0; ct < CT; ++ct)
+                    ub[m][ct] = TR::cat(TR::from_f32(part[2 * m][ct]), TR::from_f32(part[2 * m + 1][ct]));
+            };
+            auto kt_half = [&](int m) {
+#pragma unroll
+                for (int t = 0; t < NT; ++t)
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct) Hacc[t][ct] = TR::mma(kf[t][m], ub[m][ct], Hacc[t][ct]);
+            };
+            wh_half(0);
+            wh_half(1);
+            cvt_half(0);
+            lgam += gC;
+            const float gam = expf((float)gC);
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) Hacc[t][ct] *= gam;
+            kt_half(0);
+            cvt_half(1);
+            kt_half(1);
+            if constexpr (FUSE) {
+                // hand H_{c-1} and U to the output wave (it reads them after
+                // the next barrier; the buffers alternate per chunk)
+                const int i = (c - c_begin) & 1;
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
+#pragma unroll
+                    for (int kb = 0; kb < KB; ++kb) *hoff_at(i, w, ct, kb) = hb[kb][ct];
+                    *hoff_at(i, w, ct, KB) = ub[0][ct];
+                    *hoff_at(i, w, ct, KB + 1) = ub[1][ct];
+                }
+            } else if (PHASE == SCAN_STATES) {
+#pragma unroll
+                for (int ct = 0; ct < CT; ++ct) {
 #pragma unroll
                     for (int kb = 0; kb < KB; ++kb)
                         TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)(jw + 16 * ct + li) * DK + 32 * kb + 8 * lg,
                                    hb[kb][ct]);
-            }
-            frag ub[2][CT];
-#pragma unroll
-            for (int ct = 0; ct < CT; ++ct) {
-                ub[0][ct] = TR::cat(TR::from_f32(part[0][ct]), TR::from_f32(part[1][ct]));
-                ub[1][ct] = TR::cat(TR::from_f32(part[2][ct]), TR::from_f32(part[3][ct]));
-            }
-            lgam += gC;
-            const float gam = expf((float)gC);
-#pragma unroll
-            for (int m = 0; m < 2; ++m)
-#pragma unroll
-                for (int t = 0; t < NT; ++t)
-#pragma unroll
-                    for (int ct = 0; ct < CT; ++ct)
-                        Hacc[t][ct] = TR::mma(kf[t][m], ub[m][ct], m == 0 ? Hacc[t][ct] * gam : Hacc[t][ct]);
-            if (PHASE == SCAN_STATES) {
-#pragma unroll
-                for (int ct = 0; ct < CT; ++ct) {
                     E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)(jw + 16 * ct + li) * kChunk + 8 * lg;
                     TR::store8(Us, ub[0][ct]);
                     TR::store8(Us + 32, ub[1][ct]);

@@ -66,21 +66,35 @@ constexpr float kLogAlphaMin = -87.3f;  // ~ log(FLT_MIN): alpha below this acts
 // --------------------------------------------------------------------------
 // Stage 1: per-chunk WY / UT transform.  Grid (NC, B*H), 256 threads.
 // --------------------------------------------------------------------------
+// LDS: K rows, A (fp32; V rows take its place once the solve is done), T
+// (fp32), gates.  52.5 KB on the bf16 path at D = 128: three workgroups per CU.
 template <class E, int DK, int DV> struct WyLds {
     static constexpr int PAD = 16 / (int)sizeof(E);
     static constexpr int LDK = DK + PAD;      // K, row-major (token rows)
     static constexpr int LDV = DV + PAD;      // V, row-major
     static constexpr int LDA = kChunk + 4;    // A and T (fp32)
-    static constexpr int LDB = kChunk + PAD;  // T diag(beta e^g) and T diag(beta) (E)
     static constexpr size_t szA = 4 * kChunk * LDA;
-    static constexpr size_t szB = 2 * sizeof(E) * kChunk * LDB;
+    static constexpr size_t szV = sizeof(E) * kChunk * LDV;
     static constexpr size_t oK = 0;
-    static constexpr size_t oV = oK + sizeof(E) * kChunk * LDK;
-    static constexpr size_t oA = oV + sizeof(E) * kChunk * LDV;  // A, then the scaled T pair
-    static constexpr size_t oT = oA + (szA > szB ? szA : szB);
+    static constexpr size_t oA = oK + sizeof(E) * kChunk * LDK;  // A, then V
+    static constexpr size_t oT = oA + (szA > szV ? szA : szV);
     static constexpr size_t oG = oT + szA;
-    static constexpr size_t bytes = oG + 8 * kChunk + 4 * 3 * kChunk;
+    static constexpr size_t bytes = oG + 8 * kChunk + 4 * 4 * kChunk;
 };
+
+// Decay ratio e^{g_r - g_s} (s <= r) inside the WY kernel.  The fp32 path
+// takes the difference of the fp64 cumulative sums (full precision even when
+// the decay over a chunk is huge); the bf16 path takes it from fp32 copies of
+// g * log2(e), whose rounding (at most ~1e-3 relative to the ratio when
+// |g| ~ 5600, the extreme of a chunk of alpha ~ 0) is far below bf16's.
+template <class E>
+__device__ __forceinline__ float wy_decay(const double *sg, const float *sgl, int r, int s) {
+    constexpr double kLog2e = 1.4426950408889634;
+    if constexpr (sizeof(E) == 2)
+        return __builtin_amdgcn_exp2f(sgl[r] - sgl[s]);
+    else
+        return __builtin_amdgcn_exp2f((float)((sg[r] - sg[s]) * kLog2e));
+}
 
 template <class E, int DK, int DV>
 __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
@@ -94,15 +108,14 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     constexpr double kLog2e = 1.4426950408889634;
     extern __shared__ __align__(16) unsigned char smem[];
     E *sK = (E *)(smem + L::oK);
-    E *sV = (E *)(smem + L::oV);
     float *sA = (float *)(smem + L::oA);
-    E *sTw = (E *)(smem + L::oA);                 // T diag(beta e^g), once A is dead
-    E *sTu = sTw + kChunk * L::LDB;               // T diag(beta)
+    E *sV = (E *)(smem + L::oA);                  // V rows, once A is dead
     float *sT = (float *)(smem + L::oT);
     double *sg = (double *)(smem + L::oG);        // g_r
     float *sb = (float *)(sg + kChunk);           // beta_r
     float *sw = sb + kChunk;                      // beta_r e^{g_r}
     float *sd = sw + kChunk;                      // e^{g_C - g_r}
+    float *sgl = sd + kChunk;                     // g_r log2(e) in fp32 (bf16 path)
 
     const int c = blockIdx.x, bh = blockIdx.y;
     const int b = bh / p.H, h = bh - b * p.H;
@@ -113,7 +126,13 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     const size_t row0 = ((size_t)b * p.T + t0) * p.H + h;  // token-row index of token t0
     const size_t rstride = (size_t)p.H;                    // token-row stride
 
-    // K and V rows, 16-byte coalesced loads (padding rows are zero).
+    // Gates first (they head the dependency chain), then K and V rows with
+    // 16-byte coalesced loads (padding rows are zero).
+    float ga = 1.f, gbe = 0.f;  // alpha, beta of token l (wave 0; padding: 1, 0)
+    if (w == 0 && l < nvalid) {
+        ga = p.alpha[row0 + l * rstride];
+        gbe = p.beta[row0 + l * rstride];
+    }
     uint4 kreg[NKV], vreg[NVV];
 #pragma unroll
     for (int n = 0; n < NKV; ++n) {
@@ -142,12 +161,8 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     // Gates: wave-wide inclusive prefix sum of clamped log alpha in fp64
     // (padding tokens: alpha = 1, beta = 0).
     if (w == 0) {
-        float a = 1.f, be = 0.f;
-        if (l < nvalid) {
-            a = p.alpha[row0 + l * rstride];
-            be = p.beta[row0 + l * rstride];
-        }
-        float la = logf(a);
+        const float be = gbe;
+        float la = logf(ga);
         la = (la < kLogAlphaMin) ? kLogAlphaMin : la;  // keeps NaN
         double g = (double)la;
 #pragma unroll
@@ -157,6 +172,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         }
         const double gC = __shfl(g, kChunk - 1);
         sg[l] = g;
+        sgl[l] = (float)(g * kLog2e);
         sb[l] = be;
         sw[l] = be * __builtin_amdgcn_exp2f((float)(g * kLog2e));
         sd[l] = __builtin_amdgcn_exp2f((float)((gC - g) * kLog2e));
@@ -168,11 +184,6 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         const int idx = tid + 256 * n, r = idx / (DK / VE), cv = idx % (DK / VE);
         *(uint4 *)(sK + r * L::LDK + cv * VE) = kreg[n];
     }
-#pragma unroll
-    for (int n = 0; n < NVV; ++n) {
-        const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
-        *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
-    }
     lds_barrier();
 
     // Fused output: wave w writes, for its token tile rt = w,
@@ -183,8 +194,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     // block m = 1 only matters for r >= 32.
     if constexpr (sizeof(E) == 2) {
         if (p.fused) {
-            const double gr = sg[rq];
-            const float er = expf((float)gr);
+            const float er = expf((float)sg[rq]);
             E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
 #pragma unroll
             for (int kb = 0; kb < DK / 32; ++kb) {
@@ -205,7 +215,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         const int s2 = 32 * m + 8 * lg + 4 * a + q;
-                        acc[q] = (s2 <= rq) ? __builtin_amdgcn_exp2f((float)((gr - sg[s2]) * kLog2e)) * acc[q] : 0.f;
+                        acc[q] = (s2 <= rq) ? wy_decay<E>(sg, sgl, rq, s2) * acc[q] : 0.f;
                     }
                     pq[a] = TR::from_f32(acc);
                 }
@@ -224,12 +234,11 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
             acc = TR::mma(load_frag<E>(sK + (16 * bi + li) * L::LDK + 32 * kb, lg),
                           load_frag<E>(sK + (16 * bj + li) * L::LDK + 32 * kb, lg), acc);
         const int s2 = 16 * bj + li;
-        const double gs = sg[s2];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int r = 16 * bi + 4 * lg + q;
             float val = 0.f;
-            if (s2 < r) val = sb[r] * __builtin_amdgcn_exp2f((float)((sg[r] - gs) * kLog2e)) * acc[q];
+            if (s2 < r) val = sb[r] * wy_decay<E>(sg, sgl, r, s2) * acc[q];
             sA[r * L::LDA + s2] = val;
         }
     }
@@ -295,25 +304,32 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         }
         lds_barrier();
     }
-    // A is dead: T diag(beta e^g) and T diag(beta), rounded to E, take its place.
-    // (Only the lower block-triangle of sT was written; the upper blocks of T
-    // are zero.)
-    for (int idx = tid; idx < kChunk * kChunk / 8; idx += 256) {
-        const int r = idx >> 3, s0 = (idx & 7) * 8;
-        const bool upper = (s0 >> 4) > (r >> 4);
-        const f32x4 t0v = upper ? f32x4{0.f, 0.f, 0.f, 0.f} : *(const f32x4 *)(sT + r * L::LDA + s0);
-        const f32x4 t1v = upper ? f32x4{0.f, 0.f, 0.f, 0.f} : *(const f32x4 *)(sT + r * L::LDA + s0 + 4);
-        f32x4 w0, w1, u0, u1;
+    // A is dead: V rows take its place (they waited in registers).
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            w0[q] = t0v[q] * sw[s0 + q];
-            w1[q] = t1v[q] * sw[s0 + 4 + q];
-            u0[q] = t0v[q] * sb[s0 + q];
-            u1[q] = t1v[q] * sb[s0 + 4 + q];
-        }
-        TR::store8(sTw + r * L::LDB + s0, TR::cat(TR::from_f32(w0), TR::from_f32(w1)));
-        TR::store8(sTu + r * L::LDB + s0, TR::cat(TR::from_f32(u0), TR::from_f32(u1)));
+    for (int n = 0; n < NVV; ++n) {
+        const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
+        *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
     }
+    // Rows of T diag(c) (c = beta e^g for W, beta for U~) as 8-element
+    // fragments, formed in registers from fp32 T: T[row][32 sk + 8 lg + e] c_s.
+    // The blocks of T above its diagonal 16x16 blocks were never written and
+    // are zero; with row = 32 m + p32_row(a, li) and sk = m they are the lanes
+    // li < 8 with lg >= 2.
+    f32x4 wsc[2][2], bsc[2][2];  // c_s for s = 32 sk + 8 lg + 4 h + q
+#pragma unroll
+    for (int sk = 0; sk < 2; ++sk)
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+            wsc[sk][hh] = *(const f32x4 *)(sw + 32 * sk + 8 * lg + 4 * hh);
+            bsc[sk][hh] = *(const f32x4 *)(sb + 32 * sk + 8 * lg + 4 * hh);
+        }
+    auto t_frag = [&](int m, int as, int sk, const f32x4 (&c)[2][2]) {
+        const float *trow = sT + (32 * m + p32_row(as, li)) * L::LDA + 32 * sk + 8 * lg;
+        const bool upper = sk == m && lg >= 2 && li < 8;
+        f32x4 t0 = *(const f32x4 *)trow, t1 = *(const f32x4 *)(trow + 4);
+        if (upper) t0 = t1 = f32x4{0.f, 0.f, 0.f, 0.f};
+        return TR::cat(TR::from_f32(t0 * c[sk][0]), TR::from_f32(t1 * c[sk][1]));
+    };
     lds_barrier();
 
     // -W fragments, computed transposed (W^T = K^T (T diag(beta e^g))^T) so that
@@ -324,12 +340,11 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     for (int f = w; f < NFR; f += 4) {
         const int wv = f >> 3, st = (f >> 1) & 3, kb = f & 1, m = st >> 1, as = st & 1;
         const int d0 = 64 * wv + 32 * kb;
-        const E *trow = sTw + (32 * m + p32_row(as, li)) * L::LDB;
         f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
         for (int sk = 0; sk < 2; ++sk) {
             if (sk > m) break;
-            const frag bt = load_frag<E>(trow + 32 * sk, lg);
+            const frag bt = t_frag(m, as, sk, wsc);
 #pragma unroll
             for (int a = 0; a < 2; ++a)
                 acc[a] = TR::mma(tr_frag<E>(sK, L::LDK, 32 * sk, d0, true, a, li, lg), bt, acc[a]);
@@ -341,13 +356,11 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     E *Uf = p.Ut + cidx * (size_t)DV * kChunk + l * 4;
     for (int u = w; u < (DV / 16) * 4; u += 4) {
         const int jt = u >> 2, st = u & 3, m = st >> 1, as = st & 1;
-        const E *trow = sTu + (32 * m + p32_row(as, li)) * L::LDB;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int sk = 0; sk < 2; ++sk) {
             if (sk > m) break;
-            acc = TR::mma(load_frag<E>(trow + 32 * sk, lg),
-                          tr_frag<E>(sV, L::LDV, 32 * sk, 16 * jt, false, 0, li, lg), acc);
+            acc = TR::mma(t_frag(m, as, sk, bsc), tr_frag<E>(sV, L::LDV, 32 * sk, 16 * jt, false, 0, li, lg), acc);
         }
         TR::store(Uf + u * 256, TR::from_f32(acc));
     }

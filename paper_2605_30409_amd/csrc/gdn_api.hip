@@ -204,7 +204,8 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
     auto stage = [&](int i) {
         switch (i) {
         case 0:
-            hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds1, s, p);
+            hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(64 * gdn::kWyWaves), lds1,
+                               s, p);
             break;
         case 1:
             hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT, NCW>),

@@ -64,7 +64,7 @@ template <class E> struct Params {
 constexpr float kLogAlphaMin = -87.3f;  // ~ log(FLT_MIN): alpha below this acts as 1.2e-38
 
 // --------------------------------------------------------------------------
-// Stage 1: per-chunk WY / UT transform.  Grid (NC, B*H), 256 threads.
+// Stage 1: per-chunk WY / UT transform.  Grid (NC, B*H), kWyWaves waves.
 // --------------------------------------------------------------------------
 // LDS: K rows, A (fp32; V rows take its place once the solve is done), T
 // (fp32), gates.  52.5 KB on the bf16 path at D = 128: three workgroups per CU.
@@ -96,14 +96,18 @@ __device__ __forceinline__ float wy_decay(const double *sg, const float *sgl, in
         return __builtin_amdgcn_exp2f((float)((sg[r] - sg[s]) * kLog2e));
 }
 
+constexpr int kWyWaves = 8;
+
 template <class E, int DK, int DV>
-__global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
+__global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
     using L = WyLds<E, DK, DV>;
     using TR = Tr<E>;
     using frag = typename TR::frag;
+    constexpr int NWV = kWyWaves, NT = 64 * NWV;
     constexpr int VE = 16 / (int)sizeof(E);       // elements per 16-byte vector
-    constexpr int NKV = kChunk * (DK / VE) / 256;  // K vectors per thread
-    constexpr int NVV = kChunk * (DV / VE) / 256;  // V vectors per thread
+    constexpr int NKV = kChunk * (DK / VE) / NT;   // K vectors per thread
+    constexpr int NVV = kChunk * (DV / VE) / NT;   // V vectors per thread
+    static_assert(NKV * NT == kChunk * (DK / VE) && NVV * NT == kChunk * (DV / VE), "whole vectors per thread");
     constexpr int NFR = (DK / 64) * 8;             // W (and Kt) fragments per chunk
     constexpr double kLog2e = 1.4426950408889634;
     extern __shared__ __align__(16) unsigned char smem[];
@@ -136,22 +140,26 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     uint4 kreg[NKV], vreg[NVV];
 #pragma unroll
     for (int n = 0; n < NKV; ++n) {
-        const int idx = tid + 256 * n, r = idx / (DK / VE), cv = idx % (DK / VE);
+        const int idx = tid + NT * n, r = idx / (DK / VE), cv = idx % (DK / VE);
         kreg[n] = make_uint4(0u, 0u, 0u, 0u);
         if (r < nvalid) kreg[n] = *(const uint4 *)(p.k + (row0 + r * rstride) * DK + cv * VE);
     }
 #pragma unroll
     for (int n = 0; n < NVV; ++n) {
-        const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
+        const int idx = tid + NT * n, r = idx / (DV / VE), cv = idx % (DV / VE);
         vreg[n] = make_uint4(0u, 0u, 0u, 0u);
         if (r < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + r * rstride) * DV + cv * VE);
     }
-    // Fused output: Q rows of this wave's 16 tokens as row fragments
-    // (Q[r][32 kb + 8 lg + e], r = 16 w + li; padded tokens are 0).
-    const int rq = 16 * w + li;
+    // Fused output: six (token tile rt, s block m) jobs on waves 0..5:
+    // (w, 0) for w < 4 (these also write the tile's Qf), (w - 2, 1) for w = 4, 5.
+    // Q rows of the job's 16 tokens as row fragments (Q[r][32 kb + 8 lg + e],
+    // r = 16 rt + li; padded tokens are 0).
+    const int qjob_rt = w < 4 ? w : w - 2, qjob_m = w < 4 ? 0 : 1;
+    const bool qjob = w < 6;
+    const int rq = 16 * qjob_rt + li;
     frag qf[DK / 32];
     if constexpr (sizeof(E) == 2) {
-        if (p.fused) {
+        if (p.fused && qjob) {
 #pragma unroll
             for (int kb = 0; kb < DK / 32; ++kb)
                 qf[kb] = rq < nvalid ? load_frag<E>(p.q + (row0 + rq * rstride) * DK + 32 * kb, lg)
@@ -181,30 +189,32 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     }
 #pragma unroll
     for (int n = 0; n < NKV; ++n) {
-        const int idx = tid + 256 * n, r = idx / (DK / VE), cv = idx % (DK / VE);
+        const int idx = tid + NT * n, r = idx / (DK / VE), cv = idx % (DK / VE);
         *(uint4 *)(sK + r * L::LDK + cv * VE) = kreg[n];
     }
     lds_barrier();
 
-    // Fused output: wave w writes, for its token tile rt = w,
-    //   Qf[rt][kb][lane][e] = e^{g_r} Q[r][32 kb + 8 lg + e]
+    // Fused output: job (rt, m) writes, for token tile rt,
+    //   Qf[rt][kb][lane][e] = e^{g_r} Q[r][32 kb + 8 lg + e]      (m = 0 jobs)
     //   Pf[rt][m][lane][e]  = e^{g_r - g_s} q_r . k_s (s <= r, else 0), s = 32 m + 8 lg + e,
     // the row fragments (B operands over d, resp. s) of the fused output.  P^T
     // tiles take their s rows in P32 order, so a tile pair is one fragment;
     // block m = 1 only matters for r >= 32.
     if constexpr (sizeof(E) == 2) {
-        if (p.fused) {
-            const float er = expf((float)sg[rq]);
-            E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
+        if (p.fused && qjob) {
+            if (qjob_m == 0) {
+                const float er = expf((float)sg[rq]);
+                E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
 #pragma unroll
-            for (int kb = 0; kb < DK / 32; ++kb) {
-                const f32x4 lo = TR::to_f32(TR::lo(qf[kb])) * er, hi = TR::to_f32(TR::hi(qf[kb])) * er;
-                TR::store8(Qf + (size_t)(w * (DK / 32) + kb) * 512, TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
+                for (int kb = 0; kb < DK / 32; ++kb) {
+                    const f32x4 lo = TR::to_f32(TR::lo(qf[kb])) * er, hi = TR::to_f32(TR::hi(qf[kb])) * er;
+                    TR::store8(Qf + (size_t)(qjob_rt * (DK / 32) + kb) * 512,
+                               TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
+                }
             }
             E *Pf = p.Pf + cidx * (size_t)kChunk * kChunk + l * 8;
-#pragma unroll
-            for (int m = 0; m < 2; ++m) {
-                if (m == 1 && w < 2) break;
+            {
+                const int m = qjob_m;
                 typename TR::quad pq[2];
 #pragma unroll
                 for (int a = 0; a < 2; ++a) {
@@ -219,13 +229,13 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
                     }
                     pq[a] = TR::from_f32(acc);
                 }
-                TR::store8(Pf + (size_t)(w * 2 + m) * 512, TR::cat(pq[0], pq[1]));
+                TR::store8(Pf + (size_t)(qjob_rt * 2 + m) * 512, TR::cat(pq[0], pq[1]));
             }
         }
     }
 
     // A = strict_lower(beta_r e^{g_r - g_s} K K^T): the 10 lower 16x16 blocks.
-    for (int t = w; t < 10; t += 4) {
+    for (int t = w; t < 10; t += NWV) {
         const int bi = (t >= 6) ? 3 : (t >= 3) ? 2 : (t >= 1) ? 1 : 0;
         const int bj = t - bi * (bi + 1) / 2;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
@@ -269,7 +279,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
         // Kt fragment f = (wave * 4 + t) * 2 + m holds, for lane (li, lg),
         // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
         E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
-        for (int f = w - 1; f < NFR; f += 3) {
+        for (int f = w - 1; f < NFR; f += NWV - 1) {
             const int wv = f >> 3, t = (f >> 1) & 3, m = f & 1;
             const frag kv = tr_frag<E>(sK, L::LDK, 32 * m, 64 * wv + 32 * (t >> 1), true, t & 1, li, lg);
             const f32x4 k0 = TR::to_f32(TR::lo(kv)), k1 = TR::to_f32(TR::hi(kv));
@@ -307,7 +317,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     // A is dead: V rows take its place (they waited in registers).
 #pragma unroll
     for (int n = 0; n < NVV; ++n) {
-        const int idx = tid + 256 * n, r = idx / (DV / VE), cv = idx % (DV / VE);
+        const int idx = tid + NT * n, r = idx / (DV / VE), cv = idx % (DV / VE);
         *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
     }
     // Rows of T diag(c) (c = beta e^g for W, beta for U~) as 8-element
@@ -337,7 +347,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     // fragment f = (wave * 4 + st) * 2 + kb, lane (li, lg) =
     // -W[32 m + p32_row(a_s, li)][64 wave + 32 kb + 8 lg + e]  (st = 2 m + a_s).
     E *Wf = p.W + cidx * (size_t)kChunk * DK + l * 8;
-    for (int f = w; f < NFR; f += 4) {
+    for (int f = w; f < NFR; f += NWV) {
         const int wv = f >> 3, st = (f >> 1) & 3, kb = f & 1, m = st >> 1, as = st & 1;
         const int d0 = 64 * wv + 32 * kb;
         f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
@@ -354,7 +364,7 @@ __global__ __launch_bounds__(256) void gdn_wy_kernel(Params<E> p) {
     // Ut tiles (jt, st) in P32 row order, written as fragment-major quads:
     // lane (li, lg) = Ut[32 m + 8 lg + 4 a_s + q][16 jt + li].
     E *Uf = p.Ut + cidx * (size_t)DV * kChunk + l * 4;
-    for (int u = w; u < (DV / 16) * 4; u += 4) {
+    for (int u = w; u < (DV / 16) * 4; u += NWV) {
         const int jt = u >> 2, st = u & 3, m = st >> 1, as = st & 1;
         f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll

@@ -150,12 +150,14 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
         vreg[n] = make_uint4(0u, 0u, 0u, 0u);
         if (r < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + r * rstride) * DV + cv * VE);
     }
-    // Fused output: six (token tile rt, s block m) jobs on waves 0..5:
-    // (w, 0) for w < 4 (these also write the tile's Qf), (w - 2, 1) for w = 4, 5.
+    // Fused output: six (token tile rt, s block m) jobs on waves 1..6, run
+    // while wave 0 inverts the diagonal blocks: job j = w - 1 is (j, 0) for
+    // j < 4 (these also write the tile's Qf) and (j - 2, 1) for j = 4, 5.
     // Q rows of the job's 16 tokens as row fragments (Q[r][32 kb + 8 lg + e],
     // r = 16 rt + li; padded tokens are 0).
-    const int qjob_rt = w < 4 ? w : w - 2, qjob_m = w < 4 ? 0 : 1;
-    const bool qjob = w < 6;
+    const int qj = w - 1;
+    const int qjob_rt = qj < 4 ? qj : qj - 2, qjob_m = qj < 4 ? 0 : 1;
+    const bool qjob = w >= 1 && w <= 6;
     const int rq = 16 * qjob_rt + li;
     frag qf[DK / 32];
     if constexpr (sizeof(E) == 2) {
@@ -194,46 +196,6 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
     }
     lds_barrier();
 
-    // Fused output: job (rt, m) writes, for token tile rt,
-    //   Qf[rt][kb][lane][e] = e^{g_r} Q[r][32 kb + 8 lg + e]      (m = 0 jobs)
-    //   Pf[rt][m][lane][e]  = e^{g_r - g_s} q_r . k_s (s <= r, else 0), s = 32 m + 8 lg + e,
-    // the row fragments (B operands over d, resp. s) of the fused output.  P^T
-    // tiles take their s rows in P32 order, so a tile pair is one fragment;
-    // block m = 1 only matters for r >= 32.
-    if constexpr (sizeof(E) == 2) {
-        if (p.fused && qjob) {
-            if (qjob_m == 0) {
-                const float er = expf((float)sg[rq]);
-                E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
-#pragma unroll
-                for (int kb = 0; kb < DK / 32; ++kb) {
-                    const f32x4 lo = TR::to_f32(TR::lo(qf[kb])) * er, hi = TR::to_f32(TR::hi(qf[kb])) * er;
-                    TR::store8(Qf + (size_t)(qjob_rt * (DK / 32) + kb) * 512,
-                               TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
-                }
-            }
-            E *Pf = p.Pf + cidx * (size_t)kChunk * kChunk + l * 8;
-            {
-                const int m = qjob_m;
-                typename TR::quad pq[2];
-#pragma unroll
-                for (int a = 0; a < 2; ++a) {
-                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int kb = 0; kb < DK / 32; ++kb)
-                        acc = TR::mma(load_frag<E>(sK + (32 * m + p32_row(a, li)) * L::LDK + 32 * kb, lg), qf[kb], acc);
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        const int s2 = 32 * m + 8 * lg + 4 * a + q;
-                        acc[q] = (s2 <= rq) ? wy_decay<E>(sg, sgl, rq, s2) * acc[q] : 0.f;
-                    }
-                    pq[a] = TR::from_f32(acc);
-                }
-                TR::store8(Pf + (size_t)(qjob_rt * 2 + m) * 512, TR::cat(pq[0], pq[1]));
-            }
-        }
-    }
-
     // A = strict_lower(beta_r e^{g_r - g_s} K K^T): the 10 lower 16x16 blocks.
     for (int t = w; t < 10; t += NWV) {
         const int bi = (t >= 6) ? 3 : (t >= 3) ? 2 : (t >= 1) ? 1 : 0;
@@ -256,7 +218,8 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
 
     // T = (I + A)^{-1} in fp32.  Wave 0 inverts the four diagonal 16x16 blocks
     // by forward substitution (lane = block * 16 + column) while the other
-    // waves emit the Kt fragments, which need only K and the gates.
+    // waves produce the fused-output fragments and the Kt fragments, which
+    // need only Q, K and the gates.
     if (w == 0) {
         const int base = 16 * (l >> 4), j = l & 15;
         float x[16];
@@ -276,10 +239,52 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) sT[(base + r) * L::LDA + base + j] = x[r];
     } else {
+        // Fused output: job (rt, m) writes, for token tile rt,
+        //   Qf[rt][kb][lane][e] = e^{g_r} Q[r][32 kb + 8 lg + e]      (m = 0 jobs)
+        //   Pf[rt][m][lane][e]  = e^{g_r - g_s} q_r . k_s (s <= r, else 0), s = 32 m + 8 lg + e,
+        // the row fragments (B operands over d, resp. s) of the fused output.  P^T
+        // tiles take their s rows in P32 order, so a tile pair is one fragment;
+        // block m = 1 only matters for r >= 32.
+        if constexpr (sizeof(E) == 2) {
+            if (p.fused && qjob) {
+                if (qjob_m == 0) {
+                    const float er = expf((float)sg[rq]);
+                    E *Qf = p.Qf + cidx * (size_t)kChunk * DK + l * 8;
+#pragma unroll
+                    for (int kb = 0; kb < DK / 32; ++kb) {
+                        const f32x4 lo = TR::to_f32(TR::lo(qf[kb])) * er, hi = TR::to_f32(TR::hi(qf[kb])) * er;
+                        TR::store8(Qf + (size_t)(qjob_rt * (DK / 32) + kb) * 512,
+                                   TR::cat(TR::from_f32(lo), TR::from_f32(hi)));
+                    }
+                }
+                E *Pf = p.Pf + cidx * (size_t)kChunk * kChunk + l * 8;
+                {
+                    const int m = qjob_m;
+                    typename TR::quad pq[2];
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) {
+                        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int kb = 0; kb < DK / 32; ++kb)
+                            acc = TR::mma(load_frag<E>(sK + (32 * m + p32_row(a, li)) * L::LDK + 32 * kb, lg), qf[kb], acc);
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const int s2 = 32 * m + 8 * lg + 4 * a + q;
+                            acc[q] = (s2 <= rq) ? wy_decay<E>(sg, sgl, rq, s2) * acc[q] : 0.f;
+                        }
+                        pq[a] = TR::from_f32(acc);
+                    }
+                    TR::store8(Pf + (size_t)(qjob_rt * 2 + m) * 512, TR::cat(pq[0], pq[1]));
+                }
+            }
+        }
         // Kt fragment f = (wave * 4 + t) * 2 + m holds, for lane (li, lg),
-        // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
+        // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}
+        // (on wave 7, or on waves 1..7 when there is no fused output).
         E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
-        for (int f = w - 1; f < NFR; f += NWV - 1) {
+        const bool fused = sizeof(E) == 2 && p.fused;
+        for (int f = fused ? w - 7 : w - 1; f < NFR; f += fused ? 1 : NWV - 1) {
+            if (f < 0) break;
             const int wv = f >> 3, t = (f >> 1) & 3, m = f & 1;
             const frag kv = tr_frag<E>(sK, L::LDK, 32 * m, 64 * wv + 32 * (t >> 1), true, t & 1, li, lg);
             const f32x4 k0 = TR::to_f32(TR::lo(kv)), k1 = TR::to_f32(TR::hi(kv));

@@ -1,10 +1,11 @@
 """Benchmark of the GDN chunk forward on one MI355X.
 
-A step is one full pass of the hot path (WY transform, grouped state scan,
+A step is one full pass of the hot path (gates, WY transform, state scan,
 output) over one 1280x704 latent frame: B=1, T=3520 tokens (44x80), H=16
 heads, Dk=Dv=128, chunk 64, bf16 q/k/v with an fp32 state carried in and out.
 The inputs are seeded synthetic tensors already resident in HBM; the workspace
-is preallocated, so the timed region only enqueues the five kernels per step.
+is preallocated, so the timed region only enqueues the path's kernels (on this
+workload two: the WY kernel and the state scan with the output fused into it).
 
 Prints ONE JSON line.  Besides throughput it reports the roofline of the
 dominant kernel (per-stage durations from HIP events recorded on the stream
@@ -33,30 +34,44 @@ PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 KERNELS = {"wy": "gdn_wy_kernel", "group_transfer": "gdn_chunkscan_kernel<SCAN_TRANS>",
            "group_scan": "gdn_groupscan_kernel", "chunk_states": "gdn_chunkscan_kernel<SCAN_STATES>",
            "output": "gdn_output_kernel"}
+KERNEL_FUSED = "gdn_chunkscan_kernel<SCAN_STATES, output fused>"
 
 
-def algorithmic_counts(B, T, H, Dk, Dv, G, C=64, esz=2):
+def algorithmic_counts(B, T, H, Dk, Dv, G, C=64, esz=2, fused=None):
     """Per-stage algorithmic flops and bytes (each stage's own inputs and outputs,
-    workspace included, every byte once), and the path's external I/O bytes."""
+    workspace included, every byte once), and the path's external I/O bytes.
+
+    `fused` (default: bf16 with a single scan group, the library's own rule) moves
+    the output into the chunk-state scan: the WY kernel then also forms the
+    decay-scaled queries and the masked decayed Q K^T tile of each chunk, and the
+    scan reads those and writes `out` instead of the chunk states."""
     n = B * T * H                       # token-heads
     NC = -(-T // C)
     NG = -(-NC // G)
+    if fused is None:
+        fused = esz == 2 and NG == 1
     nch = B * H * NC                    # chunks (the ragged tail counts as a whole chunk)
     ngr = B * H * NG if NG > 1 else 0   # scan groups (none with a single group)
     st = B * H * Dk * Dv * 4            # one fp32 state per (b, h)
-    wy_out = nch * C * (8 + (2 * Dk + Dv) * esz)      # g, -W, Kt, Ut
-    f = {"wy": n * ((C - 1) * (2 * Dk + Dv) + C * C / 3.0),
+    wy_fac = nch * (C * (2 * Dk + Dv) * esz + 8)       # -W, Kt, Ut and the chunk decay
+    wy_out = wy_fac + nch * C * 8                      # ... and the fp64 prefix g
+    qp = nch * C * (Dk + C) * esz if fused else 0      # scaled Q and masked P tiles
+    qk_f = n * (C + 1) * Dk                            # causal Q K^T
+    out_f = n * (2.0 * Dk * Dv + (C + 1) * Dv)         # Q H and P U
+    f = {"wy": n * ((C - 1) * (2 * Dk + Dv) + C * C / 3.0) + (qk_f if fused else 0),
          "group_transfer": nch * C * 4.0 * Dk * (Dk + Dv) if ngr else 0.0,
          "group_scan": ngr * (2.0 * Dk * Dk * Dv + 2.0 * Dk * Dv),
-         "chunk_states": nch * C * 4.0 * Dk * Dv,
-         "output": n * (2.0 * Dk * Dv + (C + 1) * (Dk + Dv))}
-    b = {"wy": n * ((Dk + Dv) * esz + 8) + wy_out,
-         "group_transfer": (wy_out + ngr * (Dk * Dk * esz + Dv * Dk * 4 + 8)) if ngr else 0,
+         "chunk_states": nch * C * 4.0 * Dk * Dv + (out_f if fused else 0),
+         "output": 0.0 if fused else out_f + qk_f}
+    b = {"wy": n * ((Dk + Dv + (Dk if fused else 0)) * esz + 8) + wy_out + qp,
+         "group_transfer": (wy_fac + ngr * (Dk * Dk * esz + Dv * Dk * 4 + 8)) if ngr else 0,
          "group_scan": (ngr * (Dk * Dk * esz + 2 * Dv * Dk * 4 + 8) + 2 * st) if ngr else 0,
-         "chunk_states": wy_out + (ngr * Dv * Dk * 4 if ngr else 2 * st) + nch * Dv * (Dk + C) * esz,
-         "output": n * (2 * Dk + Dv) * esz + nch * (C * 8 + Dv * (Dk + C) * esz)}
+         "chunk_states": wy_fac + (ngr * Dv * Dk * 4 if ngr else 2 * st)
+                         + (qp + n * Dv * esz if fused else nch * Dv * (Dk + C) * esz),
+         "output": 0 if fused else
+                   n * (2 * Dk + Dv) * esz + nch * (C * 8 + Dv * (Dk + C) * esz)}
     io_bytes = n * ((2 * Dk + Dv) * esz + 8 + Dv * esz) + 2 * st
-    return dict(flops=f, bytes=b, io_bytes=io_bytes, groups=NG, group_size=G)
+    return dict(flops=f, bytes=b, io_bytes=io_bytes, groups=NG, group_size=G, fused=fused)
 
 
 def binding_roof(flops, nbytes, ms):
@@ -207,7 +222,8 @@ def main():
     tflops = sum(cnt["flops"].values()) / sec / 1e12
     dom = max(names, key=names.get)
     roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
-    roofline.update({"traffic": load_traffic(dom), "kernel": KERNELS[dom],
+    kname = KERNEL_FUSED if (dom == "chunk_states" and cnt["fused"]) else KERNELS[dom]
+    roofline.update({"traffic": load_traffic(dom), "kernel": kname,
                      "duration_ms": round(names[dom], 5),
                      "algorithmic_flops_per_launch": cnt["flops"][dom],
                      "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
@@ -230,7 +246,7 @@ def main():
         "config": {"workload": "one 1280x704 latent frame: B=1 T=3520 (44x80) H=16 Dk=Dv=128 "
                                "chunk=64, bf16 q/k/v, fp32 state in/out",
                    "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C,
-                   "scan_group": G, "scan_groups": cnt["groups"]},
+                   "scan_group": G, "scan_groups": cnt["groups"], "output_fused": cnt["fused"]},
         "tflops": round(tflops, 2),
         "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
         "hbm_frac_io": round(cnt["io_bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),

@@ -80,6 +80,10 @@ template <class E, int DK, int DV> struct WyLds {
     static constexpr size_t oT = oA + (szA > szV ? szA : szV);
     static constexpr size_t oG = oT + szA;
     static constexpr size_t bytes = oG + 8 * kChunk + 4 * 4 * kChunk;
+    // waves per SIMD when as many eight-wave workgroups as fit in 160 KB share
+    // a CU (the register budget the kernel is compiled for)
+    static constexpr int fit = (int)((160 * 1024) / bytes);
+    static constexpr int waves_per_simd = fit >= 4 ? 8 : (fit < 1 ? 2 : 2 * fit);
 };
 
 // Decay ratio e^{g_r - g_s} (s <= r) inside the WY kernel.  The fp32 path
@@ -99,7 +103,8 @@ __device__ __forceinline__ float wy_decay(const double *sg, const float *sgl, in
 constexpr int kWyWaves = 8;
 
 template <class E, int DK, int DV>
-__global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
+__global__ __launch_bounds__(64 * kWyWaves)
+__attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_wy_kernel(Params<E> p) {
     using L = WyLds<E, DK, DV>;
     using TR = Tr<E>;
     using frag = typename TR::frag;
@@ -117,7 +122,7 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
     float *sT = (float *)(smem + L::oT);
     double *sg = (double *)(smem + L::oG);        // g_r
     float *sb = (float *)(sg + kChunk);           // beta_r
-    float *sw = sb + kChunk;                      // beta_r e^{g_r}
+    float *sw = sb + kChunk;                      // -beta_r e^{g_r}
     float *sd = sw + kChunk;                      // e^{g_C - g_r}
     float *sgl = sd + kChunk;                     // g_r log2(e) in fp32 (bf16 path)
 
@@ -184,7 +189,7 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
         sg[l] = g;
         sgl[l] = (float)(g * kLog2e);
         sb[l] = be;
-        sw[l] = be * __builtin_amdgcn_exp2f((float)(g * kLog2e));
+        sw[l] = -be * __builtin_amdgcn_exp2f((float)(g * kLog2e));
         sd[l] = __builtin_amdgcn_exp2f((float)((gC - g) * kLog2e));
         p.g[cidx * kChunk + l] = g;
         if (l == 0) p.gc[cidx] = gC;
@@ -279,23 +284,32 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
             }
         }
         // Kt fragment f = (wave * 4 + t) * 2 + m holds, for lane (li, lg),
-        // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}
-        // (on wave 7, or on waves 1..7 when there is no fused output).
+        // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
+        // Spread over waves 1..7; with the fused output waves 1..6 also run the
+        // query/score jobs (the four with a Qf tile the heaviest), so the later
+        // waves take more: fragments [kt_split[7 - w], kt_split[8 - w]) * NFR / 16.
         E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
         const bool fused = sizeof(E) == 2 && p.fused;
-        for (int f = fused ? w - 7 : w - 1; f < NFR; f += fused ? 1 : NWV - 1) {
+        static_assert(NWV == 8, "the Kt split assumes eight waves");
+        constexpr int kt_split[8] = {0, 4, 7, 10, 12, 14, 15, 16};
+        const int f_lo = fused ? kt_split[7 - w] * NFR / 16 : (w - 1) * NFR / (NWV - 1);
+        const int f_hi = fused ? kt_split[8 - w] * NFR / 16 : w * NFR / (NWV - 1);
+        constexpr int KT_MAX = (NFR * 4 + 15) / 16 > (NFR + NWV - 2) / (NWV - 1) ? (NFR * 4 + 15) / 16
+                                                                               : (NFR + NWV - 2) / (NWV - 1);
+        // fixed trip count (iterations past f_hi recompute the wave's last
+        // fragment and skip its store), so the LDS reads of all iterations can
+        // be issued together
+#pragma unroll
+        for (int i = 0; i < KT_MAX; ++i) {
+            const int f = min(f_lo + i, f_hi - 1);
             if (f < 0) break;
             const int wv = f >> 3, t = (f >> 1) & 3, m = f & 1;
             const frag kv = tr_frag<E>(sK, L::LDK, 32 * m, 64 * wv + 32 * (t >> 1), true, t & 1, li, lg);
             const f32x4 k0 = TR::to_f32(TR::lo(kv)), k1 = TR::to_f32(TR::hi(kv));
             const int s0 = 32 * m + 8 * lg;
-            f32x4 o0, o1;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                o0[q] = k0[q] * sd[s0 + q];
-                o1[q] = k1[q] * sd[s0 + 4 + q];
-            }
-            TR::store8(Kf + f * 512, TR::cat(TR::from_f32(o0), TR::from_f32(o1)));
+            const f32x4 d0 = *(const f32x4 *)(sd + s0), d1 = *(const f32x4 *)(sd + s0 + 4);
+            if (f_lo + i < f_hi)
+                TR::store8(Kf + f * 512, TR::cat(TR::from_f32(k0 * d0), TR::from_f32(k1 * d1)));
         }
     }
     lds_barrier();
@@ -325,7 +339,7 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
         const int idx = tid + NT * n, r = idx / (DV / VE), cv = idx % (DV / VE);
         *(uint4 *)(sV + r * L::LDV + cv * VE) = vreg[n];
     }
-    // Rows of T diag(c) (c = beta e^g for W, beta for U~) as 8-element
+    // Rows of T diag(c) (c = -beta e^g for -W, beta for U~) as 8-element
     // fragments, formed in registers from fp32 T: T[row][32 sk + 8 lg + e] c_s.
     // The blocks of T above its diagonal 16x16 blocks were never written and
     // are zero; with row = 32 m + p32_row(a, li) and sk = m they are the lanes
@@ -338,46 +352,58 @@ __global__ __launch_bounds__(64 * kWyWaves) void gdn_wy_kernel(Params<E> p) {
             wsc[sk][hh] = *(const f32x4 *)(sw + 32 * sk + 8 * lg + 4 * hh);
             bsc[sk][hh] = *(const f32x4 *)(sb + 32 * sk + 8 * lg + 4 * hh);
         }
-    auto t_frag = [&](int m, int as, int sk, const f32x4 (&c)[2][2]) {
-        const float *trow = sT + (32 * m + p32_row(as, li)) * L::LDA + 32 * sk + 8 * lg;
-        const bool upper = sk == m && lg >= 2 && li < 8;
-        f32x4 t0 = *(const f32x4 *)trow, t1 = *(const f32x4 *)(trow + 4);
-        if (upper) t0 = t1 = f32x4{0.f, 0.f, 0.f, 0.f};
-        return TR::cat(TR::from_f32(t0 * c[sk][0]), TR::from_f32(t1 * c[sk][1]));
-    };
     lds_barrier();
 
-    // -W fragments, computed transposed (W^T = K^T (T diag(beta e^g))^T) so that
-    // each lane ends up holding the 8 consecutive Dk entries the scan consumes:
-    // fragment f = (wave * 4 + st) * 2 + kb, lane (li, lg) =
-    // -W[32 m + p32_row(a_s, li)][64 wave + 32 kb + 8 lg + e]  (st = 2 m + a_s).
-    E *Wf = p.W + cidx * (size_t)kChunk * DK + l * 8;
-    for (int f = w; f < NFR; f += NWV) {
-        const int wv = f >> 3, st = (f >> 1) & 3, kb = f & 1, m = st >> 1, as = st & 1;
-        const int d0 = 64 * wv + 32 * kb;
-        f32x4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    // -W fragments and Ut quads.  Wave w serves the two token tiles with
+    // a_s = w & 1 (st = a_s, i.e. m = 0, and st = 2 + a_s, m = 1) and takes the
+    // quarter q4 = w >> 1 of their outputs, so it forms the T diag(c) row
+    // fragments of its tiles once -- three (m, s block) pairs, T being lower
+    // triangular -- and shares the K^T and V fragments of s block 0 between
+    // the two tiles.  Every wave issues the same number of MFMAs.
+    static_assert(NWV == 8, "two token-tile parities x four quarters");
+    const int as = w & 1, q4 = w >> 1;
+    frag tw[3], tb[3];  // (m, sk) = (0, 0), (1, 0), (1, 1)
 #pragma unroll
-        for (int sk = 0; sk < 2; ++sk) {
-            if (sk > m) break;
-            const frag bt = t_frag(m, as, sk, wsc);
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-                acc[a] = TR::mma(tr_frag<E>(sK, L::LDK, 32 * sk, d0, true, a, li, lg), bt, acc[a]);
-        }
-        TR::store8(Wf + f * 512, TR::cat(TR::from_f32(-acc[0]), TR::from_f32(-acc[1])));
+    for (int i = 0; i < 3; ++i) {
+        const int m = i > 0 ? 1 : 0, sk = i == 2 ? 1 : 0;
+        const float *trow = sT + (32 * m + p32_row(as, li)) * L::LDA + 32 * sk + 8 * lg;
+        f32x4 t0 = *(const f32x4 *)trow, t1 = *(const f32x4 *)(trow + 4);
+        if (sk == m && lg >= 2 && li < 8) t0 = t1 = f32x4{0.f, 0.f, 0.f, 0.f};
+        tw[i] = TR::cat(TR::from_f32(t0 * wsc[sk][0]), TR::from_f32(t1 * wsc[sk][1]));
+        tb[i] = TR::cat(TR::from_f32(t0 * bsc[sk][0]), TR::from_f32(t1 * bsc[sk][1]));
     }
-    // Ut tiles (jt, st) in P32 row order, written as fragment-major quads:
-    // lane (li, lg) = Ut[32 m + 8 lg + 4 a_s + q][16 jt + li].
-    E *Uf = p.Ut + cidx * (size_t)DV * kChunk + l * 4;
-    for (int u = w; u < (DV / 16) * 4; u += NWV) {
-        const int jt = u >> 2, st = u & 3, m = st >> 1, as = st & 1;
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    // -W, computed transposed (W^T = K^T (T diag(beta e^g))^T) so that each lane
+    // ends up holding the 8 consecutive Dk entries the scan consumes: fragment
+    // f = (wave * 4 + st) * 2 + kb, lane (li, lg) =
+    // -W[32 m + p32_row(a_s, li)][64 wave + 32 kb + 8 lg + e]  (st = 2 m + a_s).
+    constexpr int NWC = NFR / 4;  // (wave, kb) combinations per token tile
+    if (q4 < NWC) {
+        const int wv = q4 >> 1, kb = q4 & 1, d0 = 64 * wv + 32 * kb;
+        f32x4 w0[2], w1[2];  // tiles m = 0 and m = 1
 #pragma unroll
-        for (int sk = 0; sk < 2; ++sk) {
-            if (sk > m) break;
-            acc = TR::mma(t_frag(m, as, sk, bsc), tr_frag<E>(sV, L::LDV, 32 * sk, 16 * jt, false, 0, li, lg), acc);
+        for (int a = 0; a < 2; ++a) {
+            const frag k0 = tr_frag<E>(sK, L::LDK, 0, d0, true, a, li, lg);
+            const frag k1 = tr_frag<E>(sK, L::LDK, 32, d0, true, a, li, lg);
+            const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+            w0[a] = TR::mma(k0, tw[0], z);
+            w1[a] = TR::mma(k1, tw[2], TR::mma(k0, tw[1], z));
         }
-        TR::store(Uf + u * 256, TR::from_f32(acc));
+        E *Wf = p.W + cidx * (size_t)kChunk * DK + l * 8;
+        TR::store8(Wf + ((wv * 4 + as) * 2 + kb) * 512, TR::cat(TR::from_f32(w0[0]), TR::from_f32(w0[1])));
+        TR::store8(Wf + ((wv * 4 + 2 + as) * 2 + kb) * 512, TR::cat(TR::from_f32(w1[0]), TR::from_f32(w1[1])));
+    }
+    // Ut tiles (jt, st) in P32 row order, written as fragment-major quads
+    // u = 4 jt + st: lane (li, lg) = Ut[32 m + 8 lg + 4 a_s + q][16 jt + li].
+    constexpr int NJ = DV / 16;
+    E *Uf = p.Ut + cidx * (size_t)DV * kChunk + l * 4;
+#pragma unroll
+    for (int j = 0; j < NJ / 4; ++j) {
+        const int jt = q4 * (NJ / 4) + j;
+        const frag v0 = tr_frag<E>(sV, L::LDV, 0, 16 * jt, false, 0, li, lg);
+        const frag v1 = tr_frag<E>(sV, L::LDV, 32, 16 * jt, false, 0, li, lg);
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        TR::store(Uf + (4 * jt + as) * 256, TR::from_f32(TR::mma(tb[0], v0, z)));
+        TR::store(Uf + (4 * jt + 2 + as) * 256, TR::from_f32(TR::mma(tb[2], v1, TR::mma(tb[1], v0, z))));
     }
 }
 

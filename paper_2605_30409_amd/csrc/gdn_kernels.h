@@ -135,8 +135,10 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
     const size_t row0 = ((size_t)b * p.T + t0) * p.H + h;  // token-row index of token t0
     const size_t rstride = (size_t)p.H;                    // token-row stride
 
-    // Gates first (they head the dependency chain), then K and V rows with
-    // 16-byte coalesced loads (padding rows are zero).
+    // Gates first (they head the dependency chain), then K rows with 16-byte
+    // coalesced loads (padding rows are zero); V, needed only for U~ at the
+    // end, is requested after the first barrier, so that the K and query
+    // requests of all workgroups starting together are served first.
     float ga = 1.f, gbe = 0.f;  // alpha, beta of token l (wave 0; padding: 1, 0)
     if (w == 0 && l < nvalid) {
         ga = p.alpha[row0 + l * rstride];
@@ -148,12 +150,6 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
         const int idx = tid + NT * n, r = idx / (DK / VE), cv = idx % (DK / VE);
         kreg[n] = make_uint4(0u, 0u, 0u, 0u);
         if (r < nvalid) kreg[n] = *(const uint4 *)(p.k + (row0 + r * rstride) * DK + cv * VE);
-    }
-#pragma unroll
-    for (int n = 0; n < NVV; ++n) {
-        const int idx = tid + NT * n, r = idx / (DV / VE), cv = idx % (DV / VE);
-        vreg[n] = make_uint4(0u, 0u, 0u, 0u);
-        if (r < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + r * rstride) * DV + cv * VE);
     }
     // Fused output: six (token tile rt, s block m) jobs on waves 1..6, run
     // while wave 0 inverts the diagonal blocks: job j = w - 1 is (j, 0) for
@@ -200,6 +196,12 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
         *(uint4 *)(sK + r * L::LDK + cv * VE) = kreg[n];
     }
     lds_barrier();
+#pragma unroll
+    for (int n = 0; n < NVV; ++n) {
+        const int idx = tid + NT * n, r = idx / (DV / VE), cv = idx % (DV / VE);
+        vreg[n] = make_uint4(0u, 0u, 0u, 0u);
+        if (r < nvalid) vreg[n] = *(const uint4 *)(p.v + (row0 + r * rstride) * DV + cv * VE);
+    }
 
     // A = strict_lower(beta_r e^{g_r - g_s} K K^T): the 10 lower 16x16 blocks.
     for (int t = w; t < 10; t += NWV) {

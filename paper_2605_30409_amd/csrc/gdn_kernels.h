@@ -136,9 +136,10 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
     const size_t rstride = (size_t)p.H;                    // token-row stride
 
     // Gates first (they head the dependency chain), then K rows with 16-byte
-    // coalesced loads (padding rows are zero); V, needed only for U~ at the
-    // end, is requested after the first barrier, so that the K and query
-    // requests of all workgroups starting together are served first.
+    // coalesced loads (padding rows are zero).  The queries (first needed after
+    // the A tiles) and V (needed only for U~ at the end) are requested after
+    // the first barrier, so that the gate and K requests of all the workgroups
+    // starting together are served first.
     float ga = 1.f, gbe = 0.f;  // alpha, beta of token l (wave 0; padding: 1, 0)
     if (w == 0 && l < nvalid) {
         ga = p.alpha[row0 + l * rstride];
@@ -161,14 +162,6 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
     const bool qjob = w >= 1 && w <= 6;
     const int rq = 16 * qjob_rt + li;
     frag qf[DK / 32];
-    if constexpr (sizeof(E) == 2) {
-        if (p.fused && qjob) {
-#pragma unroll
-            for (int kb = 0; kb < DK / 32; ++kb)
-                qf[kb] = rq < nvalid ? load_frag<E>(p.q + (row0 + rq * rstride) * DK + 32 * kb, lg)
-                                     : TR::cat(TR::zero(), TR::zero());
-        }
-    }
     // Gates: wave-wide inclusive prefix sum of clamped log alpha in fp64
     // (padding tokens: alpha = 1, beta = 0).
     if (w == 0) {
@@ -196,6 +189,14 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
         *(uint4 *)(sK + r * L::LDK + cv * VE) = kreg[n];
     }
     lds_barrier();
+    if constexpr (sizeof(E) == 2) {
+        if (p.fused && qjob) {
+#pragma unroll
+            for (int kb = 0; kb < DK / 32; ++kb)
+                qf[kb] = rq < nvalid ? load_frag<E>(p.q + (row0 + rq * rstride) * DK + 32 * kb, lg)
+                                     : TR::cat(TR::zero(), TR::zero());
+        }
+    }
 #pragma unroll
     for (int n = 0; n < NVV; ++n) {
         const int idx = tid + NT * n, r = idx / (DV / VE), cv = idx % (DV / VE);

@@ -128,7 +128,9 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
 
     const int c = blockIdx.x, bh = blockIdx.y;
     const int b = bh / p.H, h = bh - b * p.H;
-    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
+    // w is wave-uniform: scalar branches and table lookups
+    const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63, li = l & 15,
+              lg = l >> 4;
     const int t0 = c * kChunk;
     const int nvalid = min(kChunk, p.T - t0);
     const size_t cidx = (size_t)bh * p.NC + c;
@@ -290,13 +292,17 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
         // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
         // Spread over waves 1..7; with the fused output waves 1..6 also run the
         // query/score jobs (the four with a Qf tile the heaviest), so the later
-        // waves take more: fragments [kt_split[7 - w], kt_split[8 - w]) * NFR / 16.
+        // waves take more: fragments [kt_split(7 - w), kt_split(8 - w)) * NFR / 16.
         E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
         const bool fused = sizeof(E) == 2 && p.fused;
         static_assert(NWV == 8, "the Kt split assumes eight waves");
-        constexpr int kt_split[8] = {0, 4, 7, 10, 12, 14, 15, 16};
-        const int f_lo = fused ? kt_split[7 - w] * NFR / 16 : (w - 1) * NFR / (NWV - 1);
-        const int f_hi = fused ? kt_split[8 - w] * NFR / 16 : w * NFR / (NWV - 1);
+        // (a select chain on the wave-uniform w: a constant table indexed by
+        // it would be read from memory)
+        auto kt_split = [](int i) {
+            return i == 0 ? 0 : i == 1 ? 4 : i == 2 ? 7 : i == 3 ? 10 : i == 4 ? 12 : i == 5 ? 14 : i == 6 ? 15 : 16;
+        };
+        const int f_lo = fused ? kt_split(7 - w) * NFR / 16 : (w - 1) * NFR / (NWV - 1);
+        const int f_hi = fused ? kt_split(8 - w) * NFR / 16 : w * NFR / (NWV - 1);
         constexpr int KT_MAX = (NFR * 4 + 15) / 16 > (NFR + NWV - 2) / (NWV - 1) ? (NFR * 4 + 15) / 16
                                                                                : (NFR + NWV - 2) / (NWV - 1);
         // fixed trip count (iterations past f_hi recompute the wave's last

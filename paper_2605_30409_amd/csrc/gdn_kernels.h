@@ -288,37 +288,36 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
                 }
             }
         }
+    }
+    {
         // Kt fragment f = (wave * 4 + t) * 2 + m holds, for lane (li, lg),
         // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
-        // Spread over waves 1..7; with the fused output waves 1..6 also run the
-        // query/score jobs (the four with a Qf tile the heaviest), so the later
-        // waves take more: fragments [kt_split(7 - w), kt_split(8 - w)) * NFR / 16.
+        // Every wave takes a share sized to its other work in this phase:
+        // with the fused output, wave 0 (diagonal inversion) takes 2 of 16,
+        // waves 1..4 (a score job and a Qf tile) 1 each, waves 5, 6 (a score
+        // job) 3 each and wave 7 4: fragments [kt_split(w), kt_split(w + 1))
+        // * NFR / 16; without it the waves split them evenly.
         E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
         const bool fused = sizeof(E) == 2 && p.fused;
         static_assert(NWV == 8, "the Kt split assumes eight waves");
         // (a select chain on the wave-uniform w: a constant table indexed by
         // it would be read from memory)
         auto kt_split = [](int i) {
-            return i == 0 ? 0 : i == 1 ? 4 : i == 2 ? 7 : i == 3 ? 10 : i == 4 ? 12 : i == 5 ? 14 : i == 6 ? 15 : 16;
+            return i <= 0 ? 0 : i == 1 ? 2 : i == 2 ? 3 : i == 3 ? 4 : i == 4 ? 5 : i == 5 ? 6 : i == 6 ? 9 : i == 7 ? 12 : 16;
         };
-        const int f_lo = fused ? kt_split(7 - w) * NFR / 16 : (w - 1) * NFR / (NWV - 1);
-        const int f_hi = fused ? kt_split(8 - w) * NFR / 16 : w * NFR / (NWV - 1);
-        constexpr int KT_MAX = (NFR * 4 + 15) / 16 > (NFR + NWV - 2) / (NWV - 1) ? (NFR * 4 + 15) / 16
-                                                                               : (NFR + NWV - 2) / (NWV - 1);
-        // fixed trip count (iterations past f_hi recompute the wave's last
-        // fragment and skip its store), so the LDS reads of all iterations can
-        // be issued together
+        const int f_lo = fused ? kt_split(w) * NFR / 16 : w * NFR / NWV;
+        const int f_cnt = (fused ? kt_split(w + 1) * NFR / 16 : (w + 1) * NFR / NWV) - f_lo;
+        constexpr int KT_MAX = (NFR * 4 + 15) / 16 > (NFR + NWV - 1) / NWV ? (NFR * 4 + 15) / 16 : (NFR + NWV - 1) / NWV;
 #pragma unroll
         for (int i = 0; i < KT_MAX; ++i) {
-            const int f = min(f_lo + i, f_hi - 1);
-            if (f < 0) break;
+            if (i >= f_cnt) break;
+            const int f = f_lo + i;
             const int wv = f >> 3, t = (f >> 1) & 3, m = f & 1;
             const frag kv = tr_frag<E>(sK, L::LDK, 32 * m, 64 * wv + 32 * (t >> 1), true, t & 1, li, lg);
             const f32x4 k0 = TR::to_f32(TR::lo(kv)), k1 = TR::to_f32(TR::hi(kv));
             const int s0 = 32 * m + 8 * lg;
             const f32x4 d0 = *(const f32x4 *)(sd + s0), d1 = *(const f32x4 *)(sd + s0 + 4);
-            if (f_lo + i < f_hi)
-                TR::store8(Kf + f * 512, TR::cat(TR::from_f32(k0 * d0), TR::from_f32(k1 * d1)));
+            TR::store8(Kf + f * 512, TR::cat(TR::from_f32(k0 * d0), TR::from_f32(k1 * d1)));
         }
     }
     lds_barrier();

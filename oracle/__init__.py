@@ -9,7 +9,10 @@ and the product path never calls it.
 * :mod:`oracle.chunked` -- the chunked (WY / UT) rewrite in fp64 numpy, used
   only to pin the recurrence against an independent algebraic form.
 * :mod:`oracle.framewise` -- the paper's frame-wise compact update written as
-  printed, used to tie the recurrence to the paper's own equation.
+  printed, used to tie the recurrences to the paper's own equation.
+* :func:`gdn_frame_forward` -- the frame-wise recurrence (one decay per frame,
+  the frame's tokens writing at once, rescaled keys) in fp64 (C library), the
+  reference for the GPU frame-wise path.
 """
 import ctypes
 import os
@@ -33,6 +36,9 @@ def _lib():
         lib.gdn_oracle_forward.restype = ctypes.c_int
         lib.gdn_oracle_forward.argtypes = [vp, vp, vp, i, vp, vp, i, vp, i, vp, vp,
                                            i, i, i, i, i, i]
+        lib.gdn_oracle_frame_forward.restype = ctypes.c_int
+        lib.gdn_oracle_frame_forward.argtypes = [vp, vp, vp, i, vp, vp, i, vp, i, vp, vp,
+                                                 i, i, i, i, i, i, ctypes.c_double, i]
         _LIB = lib
     return _LIB
 
@@ -83,4 +89,52 @@ def gdn_forward(q, k, v, alpha, beta, state_in=None, nthreads=None,
         B, H, T, Dk, Dv, int(nthreads))
     if rc != 0:
         raise RuntimeError(f"gdn_oracle_forward failed with {rc}")
+    return out, state_out
+
+
+def gdn_frame_forward(q, k, v, alpha, beta, state_in=None, frame_tokens=1, key_scale=None,
+                      nthreads=None, want_state=True):
+    """Run the fp64 frame-wise recurrence.
+
+    q, k: [B, T, H, Dk]; v: [B, T, H, Dv] (float32, float64 or bf16 bits as
+    uint16); T = F * frame_tokens.  alpha: [B, F, H] (one decay per frame);
+    beta: [B, T, H].  key_scale multiplies every key (None: the paper's
+    1 / sqrt(Dk * frame_tokens)).  Returns (out [B, T, H, Dv], state_out).
+    """
+    q, k, v = (np.ascontiguousarray(x) for x in (q, k, v))
+    if not (q.dtype == k.dtype == v.dtype) or q.dtype not in _DT_QKV:
+        raise TypeError("q/k/v dtype mismatch or unsupported")
+    alpha = np.ascontiguousarray(alpha)
+    beta = np.ascontiguousarray(beta, dtype=alpha.dtype)
+    if alpha.dtype not in _DT_GATE:
+        raise TypeError(f"alpha/beta dtype {alpha.dtype} unsupported")
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    N = int(frame_tokens)
+    if N < 1 or T % N:
+        raise ValueError("T must be a whole number of frames")
+    F = T // N
+    if k.shape != (B, T, H, Dk) or v.shape != (B, T, H, Dv):
+        raise ValueError("q/k/v shape mismatch")
+    if alpha.shape != (B, F, H) or beta.shape != (B, T, H):
+        raise ValueError("alpha must be [B, F, H] and beta [B, T, H]")
+    sdt = 0
+    if state_in is not None:
+        state_in = np.ascontiguousarray(state_in)
+        if state_in.dtype not in _DT_GATE or state_in.shape != (B, H, Dk, Dv):
+            raise ValueError("state_in must be float32/float64 [B, H, Dk, Dv]")
+        sdt = _DT_GATE[state_in.dtype]
+    if key_scale is None:
+        key_scale = 1.0 / np.sqrt(Dk * N)
+    out = np.empty((B, T, H, Dv), dtype=np.float64)
+    state_out = np.empty((B, H, Dk, Dv), dtype=np.float64) if want_state else None
+    if nthreads is None:
+        nthreads = os.cpu_count() or 1
+    rc = _lib().gdn_oracle_frame_forward(
+        _ptr(q), _ptr(k), _ptr(v), _DT_QKV[q.dtype],
+        _ptr(alpha), _ptr(beta), _DT_GATE[alpha.dtype],
+        _ptr(state_in), sdt, _ptr(out), _ptr(state_out),
+        B, H, F, N, Dk, Dv, float(key_scale), int(nthreads))
+    if rc != 0:
+        raise RuntimeError(f"gdn_oracle_frame_forward failed with {rc}")
     return out, state_out

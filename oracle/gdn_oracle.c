@@ -191,3 +191,161 @@ int gdn_oracle_forward(const void *q, const void *k, const void *v, int qkv_dtyp
     free(tids);
     return status;
 }
+
+/*
+ * Frame-wise form (the paper's own update: Section "Frame-wise Gated
+ * DeltaNet", equations appendix_gdn_kv_update / appendix_gdn_kv_compact with a
+ * frame of N tokens; eq. gdn_combined): one decay alpha_f per frame and head,
+ * shared by the frame's N tokens, which all write at once; a write gate beta
+ * per token; the keys rescaled by key_scale before entering the recurrence
+ * (the paper uses 1/sqrt(D N), subsection "Attention features").  With the
+ * keys k~ = key_scale k, in the H = S^T orientation, per frame f:
+ *       p_n  = H^T k~_n                  for every token n of the frame (old H)
+ *       u_n  = beta_n (v_n - alpha_f p_n)
+ *       H   <- alpha_f H + sum_n k~_n u_n^T
+ *       o_n  = H^T q_n                   (read from the updated state)
+ * i.e. S_f = alpha_f S_{f-1} (I - K~ B K~^T) + V B K~^T and Y_f = S_f Q_f.
+ */
+struct fjob {
+    const void *q, *k, *v;
+    int qkv_dtype;
+    const void *alpha, *beta, *state_in;
+    int gate_dtype, state_dtype;
+    double *out, *state_out;
+    int B, H, F, N, Dk, Dv;
+    double key_scale;
+    int nthreads, worker, status;
+};
+
+static int run_frame_head(const struct fjob *J, int b, int h)
+{
+    const int H = J->H, F = J->F, N = J->N, Dk = J->Dk, Dv = J->Dv;
+    const size_t T = (size_t)F * N;
+    double *S = (double *)calloc((size_t)Dk * Dv, sizeof(double));
+    double *kk = (double *)malloc(sizeof(double) * (size_t)N * Dk);
+    double *uu = (double *)malloc(sizeof(double) * (size_t)N * Dv);
+    double *qq = (double *)malloc(sizeof(double) * (size_t)Dk);
+    if (!S || !kk || !uu || !qq) {
+        free(S); free(kk); free(uu); free(qq);
+        return -1;
+    }
+    const size_t sbase = ((size_t)b * H + h) * (size_t)Dk * Dv;
+    if (J->state_in)
+        for (size_t e = 0; e < (size_t)Dk * Dv; e++)
+            S[e] = load_elem(J->state_in, J->state_dtype, sbase + e);
+    for (int f = 0; f < F; f++) {
+        const double a = load_elem(J->alpha, J->gate_dtype, ((size_t)b * F + f) * H + h);
+        /* residuals of every token against the decayed state of the previous frame */
+        for (int n = 0; n < N; n++) {
+            const size_t row = ((size_t)b * T + (size_t)f * N + n) * H + h;
+            const double be = load_elem(J->beta, J->gate_dtype, row);
+            double *kn = kk + (size_t)n * Dk, *un = uu + (size_t)n * Dv;
+            for (int i = 0; i < Dk; i++)
+                kn[i] = J->key_scale * load_elem(J->k, J->qkv_dtype, row * Dk + i);
+            for (int j = 0; j < Dv; j++)
+                un[j] = 0.0;
+            for (int i = 0; i < Dk; i++)
+                for (int j = 0; j < Dv; j++)
+                    un[j] += S[(size_t)i * Dv + j] * kn[i];
+            for (int j = 0; j < Dv; j++)
+                un[j] = be * (load_elem(J->v, J->qkv_dtype, row * Dv + j) - a * un[j]);
+        }
+        /* simultaneous write of the whole frame */
+        for (size_t e = 0; e < (size_t)Dk * Dv; e++)
+            S[e] *= a;
+        for (int n = 0; n < N; n++) {
+            const double *kn = kk + (size_t)n * Dk, *un = uu + (size_t)n * Dv;
+            for (int i = 0; i < Dk; i++)
+                for (int j = 0; j < Dv; j++)
+                    S[(size_t)i * Dv + j] += kn[i] * un[j];
+        }
+        /* readout from the updated state */
+        for (int n = 0; n < N; n++) {
+            const size_t row = ((size_t)b * T + (size_t)f * N + n) * H + h;
+            for (int i = 0; i < Dk; i++)
+                qq[i] = load_elem(J->q, J->qkv_dtype, row * Dk + i);
+            double *o = J->out + row * Dv;
+            for (int j = 0; j < Dv; j++)
+                o[j] = 0.0;
+            for (int i = 0; i < Dk; i++)
+                for (int j = 0; j < Dv; j++)
+                    o[j] += S[(size_t)i * Dv + j] * qq[i];
+        }
+    }
+    if (J->state_out)
+        memcpy(J->state_out + sbase, S, sizeof(double) * (size_t)Dk * Dv);
+    free(S); free(kk); free(uu); free(qq);
+    return 0;
+}
+
+static void *frame_worker_main(void *arg)
+{
+    struct fjob *J = (struct fjob *)arg;
+    const int nbh = J->B * J->H;
+    for (int bh = J->worker; bh < nbh; bh += J->nthreads) {
+        if (run_frame_head(J, bh / J->H, bh % J->H) != 0) {
+            J->status = -1;
+            break;
+        }
+    }
+    return NULL;
+}
+
+/*
+ * q, k : [B, F*N, H, Dk]   v : [B, F*N, H, Dv]   stored as qkv_dtype (0 f32, 1 bf16 bits, 2 f64)
+ * alpha : [B, F, H] (one per frame)   beta : [B, F*N, H]   stored as gate_dtype (0 f32, 2 f64)
+ * state_in : [B, H, Dk, Dv] or NULL (zero)   out : [B, F*N, H, Dv] fp64   state_out : fp64 or NULL
+ * key_scale : factor applied to every key (the paper's 1/sqrt(D N))
+ * Returns 0, or -1 on bad arguments / allocation failure.
+ */
+int gdn_oracle_frame_forward(const void *q, const void *k, const void *v, int qkv_dtype,
+                             const void *alpha, const void *beta, int gate_dtype,
+                             const void *state_in, int state_dtype,
+                             double *out, double *state_out,
+                             int B, int H, int F, int N, int Dk, int Dv, double key_scale, int nthreads)
+{
+    if (!q || !k || !v || !alpha || !beta || !out)
+        return -1;
+    if (B < 1 || H < 1 || F < 0 || N < 1 || Dk < 1 || Dv < 1)
+        return -1;
+    if (qkv_dtype < 0 || qkv_dtype > 2 || (gate_dtype != 0 && gate_dtype != 2) ||
+        (state_dtype != 0 && state_dtype != 2))
+        return -1;
+    const int nbh = B * H;
+    if (nthreads < 1)
+        nthreads = 1;
+    if (nthreads > nbh)
+        nthreads = nbh;
+    struct fjob *jobs = (struct fjob *)calloc((size_t)nthreads, sizeof(struct fjob));
+    pthread_t *tids = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+    char *running = (char *)calloc((size_t)nthreads, 1);
+    if (!jobs || !tids || !running) {
+        free(jobs); free(tids); free(running);
+        return -1;
+    }
+    int status = 0;
+    for (int w = 0; w < nthreads; w++) {
+        struct fjob *J = &jobs[w];
+        J->q = q; J->k = k; J->v = v; J->qkv_dtype = qkv_dtype;
+        J->alpha = alpha; J->beta = beta; J->gate_dtype = gate_dtype;
+        J->state_in = state_in; J->state_dtype = state_dtype;
+        J->out = out; J->state_out = state_out;
+        J->B = B; J->H = H; J->F = F; J->N = N; J->Dk = Dk; J->Dv = Dv;
+        J->key_scale = key_scale;
+        J->nthreads = nthreads; J->worker = w; J->status = 0;
+        if (nthreads > 1 && pthread_create(&tids[w], NULL, frame_worker_main, J) == 0)
+            running[w] = 1;
+        else
+            frame_worker_main(J);
+    }
+    for (int w = 0; w < nthreads; w++)
+        if (running[w])
+            pthread_join(tids[w], NULL);
+    for (int w = 0; w < nthreads; w++)
+        if (jobs[w].status)
+            status = -1;
+    free(running);
+    free(jobs);
+    free(tids);
+    return status;
+}

@@ -270,3 +270,119 @@ def test_inputs_recipe():
     x = np.array([1.0, 1.00390625, 1.01171875, -3.0e-3], dtype=np.float32)
     # RNE ties: 1+2^-8 rounds to 1 (even), 1+3*2^-8 rounds up to 1+2^-6
     assert list(gdn_inputs.bf16_bits_to_f32(gdn_inputs.f32_to_bf16_bits(x))[:3]) == [1.0, 1.0, 1.015625]
+
+
+# ---- frame-wise oracle (one decay per frame, the frame's tokens writing at once) ----
+
+def frame_case(seed, B=1, F=3, N=5, H=2, Dk=8, Dv=6, state=True):
+    r = rng(seed)
+    T = F * N
+    q = r.standard_normal((B, T, H, Dk))
+    k = r.standard_normal((B, T, H, Dk))
+    v = r.standard_normal((B, T, H, Dv))
+    a = r.uniform(0.3, 1.0, (B, F, H))
+    b = r.uniform(0.0, 1.0, (B, T, H))
+    s = r.standard_normal((B, H, Dk, Dv)) if state else None
+    return q, k, v, a, b, s
+
+
+@pytest.mark.parametrize("F,N", [(1, 1), (4, 1), (3, 5), (2, 17), (1, 40)])
+def test_f1_frame_oracle_equals_printed_compact_equation(F, N):
+    """The paper's compact update S_f = a S (I - K B K^T) + V B K^T written as
+    printed (matrix products, column-token orientation) against the oracle's
+    residual loop: catches a transposed state, a missing decay on the
+    prediction, a per-token instead of per-frame decay, or a readout from the
+    old state."""
+    q, k, v, a, b, s = frame_case(100 + 7 * F + N, F=F, N=N)
+    ks = 0.37
+    o, st = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks)
+    for h in range(q.shape[2]):
+        Y, S = framewise_forward(q[0, :, h], ks * k[0, :, h], v[0, :, h], a[0, :, h], b[0, :, h],
+                                 s[0, h].T, N=N)
+        assert rel(o[0, :, h], Y) < 1e-12
+        assert rel(st[0, h], S.T) < 1e-12
+
+
+def test_f2_one_token_frames_are_the_token_recurrence():
+    """With N = 1 and no key rescale the frame-wise update is the token-wise
+    one; ties the two oracles together."""
+    q, k, v, _, b, s = rand_case(11, T=30)
+    a = rng(12).uniform(0.2, 1.0, (1, 30, 2))
+    o1, s1 = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=1, key_scale=1.0)
+    o2, s2 = oracle.gdn_forward(q, k, v, a, b, s)
+    assert rel(o1, o2) < 1e-13 and rel(s1, s2) < 1e-13
+
+
+def test_f3_tokens_of_a_frame_write_simultaneously():
+    """Permuting the tokens inside every frame permutes their outputs and
+    leaves the state unchanged (a sequential in-frame update would not)."""
+    F, N = 3, 6
+    q, k, v, a, b, s = frame_case(13, F=F, N=N)
+    perm = np.concatenate([f * N + rng(14 + f).permutation(N) for f in range(F)])
+    o1, s1 = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.5)
+    o2, s2 = oracle.gdn_frame_forward(q[:, perm], k[:, perm], v[:, perm], a, b[:, perm], s,
+                                      frame_tokens=N, key_scale=0.5)
+    assert rel(o2, o1[:, perm]) < 1e-12 and rel(s2, s1) < 1e-12
+    # ... while the token-wise recurrence over the same tokens is order dependent
+    at = np.repeat(a, N, axis=1)
+    t1 = oracle.gdn_forward(q, k, v, at, b, s)[1]
+    t2 = oracle.gdn_forward(q[:, perm], k[:, perm], v[:, perm], at, b[:, perm], s)[1]
+    assert rel(t2, t1) > 1e-6
+
+
+def test_f4_no_write_only_decays():
+    """beta = 0: the state is the initial one times the product of the frame
+    decays, and every output reads the state of its own frame."""
+    F, N = 4, 3
+    q, k, v, a, _, s = frame_case(15, F=F, N=N)
+    b = np.zeros((1, F * N, 2))
+    o, st = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.8)
+    cum = np.cumprod(a[0], axis=0)                       # [F, H]
+    assert rel(st[0], cum[-1][:, None, None] * s[0]) < 1e-14
+    for f in range(F):
+        for h in range(2):
+            ref = q[0, f * N:(f + 1) * N, h] @ (cum[f, h] * s[0, h])
+            assert rel(o[0, f * N:(f + 1) * N, h], ref) < 1e-13
+
+
+@pytest.mark.parametrize("split", [1, 2, 3])
+def test_f5_streaming_split_at_frame_boundaries(split):
+    """Carrying the terminal state between calls split at a frame boundary is
+    the same computation as one call."""
+    F, N = 4, 5
+    q, k, v, a, b, s = frame_case(16, F=F, N=N)
+    o, st = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.4)
+    m = split * N
+    oa, sa = oracle.gdn_frame_forward(q[:, :m], k[:, :m], v[:, :m], a[:, :split], b[:, :m], s,
+                                      frame_tokens=N, key_scale=0.4)
+    ob, sb = oracle.gdn_frame_forward(q[:, m:], k[:, m:], v[:, m:], a[:, split:], b[:, m:], sa,
+                                      frame_tokens=N, key_scale=0.4)
+    assert np.array_equal(np.concatenate([oa, ob], axis=1), o) and np.array_equal(sb, st)
+
+
+def test_f6_frame_summaries_then_scan():
+    """The paper's frame-parallel rewrite: per frame P_f = I - K~^T B K~ and
+    A_f = K~^T B V, then H_f = a_f P_f H_{f-1} + A_f and Y_f = Q_f H_f."""
+    F, N = 3, 7
+    q, k, v, a, b, s = frame_case(17, F=F, N=N, Dk=6, Dv=5)
+    ks = 1.0 / np.sqrt(6 * N)
+    o, st = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N)   # default key scale
+    for h in range(2):
+        Hs = s[0, h].copy()
+        for f in range(F):
+            sl = slice(f * N, (f + 1) * N)
+            K = ks * k[0, sl, h]
+            Bm = np.diag(b[0, sl, h])
+            P = np.eye(6) - K.T @ Bm @ K
+            A = K.T @ Bm @ v[0, sl, h]
+            Hs = a[0, f, h] * P @ Hs + A
+            assert rel(o[0, sl, h], q[0, sl, h] @ Hs) < 1e-12
+        assert rel(st[0, h], Hs) < 1e-12
+
+
+def test_f7_frame_oracle_rejects_bad_arguments():
+    q, k, v, a, b, s = frame_case(18, F=2, N=4)
+    with pytest.raises(ValueError):
+        oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=3)      # T not whole frames
+    with pytest.raises(ValueError):
+        oracle.gdn_frame_forward(q, k, v, b, b, s, frame_tokens=4)      # alpha per token

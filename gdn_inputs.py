@@ -121,3 +121,57 @@ def make_inputs(workload, call=0, *, B=None, T=None, H=None, Dk=None, Dv=None,
     elif dtype != "f32":
         raise ValueError(dtype)
     return dict(q=q, k=k, v=v, alpha=alpha, beta=beta, state_in=state_in, dtype=dtype)
+
+
+def make_frame_inputs(workload, frames, *, frame_tokens=None, call=0, B=None, H=None, Dk=None,
+                      Dv=None, dtype=None, state=None, seed=None):
+    """Draw one call's inputs for the frame-wise forward: ``frames`` frames of
+    ``frame_tokens`` tokens (default 3520, one 44 x 80 latent frame), with the
+    value distributions of ``workload``.  The decay is drawn once per (b, frame,
+    h); everything else as in make_inputs, in the same order (q, k, v, the alpha
+    noise, the beta noise, state_in).  Returns the dict of make_inputs plus
+    "frame_tokens", with alpha of shape [B, F, H].
+    """
+    w = WORKLOADS[workload] if isinstance(workload, int) else workload
+    idx = WORKLOADS.index(w) if w in WORKLOADS else 99
+    B = w.B if B is None else B
+    H = w.H if H is None else H
+    Dk = w.Dk if Dk is None else Dk
+    Dv = w.Dv if Dv is None else Dv
+    N = 3520 if frame_tokens is None else int(frame_tokens)
+    F = int(frames)
+    T = F * N
+    dtype = w.dtype if dtype is None else dtype
+    state = w.state if state is None else state
+    rng = np.random.default_rng(500000 + 1000 * idx + call if seed is None else seed)
+
+    q = _unit_rows(rng.standard_normal((B, T, H, Dk), dtype=np.float32))
+    k = _unit_rows(rng.standard_normal((B, T, H, Dk), dtype=np.float32))
+    v = rng.standard_normal((B, T, H, Dv), dtype=np.float32)
+    if w.alpha.startswith("softplus"):
+        mu = float(w.alpha[len("softplus"):])
+        z = rng.standard_normal((B, F, H)).astype(np.float64) + mu
+        alpha = np.exp(-np.logaddexp(0.0, z)).astype(np.float32)
+    elif w.alpha == "uniform0.5":
+        alpha = rng.uniform(0.5, 1.0, (B, F, H)).astype(np.float32)
+    else:
+        raise ValueError(w.alpha)
+    if w.beta == "sigmoid":
+        z = rng.standard_normal((B, T, H)).astype(np.float64)
+        beta = (1.0 / (1.0 + np.exp(-z))).astype(np.float32)
+    elif w.beta == "uniform":
+        beta = rng.uniform(0.0, 1.0, (B, T, H)).astype(np.float32)
+    else:
+        raise ValueError(w.beta)
+    if state == "zero":
+        state_in = None
+    elif state == "normal0.02":
+        state_in = (0.02 * rng.standard_normal((B, H, Dk, Dv), dtype=np.float32)).astype(np.float32)
+    else:
+        raise ValueError(state)
+    if dtype == "bf16":
+        q, k, v = f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
+    elif dtype != "f32":
+        raise ValueError(dtype)
+    return dict(q=q, k=k, v=v, alpha=alpha, beta=beta, state_in=state_in, dtype=dtype,
+                frame_tokens=N)

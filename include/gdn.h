@@ -62,7 +62,7 @@ extern "C" {
 typedef enum {
     GDN_OK = 0,
     GDN_ERR_NULL = -1,        /* a required pointer is NULL */
-    GDN_ERR_SHAPE = -2,       /* B, H or T < 1, or an index would overflow */
+    GDN_ERR_SHAPE = -2,       /* a size < 1, or an index would overflow */
     GDN_ERR_UNSUPPORTED = -3, /* Dk/Dv not in {64,128} or chunk != 64 */
     GDN_ERR_WORKSPACE = -4,   /* workspace missing, too small or misaligned */
     GDN_ERR_HIP = -5,         /* a HIP runtime call or kernel launch failed */
@@ -159,6 +159,87 @@ int gdn_profile_stages(const void *q, const void *k, const void *v,
                        int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
                        int scan_group, void *ws, size_t ws_bytes, int reps, float *stage_ms,
                        void *stream);
+
+/*
+ * ---------------------------------------------------------------------------
+ * Frame-wise GDN forward: the paper's own form (Section "Frame-wise Gated
+ * DeltaNet", equations gdn_combined, appendix_gdn_kv_update and
+ * appendix_gdn_kv_compact; the three-phase kernel of Section "Efficient
+ * System Co-design" and its Algorithm).  The sequence is F frames of N tokens
+ * (T = F * N).  One decay alpha_f per (b, f, h) is shared by the frame's
+ * tokens, beta is per token, and all N tokens of a frame update the state at
+ * once, with keys multiplied by key_scale (the paper uses 1 / sqrt(Dk * N)):
+ *
+ *   with K~_f = key_scale K_f ([N][Dk]), B_f = diag(beta_f), H = S^T [Dk][Dv]:
+ *     H_f = alpha_f (I - K~_f^T B_f K~_f) H_{f-1} + K~_f^T B_f V_f
+ *     o_t = H_f^T q_t  for every token t of frame f (the readout after the
+ *                      frame's own update, without normalizer or gate)
+ *
+ * Layouts as for the token-wise calls, with T = F * N, except
+ *   alpha     [B][F][H]          fp32, one decay per frame and head.
+ * q, k, v, out, beta, state_in and state_out have the token-wise layouts; the
+ * state is H = S^T, fp32, carried in and out exactly as above (state_in ==
+ * state_out allowed).  Supported: B, H, F, N >= 1 with B*H <= 65535 and
+ * F*N + 64*F + N < 2^31; Dk, Dv in {64, 128}; any N (a frame need not be a
+ * multiple of 64 tokens).  key_scale is used as given (a non-finite value
+ * propagates).
+ *
+ * Evaluation: frame summaries G_f = K~^T B K~ and A_f = K~^T B V are formed in
+ * parallel over token splits of every frame (fp32 partial sums, reduced in a
+ * fixed order, so results are deterministic), the scan over frames runs one
+ * wave per (b, h, 16 state columns), and the output is parallel over tokens.
+ * The bf16 path rounds beta * k and beta * v, G_f, and the state operand of
+ * the products to bf16 (fp32 accumulation; the state itself stays fp32).
+ * Asynchronous on `stream`, errors as for the token-wise calls.
+ */
+int gdn_frame_forward(const void *q, const void *k, const void *v,
+                      const float *alpha, const float *beta, const float *state_in,
+                      void *out, float *state_out,
+                      int B, int H, int F, int N, int Dk, int Dv, float key_scale, void *stream);
+
+int gdn_frame_forward_f32(const float *q, const float *k, const float *v,
+                          const float *alpha, const float *beta, const float *state_in,
+                          float *out, float *state_out,
+                          int B, int H, int F, int N, int Dk, int Dv, float key_scale,
+                          void *stream);
+
+/*
+ * Token splits per frame used for the summaries (token_splits <= 0: the
+ * library's choice, about 512 summary workgroups; otherwise the value given,
+ * capped at ceil(N / 64) and reduced so that no split is empty).  0 for
+ * unsupported arguments.
+ */
+int gdn_frame_token_splits(int B, int H, int F, int N, int Dk, int Dv, int token_splits);
+
+/* Workspace bytes gdn_frame_forward_ex needs (0 for unsupported arguments). */
+size_t gdn_frame_workspace_bytes(int B, int H, int F, int N, int Dk, int Dv, int is_bf16,
+                                 int token_splits);
+
+/*
+ * Explicit workspace and token-split count (is_bf16 selects the element type
+ * of q, k, v and out).  `ws`: caller-owned device buffer, 256-byte aligned, at
+ * least gdn_frame_workspace_bytes(...) bytes; nothing is allocated.
+ */
+int gdn_frame_forward_ex(const void *q, const void *k, const void *v,
+                         const float *alpha, const float *beta, const float *state_in,
+                         void *out, float *state_out,
+                         int B, int H, int F, int N, int Dk, int Dv, float key_scale,
+                         int is_bf16, int token_splits, void *ws, size_t ws_bytes, void *stream);
+
+/*
+ * Per-stage timing of the frame-wise path (measurement aid, arguments as
+ * gdn_frame_forward_ex): each of the four stages is launched `reps` times back
+ * to back between two events; stage_ms[0..3] (host memory) receives the mean
+ * duration of one launch of [0] frame summaries, [1] reduction over splits,
+ * [2] scan over frames, [3] output.  state_in == state_out is rejected with
+ * GDN_ERR_ALIAS.  Synchronizes the stream.
+ */
+int gdn_frame_profile_stages(const void *q, const void *k, const void *v,
+                             const float *alpha, const float *beta, const float *state_in,
+                             void *out, float *state_out,
+                             int B, int H, int F, int N, int Dk, int Dv, float key_scale,
+                             int is_bf16, int token_splits, void *ws, size_t ws_bytes, int reps,
+                             float *stage_ms, void *stream);
 
 /* Static, human-readable text for a status code. */
 const char *gdn_status_string(int status);

@@ -8,7 +8,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libgdn.so")
 SOURCES = [os.path.join(CSRC, "gdn_api.hip")]
-HEADERS = [os.path.join(CSRC, f) for f in ("gdn_device.h", "gdn_kernels.h")] + \
+HEADERS = [os.path.join(CSRC, f) for f in ("gdn_device.h", "gdn_frame.h", "gdn_kernels.h")] + \
           [os.path.join(INCLUDE, "gdn.h")]
 
 HIPCC_FLAGS = [

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "gdn.h"
+#include "gdn_frame.h"
 #include "gdn_kernels.h"
 
 namespace {
@@ -323,6 +324,217 @@ int run_cached(const void *q, const void *k, const void *v, const float *alpha, 
                need, stream, nullptr);
 }
 
+// ---------------------------------------------------------------------------
+// Frame-wise path (gdn_frame_forward*): frame summaries, their reduction over
+// token splits, the scan over frames, and the output.
+
+struct FrameWs {
+    size_t PG, PA, Gf, Af, Hf, total;
+};
+
+int frame_blocks(int N) { return (N + 63) / 64; }
+
+// Token splits per frame: a split is a whole number of 64-token blocks, and
+// the library's choice (token_splits <= 0) aims at about 2 * 256 summary
+// workgroups, two halves per split.
+int frame_splits(long long units, int N, int token_splits) {
+    const int nb = frame_blocks(N);
+    int ns = token_splits;
+    if (ns <= 0) ns = (int)((256 + units - 1) / units);
+    if (ns > nb) ns = nb;
+    if (ns < 1) ns = 1;
+    const int per = (nb + ns - 1) / ns;   // blocks per split
+    return (nb + per - 1) / per;          // no empty split
+}
+
+FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS) {
+    const size_t bhf = (size_t)B * H * F;
+    FrameWs L;
+    size_t off = 0;
+    L.PG = off; off = align256(off + bhf * NS * Dk * Dk * 4);
+    L.PA = off; off = align256(off + bhf * NS * Dk * Dv * 4);
+    L.Gf = off; off = align256(off + bhf * Dk * Dk * esz);
+    L.Af = off; off = align256(off + bhf * Dk * Dv * 4);
+    L.Hf = off; off = align256(off + bhf * Dk * Dv * esz);
+    L.total = off;
+    return L;
+}
+
+template <class E> constexpr int frame_out_tokens() { return 64 * gdn::FrameOutNTW<E>::value; }
+
+bool frame_shape_ok(int B, int H, int F, int N, size_t esz) {
+    if (B < 1 || H < 1 || F < 1 || N < 1) return false;
+    const long long bh = (long long)B * H;
+    if (bh > 65535) return false;
+    // token indices (and a split's end, up to 64 * F past the last token) fit in int
+    if ((long long)F * N + 64LL * F + N > 0x7fffffffLL) return false;
+    // grid sizes of the summary and output kernels stay below 2^31
+    const long long units = bh * F;
+    const long long ob = (N + (esz == 2 ? 255 : 127)) / (esz == 2 ? 256 : 128);
+    if (16LL * frame_blocks(N) * ((units + 7) / 8) > 0x7fffffffLL) return false;
+    if (8LL * ob * ((units + 7) / 8) > 0x7fffffffLL) return false;
+    return true;
+}
+
+bool frame_dims_ok(int Dk, int Dv) { return (Dk == 64 || Dk == 128) && (Dv == 64 || Dv == 128); }
+
+int frame_validate(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                   const float *state_in, const void *out, const float *state_out, int B, int H, int F,
+                   int N, int Dk, int Dv, size_t esz) {
+    if (!q || !k || !v || !alpha || !beta || !out) return GDN_ERR_NULL;
+    if (!frame_shape_ok(B, H, F, N, esz)) return GDN_ERR_SHAPE;
+    if (!frame_dims_ok(Dk, Dv)) return GDN_ERR_UNSUPPORTED;
+    if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(alpha) || misaligned(beta) ||
+        misaligned(state_in) || misaligned(out) || misaligned(state_out))
+        return GDN_ERR_ALIGN;
+    const size_t ntok = (size_t)B * F * N * H;
+    const Range rq = range(q, ntok * Dk * esz), rk = range(k, ntok * Dk * esz),
+                rv = range(v, ntok * Dv * esz), ra = range(alpha, (size_t)B * F * H * 4),
+                rb = range(beta, ntok * 4), ro = range(out, ntok * Dv * esz);
+    const size_t sbytes = (size_t)B * H * Dk * Dv * 4;
+    const Range rsi = range(state_in, sbytes), rso = range(state_out, sbytes);
+    const Range ins[] = {rq, rk, rv, ra, rb, rsi};
+    for (const Range &r : ins)
+        if (ro.overlaps(r)) return GDN_ERR_ALIAS;
+    if (rso.valid()) {
+        for (int i = 0; i < 5; ++i)
+            if (rso.overlaps(ins[i])) return GDN_ERR_ALIAS;
+        if (rso.overlaps(ro)) return GDN_ERR_ALIAS;
+        if (rsi.valid() && rso.overlaps(rsi) && rso.lo != rsi.lo) return GDN_ERR_ALIAS;
+    }
+    return GDN_OK;
+}
+
+template <class E>
+gdn::FrameParams<E> make_frame_params(const void *q, const void *k, const void *v, const float *alpha,
+                                      const float *beta, const float *state_in, void *out,
+                                      float *state_out, int B, int H, int F, int N, int Dk, int Dv,
+                                      float key_scale, int NS, void *ws) {
+    gdn::FrameParams<E> p;
+    p.q = (const E *)q;
+    p.k = (const E *)k;
+    p.v = (const E *)v;
+    p.alpha = alpha;
+    p.beta = beta;
+    p.state_in = state_in;
+    p.out = (E *)out;
+    p.state_out = state_out;
+    p.B = B;
+    p.H = H;
+    p.F = F;
+    p.N = N;
+    p.NS = NS;
+    p.NBT = 64 * ((frame_blocks(N) + NS - 1) / NS);
+    p.OB = (N + frame_out_tokens<E>() - 1) / frame_out_tokens<E>();
+    p.key_scale = key_scale;
+    const FrameWs L = frame_ws_layout(B, H, F, Dk, Dv, sizeof(E), NS);
+    unsigned char *base = (unsigned char *)ws;
+    p.PG = (float *)(base + L.PG);
+    p.PA = (float *)(base + L.PA);
+    p.Gf = (E *)(base + L.Gf);
+    p.Af = (float *)(base + L.Af);
+    p.Hf = (E *)(base + L.Hf);
+    return p;
+}
+
+constexpr int kFrameStages = 4;  // summaries, reduction, scan, output
+
+template <class E, int DK, int DV>
+hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, hipEvent_t *ev) {
+    using LS = gdn::FrameSumLds<E, DK, DV>;
+    using LO = gdn::FrameOutLds<E, DK, DV>;
+    static std::once_flag attr_once;
+    static hipError_t attr_err = hipSuccess;
+    std::call_once(attr_once, [&] {
+        hipError_t e = hipFuncSetAttribute((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)LS::bytes);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)gdn::gdn_frame_output_kernel<E, DK, DV>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)LO::bytes);
+        attr_err = e;
+    });
+    if (attr_err != hipSuccess) return attr_err;
+    const long long BH = (long long)p.B * p.H, units = BH * p.F;
+    constexpr int NI = (DK / 16) * (DK / 32) + (DK / 16) * (DV / 16);  // reduction items per unit
+    auto stage = [&](int i) {
+        switch (i) {
+        case 0:
+            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV>),
+                               dim3(gdn::frame_summary_blocks(units * p.NS)), dim3(256), LS::bytes, s, p);
+            break;
+        case 1:
+            hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV>), dim3((unsigned)units, (NI + 3) / 4),
+                               dim3(256), 0, s, p);
+            break;
+        case 2:
+            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV>), dim3(gdn::xcd_blocks(BH, DV / 16)),
+                               dim3(64), 0, s, p);
+            break;
+        default:
+            hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV>), dim3(gdn::xcd_blocks(units, p.OB)),
+                               dim3(256), LO::bytes, s, p);
+        }
+    };
+    hipError_t er = hipSuccess;
+    for (int i = 0; i < kFrameStages && er == hipSuccess; ++i) {
+        if (!ev) {
+            stage(i);
+            continue;
+        }
+        er = hipEventRecord(ev[2 * i], s);
+        for (int r = 0; r < reps && er == hipSuccess; ++r) stage(i);
+        if (er == hipSuccess) er = hipEventRecord(ev[2 * i + 1], s);
+    }
+    const hipError_t le = hipGetLastError();
+    return le != hipSuccess ? le : er;
+}
+
+template <class E>
+hipError_t frame_dispatch(const gdn::FrameParams<E> &p, int Dk, int Dv, hipStream_t s, int reps, hipEvent_t *ev) {
+    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128>(p, s, reps, ev);
+    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64>(p, s, reps, ev);
+    return launch_frame<E, 64, 128>(p, s, reps, ev);
+}
+
+int frame_run(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+              const float *state_in, void *out, float *state_out, int B, int H, int F, int N, int Dk,
+              int Dv, float key_scale, bool bf16, int token_splits, void *ws, size_t ws_bytes, void *stream,
+              int reps, hipEvent_t *ev) {
+    const size_t esz = bf16 ? 2 : 4;
+    int st = frame_validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, esz);
+    if (st != GDN_OK) return st;
+    const int NS = frame_splits((long long)B * H * F, N, token_splits);
+    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < frame_ws_layout(B, H, F, Dk, Dv, esz, NS).total)
+        return GDN_ERR_WORKSPACE;
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e;
+    if (bf16)
+        e = frame_dispatch(make_frame_params<uint16_t>(q, k, v, alpha, beta, state_in, out, state_out, B, H, F,
+                                                       N, Dk, Dv, key_scale, NS, ws),
+                           Dk, Dv, s, reps, ev);
+    else
+        e = frame_dispatch(make_frame_params<float>(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N,
+                                                    Dk, Dv, key_scale, NS, ws),
+                           Dk, Dv, s, reps, ev);
+    return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
+}
+
+int frame_run_cached(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                     const float *state_in, void *out, float *state_out, int B, int H, int F, int N, int Dk,
+                     int Dv, float key_scale, bool bf16, void *stream) {
+    const size_t esz = bf16 ? 2 : 4;
+    int st = frame_validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, esz);
+    if (st != GDN_OK) return st;
+    const size_t need =
+        frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, 0)).total;
+    void *ws = nullptr;
+    st = cached_workspace(need, &ws);
+    if (st != GDN_OK) return st;
+    return frame_run(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale, bf16, 0,
+                     ws, need, stream, 1, nullptr);
+}
+
 }  // namespace
 
 extern "C" {
@@ -413,11 +625,72 @@ int gdn_profile_stages(const void *q, const void *k, const void *v, const float 
     return status;
 }
 
+int gdn_frame_forward(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                      const float *state_in, void *out, float *state_out, int B, int H, int F, int N,
+                      int Dk, int Dv, float key_scale, void *stream) {
+    return frame_run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
+                            true, stream);
+}
+
+int gdn_frame_forward_f32(const float *q, const float *k, const float *v, const float *alpha,
+                          const float *beta, const float *state_in, float *out, float *state_out, int B,
+                          int H, int F, int N, int Dk, int Dv, float key_scale, void *stream) {
+    return frame_run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
+                            false, stream);
+}
+
+int gdn_frame_token_splits(int B, int H, int F, int N, int Dk, int Dv, int token_splits) {
+    if (!frame_shape_ok(B, H, F, N, 2) || !frame_dims_ok(Dk, Dv)) return 0;
+    return frame_splits((long long)B * H * F, N, token_splits);
+}
+
+size_t gdn_frame_workspace_bytes(int B, int H, int F, int N, int Dk, int Dv, int is_bf16, int token_splits) {
+    const size_t esz = is_bf16 ? 2 : 4;
+    if (!frame_shape_ok(B, H, F, N, esz) || !frame_dims_ok(Dk, Dv)) return 0;
+    return frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, token_splits)).total;
+}
+
+int gdn_frame_forward_ex(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                         const float *state_in, void *out, float *state_out, int B, int H, int F, int N,
+                         int Dk, int Dv, float key_scale, int is_bf16, int token_splits, void *ws,
+                         size_t ws_bytes, void *stream) {
+    return frame_run(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
+                     is_bf16 != 0, token_splits, ws, ws_bytes, stream, 1, nullptr);
+}
+
+int gdn_frame_profile_stages(const void *q, const void *k, const void *v, const float *alpha,
+                             const float *beta, const float *state_in, void *out, float *state_out, int B,
+                             int H, int F, int N, int Dk, int Dv, float key_scale, int is_bf16,
+                             int token_splits, void *ws, size_t ws_bytes, int reps, float *stage_ms,
+                             void *stream) {
+    if (!stage_ms || reps < 1) return GDN_ERR_NULL;
+    if (state_in && state_in == state_out) return GDN_ERR_ALIAS;
+    hipEvent_t ev[2 * kFrameStages] = {};
+    int status = GDN_OK;
+    for (auto &e : ev)
+        if (status == GDN_OK && hipEventCreate(&e) != hipSuccess) {
+            e = nullptr;
+            status = GDN_ERR_HIP;
+        }
+    if (status == GDN_OK)
+        status = frame_run(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
+                           is_bf16 != 0, token_splits, ws, ws_bytes, stream, reps, ev);
+    if (status == GDN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess) status = GDN_ERR_HIP;
+    for (int i = 0; i < kFrameStages && status == GDN_OK; ++i) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]) != hipSuccess) status = GDN_ERR_HIP;
+        stage_ms[i] = ms / reps;
+    }
+    for (auto &e : ev)
+        if (e) (void)hipEventDestroy(e);
+    return status;
+}
+
 const char *gdn_status_string(int status) {
     switch (status) {
     case GDN_OK: return "ok";
     case GDN_ERR_NULL: return "a required pointer is NULL";
-    case GDN_ERR_SHAPE: return "invalid shape (B, H, T must be >= 1 and B*H <= 65535)";
+    case GDN_ERR_SHAPE: return "invalid shape (sizes must be >= 1, B*H <= 65535, token and grid indices within int range)";
     case GDN_ERR_UNSUPPORTED: return "unsupported configuration (Dk, Dv in {64,128}; chunk == 64)";
     case GDN_ERR_WORKSPACE: return "workspace missing, too small or not 256-byte aligned";
     case GDN_ERR_HIP: return "HIP runtime error or kernel launch failure";

@@ -51,6 +51,19 @@ def lib():
         L.gdn_chunk_forward_ex.argtypes = core + [i, i, vp, sz, vp]
         L.gdn_profile_stages.restype = i
         L.gdn_profile_stages.argtypes = core + [i, i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        fl = ctypes.c_float
+        fcore = [vp, vp, vp, f_p, f_p, f_p, vp, f_p, i, i, i, i, i, i, fl]
+        for name in ("gdn_frame_forward", "gdn_frame_forward_f32"):
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = i, fcore + [vp]
+        L.gdn_frame_token_splits.restype = i
+        L.gdn_frame_token_splits.argtypes = [i, i, i, i, i, i, i]
+        L.gdn_frame_workspace_bytes.restype = sz
+        L.gdn_frame_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
+        L.gdn_frame_forward_ex.restype = i
+        L.gdn_frame_forward_ex.argtypes = fcore + [i, i, vp, sz, vp]
+        L.gdn_frame_profile_stages.restype = i
+        L.gdn_frame_profile_stages.argtypes = fcore + [i, i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
         L.gdn_status_string.restype = ctypes.c_char_p
         L.gdn_status_string.argtypes = [i]
         _lib = L
@@ -74,8 +87,9 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _check(q, k, v, alpha, beta, state_in, out, state_out):
-    """Shape/dtype/device/contiguity checks; returns (B, H, T, Dk, Dv, is_bf16)."""
+def _check(q, k, v, alpha, beta, state_in, out, state_out, frame_tokens=None):
+    """Shape/dtype/device/contiguity checks; returns (B, H, T, Dk, Dv, is_bf16).
+    With frame_tokens = N, alpha is one decay per frame, [B, T / N, H]."""
     if q.dtype not in (torch.bfloat16, torch.float32):
         raise TypeError(f"q must be bfloat16 or float32, got {q.dtype}")
     for name, t in (("k", k), ("v", v), ("out", out)):
@@ -99,8 +113,15 @@ def _check(q, k, v, alpha, beta, state_in, out, state_out):
     Dv = v.shape[-1]
     if tuple(k.shape) != (B, T, H, Dk) or tuple(v.shape) != (B, T, H, Dv):
         raise ValueError("k must be [B, T, H, Dk] and v [B, T, H, Dv]")
-    if tuple(alpha.shape) != (B, T, H) or tuple(beta.shape) != (B, T, H):
-        raise ValueError("alpha and beta must be [B, T, H]")
+    if frame_tokens is None:
+        if tuple(alpha.shape) != (B, T, H) or tuple(beta.shape) != (B, T, H):
+            raise ValueError("alpha and beta must be [B, T, H]")
+    else:
+        N = int(frame_tokens)
+        if N < 1 or T % N:
+            raise ValueError("T must be a whole number of frames of frame_tokens tokens")
+        if tuple(alpha.shape) != (B, T // N, H) or tuple(beta.shape) != (B, T, H):
+            raise ValueError("alpha must be [B, F, H] (one decay per frame) and beta [B, T, H]")
     for name, t in (("state_in", state_in), ("state_out", state_out)):
         if t is not None and tuple(t.shape) != (B, H, Dk, Dv):
             raise ValueError(f"{name} must be [B, H, Dk, Dv]")
@@ -206,4 +227,94 @@ def forward(q, k, v, alpha, beta, state_in=None, *, out=None, state_out=None, wa
     else:
         fn = gdn_chunk_forward_ws if bf else gdn_chunk_forward_f32_ws
         fn(q, k, v, alpha, beta, state_in, out, state_out, ws, chunk=chunk, stream=stream)
+    return out, state_out
+
+
+# ---------------------------------------------------------------------------
+# Frame-wise GDN (gdn_frame_* in include/gdn.h): F frames of N tokens, one
+# decay per frame, all tokens of a frame written at once, keys multiplied by
+# key_scale (default 1 / sqrt(Dk * N)).
+
+FRAME_STAGE_NAMES = ("summaries", "reduce", "scan", "output")
+
+
+def default_key_scale(Dk, frame_tokens):
+    return 1.0 / float(Dk * frame_tokens) ** 0.5
+
+
+def gdn_frame_token_splits(B, H, F, N, Dk, Dv, token_splits=0):
+    return int(lib().gdn_frame_token_splits(B, H, F, N, Dk, Dv, int(token_splits)))
+
+
+def gdn_frame_workspace_bytes(B, H, F, N, Dk, Dv, is_bf16=True, token_splits=0):
+    return int(lib().gdn_frame_workspace_bytes(B, H, F, N, Dk, Dv, 1 if is_bf16 else 0,
+                                               int(token_splits)))
+
+
+def frame_workspace(q, v, frame_tokens, token_splits=0):
+    """Workspace tensor for gdn_frame_forward_ex on inputs shaped like q and v."""
+    B, T, H, Dk = q.shape
+    N = int(frame_tokens)
+    n = gdn_frame_workspace_bytes(B, H, T // N, N, Dk, v.shape[-1], q.dtype == torch.bfloat16,
+                                  token_splits)
+    if n == 0:
+        raise ValueError("unsupported shape for the frame-wise GDN forward")
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
+def _frame_call(name, q, k, v, alpha, beta, state_in, out, state_out, frame_tokens, key_scale,
+                extra, stream):
+    B, H, T, Dk, Dv, _ = _check(q, k, v, alpha, beta, state_in, out, state_out, frame_tokens)
+    N = int(frame_tokens)
+    ks = default_key_scale(Dk, N) if key_scale is None else float(key_scale)
+    with torch.cuda.device(q.device):
+        rc = getattr(lib(), name)(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(beta), _ptr(state_in),
+                                  _ptr(out), _ptr(state_out), B, H, T // N, N, Dk, Dv,
+                                  ctypes.c_float(ks), *extra, _stream(q.device, stream))
+    if rc != GDN_OK:
+        raise GdnError(name, rc)
+
+
+def gdn_frame_forward_ex(q, k, v, alpha, beta, state_in, out, state_out, ws, frame_tokens,
+                         key_scale=None, token_splits=0, stream=None):
+    """Either element type (q's dtype selects), explicit workspace and token-split count."""
+    is_bf16 = q.dtype == torch.bfloat16
+    _frame_call("gdn_frame_forward_ex", q, k, v, alpha, beta, state_in, out, state_out, frame_tokens,
+                key_scale, (1 if is_bf16 else 0, int(token_splits), _ptr(ws), ws.numel()), stream)
+
+
+def gdn_frame_profile_stages(q, k, v, alpha, beta, state_in, out, state_out, ws, frame_tokens,
+                             key_scale=None, token_splits=0, reps=20, stream=None):
+    """Mean per-stage durations in ms over `reps` runs, in the order of FRAME_STAGE_NAMES."""
+    is_bf16 = q.dtype == torch.bfloat16
+    ms = (ctypes.c_float * len(FRAME_STAGE_NAMES))()
+    _frame_call("gdn_frame_profile_stages", q, k, v, alpha, beta, state_in, out, state_out,
+                frame_tokens, key_scale,
+                (1 if is_bf16 else 0, int(token_splits), _ptr(ws), ws.numel(), int(reps), ms), stream)
+    return [float(x) for x in ms]
+
+
+def frame_forward(q, k, v, alpha, beta, state_in=None, *, frame_tokens, key_scale=None, out=None,
+                  state_out=None, want_state=True, ws=None, token_splits=None, stream=None):
+    """Frame-wise GDN forward.  q, k [B,T,H,Dk], v [B,T,H,Dv] (bf16 or fp32, on the GPU) with
+    T = F * frame_tokens; alpha [B,F,H] and beta [B,T,H] fp32; state_in [B,H,Dk,Dv] fp32 or
+    None.  key_scale None means 1 / sqrt(Dk * frame_tokens).  With ws or token_splits given,
+    gdn_frame_forward_ex runs; otherwise the library-cached workspace is used.
+    Returns (out [B,T,H,Dv] like v, state_out [B,H,Dk,Dv] fp32 or None)."""
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if out is None:
+        out = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    if state_out is None and want_state:
+        state_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+    if ws is not None or token_splits is not None:
+        ts = 0 if token_splits is None else int(token_splits)
+        if ws is None:
+            ws = frame_workspace(q, v, frame_tokens, ts)
+        gdn_frame_forward_ex(q, k, v, alpha, beta, state_in, out, state_out, ws, frame_tokens,
+                             key_scale, ts, stream)
+    else:
+        name = "gdn_frame_forward" if q.dtype == torch.bfloat16 else "gdn_frame_forward_f32"
+        _frame_call(name, q, k, v, alpha, beta, state_in, out, state_out, frame_tokens, key_scale,
+                    (), stream)
     return out, state_out

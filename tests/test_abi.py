@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 10 and "gdn_workspace_bytes" in names, names
+    assert len(names) == 16 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -119,3 +119,63 @@ def test_binding_rejects_bad_tensors_on_cpu():
         gdn.forward(q, q, q, torch.zeros(1, 64, 2), torch.zeros(1, 64, 2))
     with pytest.raises(TypeError):
         gdn.forward(q.half(), q, q, torch.zeros(1, 64, 2), torch.zeros(1, 64, 2))
+
+
+def test_frame_token_splits_and_workspace():
+    ts = gdn.gdn_frame_token_splits
+    assert ts(1, 16, 3, 3520, 128, 128) == 6             # 48 (frame, head) units: ceil(256 / 48)
+    assert ts(1, 16, 1, 3520, 128, 128) == 14            # 55 blocks, 4 per split
+    assert ts(1, 16, 3, 3520, 128, 128, 1) == 1
+    assert ts(1, 16, 3, 3520, 128, 128, 1000) == 55      # at most one 64-token block per split
+    assert ts(1, 2, 1, 100, 64, 64, 5) == 2
+    assert ts(1, 2, 1, 1, 64, 64) == 1
+    assert ts(0, 2, 1, 1, 64, 64) == 0
+    assert ts(1, 2, 1, 1, 96, 64) == 0
+    wb = gdn.gdn_frame_workspace_bytes
+    bhf = 16 * 3
+    n = wb(1, 16, 3, 3520, 128, 128, True, 1)
+    expect = bhf * (2 * 128 * 128 * 4 + 128 * 128 * (2 + 4 + 2))
+    assert expect <= n < expect + 5 * 256
+    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 128 * 128 * 4
+    assert wb(1, 16, 3, 3520, 128, 128, False, 1) > n
+    assert wb(1, 16, 3, 0, 128, 128, True, 0) == 0
+    assert wb(1, 16, 3, 3520, 128, 32, True, 0) == 0
+
+
+def fcall(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, a=BASE + 192 * MB, b=BASE + 200 * MB,
+          si=None, o=BASE + 256 * MB, so=None, B=1, H=2, F=2, N=100, Dk=64, Dv=64, ks=0.1,
+          ws=None, ws_bytes=0):
+    L = gdn.lib()
+    args = [q, k, v, a, b, si, o, so, B, H, F, N, Dk, Dv, ctypes.c_float(ks)]
+    if fn.endswith("_ex"):
+        args += [1, 0, ws, ws_bytes]
+    return getattr(L, fn)(*args, None)
+
+
+@pytest.mark.parametrize("fn", ["gdn_frame_forward", "gdn_frame_forward_f32", "gdn_frame_forward_ex"])
+def test_frame_validation_errors(fn):
+    assert fcall(fn, q=None) == -1
+    assert fcall(fn, a=None) == -1
+    assert fcall(fn, o=None) == -1
+    assert fcall(fn, F=0) == -2
+    assert fcall(fn, N=0) == -2
+    assert fcall(fn, H=300, B=300) == -2
+    assert fcall(fn, F=1 << 16, N=1 << 16) == -2         # token index beyond int
+    assert fcall(fn, Dk=96) == -3
+    assert fcall(fn, Dv=32) == -3
+    assert fcall(fn, b=BASE + 200 * MB + 4) == -6
+    assert fcall(fn, o=BASE + 4096) == -7                # out overlaps q
+    assert fcall(fn, o=BASE + 192 * MB) == -7            # out overlaps alpha
+    assert fcall(fn, so=BASE + 128 * MB) == -7           # state_out overlaps v
+    assert fcall(fn, si=BASE + 300 * MB, so=BASE + 300 * MB + 4096) == -7
+    if fn.endswith("_ex"):
+        assert fcall(fn) == -4
+        assert fcall(fn, ws=BASE + 512 * MB, ws_bytes=100) == -4
+        assert fcall(fn, ws=BASE + 512 * MB + 16, ws_bytes=1 << 30) == -4
+
+
+def test_frame_binding_rejects_bad_tensors_on_cpu():
+    import torch
+    q = torch.zeros(1, 100, 2, 64)
+    with pytest.raises(ValueError):
+        gdn.frame_forward(q, q, q, torch.zeros(1, 2, 2), torch.zeros(1, 100, 2), frame_tokens=50)

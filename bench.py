@@ -11,6 +11,12 @@ Prints ONE JSON line.  Besides throughput it reports the roofline of the
 dominant kernel (per-stage durations from HIP events recorded on the stream
 the kernels run on) and, on rank 0, the fp64 CPU oracle timed on the host
 cores as a reported baseline.
+
+``--path frame`` measures the frame-wise forward instead (one decay per frame,
+all tokens of a frame written at once): a step is one streaming call of 3
+latent frames of 44x80 tokens, B=1, F=3, N=3520, H=16, Dk=Dv=128, bf16, with
+the fp32 state carried in and out; its four kernels are the frame summaries,
+their reduction over token splits, the scan over frames and the output.
 """
 import argparse
 import json
@@ -113,10 +119,10 @@ def cpu_baseline(inp, B, T, min_seconds=10.0):
                       f"fp64 token recurrence, {elapsed:.1f} s"}
 
 
-def load_traffic(stage):
+def load_traffic(stage, summary="traffic_frame1280x704.json"):
     """HBM traffic per launch of `stage`'s kernel from the committed counter summary,
     or None when the summary is missing or was taken on different kernel source."""
-    path = os.path.join(ROOT, "profiles", "traffic_frame1280x704.json")
+    path = os.path.join(ROOT, "profiles", summary)
     if not os.path.exists(path):
         return None
     try:
@@ -133,6 +139,114 @@ def load_traffic(stage):
         return None
 
 
+FRAME_METRIC = ("frame-wise GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, "
+                "H=16, D=128 bf16")
+FRAME_KERNELS = {"summaries": "gdn_frame_summary_kernel", "reduce": "gdn_frame_reduce_kernel",
+                 "scan": "gdn_frame_scan_kernel", "output": "gdn_frame_output_kernel"}
+
+
+def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2):
+    """Per-stage algorithmic flops and bytes of the frame-wise path (each stage's own
+    inputs and outputs, workspace included, every byte once) and its external I/O.
+
+    summaries: G = K^T B K and A = K^T B V over every token (fp32 partial tiles per
+    token split); reduce: the splits' partials -> G (operand fragments) and A;
+    scan: H_f = alpha (H - G H) + A per frame; output: O = Q H_f per token."""
+    n = B * F * N * H                   # token-heads
+    u = B * H * F                       # (frame, head) units
+    st = B * H * Dk * Dv * 4
+    part = u * NS * Dk * (Dk + Dv) * 4
+    f = {"summaries": 2.0 * n * Dk * (Dk + Dv),
+         "reduce": float(u * NS * Dk * (Dk + Dv)),
+         "scan": u * (2.0 * Dk * Dk * Dv + 3.0 * Dk * Dv),
+         "output": 2.0 * n * Dk * Dv}
+    b = {"summaries": n * ((Dk + Dv) * esz + 4) + part,
+         "reduce": part + u * (Dk * Dk * esz + Dk * Dv * 4),
+         "scan": u * (Dk * Dk * esz + Dk * Dv * 4 + 4 + Dk * Dv * esz) + 2 * st,
+         "output": n * (Dk + Dv) * esz + u * Dk * Dv * esz}
+    io_bytes = n * ((2 * Dk + 2 * Dv) * esz + 4) + u * 4 + 2 * st
+    return dict(flops=f, bytes=b, io_bytes=io_bytes)
+
+
+def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0):
+    """Time the fp64 frame-wise oracle (as it stands) on whole calls for ~10 s."""
+    import oracle
+    threads = host_threads()
+    reps, elapsed = 0, 0.0
+    while elapsed < min_seconds and reps < 50:
+        t0 = time.perf_counter()
+        oracle.gdn_frame_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
+                                 inp["state_in"], frame_tokens=inp["frame_tokens"], nthreads=threads)
+        elapsed += time.perf_counter() - t0
+        reps += 1
+    return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H={H}, D={Dk}), "
+                      f"fp64 frame-wise recurrence, {elapsed:.1f} s"}
+
+
+def run_frame(args, torch, gdn, dev, to_dev, timed):
+    F, N = 3, 3520
+    inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02")
+    B, T, H, Dk = inp["q"].shape
+    Dv = inp["v"].shape[-1]
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
+    out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
+    s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
+    ts = args.token_splits
+    ws = gdn.frame_workspace(q, v, N, ts)
+    NS = gdn.gdn_frame_token_splits(B, H, F, N, Dk, Dv, ts)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        gdn.gdn_frame_forward_ex(q, k, v, alpha, beta, s_in, out, s_out, ws, N, token_splits=ts,
+                                 stream=stream)
+
+    ms_per_step, cold_ms = timed(step, stream)
+    stage_ms = gdn.gdn_frame_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws, N,
+                                            token_splits=ts, reps=args.steps, stream=stream)
+    names = dict(zip(gdn.FRAME_STAGE_NAMES, stage_ms))
+    torch.cuda.synchronize()
+    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS)
+    sec = ms_per_step / 1e3
+    tflops = sum(cnt["flops"].values()) / sec / 1e12
+    dom = max(names, key=names.get)
+    roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
+    roofline.update({"traffic": load_traffic(dom, "traffic_frames3x1280x704.json"),
+                     "kernel": FRAME_KERNELS[dom], "duration_ms": round(names[dom], 5),
+                     "algorithmic_flops_per_launch": cnt["flops"][dom],
+                     "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
+    stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_) for k_, v_ in names.items()}
+    rec = {
+        "metric": FRAME_METRIC,
+        "value": round(B * T / sec, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "frame-wise streaming call of 3 latent 1280x704 frames: B=1 F=3 "
+                               "N=3520 (44x80) H=16 Dk=Dv=128, bf16 q/k/v, one decay per frame, "
+                               "key scale 1/sqrt(Dk N), fp32 state in/out",
+                   "B": B, "F": F, "N": N, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "token_splits": NS},
+        "tflops": round(tflops, 2),
+        "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "hbm_frac_io": round(cnt["io_bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
+        "ms_per_step_cold": None if cold_ms is None else round(cold_ms, 5),
+        "stage_ms": {k_: round(v_, 5) for k_, v_ in names.items()},
+        "stage_roofline": {k_: (v_["bound"], v_["frac"]) for k_, v_ in stage_roofs.items()},
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk)
+    print(json.dumps(rec), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -144,6 +258,10 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a known-size "
                          "reference for hardware traffic counters)")
+    ap.add_argument("--path", choices=("token", "frame"), default="token",
+                    help="token: the token-wise chunk forward (default); frame: the frame-wise forward")
+    ap.add_argument("--token-splits", type=int, default=0,
+                    help="frame path: token splits per frame (0 = the library's choice)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -154,9 +272,6 @@ def main():
     import torch
     import paper_2605_30409_amd as gdn
 
-    w = gdn_inputs.WORKLOADS[WORKLOAD]
-    B, T, H, Dk, Dv, C = w.B, w.T, w.H, w.Dk, w.Dv, w.chunk
-    inp = gdn_inputs.make_inputs(WORKLOAD)
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
 
@@ -165,12 +280,6 @@ def main():
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
         return torch.from_numpy(a).to(dev)
 
-    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
-    alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
-    out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
-    s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
-    ws = gdn.workspace(q, v)
-    stream = torch.cuda.current_stream(dev)
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 18  # float32 elements
         src = torch.ones(n, dtype=torch.float32, device=dev)
@@ -180,41 +289,60 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    def timed(step, stream):
+        """Warmup, then `steps` timed steps between two events on `stream`, then
+        cold-cache steps (each after a 1 GiB write that evicts L2 and MALL)."""
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        cold = None
+        if args.cold_steps > 0:
+            scratch = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+            times = []
+            for i in range(args.cold_steps):
+                scratch.fill_(float(i))
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                step()
+                b.record(stream)
+                torch.cuda.synchronize()
+                times.append(a.elapsed_time(b))
+            cold = float(np.median(times))
+            del scratch
+        return ms, cold
+
+    if args.path == "frame":
+        run_frame(args, torch, gdn, dev, to_dev, timed)
+        return
+
+    w = gdn_inputs.WORKLOADS[WORKLOAD]
+    B, T, H, Dk, Dv, C = w.B, w.T, w.H, w.Dk, w.Dv, w.chunk
+    inp = gdn_inputs.make_inputs(WORKLOAD)
+
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
+    out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
+    s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
+    ws = gdn.workspace(q, v)
+    stream = torch.cuda.current_stream(dev)
+
     def step():
         gdn.gdn_chunk_forward_ws(q, k, v, alpha, beta, s_in, out, s_out, ws, chunk=C, stream=stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    for _ in range(args.steps):
-        step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = e0.elapsed_time(e1) / args.steps
+    ms_per_step, cold_ms = timed(step, stream)
 
     # Per-stage durations: HIP events recorded by the library on the same stream.
     stage_ms = gdn.gdn_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws,
                                       reps=args.steps, chunk=C, stream=stream)
     names = dict(zip(gdn.STAGE_NAMES, stage_ms))
     torch.cuda.synchronize()
-
-    # Cold-cache steps: a 1 GiB write before each (outside the events) evicts L2 and MALL.
-    cold_ms = None
-    if args.cold_steps > 0:
-        scratch = torch.empty(1 << 28, dtype=torch.float32, device=dev)
-        times = []
-        for i in range(args.cold_steps):
-            scratch.fill_(float(i))
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            step()
-            b.record(stream)
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        cold_ms = float(np.median(times))
-        del scratch
 
     G = gdn.gdn_scan_group_size(B, H, T, Dk, Dv, C)
     cnt = algorithmic_counts(B, T, H, Dk, Dv, G, C)

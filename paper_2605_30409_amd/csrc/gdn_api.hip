@@ -335,12 +335,14 @@ struct FrameWs {
 int frame_blocks(int N) { return (N + 63) / 64; }
 
 // Token splits per frame: a split is a whole number of 64-token blocks, and
-// the library's choice (token_splits <= 0) aims at about 2 * 256 summary
-// workgroups, two halves per split.
-int frame_splits(long long units, int N, int token_splits) {
+// the library's choice (token_splits <= 0) is the largest count that keeps the
+// summary workgroups (one per split) within one per CU (256), at least 1.
+int frame_splits(long long units, int N, int Dk, int Dv, int token_splits) {
+    (void)Dk;
+    (void)Dv;
     const int nb = frame_blocks(N);
     int ns = token_splits;
-    if (ns <= 0) ns = (int)((256 + units - 1) / units);
+    if (ns <= 0) ns = (int)(256 / units);
     if (ns > nb) ns = nb;
     if (ns < 1) ns = 1;
     const int per = (nb + ns - 1) / ns;   // blocks per split
@@ -351,8 +353,10 @@ FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS)
     const size_t bhf = (size_t)B * H * F;
     FrameWs L;
     size_t off = 0;
-    L.PG = off; off = align256(off + bhf * NS * Dk * Dk * 4);
-    L.PA = off; off = align256(off + bhf * NS * Dk * Dv * 4);
+    // partial sums only with several token splits
+    const size_t np = NS > 1 ? (size_t)NS : 0;
+    L.PG = off; off = align256(off + bhf * np * Dk * Dk * 4);
+    L.PA = off; off = align256(off + bhf * np * Dk * Dv * 4);
     L.Gf = off; off = align256(off + bhf * Dk * Dk * esz);
     L.Af = off; off = align256(off + bhf * Dk * Dv * 4);
     L.Hf = off; off = align256(off + bhf * Dk * Dv * esz);
@@ -360,9 +364,17 @@ FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS)
     return L;
 }
 
-template <class E> constexpr int frame_out_tokens() { return 64 * gdn::FrameOutNTW<E>::value; }
+// Output workgroups per (frame, head): about `wgs` workgroups in all, each a
+// run of whole 16-token tiles, none empty.
+void frame_out_split(long long units, int N, int wgs, int &OB, int &tpw) {
+    const int ntf = (N + 15) / 16;
+    long long ob = (wgs + units - 1) / units;
+    if (ob > ntf) ob = ntf;
+    tpw = (int)((ntf + ob - 1) / ob);
+    OB = (ntf + tpw - 1) / tpw;
+}
 
-bool frame_shape_ok(int B, int H, int F, int N, size_t esz) {
+bool frame_shape_ok(int B, int H, int F, int N) {
     if (B < 1 || H < 1 || F < 1 || N < 1) return false;
     const long long bh = (long long)B * H;
     if (bh > 65535) return false;
@@ -370,9 +382,8 @@ bool frame_shape_ok(int B, int H, int F, int N, size_t esz) {
     if ((long long)F * N + 64LL * F + N > 0x7fffffffLL) return false;
     // grid sizes of the summary and output kernels stay below 2^31
     const long long units = bh * F;
-    const long long ob = (N + (esz == 2 ? 255 : 127)) / (esz == 2 ? 256 : 128);
-    if (16LL * frame_blocks(N) * ((units + 7) / 8) > 0x7fffffffLL) return false;
-    if (8LL * ob * ((units + 7) / 8) > 0x7fffffffLL) return false;
+    if (4LL * frame_blocks(N) * units > 0x7fffffffLL) return false;
+    if (8LL * ((N + 15) / 16) * ((units + 7) / 8) > 0x7fffffffLL) return false;
     return true;
 }
 
@@ -382,7 +393,7 @@ int frame_validate(const void *q, const void *k, const void *v, const float *alp
                    const float *state_in, const void *out, const float *state_out, int B, int H, int F,
                    int N, int Dk, int Dv, size_t esz) {
     if (!q || !k || !v || !alpha || !beta || !out) return GDN_ERR_NULL;
-    if (!frame_shape_ok(B, H, F, N, esz)) return GDN_ERR_SHAPE;
+    if (!frame_shape_ok(B, H, F, N)) return GDN_ERR_SHAPE;
     if (!frame_dims_ok(Dk, Dv)) return GDN_ERR_UNSUPPORTED;
     if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(alpha) || misaligned(beta) ||
         misaligned(state_in) || misaligned(out) || misaligned(state_out))
@@ -425,7 +436,7 @@ gdn::FrameParams<E> make_frame_params(const void *q, const void *k, const void *
     p.N = N;
     p.NS = NS;
     p.NBT = 64 * ((frame_blocks(N) + NS - 1) / NS);
-    p.OB = (N + frame_out_tokens<E>() - 1) / frame_out_tokens<E>();
+    frame_out_split((long long)B * H * F, N, gdn::FrameOut<E>::WGS, p.OB, p.OTPW);
     p.key_scale = key_scale;
     const FrameWs L = frame_ws_layout(B, H, F, Dk, Dv, sizeof(E), NS);
     unsigned char *base = (unsigned char *)ws;
@@ -459,12 +470,14 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
     auto stage = [&](int i) {
         switch (i) {
         case 0:
-            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV>),
-                               dim3(gdn::frame_summary_blocks(units * p.NS)), dim3(256), LS::bytes, s, p);
+            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV>), dim3((unsigned)(units * p.NS)),
+                               dim3((gdn::kSumCompute + gdn::kSumLoaders) * 64), LS::bytes, s, p);
             break;
         case 1:
-            hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV>), dim3((unsigned)units, (NI + 3) / 4),
-                               dim3(256), 0, s, p);
+            // a single split writes the summaries in their final form
+            if (p.NS > 1)
+                hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV>), dim3((unsigned)units, (NI + 3) / 4),
+                                   dim3(256), 0, s, p);
             break;
         case 2:
             hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV>), dim3(gdn::xcd_blocks(BH, DV / 16)),
@@ -504,7 +517,7 @@ int frame_run(const void *q, const void *k, const void *v, const float *alpha, c
     const size_t esz = bf16 ? 2 : 4;
     int st = frame_validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, esz);
     if (st != GDN_OK) return st;
-    const int NS = frame_splits((long long)B * H * F, N, token_splits);
+    const int NS = frame_splits((long long)B * H * F, N, Dk, Dv, token_splits);
     if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < frame_ws_layout(B, H, F, Dk, Dv, esz, NS).total)
         return GDN_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
@@ -527,7 +540,7 @@ int frame_run_cached(const void *q, const void *k, const void *v, const float *a
     int st = frame_validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, esz);
     if (st != GDN_OK) return st;
     const size_t need =
-        frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, 0)).total;
+        frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, Dk, Dv, 0)).total;
     void *ws = nullptr;
     st = cached_workspace(need, &ws);
     if (st != GDN_OK) return st;
@@ -640,14 +653,14 @@ int gdn_frame_forward_f32(const float *q, const float *k, const float *v, const 
 }
 
 int gdn_frame_token_splits(int B, int H, int F, int N, int Dk, int Dv, int token_splits) {
-    if (!frame_shape_ok(B, H, F, N, 2) || !frame_dims_ok(Dk, Dv)) return 0;
-    return frame_splits((long long)B * H * F, N, token_splits);
+    if (!frame_shape_ok(B, H, F, N) || !frame_dims_ok(Dk, Dv)) return 0;
+    return frame_splits((long long)B * H * F, N, Dk, Dv, token_splits);
 }
 
 size_t gdn_frame_workspace_bytes(int B, int H, int F, int N, int Dk, int Dv, int is_bf16, int token_splits) {
     const size_t esz = is_bf16 ? 2 : 4;
-    if (!frame_shape_ok(B, H, F, N, esz) || !frame_dims_ok(Dk, Dv)) return 0;
-    return frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, token_splits)).total;
+    if (!frame_shape_ok(B, H, F, N) || !frame_dims_ok(Dk, Dv)) return 0;
+    return frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, Dk, Dv, token_splits)).total;
 }
 
 int gdn_frame_forward_ex(const void *q, const void *k, const void *v, const float *alpha, const float *beta,

@@ -36,6 +36,8 @@
 // by lane, the A operand fragment of row tile t of G over the k block kb.
 #pragma once
 
+#include <type_traits>
+
 #include "gdn_device.h"
 
 namespace gdn {
@@ -49,7 +51,7 @@ template <class E> struct FrameParams {
     float *state_out;            // [B][H][Dk][Dv] or null
     int B, H, F, N;
     int NS, NBT;                 // token splits per frame, tokens per split (a multiple of 64)
-    int OB;                      // output workgroups per frame
+    int OB, OTPW;                // output workgroups per frame, 16-token tiles per workgroup
     float key_scale;
     float *PG;                   // [B*H][F][NS][Dk/16][Dk/16][64][4]  partial G tiles
     float *PA;                   // [B*H][F][NS][Dk/16][Dv/16][64][4]  partial A tiles
@@ -58,12 +60,9 @@ template <class E> struct FrameParams {
     E *Hf;                       // [B*H][F][Dv/16][Dk/32][64][8]      H_f operand fragments
 };
 
-// Workgroups of the summary kernel: the two halves of one (split, frame,
-// head) unit get block ids 8 apart, i.e. the same XCD (blocks are dealt to the
-// 8 XCDs round robin), so the keys both of them stage are read from HBM once.
-inline unsigned frame_summary_blocks(long long units) { return 16u * (unsigned)((units + 7) / 8); }
-// Output and scan grids: all workgroups of one unit (a (frame, head) or a
-// head) on one XCD, so the state they share is fetched into one L2.
+// Grids of per_unit workgroups per unit with all workgroups of one unit on
+// one XCD (blocks are dealt to the 8 XCDs round robin: id = 8 y + x runs on
+// XCD x), so the data they share is fetched into one L2.
 inline unsigned xcd_blocks(long long units, int per_unit) {
     return 8u * (unsigned)per_unit * (unsigned)((units + 7) / 8);
 }
@@ -73,148 +72,281 @@ __device__ __forceinline__ void xcd_unit(int id, int per_unit, int &unit, int &s
     unit = 8 * (y / per_unit) + x;
 }
 
+// LDS ring of the summary kernel: DEPTH slots, each one 64-token block of
+// raw keys, raw values and the block's 64 betas.  A 64-row tile with R
+// 16-byte chunks per row is stored in groups of four rows: chunk c of row r
+// sits at chunk position 4 R (r / 4) + 16 (c / 4) + 4 (r % 4) + c % 4.  A 1 KB
+// copy then reads contiguous runs of at least 256 bytes (4 rows of 16 chunks,
+// or whole rows when a row is shorter), and the transposed operand reads of a
+// fragment differ from one fragment to the next by a constant offset.
 template <class E, int DK, int DV> struct FrameSumLds {
-    static constexpr int PAD = 16 / (int)sizeof(E);
-    static constexpr int DY = DK > DV ? DK : DV;
-    static constexpr int LDK = DK + PAD, LDY = DY + PAD;
-    static constexpr size_t oK = 0;                              // raw keys, token rows
-    static constexpr size_t oY = oK + sizeof(E) * 64 * LDK;      // beta * (keys or values)
-    static constexpr size_t bytes = oY + sizeof(E) * 64 * LDY;
+    static constexpr int KB_ = 64 * DK * (int)sizeof(E), VB_ = 64 * DV * (int)sizeof(E);
+    static constexpr int SLOT = KB_ + VB_ + 256;
+    static constexpr int NCK = KB_ / 1024, NCV = VB_ / 1024;   // 1 KB copies per block
+    static constexpr int CAP = 160 * 1024;
+    static constexpr int DL = CAP / SLOT;
+    // loaders 0, 1 (halves of the key copies, 0 also the betas) and 2, 3
+    // (halves of the value copies) wait with DEPTH - 2 younger blocks in
+    // flight: vmcnt <= 63
+    static constexpr int PER = NCK / 2 + 1 > NCV / 2 ? NCK / 2 + 1 : NCV / 2;
+    static constexpr int DVM = 2 + 63 / PER;
+    static constexpr int D0 = DL < DVM ? DL : DVM;
+    static constexpr int DEPTH = D0 < 6 ? D0 : 6;
+    static constexpr size_t oK = 0, oV = KB_, oB = KB_ + VB_;
+    static constexpr size_t bytes = (size_t)DEPTH * SLOT;
+    static_assert(DEPTH >= 2, "summary ring needs two slots");
+    static_assert(KB_ % 2048 == 0 && VB_ % 2048 == 0, "whole 1 KB copies, two loaders each");
 };
 
-// beta times the 16 / sizeof(E) elements of a 16-byte vector, rounded to E.
-template <class E> __device__ __forceinline__ u32x4 scale_vec(u32x4 x, float b);
-template <> __device__ __forceinline__ u32x4 scale_vec<uint16_t>(u32x4 x, float b) {
-    u32x4 y;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) y[e] = pack_bf16x2(__uint_as_float(x[e] << 16) * b, __uint_as_float(x[e] & 0xffff0000u) * b);
-    return y;
-}
-template <> __device__ __forceinline__ u32x4 scale_vec<float>(u32x4 x, float b) {
-    return __builtin_bit_cast(u32x4, __builtin_bit_cast(f32x4, x) * b);
+// Element offset of (row, col) in a grouped 64-row tile of R chunks per row.
+template <class E, int R> __device__ __forceinline__ int gm_at(int row, int col) {
+    constexpr int EPC = 16 / (int)sizeof(E);                      // elements per chunk
+    const int c = col / EPC;
+    return EPC * (4 * R * (row >> 2) + 16 * (c >> 2) + 4 * (row & 3) + (c & 3)) + col % EPC;
 }
 
-// Phase A for one half.  YV = false: C = K^T B K (Dk x Dk, P32 columns);
-// YV = true: C = K^T B V (Dk x Dv).  Waves form a 2 x 2 grid over the row and
-// column tiles; a lane's 16-byte vectors of the next block are loaded into
-// registers while the current block is multiplied.
-template <class E, int DK, int DV, bool YV>
-__device__ __forceinline__ void frame_summary_half(const FrameParams<E> &p, unsigned char *smem, int s, int f,
-                                                   int bh) {
+// Row and chunk that lane l of 1 KB copy ci moves into a grouped tile of R
+// chunks per row (chunk position 64 ci + l).
+template <int R> __device__ __forceinline__ void gm_src(int ci, int l, int &row, int &chunk) {
+    const int pos = 64 * ci + l, g = pos / (4 * R), w = pos % (4 * R);
+    row = 4 * g + ((w & 15) >> 2);
+    chunk = 4 * (w >> 4) + (w & 3);
+}
+
+// Operand fragment over a 32-row k block of a grouped LDS tile: the same
+// values as tr_frag on the row-major tile.
+template <class E, int R>
+__device__ __forceinline__ typename Tr<E>::frag tr_frag_gm(const E *M, int row0, int colbase, bool p32, int a,
+                                                           int li, int lg) {
+    if constexpr (sizeof(E) == 2) {
+        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+        const int row = row0 + 8 * lg + (li >> 2);
+        const int col = p32 ? colbase + 8 * (li & 3) + 4 * a : colbase + 4 * (li & 3);
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(M + gm_at<E, R>(row, col)));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(M + gm_at<E, R>(row + 4, col)));
+        return Tr<E>::cat(__builtin_bit_cast(u32x2, lo), __builtin_bit_cast(u32x2, hi));
+    } else {
+        const int col = p32 ? colbase + p32_row(a, li) : colbase + li;
+        typename Tr<E>::frag f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) f[q] = M[gm_at<E, R>(row0 + 8 * lg + q, col)];
+        return f;
+    }
+}
+
+// The 8 k-slots of a lane's fragment times 8 per-slot scales.
+__device__ __forceinline__ Tr<uint16_t>::frag scale_frag(Tr<uint16_t>::frag x, const float (&b)[8]) {
+    Tr<uint16_t>::frag y;
+#pragma unroll
+    for (int d = 0; d < 4; ++d)
+        y[d] = pack_bf16x2(__uint_as_float(x[d] << 16) * b[2 * d], __uint_as_float(x[d] & 0xffff0000u) * b[2 * d + 1]);
+    return y;
+}
+__device__ __forceinline__ Tr<float>::frag scale_frag(Tr<float>::frag x, const float (&b)[8]) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) x[q] *= b[q];
+    return x;
+}
+
+// Phase A.  Workgroup (token split s, frame f, head): [G | A] over the split's
+// tokens (G = K^T B K with P32 rows and columns, A = K^T B V with P32 rows),
+// with 8 compute waves and 4 loader waves.  The loaders copy 64-token blocks
+// of raw K, V and beta into the LDS ring (asynchronous global->LDS copies,
+// DEPTH - 1 blocks ahead).  Compute wave w < 4 accumulates G, wave 4 + w A:
+// P32 row pair kb = w % (Dk / 32), i.e. row tiles 2 kb and 2 kb + 1, and a
+// share of the column tiles.  beta multiplies the K^T operand fragments in
+// registers (zero for tokens past the split).
+// With a single split the workgroup writes G's operand fragments (key scale
+// squared) and A's tiles (key scale) in their final form: the pair of row
+// tiles (2 kb, 2 kb + 1) of G column tile t is, lane by lane, fragment (t, kb).
+// With several splits it writes fp32 partial tiles for the reduction.
+constexpr int kSumCompute = 8, kSumLoaders = 4;
+
+template <class E, int DK, int DV>
+__global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_summary_kernel(FrameParams<E> p) {
     using L = FrameSumLds<E, DK, DV>;
     using TR = Tr<E>;
     using frag = typename TR::frag;
-    constexpr int DY = YV ? DV : DK;
-    constexpr int NR = DK / 16, NC = DY / 16, RPW = NR / 2, CPW = NC / 2;
-    constexpr int VE = 16 / (int)sizeof(E);
-    constexpr int KPR = DK / VE, YPR = DY / VE;               // 16-byte vectors per row
-    constexpr int NKV = 64 * KPR / 256, NYV = YV ? 64 * YPR / 256 : 1;
-    E *sK = (E *)(smem + L::oK), *sY = (E *)(smem + L::oY);
-
+    constexpr int D = L::DEPTH;
+    constexpr int ESZ = (int)sizeof(E);
+    constexpr int RK = DK * ESZ / 16, RV = DV * ESZ / 16;             // chunks per tile row
+    constexpr int NCK2 = L::NCK / 2, NCV2 = L::NCV / 2;
+    constexpr int NR = DK / 16, NP = NR / 2, KBN = DK / 32;           // row tiles, row pairs
+    constexpr int NCG = DK / 16, NCA = DV / 16;                       // column tiles of G, A
+    constexpr int SUB = 4 / NP;                                       // column shares per pair
+    constexpr int CPG = NCG / SUB, CPA = NCA / SUB;                   // column tiles per wave
+    extern __shared__ __align__(16) unsigned char smem[];
+    const int u = blockIdx.x;
+    if (u >= p.NS * p.F * p.B * p.H) return;
+    const int s = u % p.NS, rest = u / p.NS, f = rest % p.F, bh = rest / p.F;
     const int b = bh / p.H, h = bh - b * p.H;
     const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63, li = l & 15,
               lg = l >> 4;
-    const int wr = w >> 1, wc = w & 1;
     const size_t T = (size_t)p.F * p.N;
     const int t_lo = f * p.N + s * p.NBT;
     const int t_hi = min(f * p.N + p.N, t_lo + p.NBT);
+    const int nb = (t_hi - t_lo + 63) / 64;
     const size_t row_b = (size_t)b * T;
+    auto slot = [&](int i) { return smem + (size_t)(i % D) * L::SLOT; };
 
-    // One block's 16-byte vectors in registers.  Rows past the split are read
-    // from its last token (always in bounds) with beta = 0: their scaled
-    // copies are zero, so they add nothing.
-    struct Blk {
-        u32x4 k[NKV], y[NYV];
-        float kb[NKV], yb[NYV];
-    };
-    auto load_block = [&](int t0) {
-        Blk r;
+    if (w >= kSumCompute) {
+        // ---------------- loader waves ----------------
+        // loaders 0, 1: halves of the key copies (0 also the betas); 2, 3:
+        // halves of the value copies.  Rows past the split repeat its last
+        // token (their beta is zeroed where it is used).
+        const int ld = w - kSumCompute;
+        const bool keys = ld < 2;
+        auto issue = [&](int i) {
+            const int t0 = t_lo + 64 * i, rmax = t_hi - 1 - t0;
+            const size_t row0 = (row_b + t0) * p.H + h;
+            unsigned char *sl = slot(i);
+            if (keys) {
+                const char *base = (const char *)(p.k + row0 * DK);
+                const unsigned rstride = (unsigned)(p.H * DK * ESZ);
 #pragma unroll
-        for (int j = 0; j < NKV; ++j) {
-            const int i = tid + 256 * j, t = t0 + i / KPR;
-            const size_t row = (row_b + min(t, t_hi - 1)) * p.H + h;
-            r.k[j] = *(const u32x4 *)(p.k + row * DK + (i % KPR) * VE);
-            const float be = p.beta[row];
-            r.kb[j] = t < t_hi ? be : 0.f;
-        }
+                for (int j = 0; j < NCK2; ++j) {
+                    const int ci = (ld & 1) * NCK2 + j;
+                    int r, c;
+                    gm_src<RK>(ci, l, r, c);
+                    __builtin_amdgcn_global_load_lds(
+                        (const void *)(base + (unsigned)min(r, rmax) * rstride + 16u * (unsigned)c),
+                        (__attribute__((address_space(3))) void *)(sl + L::oK + 1024 * ci), 16, 0, 0);
+                }
+                if (ld == 0) {
+                    const char *bb = (const char *)(p.beta + row0);
+                    __builtin_amdgcn_global_load_lds(
+                        (const void *)(bb + (unsigned)min(l, rmax) * (unsigned)(4 * p.H)),
+                        (__attribute__((address_space(3))) void *)(sl + L::oB), 4, 0, 0);
+                }
+            } else {
+                const char *base = (const char *)(p.v + row0 * DV);
+                const unsigned rstride = (unsigned)(p.H * DV * ESZ);
 #pragma unroll
-        for (int j = 0; j < NYV; ++j) {
-            r.y[j] = u32x4{0u, 0u, 0u, 0u};
-            r.yb[j] = 0.f;
-            if constexpr (YV) {
-                const int i = tid + 256 * j, t = t0 + i / YPR;
-                const size_t row = (row_b + min(t, t_hi - 1)) * p.H + h;
-                r.y[j] = *(const u32x4 *)(p.v + row * DV + (i % YPR) * VE);
-                const float be = p.beta[row];
-                r.yb[j] = t < t_hi ? be : 0.f;
+                for (int j = 0; j < NCV2; ++j) {
+                    const int ci = (ld & 1) * NCV2 + j;
+                    int r, c;
+                    gm_src<RV>(ci, l, r, c);
+                    __builtin_amdgcn_global_load_lds(
+                        (const void *)(base + (unsigned)min(r, rmax) * rstride + 16u * (unsigned)c),
+                        (__attribute__((address_space(3))) void *)(sl + L::oV + 1024 * ci), 16, 0, 0);
+                }
             }
+        };
+        // block i has landed once at most D - 2 younger blocks are in flight
+        auto wait_oldest = [&]() {
+            if (ld == 0) wait_vmcnt<(D - 2) * (NCK2 + 1)>();
+            else if (ld == 1) wait_vmcnt<(D - 2) * NCK2>();
+            else wait_vmcnt<(D - 2) * NCV2>();
+        };
+#pragma unroll
+        for (int i = 0; i < D - 1; ++i) issue(min(i, nb - 1));
+        for (int i = 0; i < nb; ++i) {
+            wait_oldest();
+            lds_only_barrier();                  // block i handed to the compute waves
+            issue(min(i + D - 1, nb - 1));       // refills the slot of block i - 1
         }
-        return r;
-    };
-
-    f32x4 acc[RPW][CPW];
-#pragma unroll
-    for (int i = 0; i < RPW; ++i)
-#pragma unroll
-        for (int j = 0; j < CPW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    Blk cur = load_block(t_lo);
-    for (int t0 = t_lo; t0 < t_hi; t0 += 64) {
-#pragma unroll
-        for (int j = 0; j < NKV; ++j) {
-            const int i = tid + 256 * j, r = i / KPR, c = (i % KPR) * VE;
-            *(u32x4 *)(sK + r * L::LDK + c) = cur.k[j];
-            if (!YV) *(u32x4 *)(sY + r * L::LDY + c) = scale_vec<E>(cur.k[j], cur.kb[j]);
-        }
-        if constexpr (YV) {
-#pragma unroll
-            for (int j = 0; j < NYV; ++j) {
-                const int i = tid + 256 * j;
-                *(u32x4 *)(sY + (i / YPR) * L::LDY + (i % YPR) * VE) = scale_vec<E>(cur.y[j], cur.yb[j]);
-            }
-        }
-        lds_barrier();
-        if (t0 + 64 < t_hi) cur = load_block(t0 + 64);
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            frag af[RPW], bf[CPW];
-#pragma unroll
-            for (int i = 0; i < RPW; ++i) {
-                const int r = RPW * wr + i;
-                af[i] = tr_frag<E>(sK, L::LDK, 32 * kb, 32 * (r >> 1), true, r & 1, li, lg);
-            }
-#pragma unroll
-            for (int j = 0; j < CPW; ++j) {
-                const int c = CPW * wc + j;
-                bf[j] = YV ? tr_frag<E>(sY, L::LDY, 32 * kb, 16 * c, false, 0, li, lg)
-                           : tr_frag<E>(sY, L::LDY, 32 * kb, 32 * (c >> 1), true, c & 1, li, lg);
-            }
-#pragma unroll
-            for (int i = 0; i < RPW; ++i)
-#pragma unroll
-                for (int j = 0; j < CPW; ++j) acc[i][j] = TR::mma(af[i], bf[j], acc[i][j]);
-        }
-        lds_barrier();
+        wait_vmcnt<0>();
+        return;
     }
-    float *dst = (YV ? p.PA : p.PG) + (((size_t)bh * p.F + f) * p.NS + s) * (size_t)NR * NC * 256;
-#pragma unroll
-    for (int i = 0; i < RPW; ++i)
-#pragma unroll
-        for (int j = 0; j < CPW; ++j)
-            *(f32x4 *)(dst + ((size_t)((RPW * wr + i) * NC + CPW * wc + j) * 64 + l) * 4) = acc[i][j];
-}
 
-template <class E, int DK, int DV>
-__global__ __launch_bounds__(256) void gdn_frame_summary_kernel(FrameParams<E> p) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int id = blockIdx.x;
-    const int half = (id >> 3) & 1, u = (id & 7) + 8 * (id >> 4);
-    if (u >= p.NS * p.F * p.B * p.H) return;
-    const int s = u % p.NS, rest = u / p.NS, f = rest % p.F, bh = rest / p.F;
-    if (half == 0)
-        frame_summary_half<E, DK, DV, false>(p, smem, s, f, bh);
+    // ---------------- compute waves ----------------
+    const bool gw = w < 4;                                            // G waves, else A waves
+    const int wq = w & 3, kbw = wq % NP, c0 = wq / NP;                // row pair, column share
+    constexpr int CPW = CPG > CPA ? CPG : CPA;
+    f32x4 acc[2][CPW];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int j = 0; j < CPW; ++j) acc[a][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // the block loop, specialised for G waves (GB) and A waves, so that it has
+    // no branch inside: all operand reads of a block (the K^T fragments
+    // multiplied by beta) are issued before its products, which start as the
+    // reads return.  Nothing reads a slot after the barrier that hands the
+    // next block over (the loaders then refill it).
+    auto run = [&](auto gb) {
+        constexpr bool GB = decltype(gb)::value;
+        constexpr int NC = GB ? CPG : CPA;
+        struct Ops {
+            frag a[2], b[NC];
+        };
+        auto read = [&](int i, int kb, Ops &o) {
+            const unsigned char *sl = slot(i);
+            const E *sK = (const E *)(sl + L::oK), *sV = (const E *)(sl + L::oV);
+            const float *sB = (const float *)(sl + L::oB);
+            // betas of this lane's 8 k-slots: tokens 32 kb + 8 lg + q'
+            const f32x4 be0 = *(const f32x4 *)(sB + 32 * kb + 8 * lg);
+            const f32x4 be1 = *(const f32x4 *)(sB + 32 * kb + 8 * lg + 4);
+#pragma unroll
+            for (int a = 0; a < 2; ++a) o.a[a] = tr_frag_gm<E, RK>(sK, 32 * kb, 32 * kbw, true, a, li, lg);
+#pragma unroll
+            for (int j = 0; j < NC; ++j) {
+                const int c = c0 * NC + j;
+                if constexpr (GB)
+                    o.b[j] = tr_frag_gm<E, RK>(sK, 32 * kb, 32 * (c >> 1), true, c & 1, li, lg);
+                else
+                    o.b[j] = tr_frag_gm<E, RV>(sV, 32 * kb, 16 * c, false, 0, li, lg);
+            }
+            const int nvalid = t_hi - (t_lo + 64 * i + 32 * kb + 8 * lg);
+            float bt[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) bt[q] = q < nvalid ? (q < 4 ? be0[q] : be1[q - 4]) : 0.f;
+#pragma unroll
+            for (int a = 0; a < 2; ++a) o.a[a] = scale_frag(o.a[a], bt);
+        };
+        auto mul = [&](const Ops &o) {
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int j = 0; j < NC; ++j) acc[a][j] = TR::mma(o.a[a], o.b[j], acc[a][j]);
+        };
+        Ops o0, o1;
+        for (int i = 0; i < nb; ++i) {
+            // the barrier also completes the previous block's reads, so the
+            // loaders may refill that block's slot
+            lds_only_barrier();                  // block i has landed
+            read(i, 0, o0);
+            read(i, 1, o1);
+            mul(o0);
+            mul(o1);
+        }
+    };
+    if (gw)
+        run(std::true_type{});
     else
-        frame_summary_half<E, DK, DV, true>(p, smem, s, f, bh);
+        run(std::false_type{});
+
+    const size_t fi = (size_t)bh * p.F + f;
+    const int cpw = gw ? CPG : CPA;
+    if (p.NS == 1) {
+        const float ks = p.key_scale;
+        if (gw) {
+            const float k2 = ks * ks;
+#pragma unroll
+            for (int j = 0; j < CPG; ++j) {
+                const int t = c0 * CPG + j;                             // G column tile (P32)
+                TR::store8(p.Gf + ((fi * NR + t) * KBN + kbw) * 512 + l * 8,
+                           TR::cat(TR::from_f32(acc[0][j] * k2), TR::from_f32(acc[1][j] * k2)));
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < CPA; ++j) {
+                const int jt = c0 * CPA + j;
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NCA + jt) * 256 + l * 4) = acc[a][j] * ks;
+            }
+        }
+    } else {
+        const int NC = gw ? NCG : NCA;
+        float *dst = (gw ? p.PG : p.PA) + (fi * p.NS + s) * (size_t)NR * NC * 256;
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int j = 0; j < CPW; ++j)
+                if (j < cpw)
+                    *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + c0 * cpw + j) * 64 + l) * 4) = acc[a][j];
+    }
 }
 
 // Sum over the splits.  Items per (frame, head): the Dk/16 x Dk/32 G operand
@@ -251,7 +383,12 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
 
 // Phase B.  One wave per (head, column tile jt): Hacc[t][q] =
 // H[32 (t / 2) + 8 lg + 4 (t % 2) + q][16 jt + li], carried through the frames
-// in fp32.  The product G H takes H rounded to E as the B operand.
+// in fp32.  The product G H takes H rounded to E as the B operand.  A frame's
+// G fragments and A tiles do not depend on the state, so the next frame's are
+// requested before the current frame is computed (two register sets, used
+// alternately; bf16 only, the fp32 fragments are twice as large).
+template <class E> struct FrameScanPrefetch { static constexpr bool value = sizeof(E) == 2; };
+
 template <class E, int DK, int DV>
 __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
@@ -264,18 +401,33 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     const int l = threadIdx.x & 63, li = l & 15, lg = l >> 4;
     const int col = 16 * jt + li;
     f32x4 Hacc[NT];
+    if (p.state_in) {
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-        const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
+        for (int t = 0; t < NT; ++t) {
+            const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            Hacc[t][q] = p.state_in ? p.state_in[((size_t)bh * DK + r0 + q) * DV + col] : 0.f;
+            for (int q = 0; q < 4; ++q) Hacc[t][q] = p.state_in[((size_t)bh * DK + r0 + q) * DV + col];
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) Hacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    for (int f = 0; f < p.F; ++f) {
+    // a frame's operands: G fragments, A tiles and the decay (one load group,
+    // so that waiting for it never waits for a younger frame's loads)
+    auto load_ops = [&](int f, frag (&g)[NT][KB], f32x4 (&av)[NT], float &a) {
         const size_t fi = (size_t)bh * p.F + f;
-        const float a = p.alpha[((size_t)b * p.F + f) * p.H + h];
         const E *G = p.Gf + fi * NT * KB * 512 + l * 8;
         const float *A = p.Af + fi * NT * NJ * 256 + l * 4;
+        a = p.alpha[((size_t)b * p.F + f) * p.H + h];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) g[t][kb] = TR::load8(G + (t * KB + kb) * 512);
+            av[t] = *(const f32x4 *)(A + (t * NJ + jt) * 256);
+        }
+    };
+    auto frame = [&](int f, const frag (&g)[NT][KB], const f32x4 (&av)[NT], float a) {
+        const size_t fi = (size_t)bh * p.F + f;
         frag hb[KB];
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) hb[kb] = TR::cat(TR::from_f32(Hacc[2 * kb]), TR::from_f32(Hacc[2 * kb + 1]));
@@ -283,14 +435,36 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
         for (int t = 0; t < NT; ++t) {
             f32x4 gh = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb) gh = TR::mma(TR::load8(G + (t * KB + kb) * 512), hb[kb], gh);
-            const f32x4 av = *(const f32x4 *)(A + (t * NJ + jt) * 256);
-            Hacc[t] = a * (Hacc[t] - gh) + av;
+            for (int kb = 0; kb < KB; ++kb) gh = TR::mma(g[t][kb], hb[kb], gh);
+            Hacc[t] = a * (Hacc[t] - gh) + av[t];
         }
         E *hf = p.Hf + (fi * NJ + jt) * (size_t)KB * 512 + l * 8;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb)
             TR::store8(hf + kb * 512, TR::cat(TR::from_f32(Hacc[2 * kb]), TR::from_f32(Hacc[2 * kb + 1])));
+    };
+    frag g0[NT][KB];
+    f32x4 v0[NT];
+    float a0;
+    if constexpr (FrameScanPrefetch<E>::value) {
+        // the prefetch is unconditional (the last frame again past the end) so
+        // the wait for a set always leaves exactly one younger set in flight
+        frag g1[NT][KB];
+        f32x4 v1[NT];
+        float a1;
+        load_ops(0, g0, v0, a0);
+        for (int f = 0; f < p.F; f += 2) {
+            load_ops(min(f + 1, p.F - 1), g1, v1, a1);
+            frame(f, g0, v0, a0);
+            if (f + 1 >= p.F) break;
+            load_ops(min(f + 2, p.F - 1), g0, v0, a0);
+            frame(f + 1, g1, v1, a1);
+        }
+    } else {
+        for (int f = 0; f < p.F; ++f) {
+            load_ops(f, g0, v0, a0);
+            frame(f, g0, v0, a0);
+        }
     }
     if (p.state_out) {
 #pragma unroll
@@ -302,22 +476,32 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     }
 }
 
-// Phase C.  A workgroup takes 64 NTW tokens of one frame; wave w the 16 NTW
-// tokens from 16 NTW w.  H_f's fragments are staged in LDS once per
-// workgroup.  Lane (li, lg) of fragment (jo, kb) holds H_f[32 kb + 8 lg + q'][16 jo + li]:
-// the A operand of row 16 jo + li of H_f^T.  With the query rows as B operand
-// the product tile is O^T, and lane (li, lg) gets O[token li][16 jo + 4 lg + q].
-template <class E> struct FrameOutNTW { static constexpr int value = sizeof(E) == 2 ? 4 : 2; };
+// Phase C.  Workgroup blk of a (frame, head) unit takes the 16-token tiles
+// [TPW blk, TPW (blk + 1)) of the frame, wave w every fourth of them from w.
+// H_f's fragments are staged in LDS once per workgroup: lane (li, lg) of
+// fragment (jo, kb) holds H_f[32 kb + 8 lg + q'][16 jo + li], the A operand of
+// row 16 jo + li of H_f^T.  With the query rows as B operand the product tile
+// is O^T, and lane (li, lg) gets O[token li][16 jo + 4 lg + q].  bf16 keeps all
+// of H_f in registers; each wave streams its tiles with the queries of the
+// next QT tiles in flight while the current ones are multiplied and stored.
+template <class E> struct FrameOut {
+    static constexpr bool HREG = false;                // H_f register-resident
+    static constexpr int QT = 1;                       // tiles per query buffer
+    static constexpr int WGS = 1024;                   // workgroups to aim for
+};
 
 template <class E, int DK, int DV> struct FrameOutLds {
-    static constexpr size_t bytes = sizeof(E) * DK * DV;
+    static constexpr int LDO = DV + 16 / (int)sizeof(E);       // staged output row stride
+    static constexpr size_t oO = sizeof(E) * DK * DV;          // after H_f: one 16-row tile per wave
+    static constexpr size_t bytes = oO + sizeof(E) * 4 * 16 * LDO;
 };
 
 template <class E, int DK, int DV>
 __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
-    constexpr int KB = DK / 32, NJ = DV / 16, NTW = FrameOutNTW<E>::value;
+    constexpr int KB = DK / 32, NJ = DV / 16, QT = FrameOut<E>::QT;
+    constexpr bool HREG = FrameOut<E>::HREG;
     constexpr int HV = DV * DK * (int)sizeof(E) / 16;         // 16-byte vectors of H_f
     static_assert(HV % 256 == 0, "whole vectors per thread");
     extern __shared__ __align__(16) unsigned char smem[];
@@ -334,32 +518,70 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
     for (int j = 0; j < HV / 256; ++j) ((u32x4 *)smem)[tid + 256 * j] = src[tid + 256 * j];
 
     const size_t T = (size_t)p.F * p.N;
-    const int n0 = 64 * NTW * blk + 16 * NTW * w;
-    frag qf[NTW][KB];
+    const int ntf = (p.N + 15) / 16;                           // tiles in the frame
+    const int tile_lo = blk * p.OTPW, tile_hi = min(ntf, tile_lo + p.OTPW);
+    const size_t row_f = (size_t)b * T + (size_t)f * p.N;     // token rows of this frame
+    // query fragments of tiles i, i + 4, ..., i + 4 (QT - 1); rows past the frame read its last token
+    auto load_q = [&](int i, frag (&qf)[QT][KB]) {
 #pragma unroll
-    for (int i = 0; i < NTW; ++i) {
-        const int n = min(n0 + 16 * i + li, p.N - 1);
-        const E *qrow = p.q + (((size_t)b * T + (size_t)f * p.N + n) * p.H + h) * DK;
+        for (int u = 0; u < QT; ++u) {
+            const int n = min(16 * (i + 4 * u) + li, p.N - 1);
+            const E *qrow = p.q + ((row_f + n) * p.H + h) * DK;
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) qf[i][kb] = load_frag<E>(qrow + 32 * kb, lg);
-    }
-    lds_barrier();
-    const E *sH = (const E *)smem + l * 8;
-#pragma unroll
-    for (int jo = 0; jo < NJ; ++jo) {
-        frag hfr[KB];
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) hfr[kb] = TR::load8(sH + (jo * KB + kb) * 512);
-#pragma unroll
-        for (int i = 0; i < NTW; ++i) {
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) acc = TR::mma(hfr[kb], qf[i][kb], acc);
-            const int n = n0 + 16 * i + li;
-            if (n < p.N)
-                TR::store(p.out + (((size_t)b * T + (size_t)f * p.N + n) * p.H + h) * DV + 16 * jo + 4 * lg,
-                          TR::from_f32(acc));
+            for (int kb = 0; kb < KB; ++kb) qf[u][kb] = load_frag<E>(qrow + 32 * kb, lg);
         }
+    };
+    frag hr[HREG ? NJ : 1][KB];
+    const E *sH = (const E *)smem + l * 8;
+    // Output tile staging: the 16 x Dv tile goes through LDS so that global
+    // stores write whole rows (16 bytes per lane, a row per 16 bytes * DV / 16
+    // lanes) instead of 4-element pieces.
+    using LO = FrameOutLds<E, DK, DV>;
+    E *sO = (E *)(smem + LO::oO) + w * 16 * LO::LDO;
+    constexpr int VE = 16 / (int)sizeof(E);                   // elements per 16-byte vector
+    constexpr int RV = DV / VE;                                // vectors per output row
+    auto compute = [&](int i, const frag (&qf)[QT][KB]) {
+#pragma unroll
+        for (int u = 0; u < QT; ++u) {
+#pragma unroll
+            for (int jo = 0; jo < NJ; ++jo) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+                    acc = TR::mma(HREG ? hr[HREG ? jo : 0][kb] : TR::load8(sH + (jo * KB + kb) * 512), qf[u][kb], acc);
+                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(acc));
+            }
+            const int tile = i + 4 * u;
+            // rows r of the tile, RV lanes per row, 64 / RV rows per pass
+#pragma unroll
+            for (int pass = 0; pass < 16 * RV / 64; ++pass) {
+                const int r = pass * (64 / RV) + l / RV, c = (l % RV) * VE;
+                const u32x4 val = *(const u32x4 *)(sO + r * LO::LDO + c);
+                const int n = 16 * tile + r;
+                if (tile < tile_hi && n < p.N) *(u32x4 *)(p.out + ((row_f + n) * p.H + h) * DV + c) = val;
+            }
+        }
+    };
+    const int step = 4 * QT;                                   // tiles per buffer, all waves
+    const int i0 = tile_lo + w;
+    // the prefetch is unconditional (clamped to the workgroup's last tile) so
+    // the wait for one buffer always leaves exactly the other in flight
+    auto clampi = [&](int i) { return min(i, tile_hi - 1); };
+    frag qa[QT][KB], qb[QT][KB];
+    load_q(clampi(i0), qa);
+    lds_barrier();
+    if constexpr (HREG) {
+#pragma unroll
+        for (int jo = 0; jo < NJ; ++jo)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) hr[jo][kb] = TR::load8(sH + (jo * KB + kb) * 512);
+    }
+    for (int i = i0; i < tile_hi; i += 2 * step) {
+        load_q(clampi(i + step), qb);
+        compute(i, qa);
+        if (i + step >= tile_hi) break;
+        load_q(clampi(i + 2 * step), qa);
+        compute(i + step, qb);
     }
 }
 

@@ -481,18 +481,6 @@ template <class E, int DK, int CT, int NCW, bool FUSE = false> struct ScanLds {
     static_assert((WK * sizeof(E)) % 1024 == 0 && (UT * sizeof(E)) % 2048 == 0, "whole 1 KB copies");
 };
 
-template <int N> __device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N <= 63, "vmcnt range");
-    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
-}
-
-// Workgroup barrier for waves that communicate through LDS while asynchronous
-// global->LDS copies are in flight: waits for this wave's LDS accesses only
-// (a workgroup fence would also wait for the copies).
-__device__ __forceinline__ void lds_only_barrier() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 // Copy N whole KB from global to LDS: instruction i moves bytes
 // [1024 i, 1024 i + 1024), lane l its 16 bytes at 1024 i + 16 l.
 template <int N> __device__ __forceinline__ void copy_kb(const void *src, void *dst, int l) {

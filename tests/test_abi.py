@@ -123,20 +123,24 @@ def test_binding_rejects_bad_tensors_on_cpu():
 
 def test_frame_token_splits_and_workspace():
     ts = gdn.gdn_frame_token_splits
-    assert ts(1, 16, 3, 3520, 128, 128) == 6             # 48 (frame, head) units: ceil(256 / 48)
-    assert ts(1, 16, 1, 3520, 128, 128) == 14            # 55 blocks, 4 per split
-    assert ts(1, 16, 3, 3520, 128, 128, 1) == 1
-    assert ts(1, 16, 3, 3520, 128, 128, 1000) == 55      # at most one 64-token block per split
+    # library choice: summary workgroups (one per split) within 256
+    assert ts(1, 16, 3, 3520, 128, 128) == 5             # 48 (frame, head) units
+    assert ts(1, 16, 1, 3520, 128, 128) == 14            # 16 units: 16 splits of 4 blocks -> 14
+    assert ts(4, 20, 3, 3520, 64, 64) == 1               # 240 units
+    assert ts(1, 2, 1, 3520, 64, 64) == 55               # capped at one 64-token block per split
+    assert ts(1, 16, 3, 3520, 128, 128, 2) == 2
+    assert ts(1, 16, 3, 3520, 128, 128, 1000) == 55
+    assert ts(1, 16, 3, 3520, 128, 128, 13) == 11        # 5 blocks per split, none empty
     assert ts(1, 2, 1, 100, 64, 64, 5) == 2
     assert ts(1, 2, 1, 1, 64, 64) == 1
     assert ts(0, 2, 1, 1, 64, 64) == 0
     assert ts(1, 2, 1, 1, 96, 64) == 0
     wb = gdn.gdn_frame_workspace_bytes
     bhf = 16 * 3
-    n = wb(1, 16, 3, 3520, 128, 128, True, 1)
-    expect = bhf * (2 * 128 * 128 * 4 + 128 * 128 * (2 + 4 + 2))
+    n = wb(1, 16, 3, 3520, 128, 128, True, 1)           # one split: no partial sums
+    expect = bhf * 128 * 128 * (2 + 4 + 2)
     assert expect <= n < expect + 5 * 256
-    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 128 * 128 * 4
+    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 2 * 128 * 128 * 4
     assert wb(1, 16, 3, 3520, 128, 128, False, 1) > n
     assert wb(1, 16, 3, 0, 128, 128, True, 0) == 0
     assert wb(1, 16, 3, 3520, 128, 32, True, 0) == 0

@@ -12,7 +12,8 @@ and the product path never calls it.
   printed, used to tie the recurrences to the paper's own equation.
 * :func:`gdn_frame_forward` -- the frame-wise recurrence (one decay per frame,
   the frame's tokens writing at once, rescaled keys) in fp64 (C library), the
-  reference for the GPU frame-wise path.
+  reference for the GPU frame-wise path; with ``normalized=True`` also the
+  normalizer state and the normalized readout.
 """
 import ctypes
 import os
@@ -39,6 +40,9 @@ def _lib():
         lib.gdn_oracle_frame_forward.restype = ctypes.c_int
         lib.gdn_oracle_frame_forward.argtypes = [vp, vp, vp, i, vp, vp, i, vp, i, vp, vp,
                                                  i, i, i, i, i, i, ctypes.c_double, i]
+        lib.gdn_oracle_frame_forward_norm.restype = ctypes.c_int
+        lib.gdn_oracle_frame_forward_norm.argtypes = [vp, vp, vp, i, vp, vp, i, vp, vp, i, vp, vp, vp,
+                                                      i, i, i, i, i, i, ctypes.c_double, ctypes.c_double, i]
         _LIB = lib
     return _LIB
 
@@ -93,13 +97,18 @@ def gdn_forward(q, k, v, alpha, beta, state_in=None, nthreads=None,
 
 
 def gdn_frame_forward(q, k, v, alpha, beta, state_in=None, frame_tokens=1, key_scale=None,
-                      nthreads=None, want_state=True):
+                      nthreads=None, want_state=True, normalized=False, z_in=None, eps=1e-6):
     """Run the fp64 frame-wise recurrence.
 
     q, k: [B, T, H, Dk]; v: [B, T, H, Dv] (float32, float64 or bf16 bits as
     uint16); T = F * frame_tokens.  alpha: [B, F, H] (one decay per frame);
     beta: [B, T, H].  key_scale multiplies every key (None: the paper's
     1 / sqrt(Dk * frame_tokens)).  Returns (out [B, T, H, Dv], state_out).
+
+    normalized=True also carries the normalizer state z ([B, H, Dk], from z_in
+    or zero) and divides the readout by z . q + eps (equations
+    appendix_gdn_z_update and appendix_gdn_readout); it returns
+    (out, state_out, z_out).
     """
     q, k, v = (np.ascontiguousarray(x) for x in (q, k, v))
     if not (q.dtype == k.dtype == v.dtype) or q.dtype not in _DT_QKV:
@@ -124,12 +133,34 @@ def gdn_frame_forward(q, k, v, alpha, beta, state_in=None, frame_tokens=1, key_s
         if state_in.dtype not in _DT_GATE or state_in.shape != (B, H, Dk, Dv):
             raise ValueError("state_in must be float32/float64 [B, H, Dk, Dv]")
         sdt = _DT_GATE[state_in.dtype]
+    if z_in is not None:
+        if not normalized:
+            raise ValueError("z_in needs normalized=True")
+        z_in = np.ascontiguousarray(z_in)
+        if z_in.dtype not in _DT_GATE or z_in.shape != (B, H, Dk):
+            raise ValueError("z_in must be float32/float64 [B, H, Dk]")
+        if state_in is None:
+            sdt = _DT_GATE[z_in.dtype]
+        elif z_in.dtype != state_in.dtype:   # one stored type for both states
+            state_in = state_in.astype(np.float64)
+            z_in = z_in.astype(np.float64)
+            sdt = 2
     if key_scale is None:
         key_scale = 1.0 / np.sqrt(Dk * N)
     out = np.empty((B, T, H, Dv), dtype=np.float64)
     state_out = np.empty((B, H, Dk, Dv), dtype=np.float64) if want_state else None
     if nthreads is None:
         nthreads = os.cpu_count() or 1
+    if normalized:
+        z_out = np.empty((B, H, Dk), dtype=np.float64) if want_state else None
+        rc = _lib().gdn_oracle_frame_forward_norm(
+            _ptr(q), _ptr(k), _ptr(v), _DT_QKV[q.dtype],
+            _ptr(alpha), _ptr(beta), _DT_GATE[alpha.dtype],
+            _ptr(state_in), _ptr(z_in), sdt, _ptr(out), _ptr(state_out), _ptr(z_out),
+            B, H, F, N, Dk, Dv, float(key_scale), float(eps), int(nthreads))
+        if rc != 0:
+            raise RuntimeError(f"gdn_oracle_frame_forward_norm failed with {rc}")
+        return out, state_out, z_out
     rc = _lib().gdn_oracle_frame_forward(
         _ptr(q), _ptr(k), _ptr(v), _DT_QKV[q.dtype],
         _ptr(alpha), _ptr(beta), _DT_GATE[alpha.dtype],

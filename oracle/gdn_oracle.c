@@ -205,6 +205,17 @@ int gdn_oracle_forward(const void *q, const void *k, const void *v, int qkv_dtyp
  *       H   <- alpha_f H + sum_n k~_n u_n^T
  *       o_n  = H^T q_n                   (read from the updated state)
  * i.e. S_f = alpha_f S_{f-1} (I - K~ B K~^T) + V B K~^T and Y_f = S_f Q_f.
+ *
+ * With the normalizer (subsection "Frame-wise delta-rule update", equation
+ * appendix_gdn_z_update; subsection "Normalized readout and output
+ * projection", equation appendix_gdn_readout), a vector state z = S^z of
+ * length Dk is carried beside H and updated in the same correction-based way
+ * from the (unrotated) keys:
+ *       z~   = alpha_f z                     (decay first)
+ *       z   <- z~ + sum_n beta_n (1 - k~_n . z~) k~_n
+ *       o_n  = (H^T q_n) / (z . q_n + eps)   (both from the updated states)
+ * This path has no rotary embedding, so the rotated and unrotated keys and
+ * queries coincide.
  */
 struct fjob {
     const void *q, *k, *v;
@@ -214,6 +225,10 @@ struct fjob {
     double *out, *state_out;
     int B, H, F, N, Dk, Dv;
     double key_scale;
+    int norm;                      /* 1: carry z and divide the readout */
+    const void *z_in;              /* [B][H][Dk] or NULL, stored as state_dtype */
+    double *z_out;                 /* [B][H][Dk] or NULL */
+    double eps;
     int nthreads, worker, status;
 };
 
@@ -225,14 +240,20 @@ static int run_frame_head(const struct fjob *J, int b, int h)
     double *kk = (double *)malloc(sizeof(double) * (size_t)N * Dk);
     double *uu = (double *)malloc(sizeof(double) * (size_t)N * Dv);
     double *qq = (double *)malloc(sizeof(double) * (size_t)Dk);
-    if (!S || !kk || !uu || !qq) {
-        free(S); free(kk); free(uu); free(qq);
+    double *z = (double *)calloc((size_t)Dk, sizeof(double));
+    double *zr = (double *)malloc(sizeof(double) * (size_t)N);
+    if (!S || !kk || !uu || !qq || !z || !zr) {
+        free(S); free(kk); free(uu); free(qq); free(z); free(zr);
         return -1;
     }
     const size_t sbase = ((size_t)b * H + h) * (size_t)Dk * Dv;
+    const size_t zbase = ((size_t)b * H + h) * (size_t)Dk;
     if (J->state_in)
         for (size_t e = 0; e < (size_t)Dk * Dv; e++)
             S[e] = load_elem(J->state_in, J->state_dtype, sbase + e);
+    if (J->norm && J->z_in)
+        for (int i = 0; i < Dk; i++)
+            z[i] = load_elem(J->z_in, J->state_dtype, zbase + i);
     for (int f = 0; f < F; f++) {
         const double a = load_elem(J->alpha, J->gate_dtype, ((size_t)b * F + f) * H + h);
         /* residuals of every token against the decayed state of the previous frame */
@@ -249,6 +270,13 @@ static int run_frame_head(const struct fjob *J, int b, int h)
                     un[j] += S[(size_t)i * Dv + j] * kn[i];
             for (int j = 0; j < Dv; j++)
                 un[j] = be * (load_elem(J->v, J->qkv_dtype, row * Dv + j) - a * un[j]);
+            if (J->norm) {
+                /* normalizer residual against the decayed z: beta (1 - k~ . alpha z) */
+                double dot = 0.0;
+                for (int i = 0; i < Dk; i++)
+                    dot += kn[i] * z[i];
+                zr[n] = be * (1.0 - a * dot);
+            }
         }
         /* simultaneous write of the whole frame */
         for (size_t e = 0; e < (size_t)Dk * Dv; e++)
@@ -258,6 +286,13 @@ static int run_frame_head(const struct fjob *J, int b, int h)
             for (int i = 0; i < Dk; i++)
                 for (int j = 0; j < Dv; j++)
                     S[(size_t)i * Dv + j] += kn[i] * un[j];
+        }
+        if (J->norm) {
+            for (int i = 0; i < Dk; i++)
+                z[i] *= a;
+            for (int n = 0; n < N; n++)
+                for (int i = 0; i < Dk; i++)
+                    z[i] += zr[n] * kk[(size_t)n * Dk + i];
         }
         /* readout from the updated state */
         for (int n = 0; n < N; n++) {
@@ -270,11 +305,20 @@ static int run_frame_head(const struct fjob *J, int b, int h)
             for (int i = 0; i < Dk; i++)
                 for (int j = 0; j < Dv; j++)
                     o[j] += S[(size_t)i * Dv + j] * qq[i];
+            if (J->norm) {
+                double d = 0.0;
+                for (int i = 0; i < Dk; i++)
+                    d += z[i] * qq[i];
+                for (int j = 0; j < Dv; j++)
+                    o[j] /= d + J->eps;
+            }
         }
     }
     if (J->state_out)
         memcpy(J->state_out + sbase, S, sizeof(double) * (size_t)Dk * Dv);
-    free(S); free(kk); free(uu); free(qq);
+    if (J->norm && J->z_out)
+        memcpy(J->z_out + zbase, z, sizeof(double) * (size_t)Dk);
+    free(S); free(kk); free(uu); free(qq); free(z); free(zr);
     return 0;
 }
 
@@ -298,11 +342,12 @@ static void *frame_worker_main(void *arg)
  * key_scale : factor applied to every key (the paper's 1/sqrt(D N))
  * Returns 0, or -1 on bad arguments / allocation failure.
  */
-int gdn_oracle_frame_forward(const void *q, const void *k, const void *v, int qkv_dtype,
-                             const void *alpha, const void *beta, int gate_dtype,
-                             const void *state_in, int state_dtype,
-                             double *out, double *state_out,
-                             int B, int H, int F, int N, int Dk, int Dv, double key_scale, int nthreads)
+static int frame_forward_impl(const void *q, const void *k, const void *v, int qkv_dtype,
+                              const void *alpha, const void *beta, int gate_dtype,
+                              const void *state_in, const void *z_in, int state_dtype,
+                              double *out, double *state_out, double *z_out,
+                              int B, int H, int F, int N, int Dk, int Dv, double key_scale,
+                              int norm, double eps, int nthreads)
 {
     if (!q || !k || !v || !alpha || !beta || !out)
         return -1;
@@ -332,6 +377,7 @@ int gdn_oracle_frame_forward(const void *q, const void *k, const void *v, int qk
         J->out = out; J->state_out = state_out;
         J->B = B; J->H = H; J->F = F; J->N = N; J->Dk = Dk; J->Dv = Dv;
         J->key_scale = key_scale;
+        J->norm = norm; J->z_in = z_in; J->z_out = z_out; J->eps = eps;
         J->nthreads = nthreads; J->worker = w; J->status = 0;
         if (nthreads > 1 && pthread_create(&tids[w], NULL, frame_worker_main, J) == 0)
             running[w] = 1;
@@ -348,4 +394,31 @@ int gdn_oracle_frame_forward(const void *q, const void *k, const void *v, int qk
     free(jobs);
     free(tids);
     return status;
+}
+
+int gdn_oracle_frame_forward(const void *q, const void *k, const void *v, int qkv_dtype,
+                             const void *alpha, const void *beta, int gate_dtype,
+                             const void *state_in, int state_dtype,
+                             double *out, double *state_out,
+                             int B, int H, int F, int N, int Dk, int Dv, double key_scale, int nthreads)
+{
+    return frame_forward_impl(q, k, v, qkv_dtype, alpha, beta, gate_dtype, state_in, NULL, state_dtype,
+                              out, state_out, NULL, B, H, F, N, Dk, Dv, key_scale, 0, 0.0, nthreads);
+}
+
+/*
+ * The frame-wise forward with the normalizer state and the normalized readout
+ * (see the comment above struct fjob).  Arguments as gdn_oracle_frame_forward,
+ * plus z_in : [B, H, Dk] stored as state_dtype or NULL (zero), z_out : [B, H, Dk]
+ * fp64 or NULL, and eps (the paper uses 1e-6).
+ */
+int gdn_oracle_frame_forward_norm(const void *q, const void *k, const void *v, int qkv_dtype,
+                                  const void *alpha, const void *beta, int gate_dtype,
+                                  const void *state_in, const void *z_in, int state_dtype,
+                                  double *out, double *state_out, double *z_out,
+                                  int B, int H, int F, int N, int Dk, int Dv, double key_scale,
+                                  double eps, int nthreads)
+{
+    return frame_forward_impl(q, k, v, qkv_dtype, alpha, beta, gate_dtype, state_in, z_in, state_dtype,
+                              out, state_out, z_out, B, H, F, N, Dk, Dv, key_scale, 1, eps, nthreads);
 }

@@ -14,7 +14,7 @@ import pytest
 import gdn_inputs
 import oracle
 from oracle.chunked import gdn_chunked
-from oracle.framewise import framewise_forward
+from oracle.framewise import framewise_forward, framewise_forward_normalized
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 rng = np.random.default_rng
@@ -386,3 +386,116 @@ def test_f7_frame_oracle_rejects_bad_arguments():
         oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=3)      # T not whole frames
     with pytest.raises(ValueError):
         oracle.gdn_frame_forward(q, k, v, b, b, s, frame_tokens=4)      # alpha per token
+
+
+# ---- normalizer state and normalized readout (frame-wise) ----
+
+def norm_case(seed, B=1, F=3, N=5, H=2, Dk=8, Dv=6, state=True):
+    """Non-negative features (the paper's ReLU feature maps), so that the
+    denominators z . q are positive."""
+    q, k, v, a, b, s = frame_case(seed, B=B, F=F, N=N, H=H, Dk=Dk, Dv=Dv, state=state)
+    z = np.abs(rng(seed + 1).standard_normal((B, H, Dk))) if state else None
+    return np.abs(q), np.abs(k), v, a, b, s, z
+
+
+@pytest.mark.parametrize("F,N", [(1, 1), (4, 1), (3, 5), (2, 17)])
+def test_n1_normalizer_equals_printed_compact_equation(F, N):
+    """The oracle's correction-based z update (appendix_gdn_z_update) and
+    divided readout against the printed compact form (appendix_gdn_z_compact,
+    appendix_gdn_readout): catches a z decayed after the write, the wrong key,
+    a missing beta on the write, or a readout from the old z."""
+    q, k, v, a, b, s, z = norm_case(200 + 3 * F + N, F=F, N=N)
+    ks, eps = 0.31, 1e-3
+    o, st, zo = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks,
+                                         normalized=True, z_in=z, eps=eps)
+    for h in range(q.shape[2]):
+        Y, S, zf = framewise_forward_normalized(q[0, :, h], ks * k[0, :, h], v[0, :, h], a[0, :, h],
+                                                b[0, :, h], s[0, h].T, z[0, h], N=N, eps=eps)
+        assert rel(o[0, :, h], Y) < 1e-12
+        assert rel(st[0, h], S.T) < 1e-12
+        assert rel(zo[0, h], zf) < 1e-12
+
+
+def test_n2_normalizer_is_a_value_column_of_ones():
+    """z follows the same recurrence as a column of the state whose values are
+    all one: running the un-normalized oracle with v' = [v | 1] gives z as the
+    last state column and z . q as the last output column, so the normalized
+    output is the numerator divided by that column plus eps."""
+    F, N = 4, 6
+    q, k, v, a, b, s, z = norm_case(21, F=F, N=N)
+    ks, eps = 0.45, 1e-6
+    o, st, zo = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks,
+                                         normalized=True, z_in=z, eps=eps)
+    v1 = np.concatenate([v, np.ones(v.shape[:-1] + (1,))], axis=-1)
+    s1 = np.concatenate([s, z[..., None]], axis=-1)
+    o1, st1 = oracle.gdn_frame_forward(q, k, v1, a, b, s1, frame_tokens=N, key_scale=ks)
+    assert rel(zo, st1[..., -1]) < 1e-13
+    assert rel(st, st1[..., :-1]) < 1e-13
+    assert rel(o, o1[..., :-1] / (o1[..., -1:] + eps)) < 1e-12
+
+
+def test_n3_orthonormal_keys_store_unit_mass():
+    """beta = 1, key scale 1 and orthonormal keys inside a frame: the delta
+    rule writes the value 1 for every key, so k_n . z_f = 1 for each token n of
+    frame f whatever the earlier state (mass conservation)."""
+    Dk, N, F = 8, 5, 3
+    r = rng(22)
+    k = np.zeros((1, F * N, 1, Dk))
+    for f in range(F):
+        Qm, _ = np.linalg.qr(r.standard_normal((Dk, Dk)))
+        k[0, f * N:(f + 1) * N, 0] = Qm[:, :N].T
+    q = np.abs(r.standard_normal((1, F * N, 1, Dk)))
+    v = r.standard_normal((1, F * N, 1, 4))
+    a = r.uniform(0.2, 1.0, (1, F, 1))
+    b = np.ones((1, F * N, 1))
+    z0 = r.standard_normal((1, 1, Dk))
+    for Fc in range(1, F + 1):
+        _, _, zf = oracle.gdn_frame_forward(q[:, :Fc * N], k[:, :Fc * N], v[:, :Fc * N], a[:, :Fc],
+                                            b[:, :Fc * N], None, frame_tokens=N, key_scale=1.0,
+                                            normalized=True, z_in=z0)
+        dots = k[0, (Fc - 1) * N:Fc * N, 0] @ zf[0, 0]
+        assert np.abs(dots - 1.0).max() < 1e-13
+
+
+def test_n4_no_write_only_decays_the_normalizer():
+    """beta = 0: z_f = (prod of decays) z_0 and the output is the decayed
+    numerator over the decayed denominator plus eps."""
+    F, N = 3, 4
+    q, k, v, a, _, s, z = norm_case(23, F=F, N=N)
+    b = np.zeros((1, F * N, 2))
+    eps = 1e-2
+    o, st, zo = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.7,
+                                         normalized=True, z_in=z, eps=eps)
+    cum = np.cumprod(a[0], axis=0)
+    assert rel(zo[0], cum[-1][:, None] * z[0]) < 1e-14
+    for f in range(F):
+        for h in range(2):
+            qq = q[0, f * N:(f + 1) * N, h]
+            ref = (qq @ (cum[f, h] * s[0, h])) / (qq @ (cum[f, h] * z[0, h]) + eps)[:, None]
+            assert rel(o[0, f * N:(f + 1) * N, h], ref) < 1e-13
+
+
+def test_n5_streaming_split_carries_both_states():
+    F, N = 4, 3
+    q, k, v, a, b, s, z = norm_case(24, F=F, N=N)
+    o, st, zo = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.6,
+                                         normalized=True, z_in=z)
+    m = 2 * N
+    oa, sa, za = oracle.gdn_frame_forward(q[:, :m], k[:, :m], v[:, :m], a[:, :2], b[:, :m], s,
+                                          frame_tokens=N, key_scale=0.6, normalized=True, z_in=z)
+    ob, sb, zb = oracle.gdn_frame_forward(q[:, m:], k[:, m:], v[:, m:], a[:, 2:], b[:, m:], sa,
+                                          frame_tokens=N, key_scale=0.6, normalized=True, z_in=za)
+    assert np.array_equal(np.concatenate([oa, ob], axis=1), o)
+    assert np.array_equal(sb, st) and np.array_equal(zb, zo)
+
+
+def test_n6_empty_normalizer_divides_by_eps():
+    """No state and no writes: the denominator is exactly eps."""
+    F, N = 2, 3
+    q, k, v, a, _, s, _ = norm_case(25, F=F, N=N)
+    b = np.zeros((1, F * N, 2))
+    o, _, zo = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.5,
+                                        normalized=True, eps=0.25)
+    o0, _ = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.5)
+    assert np.array_equal(zo, np.zeros_like(zo))
+    assert rel(o, o0 / 0.25) < 1e-15

@@ -17,6 +17,8 @@ all tokens of a frame written at once): a step is one streaming call of 3
 latent frames of 44x80 tokens, B=1, F=3, N=3520, H=16, Dk=Dv=128, bf16, with
 the fp32 state carried in and out; its four kernels are the frame summaries,
 their reduction over token splits, the scan over frames and the output.
+``--path frame-norm`` measures the same call with the normalizer state and the
+normalized readout (non-negative feature maps).
 """
 import argparse
 import json
@@ -141,17 +143,24 @@ def load_traffic(stage, summary="traffic_frame1280x704.json"):
 
 FRAME_METRIC = ("frame-wise GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, "
                 "H=16, D=128 bf16")
+FRAME_NORM_METRIC = ("frame-wise normalized GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, "
+                     "H=16, D=128 bf16")
 FRAME_KERNELS = {"summaries": "gdn_frame_summary_kernel", "reduce": "gdn_frame_reduce_kernel",
                  "scan": "gdn_frame_scan_kernel", "output": "gdn_frame_output_kernel"}
 
 
-def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2):
+def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False):
     """Per-stage algorithmic flops and bytes of the frame-wise path (each stage's own
     inputs and outputs, workspace included, every byte once) and its external I/O.
 
     summaries: G = K^T B K and A = K^T B V over every token (fp32 partial tiles per
     token split); reduce: the splits' partials -> G (operand fragments) and A;
-    scan: H_f = alpha (H - G H) + A per frame; output: O = Q H_f per token."""
+    scan: H_f = alpha (H - G H) + A per frame; output: O = Q H_f per token.
+    norm: the normalizer z rides along as one more 16-column state tile (its
+    flops and bytes are counted as the kernels move them: the extra tile, of
+    which one column is z), plus one division per output element."""
+    if norm:
+        Dv = Dv + 16
     n = B * F * N * H                   # token-heads
     u = B * H * F                       # (frame, head) units
     st = B * H * Dk * Dv * 4
@@ -168,15 +177,17 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2):
     return dict(flops=f, bytes=b, io_bytes=io_bytes)
 
 
-def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0):
+def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False):
     """Time the fp64 frame-wise oracle (as it stands) on whole calls for ~10 s."""
     import oracle
     threads = host_threads()
     reps, elapsed = 0, 0.0
+    extra = dict(normalized=True, z_in=inp["z_in"]) if norm else {}
     while elapsed < min_seconds and reps < 50:
         t0 = time.perf_counter()
         oracle.gdn_frame_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
-                                 inp["state_in"], frame_tokens=inp["frame_tokens"], nthreads=threads)
+                                 inp["state_in"], frame_tokens=inp["frame_tokens"], nthreads=threads,
+                                 **extra)
         elapsed += time.perf_counter() - t0
         reps += 1
     return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
@@ -184,41 +195,54 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0):
                       f"fp64 frame-wise recurrence, {elapsed:.1f} s"}
 
 
-def run_frame(args, torch, gdn, dev, to_dev, timed):
+def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
     F, N = 3, 3520
-    inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02")
+    inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02",
+                                       features="relu" if norm else "gauss")
     B, T, H, Dk = inp["q"].shape
     Dv = inp["v"].shape[-1]
     q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
     alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
     out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
     s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
+    z_in = to_dev(inp["z_in"]) if norm else None
+    z_out = torch.empty((B, H, Dk), dtype=torch.float32, device=dev) if norm else None
     ts = args.token_splits
     ws = gdn.frame_workspace(q, v, N, ts)
     NS = gdn.gdn_frame_token_splits(B, H, F, N, Dk, Dv, ts)
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        gdn.gdn_frame_forward_ex(q, k, v, alpha, beta, s_in, out, s_out, ws, N, token_splits=ts,
-                                 stream=stream)
+        if norm:
+            gdn.frame_forward_norm(q, k, v, alpha, beta, s_in, z_in, frame_tokens=N, out=out,
+                                   state_out=s_out, z_out=z_out, ws=ws, token_splits=ts, stream=stream)
+        else:
+            gdn.gdn_frame_forward_ex(q, k, v, alpha, beta, s_in, out, s_out, ws, N, token_splits=ts,
+                                     stream=stream)
 
     ms_per_step, cold_ms = timed(step, stream)
-    stage_ms = gdn.gdn_frame_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws, N,
-                                            token_splits=ts, reps=args.steps, stream=stream)
+    if norm:
+        stage_ms = gdn.gdn_frame_profile_stages_norm(q, k, v, alpha, beta, s_in, z_in, out, s_out, z_out,
+                                                     ws, N, token_splits=ts, reps=args.steps,
+                                                     stream=stream)
+    else:
+        stage_ms = gdn.gdn_frame_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws, N,
+                                                token_splits=ts, reps=args.steps, stream=stream)
     names = dict(zip(gdn.FRAME_STAGE_NAMES, stage_ms))
     torch.cuda.synchronize()
-    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS)
+    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm)
     sec = ms_per_step / 1e3
     tflops = sum(cnt["flops"].values()) / sec / 1e12
     dom = max(names, key=names.get)
     roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
-    roofline.update({"traffic": load_traffic(dom, "traffic_frames3x1280x704.json"),
+    roofline.update({"traffic": load_traffic(dom, "traffic_frames3x1280x704_norm.json" if norm
+                                             else "traffic_frames3x1280x704.json"),
                      "kernel": FRAME_KERNELS[dom], "duration_ms": round(names[dom], 5),
                      "algorithmic_flops_per_launch": cnt["flops"][dom],
                      "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
     stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_) for k_, v_ in names.items()}
     rec = {
-        "metric": FRAME_METRIC,
+        "metric": FRAME_NORM_METRIC if norm else FRAME_METRIC,
         "value": round(B * T / sec, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -232,7 +256,9 @@ def run_frame(args, torch, gdn, dev, to_dev, timed):
         "data": "synthetic",
         "config": {"workload": "frame-wise streaming call of 3 latent 1280x704 frames: B=1 F=3 "
                                "N=3520 (44x80) H=16 Dk=Dv=128, bf16 q/k/v, one decay per frame, "
-                               "key scale 1/sqrt(Dk N), fp32 state in/out",
+                               "key scale 1/sqrt(Dk N), fp32 state in/out"
+                               + ("; normalizer state in/out and normalized readout (eps 1e-6), "
+                                  "non-negative (ReLU) feature maps" if norm else ""),
                    "B": B, "F": F, "N": N, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "token_splits": NS},
         "tflops": round(tflops, 2),
         "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
@@ -243,7 +269,7 @@ def run_frame(args, torch, gdn, dev, to_dev, timed):
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk)
+        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk, norm=norm)
     print(json.dumps(rec), flush=True)
 
 
@@ -258,8 +284,9 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a known-size "
                          "reference for hardware traffic counters)")
-    ap.add_argument("--path", choices=("token", "frame"), default="token",
-                    help="token: the token-wise chunk forward (default); frame: the frame-wise forward")
+    ap.add_argument("--path", choices=("token", "frame", "frame-norm"), default="token",
+                    help="token: the token-wise chunk forward (default); frame: the frame-wise "
+                         "forward; frame-norm: the frame-wise forward with the normalizer")
     ap.add_argument("--token-splits", type=int, default=0,
                     help="frame path: token splits per frame (0 = the library's choice)")
     args = ap.parse_args()
@@ -318,8 +345,8 @@ def main():
             del scratch
         return ms, cold
 
-    if args.path == "frame":
-        run_frame(args, torch, gdn, dev, to_dev, timed)
+    if args.path in ("frame", "frame-norm"):
+        run_frame(args, torch, gdn, dev, to_dev, timed, norm=args.path == "frame-norm")
         return
 
     w = gdn_inputs.WORKLOADS[WORKLOAD]

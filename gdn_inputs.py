@@ -124,13 +124,19 @@ def make_inputs(workload, call=0, *, B=None, T=None, H=None, Dk=None, Dv=None,
 
 
 def make_frame_inputs(workload, frames, *, frame_tokens=None, call=0, B=None, H=None, Dk=None,
-                      Dv=None, dtype=None, state=None, seed=None):
+                      Dv=None, dtype=None, state=None, seed=None, features="gauss"):
     """Draw one call's inputs for the frame-wise forward: ``frames`` frames of
     ``frame_tokens`` tokens (default 3520, one 44 x 80 latent frame), with the
     value distributions of ``workload``.  The decay is drawn once per (b, frame,
     h); everything else as in make_inputs, in the same order (q, k, v, the alpha
     noise, the beta noise, state_in).  Returns the dict of make_inputs plus
     "frame_tokens", with alpha of shape [B, F, H].
+
+    features="relu" passes the q and k draws through max(0, .) before the
+    per-token L2 normalisation (the paper's non-negative feature maps, which
+    the normalized readout needs for positive denominators) and adds
+    "z_in" [B, H, Dk], a non-negative normalizer state (|N(0, 0.02)|) when the
+    workload carries a state, drawn after state_in.
     """
     w = WORKLOADS[workload] if isinstance(workload, int) else workload
     idx = WORKLOADS.index(w) if w in WORKLOADS else 99
@@ -145,8 +151,11 @@ def make_frame_inputs(workload, frames, *, frame_tokens=None, call=0, B=None, H=
     state = w.state if state is None else state
     rng = np.random.default_rng(500000 + 1000 * idx + call if seed is None else seed)
 
-    q = _unit_rows(rng.standard_normal((B, T, H, Dk), dtype=np.float32))
-    k = _unit_rows(rng.standard_normal((B, T, H, Dk), dtype=np.float32))
+    if features not in ("gauss", "relu"):
+        raise ValueError(features)
+    feat = (lambda x: np.maximum(x, 0.0)) if features == "relu" else (lambda x: x)
+    q = _unit_rows(feat(rng.standard_normal((B, T, H, Dk), dtype=np.float32)))
+    k = _unit_rows(feat(rng.standard_normal((B, T, H, Dk), dtype=np.float32)))
     v = rng.standard_normal((B, T, H, Dv), dtype=np.float32)
     if w.alpha.startswith("softplus"):
         mu = float(w.alpha[len("softplus"):])
@@ -169,9 +178,15 @@ def make_frame_inputs(workload, frames, *, frame_tokens=None, call=0, B=None, H=
         state_in = (0.02 * rng.standard_normal((B, H, Dk, Dv), dtype=np.float32)).astype(np.float32)
     else:
         raise ValueError(state)
+    z_in = None
+    if features == "relu" and state_in is not None:
+        z_in = np.abs(0.02 * rng.standard_normal((B, H, Dk), dtype=np.float32)).astype(np.float32)
     if dtype == "bf16":
         q, k, v = f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
     elif dtype != "f32":
         raise ValueError(dtype)
-    return dict(q=q, k=k, v=v, alpha=alpha, beta=beta, state_in=state_in, dtype=dtype,
-                frame_tokens=N)
+    out = dict(q=q, k=k, v=v, alpha=alpha, beta=beta, state_in=state_in, dtype=dtype,
+               frame_tokens=N)
+    if features == "relu":
+        out["z_in"] = z_in
+    return out

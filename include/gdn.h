@@ -241,6 +241,53 @@ int gdn_frame_profile_stages(const void *q, const void *k, const void *v,
                              int is_bf16, int token_splits, void *ws, size_t ws_bytes, int reps,
                              float *stage_ms, void *stream);
 
+/*
+ * Frame-wise forward with the normalizer state and the normalized readout
+ * (Section "Frame-wise Gated DeltaNet": equation appendix_gdn_z_update /
+ * appendix_gdn_z_compact for the state, equation appendix_gdn_readout for the
+ * readout; no rotary embedding on this path, so rotated and unrotated keys and
+ * queries coincide).  Beside H, a vector state z = S^z of length Dk per (b, h)
+ * is carried from the keys alone:
+ *
+ *     z_f = alpha_f (I - K~_f^T B_f K~_f) z_{f-1} + K~_f^T beta_f
+ *     o_t = (H_f^T q_t) / (z_f . q_t + eps)      for every token t of frame f
+ *
+ * (eps: the paper uses 1e-6).  Everything else is as gdn_frame_forward;
+ * in addition
+ *   z_in   [B][H][Dk]   fp32 device pointer or NULL (zero state)
+ *   z_out  [B][H][Dk]   fp32 device pointer or NULL (terminal z dropped)
+ * z_in == z_out (in place) is allowed; z_out may not overlap any other input
+ * or output.  The denominator is not checked: the paper's non-negative
+ * feature maps keep it positive, other inputs can make it vanish.
+ * is_bf16 selects the element type of q, k, v and out.  On the bf16 path z
+ * enters the products rounded to bf16 (as H does), the states stay fp32.
+ * gdn_frame_forward_norm uses the library-cached workspace;
+ * gdn_frame_forward_norm_ex a caller-owned one of gdn_frame_workspace_bytes
+ * (the same size as for the un-normalized call) and an explicit token-split
+ * count; gdn_frame_profile_stages_norm times the four stages like
+ * gdn_frame_profile_stages (rejecting state_in == state_out and
+ * z_in == z_out).
+ */
+int gdn_frame_forward_norm(const void *q, const void *k, const void *v,
+                           const float *alpha, const float *beta, const float *state_in,
+                           const float *z_in, void *out, float *state_out, float *z_out,
+                           int B, int H, int F, int N, int Dk, int Dv, float key_scale, float eps,
+                           int is_bf16, void *stream);
+
+int gdn_frame_forward_norm_ex(const void *q, const void *k, const void *v,
+                              const float *alpha, const float *beta, const float *state_in,
+                              const float *z_in, void *out, float *state_out, float *z_out,
+                              int B, int H, int F, int N, int Dk, int Dv, float key_scale, float eps,
+                              int is_bf16, int token_splits, void *ws, size_t ws_bytes,
+                              void *stream);
+
+int gdn_frame_profile_stages_norm(const void *q, const void *k, const void *v,
+                                  const float *alpha, const float *beta, const float *state_in,
+                                  const float *z_in, void *out, float *state_out, float *z_out,
+                                  int B, int H, int F, int N, int Dk, int Dv, float key_scale,
+                                  float eps, int is_bf16, int token_splits, void *ws,
+                                  size_t ws_bytes, int reps, float *stage_ms, void *stream);
+
 /* Static, human-readable text for a status code. */
 const char *gdn_status_string(int status);
 

@@ -326,7 +326,18 @@ int run_cached(const void *q, const void *k, const void *v, const float *alpha, 
 
 // ---------------------------------------------------------------------------
 // Frame-wise path (gdn_frame_forward*): frame summaries, their reduction over
-// token splits, the scan over frames, and the output.
+// token splits, the scan over frames, and the output; optionally with the
+// normalizer state (gdn_frame_forward_norm*).
+
+struct FrameArgs {
+    const void *q, *k, *v;
+    const float *alpha, *beta, *state_in, *z_in;
+    void *out;
+    float *state_out, *z_out;
+    int B, H, F, N, Dk, Dv;
+    float key_scale, eps;
+    bool bf16, norm;
+};
 
 struct FrameWs {
     size_t PG, PA, Gf, Af, Hf, total;
@@ -337,9 +348,7 @@ int frame_blocks(int N) { return (N + 63) / 64; }
 // Token splits per frame: a split is a whole number of 64-token blocks, and
 // the library's choice (token_splits <= 0) is the largest count that keeps the
 // summary workgroups (one per split) within one per CU (256), at least 1.
-int frame_splits(long long units, int N, int Dk, int Dv, int token_splits) {
-    (void)Dk;
-    (void)Dv;
+int frame_splits(long long units, int N, int token_splits) {
     const int nb = frame_blocks(N);
     int ns = token_splits;
     if (ns <= 0) ns = (int)(256 / units);
@@ -349,17 +358,20 @@ int frame_splits(long long units, int N, int Dk, int Dv, int token_splits) {
     return (nb + per - 1) / per;          // no empty split
 }
 
+// One layout for both variants: the A tiles and the state fragments have room
+// for the normalizer's extra 16-column tile.
 FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS) {
     const size_t bhf = (size_t)B * H * F;
+    const size_t DVn = (size_t)Dv + 16;
     FrameWs L;
     size_t off = 0;
     // partial sums only with several token splits
     const size_t np = NS > 1 ? (size_t)NS : 0;
     L.PG = off; off = align256(off + bhf * np * Dk * Dk * 4);
-    L.PA = off; off = align256(off + bhf * np * Dk * Dv * 4);
+    L.PA = off; off = align256(off + bhf * np * Dk * DVn * 4);
     L.Gf = off; off = align256(off + bhf * Dk * Dk * esz);
-    L.Af = off; off = align256(off + bhf * Dk * Dv * 4);
-    L.Hf = off; off = align256(off + bhf * Dk * Dv * esz);
+    L.Af = off; off = align256(off + bhf * Dk * DVn * 4);
+    L.Hf = off; off = align256(off + bhf * Dk * DVn * esz);
     L.total = off;
     return L;
 }
@@ -389,56 +401,66 @@ bool frame_shape_ok(int B, int H, int F, int N) {
 
 bool frame_dims_ok(int Dk, int Dv) { return (Dk == 64 || Dk == 128) && (Dv == 64 || Dv == 128); }
 
-int frame_validate(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
-                   const float *state_in, const void *out, const float *state_out, int B, int H, int F,
-                   int N, int Dk, int Dv, size_t esz) {
-    if (!q || !k || !v || !alpha || !beta || !out) return GDN_ERR_NULL;
-    if (!frame_shape_ok(B, H, F, N)) return GDN_ERR_SHAPE;
-    if (!frame_dims_ok(Dk, Dv)) return GDN_ERR_UNSUPPORTED;
-    if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(alpha) || misaligned(beta) ||
-        misaligned(state_in) || misaligned(out) || misaligned(state_out))
+int frame_validate(const FrameArgs &a) {
+    if (!a.q || !a.k || !a.v || !a.alpha || !a.beta || !a.out) return GDN_ERR_NULL;
+    if (!frame_shape_ok(a.B, a.H, a.F, a.N)) return GDN_ERR_SHAPE;
+    if (!frame_dims_ok(a.Dk, a.Dv)) return GDN_ERR_UNSUPPORTED;
+    if (misaligned(a.q) || misaligned(a.k) || misaligned(a.v) || misaligned(a.alpha) || misaligned(a.beta) ||
+        misaligned(a.state_in) || misaligned(a.out) || misaligned(a.state_out) || misaligned(a.z_in) ||
+        misaligned(a.z_out))
         return GDN_ERR_ALIGN;
-    const size_t ntok = (size_t)B * F * N * H;
-    const Range rq = range(q, ntok * Dk * esz), rk = range(k, ntok * Dk * esz),
-                rv = range(v, ntok * Dv * esz), ra = range(alpha, (size_t)B * F * H * 4),
-                rb = range(beta, ntok * 4), ro = range(out, ntok * Dv * esz);
-    const size_t sbytes = (size_t)B * H * Dk * Dv * 4;
-    const Range rsi = range(state_in, sbytes), rso = range(state_out, sbytes);
-    const Range ins[] = {rq, rk, rv, ra, rb, rsi};
+    const size_t esz = a.bf16 ? 2 : 4;
+    const size_t ntok = (size_t)a.B * a.F * a.N * a.H;
+    const Range rq = range(a.q, ntok * a.Dk * esz), rk = range(a.k, ntok * a.Dk * esz),
+                rv = range(a.v, ntok * a.Dv * esz), ra = range(a.alpha, (size_t)a.B * a.F * a.H * 4),
+                rb = range(a.beta, ntok * 4), ro = range(a.out, ntok * a.Dv * esz);
+    const size_t sbytes = (size_t)a.B * a.H * a.Dk * a.Dv * 4, zbytes = (size_t)a.B * a.H * a.Dk * 4;
+    const Range rsi = range(a.state_in, sbytes), rso = range(a.state_out, sbytes);
+    const Range rzi = range(a.norm ? a.z_in : nullptr, zbytes), rzo = range(a.norm ? a.z_out : nullptr, zbytes);
+    // outputs may not overlap the inputs or each other; a state may be updated
+    // in place (the same buffer in and out)
+    const Range ins[] = {rq, rk, rv, ra, rb, rsi, rzi};
     for (const Range &r : ins)
         if (ro.overlaps(r)) return GDN_ERR_ALIAS;
-    if (rso.valid()) {
-        for (int i = 0; i < 5; ++i)
-            if (rso.overlaps(ins[i])) return GDN_ERR_ALIAS;
-        if (rso.overlaps(ro)) return GDN_ERR_ALIAS;
-        if (rsi.valid() && rso.overlaps(rsi) && rso.lo != rsi.lo) return GDN_ERR_ALIAS;
+    // state_out may share state_in's buffer exactly (in-place update), z_out z_in's
+    const Range *outs[] = {&rso, &rzo};
+    for (int o = 0; o < 2; ++o) {
+        const Range &r = *outs[o];
+        if (!r.valid()) continue;
+        const int own = o == 0 ? 5 : 6;
+        for (int i = 0; i < 7; ++i) {
+            if (!r.overlaps(ins[i])) continue;
+            if (i != own || r.lo != ins[i].lo) return GDN_ERR_ALIAS;
+        }
+        if (r.overlaps(ro)) return GDN_ERR_ALIAS;
     }
+    if (rso.overlaps(rzo)) return GDN_ERR_ALIAS;
     return GDN_OK;
 }
 
 template <class E>
-gdn::FrameParams<E> make_frame_params(const void *q, const void *k, const void *v, const float *alpha,
-                                      const float *beta, const float *state_in, void *out,
-                                      float *state_out, int B, int H, int F, int N, int Dk, int Dv,
-                                      float key_scale, int NS, void *ws) {
+gdn::FrameParams<E> make_frame_params(const FrameArgs &a, int NS, void *ws) {
     gdn::FrameParams<E> p;
-    p.q = (const E *)q;
-    p.k = (const E *)k;
-    p.v = (const E *)v;
-    p.alpha = alpha;
-    p.beta = beta;
-    p.state_in = state_in;
-    p.out = (E *)out;
-    p.state_out = state_out;
-    p.B = B;
-    p.H = H;
-    p.F = F;
-    p.N = N;
+    p.q = (const E *)a.q;
+    p.k = (const E *)a.k;
+    p.v = (const E *)a.v;
+    p.alpha = a.alpha;
+    p.beta = a.beta;
+    p.state_in = a.state_in;
+    p.out = (E *)a.out;
+    p.state_out = a.state_out;
+    p.B = a.B;
+    p.H = a.H;
+    p.F = a.F;
+    p.N = a.N;
     p.NS = NS;
-    p.NBT = 64 * ((frame_blocks(N) + NS - 1) / NS);
-    frame_out_split((long long)B * H * F, N, gdn::FrameOut<E>::WGS, p.OB, p.OTPW);
-    p.key_scale = key_scale;
-    const FrameWs L = frame_ws_layout(B, H, F, Dk, Dv, sizeof(E), NS);
+    p.NBT = 64 * ((frame_blocks(a.N) + NS - 1) / NS);
+    frame_out_split((long long)a.B * a.H * a.F, a.N, gdn::kFrameOutWgs, p.OB, p.OTPW);
+    p.key_scale = a.key_scale;
+    p.z_in = a.norm ? a.z_in : nullptr;
+    p.z_out = a.norm ? a.z_out : nullptr;
+    p.eps = a.eps;
+    const FrameWs L = frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, sizeof(E), NS);
     unsigned char *base = (unsigned char *)ws;
     p.PG = (float *)(base + L.PG);
     p.PA = (float *)(base + L.PA);
@@ -450,42 +472,43 @@ gdn::FrameParams<E> make_frame_params(const void *q, const void *k, const void *
 
 constexpr int kFrameStages = 4;  // summaries, reduction, scan, output
 
-template <class E, int DK, int DV>
+template <class E, int DK, int DV, bool NORM>
 hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, hipEvent_t *ev) {
     using LS = gdn::FrameSumLds<E, DK, DV>;
-    using LO = gdn::FrameOutLds<E, DK, DV>;
+    using LO = gdn::FrameOutLds<E, DK, DV, NORM>;
     static std::once_flag attr_once;
     static hipError_t attr_err = hipSuccess;
     std::call_once(attr_once, [&] {
-        hipError_t e = hipFuncSetAttribute((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV>,
+        hipError_t e = hipFuncSetAttribute((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, NORM>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)LS::bytes);
         if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)gdn::gdn_frame_output_kernel<E, DK, DV>,
+            e = hipFuncSetAttribute((const void *)gdn::gdn_frame_output_kernel<E, DK, DV, NORM>,
                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)LO::bytes);
         attr_err = e;
     });
     if (attr_err != hipSuccess) return attr_err;
     const long long BH = (long long)p.B * p.H, units = BH * p.F;
-    constexpr int NI = (DK / 16) * (DK / 32) + (DK / 16) * (DV / 16);  // reduction items per unit
+    constexpr int NJ = DV / 16 + NORM;
+    constexpr int NI = (DK / 16) * (DK / 32) + (DK / 16) * NJ;      // reduction items per unit
     auto stage = [&](int i) {
         switch (i) {
         case 0:
-            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV>), dim3((unsigned)(units * p.NS)),
+            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV, NORM>), dim3((unsigned)(units * p.NS)),
                                dim3((gdn::kSumCompute + gdn::kSumLoaders) * 64), LS::bytes, s, p);
             break;
         case 1:
             // a single split writes the summaries in their final form
             if (p.NS > 1)
-                hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV>), dim3((unsigned)units, (NI + 3) / 4),
-                                   dim3(256), 0, s, p);
+                hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV, NORM>),
+                                   dim3((unsigned)units, (NI + 3) / 4), dim3(256), 0, s, p);
             break;
         case 2:
-            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV>), dim3(gdn::xcd_blocks(BH, DV / 16)),
+            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV, NORM>), dim3(gdn::xcd_blocks(BH, NJ)),
                                dim3(64), 0, s, p);
             break;
         default:
-            hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV>), dim3(gdn::xcd_blocks(units, p.OB)),
-                               dim3(256), LO::bytes, s, p);
+            hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV, NORM>),
+                               dim3(gdn::xcd_blocks(units, p.OB)), dim3(256), LO::bytes, s, p);
         }
     };
     hipError_t er = hipSuccess;
@@ -502,50 +525,77 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
     return le != hipSuccess ? le : er;
 }
 
-template <class E>
-hipError_t frame_dispatch(const gdn::FrameParams<E> &p, int Dk, int Dv, hipStream_t s, int reps, hipEvent_t *ev) {
-    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128>(p, s, reps, ev);
-    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64>(p, s, reps, ev);
-    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64>(p, s, reps, ev);
-    return launch_frame<E, 64, 128>(p, s, reps, ev);
+template <class E, bool NORM>
+hipError_t frame_dispatch_n(const gdn::FrameParams<E> &p, int Dk, int Dv, hipStream_t s, int reps, hipEvent_t *ev) {
+    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128, NORM>(p, s, reps, ev);
+    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64, NORM>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64, NORM>(p, s, reps, ev);
+    return launch_frame<E, 64, 128, NORM>(p, s, reps, ev);
 }
 
-int frame_run(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
-              const float *state_in, void *out, float *state_out, int B, int H, int F, int N, int Dk,
-              int Dv, float key_scale, bool bf16, int token_splits, void *ws, size_t ws_bytes, void *stream,
-              int reps, hipEvent_t *ev) {
-    const size_t esz = bf16 ? 2 : 4;
-    int st = frame_validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, esz);
+template <class E>
+hipError_t frame_dispatch(const FrameArgs &a, int NS, void *ws, hipStream_t s, int reps, hipEvent_t *ev) {
+    const gdn::FrameParams<E> p = make_frame_params<E>(a, NS, ws);
+    return a.norm ? frame_dispatch_n<E, true>(p, a.Dk, a.Dv, s, reps, ev)
+                  : frame_dispatch_n<E, false>(p, a.Dk, a.Dv, s, reps, ev);
+}
+
+int frame_run(const FrameArgs &a, int token_splits, void *ws, size_t ws_bytes, void *stream, int reps,
+              hipEvent_t *ev) {
+    int st = frame_validate(a);
     if (st != GDN_OK) return st;
-    const int NS = frame_splits((long long)B * H * F, N, Dk, Dv, token_splits);
-    if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < frame_ws_layout(B, H, F, Dk, Dv, esz, NS).total)
+    const int NS = frame_splits((long long)a.B * a.H * a.F, a.N, token_splits);
+    if (!ws || ((uintptr_t)ws & 255u) ||
+        ws_bytes < frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, a.bf16 ? 2 : 4, NS).total)
         return GDN_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
-    hipError_t e;
-    if (bf16)
-        e = frame_dispatch(make_frame_params<uint16_t>(q, k, v, alpha, beta, state_in, out, state_out, B, H, F,
-                                                       N, Dk, Dv, key_scale, NS, ws),
-                           Dk, Dv, s, reps, ev);
-    else
-        e = frame_dispatch(make_frame_params<float>(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N,
-                                                    Dk, Dv, key_scale, NS, ws),
-                           Dk, Dv, s, reps, ev);
+    const hipError_t e = a.bf16 ? frame_dispatch<uint16_t>(a, NS, ws, s, reps, ev)
+                                : frame_dispatch<float>(a, NS, ws, s, reps, ev);
     return e == hipSuccess ? GDN_OK : GDN_ERR_HIP;
 }
 
-int frame_run_cached(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
-                     const float *state_in, void *out, float *state_out, int B, int H, int F, int N, int Dk,
-                     int Dv, float key_scale, bool bf16, void *stream) {
-    const size_t esz = bf16 ? 2 : 4;
-    int st = frame_validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, esz);
+int frame_run_cached(const FrameArgs &a, void *stream) {
+    int st = frame_validate(a);
     if (st != GDN_OK) return st;
-    const size_t need =
-        frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, Dk, Dv, 0)).total;
+    const size_t need = frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, a.bf16 ? 2 : 4,
+                                        frame_splits((long long)a.B * a.H * a.F, a.N, 0))
+                            .total;
     void *ws = nullptr;
     st = cached_workspace(need, &ws);
     if (st != GDN_OK) return st;
-    return frame_run(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale, bf16, 0,
-                     ws, need, stream, 1, nullptr);
+    return frame_run(a, 0, ws, need, stream, 1, nullptr);
+}
+
+int frame_profile(const FrameArgs &a, int token_splits, void *ws, size_t ws_bytes, int reps, float *stage_ms,
+                  void *stream) {
+    if (!stage_ms || reps < 1) return GDN_ERR_NULL;
+    // stages are re-run in place, so no state may be updated in place
+    if (a.state_in && a.state_in == a.state_out) return GDN_ERR_ALIAS;
+    if (a.norm && a.z_in && a.z_in == a.z_out) return GDN_ERR_ALIAS;
+    hipEvent_t ev[2 * kFrameStages] = {};
+    int status = GDN_OK;
+    for (auto &e : ev)
+        if (status == GDN_OK && hipEventCreate(&e) != hipSuccess) {
+            e = nullptr;
+            status = GDN_ERR_HIP;
+        }
+    if (status == GDN_OK) status = frame_run(a, token_splits, ws, ws_bytes, stream, reps, ev);
+    if (status == GDN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess) status = GDN_ERR_HIP;
+    for (int i = 0; i < kFrameStages && status == GDN_OK; ++i) {
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]) != hipSuccess) status = GDN_ERR_HIP;
+        stage_ms[i] = ms / reps;
+    }
+    for (auto &e : ev)
+        if (e) (void)hipEventDestroy(e);
+    return status;
+}
+
+FrameArgs frame_args(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                     const float *state_in, const float *z_in, void *out, float *state_out, float *z_out, int B,
+                     int H, int F, int N, int Dk, int Dv, float key_scale, float eps, bool bf16, bool norm) {
+    return FrameArgs{q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
+                     B, H, F, N, Dk, Dv, key_scale, eps, bf16, norm};
 }
 
 }  // namespace
@@ -641,34 +691,37 @@ int gdn_profile_stages(const void *q, const void *k, const void *v, const float 
 int gdn_frame_forward(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
                       const float *state_in, void *out, float *state_out, int B, int H, int F, int N,
                       int Dk, int Dv, float key_scale, void *stream) {
-    return frame_run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
-                            true, stream);
+    return frame_run_cached(frame_args(q, k, v, alpha, beta, state_in, nullptr, out, state_out, nullptr, B, H,
+                                       F, N, Dk, Dv, key_scale, 0.f, true, false),
+                            stream);
 }
 
 int gdn_frame_forward_f32(const float *q, const float *k, const float *v, const float *alpha,
                           const float *beta, const float *state_in, float *out, float *state_out, int B,
                           int H, int F, int N, int Dk, int Dv, float key_scale, void *stream) {
-    return frame_run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
-                            false, stream);
+    return frame_run_cached(frame_args(q, k, v, alpha, beta, state_in, nullptr, out, state_out, nullptr, B, H,
+                                       F, N, Dk, Dv, key_scale, 0.f, false, false),
+                            stream);
 }
 
 int gdn_frame_token_splits(int B, int H, int F, int N, int Dk, int Dv, int token_splits) {
     if (!frame_shape_ok(B, H, F, N) || !frame_dims_ok(Dk, Dv)) return 0;
-    return frame_splits((long long)B * H * F, N, Dk, Dv, token_splits);
+    return frame_splits((long long)B * H * F, N, token_splits);
 }
 
 size_t gdn_frame_workspace_bytes(int B, int H, int F, int N, int Dk, int Dv, int is_bf16, int token_splits) {
-    const size_t esz = is_bf16 ? 2 : 4;
     if (!frame_shape_ok(B, H, F, N) || !frame_dims_ok(Dk, Dv)) return 0;
-    return frame_ws_layout(B, H, F, Dk, Dv, esz, frame_splits((long long)B * H * F, N, Dk, Dv, token_splits)).total;
+    return frame_ws_layout(B, H, F, Dk, Dv, is_bf16 ? 2 : 4, frame_splits((long long)B * H * F, N, token_splits))
+        .total;
 }
 
 int gdn_frame_forward_ex(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
                          const float *state_in, void *out, float *state_out, int B, int H, int F, int N,
                          int Dk, int Dv, float key_scale, int is_bf16, int token_splits, void *ws,
                          size_t ws_bytes, void *stream) {
-    return frame_run(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
-                     is_bf16 != 0, token_splits, ws, ws_bytes, stream, 1, nullptr);
+    return frame_run(frame_args(q, k, v, alpha, beta, state_in, nullptr, out, state_out, nullptr, B, H, F, N,
+                                Dk, Dv, key_scale, 0.f, is_bf16 != 0, false),
+                     token_splits, ws, ws_bytes, stream, 1, nullptr);
 }
 
 int gdn_frame_profile_stages(const void *q, const void *k, const void *v, const float *alpha,
@@ -676,27 +729,38 @@ int gdn_frame_profile_stages(const void *q, const void *k, const void *v, const 
                              int H, int F, int N, int Dk, int Dv, float key_scale, int is_bf16,
                              int token_splits, void *ws, size_t ws_bytes, int reps, float *stage_ms,
                              void *stream) {
-    if (!stage_ms || reps < 1) return GDN_ERR_NULL;
-    if (state_in && state_in == state_out) return GDN_ERR_ALIAS;
-    hipEvent_t ev[2 * kFrameStages] = {};
-    int status = GDN_OK;
-    for (auto &e : ev)
-        if (status == GDN_OK && hipEventCreate(&e) != hipSuccess) {
-            e = nullptr;
-            status = GDN_ERR_HIP;
-        }
-    if (status == GDN_OK)
-        status = frame_run(q, k, v, alpha, beta, state_in, out, state_out, B, H, F, N, Dk, Dv, key_scale,
-                           is_bf16 != 0, token_splits, ws, ws_bytes, stream, reps, ev);
-    if (status == GDN_OK && hipStreamSynchronize((hipStream_t)stream) != hipSuccess) status = GDN_ERR_HIP;
-    for (int i = 0; i < kFrameStages && status == GDN_OK; ++i) {
-        float ms = 0.f;
-        if (hipEventElapsedTime(&ms, ev[2 * i], ev[2 * i + 1]) != hipSuccess) status = GDN_ERR_HIP;
-        stage_ms[i] = ms / reps;
-    }
-    for (auto &e : ev)
-        if (e) (void)hipEventDestroy(e);
-    return status;
+    return frame_profile(frame_args(q, k, v, alpha, beta, state_in, nullptr, out, state_out, nullptr, B, H, F,
+                                    N, Dk, Dv, key_scale, 0.f, is_bf16 != 0, false),
+                         token_splits, ws, ws_bytes, reps, stage_ms, stream);
+}
+
+int gdn_frame_forward_norm(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                           const float *state_in, const float *z_in, void *out, float *state_out, float *z_out,
+                           int B, int H, int F, int N, int Dk, int Dv, float key_scale, float eps, int is_bf16,
+                           void *stream) {
+    return frame_run_cached(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N,
+                                       Dk, Dv, key_scale, eps, is_bf16 != 0, true),
+                            stream);
+}
+
+int gdn_frame_forward_norm_ex(const void *q, const void *k, const void *v, const float *alpha,
+                              const float *beta, const float *state_in, const float *z_in, void *out,
+                              float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
+                              float key_scale, float eps, int is_bf16, int token_splits, void *ws,
+                              size_t ws_bytes, void *stream) {
+    return frame_run(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv,
+                                key_scale, eps, is_bf16 != 0, true),
+                     token_splits, ws, ws_bytes, stream, 1, nullptr);
+}
+
+int gdn_frame_profile_stages_norm(const void *q, const void *k, const void *v, const float *alpha,
+                                  const float *beta, const float *state_in, const float *z_in, void *out,
+                                  float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
+                                  float key_scale, float eps, int is_bf16, int token_splits, void *ws,
+                                  size_t ws_bytes, int reps, float *stage_ms, void *stream) {
+    return frame_profile(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk,
+                                    Dv, key_scale, eps, is_bf16 != 0, true),
+                         token_splits, ws, ws_bytes, reps, stage_ms, stream);
 }
 
 const char *gdn_status_string(int status) {

@@ -53,12 +53,30 @@ template <class E> struct FrameParams {
     int NS, NBT;                 // token splits per frame, tokens per split (a multiple of 64)
     int OB, OTPW;                // output workgroups per frame, 16-token tiles per workgroup
     float key_scale;
+    // normalizer (the kernels' NORM variant): z = S^z as one more state
+    // column tile (column 0 holds z, the others stay zero), written by a value
+    // column of ones; NJ = Dv / 16 + NORM column tiles below
+    const float *z_in;           // [B][H][Dk] or null (zero)
+    float *z_out;                // [B][H][Dk] or null
+    float eps;
     float *PG;                   // [B*H][F][NS][Dk/16][Dk/16][64][4]  partial G tiles
-    float *PA;                   // [B*H][F][NS][Dk/16][Dv/16][64][4]  partial A tiles
+    float *PA;                   // [B*H][F][NS][Dk/16][NJ][64][4]     partial A tiles
     E *Gf;                       // [B*H][F][Dk/16][Dk/32][64][8]      G operand fragments
-    float *Af;                   // [B*H][F][Dk/16][Dv/16][64][4]      A tiles
-    E *Hf;                       // [B*H][F][Dv/16][Dk/32][64][8]      H_f operand fragments
+    float *Af;                   // [B*H][F][Dk/16][NJ][64][4]         A tiles
+    E *Hf;                       // [B*H][F][NJ][Dk/32][64][8]         H_f operand fragments
 };
+
+// A fragment whose lanes li = 0 hold ones and all other lanes zeros: as the
+// B operand it is a value column of ones in column 0 of a 16-column tile.
+template <class E> __device__ __forceinline__ typename Tr<E>::frag ones_col_frag(int li);
+template <> __device__ __forceinline__ Tr<uint16_t>::frag ones_col_frag<uint16_t>(int li) {
+    const uint32_t x = li == 0 ? 0x3f803f80u : 0u;             // two bf16 ones
+    return Tr<uint16_t>::frag{x, x, x, x};
+}
+template <> __device__ __forceinline__ Tr<float>::frag ones_col_frag<float>(int li) {
+    const float x = li == 0 ? 1.f : 0.f;
+    return Tr<float>::frag{x, x, x, x, x, x, x, x};
+}
 
 // Grids of per_unit workgroups per unit with all workgroups of one unit on
 // one XCD (blocks are dealt to the 8 XCDs round robin: id = 8 y + x runs on
@@ -162,7 +180,7 @@ __device__ __forceinline__ Tr<float>::frag scale_frag(Tr<float>::frag x, const f
 // With several splits it writes fp32 partial tiles for the reduction.
 constexpr int kSumCompute = 8, kSumLoaders = 4;
 
-template <class E, int DK, int DV>
+template <class E, int DK, int DV, bool NORM>
 __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_summary_kernel(FrameParams<E> p) {
     using L = FrameSumLds<E, DK, DV>;
     using TR = Tr<E>;
@@ -173,6 +191,7 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
     constexpr int NCK2 = L::NCK / 2, NCV2 = L::NCV / 2;
     constexpr int NR = DK / 16, NP = NR / 2, KBN = DK / 32;           // row tiles, row pairs
     constexpr int NCG = DK / 16, NCA = DV / 16;                       // column tiles of G, A
+    constexpr int NJA = NCA + NORM;                                   // A tiles incl. the normalizer
     constexpr int SUB = 4 / NP;                                       // column shares per pair
     constexpr int CPG = NCG / SUB, CPA = NCA / SUB;                   // column tiles per wave
     extern __shared__ __align__(16) unsigned char smem[];
@@ -258,6 +277,11 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
     for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int j = 0; j < CPW; ++j) acc[a][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // normalizer: the A waves of the first column share also accumulate
+    // K^T B 1 (a column of ones as the value) for their row pair
+    f32x4 accz[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+    const bool zw = NORM && !gw && c0 == 0;
+    const frag ones = ones_col_frag<E>(li);
 
     // the block loop, specialised for G waves (GB) and A waves, so that it has
     // no branch inside: all operand reads of a block (the K^T fragments
@@ -299,6 +323,12 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
             for (int a = 0; a < 2; ++a)
 #pragma unroll
                 for (int j = 0; j < NC; ++j) acc[a][j] = TR::mma(o.a[a], o.b[j], acc[a][j]);
+            if constexpr (NORM && !GB) {
+                if (zw) {
+#pragma unroll
+                    for (int a = 0; a < 2; ++a) accz[a] = TR::mma(o.a[a], ones, accz[a]);
+                }
+            }
         };
         Ops o0, o1;
         for (int i = 0; i < nb; ++i) {
@@ -334,11 +364,16 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
                 const int jt = c0 * CPA + j;
 #pragma unroll
                 for (int a = 0; a < 2; ++a)
-                    *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NCA + jt) * 256 + l * 4) = acc[a][j] * ks;
+                    *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + jt) * 256 + l * 4) = acc[a][j] * ks;
+            }
+            if (zw) {
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + NCA) * 256 + l * 4) = accz[a] * ks;
             }
         }
     } else {
-        const int NC = gw ? NCG : NCA;
+        const int NC = gw ? NCG : NJA;
         float *dst = (gw ? p.PG : p.PA) + (fi * p.NS + s) * (size_t)NR * NC * 256;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
@@ -346,15 +381,20 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
             for (int j = 0; j < CPW; ++j)
                 if (j < cpw)
                     *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + c0 * cpw + j) * 64 + l) * 4) = acc[a][j];
+        if (zw) {
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+                *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + NCA) * 64 + l) * 4) = accz[a];
+        }
     }
 }
 
 // Sum over the splits.  Items per (frame, head): the Dk/16 x Dk/32 G operand
 // fragments, then the Dk/16 x Dv/16 A tiles; one wave per item.
-template <class E, int DK, int DV>
+template <class E, int DK, int DV, bool NORM>
 __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
-    constexpr int NR = DK / 16, KB = DK / 32, NCV = DV / 16;
+    constexpr int NR = DK / 16, KB = DK / 32, NCV = DV / 16 + NORM;
     constexpr int NGI = NR * KB, NI = NGI + NR * NCV;
     const int item = blockIdx.y * 4 + (threadIdx.x >> 6);
     const size_t fi = blockIdx.x;                                // (b*H + h) * F + f
@@ -389,19 +429,28 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
 // alternately; bf16 only, the fp32 fragments are twice as large).
 template <class E> struct FrameScanPrefetch { static constexpr bool value = sizeof(E) == 2; };
 
-template <class E, int DK, int DV>
+template <class E, int DK, int DV, bool NORM>
 __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
-    constexpr int NT = DK / 16, KB = DK / 32, NJ = DV / 16;
+    constexpr int NT = DK / 16, KB = DK / 32, NJ = DV / 16 + NORM;    // NORM: tile DV / 16 carries z
     int bh, jt;
     xcd_unit(blockIdx.x, NJ, bh, jt);
     if (bh >= p.B * p.H) return;
     const int b = bh / p.H, h = bh - b * p.H;
     const int l = threadIdx.x & 63, li = l & 15, lg = l >> 4;
     const int col = 16 * jt + li;
+    const bool ztile = NORM && jt == DV / 16;                         // column 0 of this tile is z
     f32x4 Hacc[NT];
-    if (p.state_in) {
+    if (ztile) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                Hacc[t][q] = (p.z_in && li == 0) ? p.z_in[(size_t)bh * DK + r0 + q] : 0.f;
+        }
+    } else if (p.state_in) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
@@ -466,7 +515,16 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
             frame(f, g0, v0, a0);
         }
     }
-    if (p.state_out) {
+    if (ztile) {
+        if (p.z_out && li == 0) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t) {
+                const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) p.z_out[(size_t)bh * DK + r0 + q] = Hacc[t][q];
+            }
+        }
+    } else if (p.state_out) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
             const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
@@ -481,29 +539,29 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
 // H_f's fragments are staged in LDS once per workgroup: lane (li, lg) of
 // fragment (jo, kb) holds H_f[32 kb + 8 lg + q'][16 jo + li], the A operand of
 // row 16 jo + li of H_f^T.  With the query rows as B operand the product tile
-// is O^T, and lane (li, lg) gets O[token li][16 jo + 4 lg + q].  bf16 keeps all
-// of H_f in registers; each wave streams its tiles with the queries of the
-// next QT tiles in flight while the current ones are multiplied and stored.
-template <class E> struct FrameOut {
-    static constexpr bool HREG = false;                // H_f register-resident
-    static constexpr int QT = 1;                       // tiles per query buffer
-    static constexpr int WGS = 1024;                   // workgroups to aim for
-};
+// is O^T, and lane (li, lg) gets O[token li][16 jo + 4 lg + q].  Each wave
+// streams its tiles with the next tile's queries in flight.  The 16 x Dv
+// result goes through LDS so that global stores write whole rows.
+// NORM: the extra column tile of H_f holds z in its column 0, so its product
+// row 0 (lanes lg = 0, q = 0) is the denominator z . q of token li; it is
+// formed first, shared with the lanes of the same token, and every output
+// element is divided by it plus eps.
+constexpr int kFrameOutWgs = 1024;                 // output workgroups to aim for
 
-template <class E, int DK, int DV> struct FrameOutLds {
+template <class E, int DK, int DV, bool NORM> struct FrameOutLds {
+    static constexpr int NJ = DV / 16 + NORM;
     static constexpr int LDO = DV + 16 / (int)sizeof(E);       // staged output row stride
-    static constexpr size_t oO = sizeof(E) * DK * DV;          // after H_f: one 16-row tile per wave
+    static constexpr size_t oO = sizeof(E) * DK * 16 * NJ;     // after H_f: one 16-row tile per wave
     static constexpr size_t bytes = oO + sizeof(E) * 4 * 16 * LDO;
 };
 
-template <class E, int DK, int DV>
+template <class E, int DK, int DV, bool NORM>
 __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
-    constexpr int KB = DK / 32, NJ = DV / 16, QT = FrameOut<E>::QT;
-    constexpr bool HREG = FrameOut<E>::HREG;
-    constexpr int HV = DV * DK * (int)sizeof(E) / 16;         // 16-byte vectors of H_f
-    static_assert(HV % 256 == 0, "whole vectors per thread");
+    using LO = FrameOutLds<E, DK, DV, NORM>;
+    constexpr int KB = DK / 32, NV = DV / 16, NJ = LO::NJ;
+    constexpr int HV = NJ * 16 * DK * (int)sizeof(E) / 16;    // 16-byte vectors of H_f
     extern __shared__ __align__(16) unsigned char smem[];
     int unit, blk;
     xcd_unit(blockIdx.x, p.OB, unit, blk);
@@ -513,75 +571,68 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
     const size_t fi = (size_t)bh * p.F + f;
 
-    const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)DV * DK);
-#pragma unroll
-    for (int j = 0; j < HV / 256; ++j) ((u32x4 *)smem)[tid + 256 * j] = src[tid + 256 * j];
+    const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
+    for (int j = tid; j < HV; j += 256) ((u32x4 *)smem)[j] = src[j];
 
     const size_t T = (size_t)p.F * p.N;
     const int ntf = (p.N + 15) / 16;                           // tiles in the frame
     const int tile_lo = blk * p.OTPW, tile_hi = min(ntf, tile_lo + p.OTPW);
     const size_t row_f = (size_t)b * T + (size_t)f * p.N;     // token rows of this frame
-    // query fragments of tiles i, i + 4, ..., i + 4 (QT - 1); rows past the frame read its last token
-    auto load_q = [&](int i, frag (&qf)[QT][KB]) {
+    // query fragments of tile i; rows past the frame read its last token
+    auto load_q = [&](int i, frag (&qf)[KB]) {
+        const int n = min(16 * i + li, p.N - 1);
+        const E *qrow = p.q + ((row_f + n) * p.H + h) * DK;
 #pragma unroll
-        for (int u = 0; u < QT; ++u) {
-            const int n = min(16 * (i + 4 * u) + li, p.N - 1);
-            const E *qrow = p.q + ((row_f + n) * p.H + h) * DK;
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) qf[u][kb] = load_frag<E>(qrow + 32 * kb, lg);
-        }
+        for (int kb = 0; kb < KB; ++kb) qf[kb] = load_frag<E>(qrow + 32 * kb, lg);
     };
-    frag hr[HREG ? NJ : 1][KB];
     const E *sH = (const E *)smem + l * 8;
-    // Output tile staging: the 16 x Dv tile goes through LDS so that global
-    // stores write whole rows (16 bytes per lane, a row per 16 bytes * DV / 16
-    // lanes) instead of 4-element pieces.
-    using LO = FrameOutLds<E, DK, DV>;
     E *sO = (E *)(smem + LO::oO) + w * 16 * LO::LDO;
     constexpr int VE = 16 / (int)sizeof(E);                   // elements per 16-byte vector
     constexpr int RV = DV / VE;                                // vectors per output row
-    auto compute = [&](int i, const frag (&qf)[QT][KB]) {
+    auto tile_product = [&](int jo, const frag (&qf)[KB]) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int u = 0; u < QT; ++u) {
+        for (int kb = 0; kb < KB; ++kb) acc = TR::mma(TR::load8(sH + (jo * KB + kb) * 512), qf[kb], acc);
+        return acc;
+    };
+    auto compute = [&](int tile, const frag (&qf)[KB]) {
+        if constexpr (NORM) {
+            // all products first (independent chains), then the division
+            f32x4 acc[NV];
 #pragma unroll
-            for (int jo = 0; jo < NJ; ++jo) {
-                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+            for (int jo = 0; jo < NV; ++jo) acc[jo] = tile_product(jo, qf);
+            const f32x4 dz = tile_product(NV, qf);
+            const float inv = 1.f / (__shfl(dz[0], li) + p.eps);   // the denominator of token li
 #pragma unroll
-                for (int kb = 0; kb < KB; ++kb)
-                    acc = TR::mma(HREG ? hr[HREG ? jo : 0][kb] : TR::load8(sH + (jo * KB + kb) * 512), qf[u][kb], acc);
-                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(acc));
-            }
-            const int tile = i + 4 * u;
-            // rows r of the tile, RV lanes per row, 64 / RV rows per pass
+            for (int jo = 0; jo < NV; ++jo)
+                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(acc[jo] * inv));
+        } else {
 #pragma unroll
-            for (int pass = 0; pass < 16 * RV / 64; ++pass) {
-                const int r = pass * (64 / RV) + l / RV, c = (l % RV) * VE;
-                const u32x4 val = *(const u32x4 *)(sO + r * LO::LDO + c);
-                const int n = 16 * tile + r;
-                if (tile < tile_hi && n < p.N) *(u32x4 *)(p.out + ((row_f + n) * p.H + h) * DV + c) = val;
-            }
+            for (int jo = 0; jo < NV; ++jo)
+                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(tile_product(jo, qf)));
+        }
+        // rows r of the tile, RV lanes per row, 64 / RV rows per pass
+#pragma unroll
+        for (int pass = 0; pass < 16 * RV / 64; ++pass) {
+            const int r = pass * (64 / RV) + l / RV, c = (l % RV) * VE;
+            const u32x4 val = *(const u32x4 *)(sO + r * LO::LDO + c);
+            const int n = 16 * tile + r;
+            if (tile < tile_hi && n < p.N) *(u32x4 *)(p.out + ((row_f + n) * p.H + h) * DV + c) = val;
         }
     };
-    const int step = 4 * QT;                                   // tiles per buffer, all waves
-    const int i0 = tile_lo + w;
     // the prefetch is unconditional (clamped to the workgroup's last tile) so
     // the wait for one buffer always leaves exactly the other in flight
     auto clampi = [&](int i) { return min(i, tile_hi - 1); };
-    frag qa[QT][KB], qb[QT][KB];
+    frag qa[KB], qb[KB];
+    const int i0 = tile_lo + w;
     load_q(clampi(i0), qa);
     lds_barrier();
-    if constexpr (HREG) {
-#pragma unroll
-        for (int jo = 0; jo < NJ; ++jo)
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) hr[jo][kb] = TR::load8(sH + (jo * KB + kb) * 512);
-    }
-    for (int i = i0; i < tile_hi; i += 2 * step) {
-        load_q(clampi(i + step), qb);
+    for (int i = i0; i < tile_hi; i += 8) {
+        load_q(clampi(i + 4), qb);
         compute(i, qa);
-        if (i + step >= tile_hi) break;
-        load_q(clampi(i + 2 * step), qa);
-        compute(i + step, qb);
+        if (i + 4 >= tile_hi) break;
+        load_q(clampi(i + 8), qa);
+        compute(i + 4, qb);
     }
 }
 

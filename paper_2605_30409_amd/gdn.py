@@ -64,6 +64,13 @@ def lib():
         L.gdn_frame_forward_ex.argtypes = fcore + [i, i, vp, sz, vp]
         L.gdn_frame_profile_stages.restype = i
         L.gdn_frame_profile_stages.argtypes = fcore + [i, i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        ncore = [vp, vp, vp, f_p, f_p, f_p, f_p, vp, f_p, f_p, i, i, i, i, i, i, fl, fl, i]
+        L.gdn_frame_forward_norm.restype = i
+        L.gdn_frame_forward_norm.argtypes = ncore + [vp]
+        L.gdn_frame_forward_norm_ex.restype = i
+        L.gdn_frame_forward_norm_ex.argtypes = ncore + [i, vp, sz, vp]
+        L.gdn_frame_profile_stages_norm.restype = i
+        L.gdn_frame_profile_stages_norm.argtypes = ncore + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
         L.gdn_status_string.restype = ctypes.c_char_p
         L.gdn_status_string.argtypes = [i]
         _lib = L
@@ -318,3 +325,69 @@ def frame_forward(q, k, v, alpha, beta, state_in=None, *, frame_tokens, key_scal
         _frame_call(name, q, k, v, alpha, beta, state_in, out, state_out, frame_tokens, key_scale,
                     (), stream)
     return out, state_out
+
+
+# ---------------------------------------------------------------------------
+# Frame-wise GDN with the normalizer state (gdn_frame_forward_norm*).
+
+def _check_z(z, B, H, Dk, dev, name):
+    if z is None:
+        return
+    if z.dtype != torch.float32 or tuple(z.shape) != (B, H, Dk):
+        raise ValueError(f"{name} must be float32 [B, H, Dk]")
+    if z.device != dev or not z.is_contiguous():
+        raise ValueError(f"{name} must be contiguous on {dev}")
+
+
+def _norm_call(name, q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, frame_tokens,
+               key_scale, eps, extra, stream):
+    B, H, T, Dk, Dv, is_bf16 = _check(q, k, v, alpha, beta, state_in, out, state_out, frame_tokens)
+    _check_z(z_in, B, H, Dk, q.device, "z_in")
+    _check_z(z_out, B, H, Dk, q.device, "z_out")
+    N = int(frame_tokens)
+    ks = default_key_scale(Dk, N) if key_scale is None else float(key_scale)
+    with torch.cuda.device(q.device):
+        rc = getattr(lib(), name)(_ptr(q), _ptr(k), _ptr(v), _ptr(alpha), _ptr(beta), _ptr(state_in),
+                                  _ptr(z_in), _ptr(out), _ptr(state_out), _ptr(z_out), B, H, T // N, N,
+                                  Dk, Dv, ctypes.c_float(ks), ctypes.c_float(eps), 1 if is_bf16 else 0,
+                                  *extra, _stream(q.device, stream))
+    if rc != GDN_OK:
+        raise GdnError(name, rc)
+
+
+def gdn_frame_profile_stages_norm(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, ws,
+                                  frame_tokens, key_scale=None, eps=1e-6, token_splits=0, reps=20,
+                                  stream=None):
+    """Mean per-stage durations in ms of the normalized frame-wise path."""
+    ms = (ctypes.c_float * len(FRAME_STAGE_NAMES))()
+    _norm_call("gdn_frame_profile_stages_norm", q, k, v, alpha, beta, state_in, z_in, out, state_out,
+               z_out, frame_tokens, key_scale, eps,
+               (int(token_splits), _ptr(ws), ws.numel(), int(reps), ms), stream)
+    return [float(x) for x in ms]
+
+
+def frame_forward_norm(q, k, v, alpha, beta, state_in=None, z_in=None, *, frame_tokens, key_scale=None,
+                       eps=1e-6, out=None, state_out=None, z_out=None, want_state=True, ws=None,
+                       token_splits=None, stream=None):
+    """Frame-wise GDN forward with the normalizer state z ([B, H, Dk] fp32) and the
+    normalized readout out = (H^T q) / (z . q + eps).  Arguments as frame_forward.
+    Returns (out, state_out, z_out)."""
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if out is None:
+        out = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    if want_state:
+        if state_out is None:
+            state_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+        if z_out is None:
+            z_out = torch.empty((B, H, Dk), dtype=torch.float32, device=q.device)
+    if ws is not None or token_splits is not None:
+        ts = 0 if token_splits is None else int(token_splits)
+        if ws is None:
+            ws = frame_workspace(q, v, frame_tokens, ts)
+        _norm_call("gdn_frame_forward_norm_ex", q, k, v, alpha, beta, state_in, z_in, out, state_out,
+                   z_out, frame_tokens, key_scale, eps, (ts, _ptr(ws), ws.numel()), stream)
+    else:
+        _norm_call("gdn_frame_forward_norm", q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
+                   frame_tokens, key_scale, eps, (), stream)
+    return out, state_out, z_out

@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 16 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
+    assert len(names) == 19 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -138,9 +138,11 @@ def test_frame_token_splits_and_workspace():
     wb = gdn.gdn_frame_workspace_bytes
     bhf = 16 * 3
     n = wb(1, 16, 3, 3520, 128, 128, True, 1)           # one split: no partial sums
-    expect = bhf * 128 * 128 * (2 + 4 + 2)
+    # G fragments (bf16), A tiles (fp32) and state fragments (bf16), the last
+    # two with room for the normalizer's extra 16-column tile
+    expect = bhf * (128 * 128 * 2 + 128 * 144 * (4 + 2))
     assert expect <= n < expect + 5 * 256
-    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 2 * 128 * 128 * 4
+    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 128 * (128 + 144) * 4
     assert wb(1, 16, 3, 3520, 128, 128, False, 1) > n
     assert wb(1, 16, 3, 0, 128, 128, True, 0) == 0
     assert wb(1, 16, 3, 3520, 128, 32, True, 0) == 0
@@ -183,3 +185,40 @@ def test_frame_binding_rejects_bad_tensors_on_cpu():
     q = torch.zeros(1, 100, 2, 64)
     with pytest.raises(ValueError):
         gdn.frame_forward(q, q, q, torch.zeros(1, 2, 2), torch.zeros(1, 100, 2), frame_tokens=50)
+
+
+def ncall(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, a=BASE + 192 * MB, b=BASE + 200 * MB,
+          si=None, zi=None, o=BASE + 256 * MB, so=None, zo=None, B=1, H=2, F=2, N=100, Dk=64, Dv=64,
+          ws=None, ws_bytes=0):
+    L = gdn.lib()
+    args = [q, k, v, a, b, si, zi, o, so, zo, B, H, F, N, Dk, Dv, ctypes.c_float(0.1),
+            ctypes.c_float(1e-6), 1]
+    if fn.endswith("_ex"):
+        args += [0, ws, ws_bytes]
+    return getattr(L, fn)(*args, None)
+
+
+@pytest.mark.parametrize("fn", ["gdn_frame_forward_norm", "gdn_frame_forward_norm_ex"])
+def test_frame_norm_validation_errors(fn):
+    Z = BASE + 320 * MB
+    assert ncall(fn, q=None) == -1
+    assert ncall(fn, F=0) == -2
+    assert ncall(fn, Dk=96) == -3
+    assert ncall(fn, zi=Z + 4) == -6
+    assert ncall(fn, zo=BASE + 64 * MB) == -7            # z_out overlaps k
+    assert ncall(fn, zo=BASE + 256 * MB + 64) == -7      # z_out overlaps out
+    assert ncall(fn, zi=Z, zo=Z + 16) == -7              # partial overlap of z_in and z_out
+    assert ncall(fn, zi=BASE + 256 * MB) == -7           # out overlaps z_in
+    assert ncall(fn, si=Z, zo=Z) == -7                   # z_out overlaps state_in
+    assert ncall(fn, so=Z, zo=Z + 1024) == -7            # z_out overlaps state_out
+    if fn.endswith("_ex"):
+        assert ncall(fn, zi=Z, zo=Z) == -4               # in place is fine; no workspace
+        assert ncall(fn, ws=BASE + 512 * MB, ws_bytes=100) == -4
+
+
+def test_frame_norm_binding_rejects_bad_z_on_cpu():
+    import torch
+    q = torch.zeros(1, 100, 2, 64)
+    with pytest.raises(ValueError):
+        gdn.frame_forward_norm(q, q, q, torch.zeros(1, 2, 2), torch.zeros(1, 100, 2),
+                               z_in=torch.zeros(1, 2, 32), frame_tokens=50)

@@ -40,6 +40,10 @@ def _lib():
         lib.gdn_oracle_frame_forward.restype = ctypes.c_int
         lib.gdn_oracle_frame_forward.argtypes = [vp, vp, vp, i, vp, vp, i, vp, i, vp, vp,
                                                  i, i, i, i, i, i, ctypes.c_double, i]
+        lib.gdn_oracle_frame_forward_ex.restype = ctypes.c_int
+        lib.gdn_oracle_frame_forward_ex.argtypes = [vp, vp, vp, i, vp, vp, i, vp, vp, i, vp, vp, vp,
+                                                    i, i, i, i, i, i, ctypes.c_double, i, ctypes.c_double,
+                                                    i, i]
         lib.gdn_oracle_frame_forward_norm.restype = ctypes.c_int
         lib.gdn_oracle_frame_forward_norm.argtypes = [vp, vp, vp, i, vp, vp, i, vp, vp, i, vp, vp, vp,
                                                       i, i, i, i, i, i, ctypes.c_double, ctypes.c_double, i]
@@ -97,7 +101,8 @@ def gdn_forward(q, k, v, alpha, beta, state_in=None, nthreads=None,
 
 
 def gdn_frame_forward(q, k, v, alpha, beta, state_in=None, frame_tokens=1, key_scale=None,
-                      nthreads=None, want_state=True, normalized=False, z_in=None, eps=1e-6):
+                      nthreads=None, want_state=True, normalized=False, z_in=None, eps=1e-6,
+                      bidirectional=False):
     """Run the fp64 frame-wise recurrence.
 
     q, k: [B, T, H, Dk]; v: [B, T, H, Dv] (float32, float64 or bf16 bits as
@@ -109,6 +114,11 @@ def gdn_frame_forward(q, k, v, alpha, beta, state_in=None, frame_tokens=1, key_s
     or zero) and divides the readout by z . q + eps (equations
     appendix_gdn_z_update and appendix_gdn_readout); it returns
     (out, state_out, z_out).
+
+    bidirectional=True adds to every readout of frame f the backward history
+    of the call: the same frame recurrence run over the later frames
+    F-1 .. f+1 from a zero state (Algorithm alg:gdn-kernel, Phase B).  The
+    returned states are the forward terminal ones.
     """
     q, k, v = (np.ascontiguousarray(x) for x in (q, k, v))
     if not (q.dtype == k.dtype == v.dtype) or q.dtype not in _DT_QKV:
@@ -151,6 +161,16 @@ def gdn_frame_forward(q, k, v, alpha, beta, state_in=None, frame_tokens=1, key_s
     state_out = np.empty((B, H, Dk, Dv), dtype=np.float64) if want_state else None
     if nthreads is None:
         nthreads = os.cpu_count() or 1
+    if bidirectional:
+        z_out = np.empty((B, H, Dk), dtype=np.float64) if (want_state and normalized) else None
+        rc = _lib().gdn_oracle_frame_forward_ex(
+            _ptr(q), _ptr(k), _ptr(v), _DT_QKV[q.dtype],
+            _ptr(alpha), _ptr(beta), _DT_GATE[alpha.dtype],
+            _ptr(state_in), _ptr(z_in), sdt, _ptr(out), _ptr(state_out), _ptr(z_out),
+            B, H, F, N, Dk, Dv, float(key_scale), 1 if normalized else 0, float(eps), 1, int(nthreads))
+        if rc != 0:
+            raise RuntimeError(f"gdn_oracle_frame_forward_ex failed with {rc}")
+        return (out, state_out, z_out) if normalized else (out, state_out)
     if normalized:
         z_out = np.empty((B, H, Dk), dtype=np.float64) if want_state else None
         rc = _lib().gdn_oracle_frame_forward_norm(

@@ -216,6 +216,15 @@ int gdn_oracle_forward(const void *q, const void *k, const void *v, int qkv_dtyp
  *       o_n  = (H^T q_n) / (z . q_n + eps)   (both from the updated states)
  * This path has no rotary embedding, so the rotated and unrotated keys and
  * queries coincide.
+ *
+ * Bidirectional (the paper's bidirectional GDN: a forward scan from the
+ * cache plus a backward scan within the call started from zero, Algorithm
+ * alg:gdn-kernel, Phase B; the two histories are added before the readout):
+ * the backward state of frame f is the same frame recurrence run over the
+ * later frames F-1, F-2, .., f+1 of the call from a zero state (and z = 0),
+ *       Hb_{F-1} = 0,   Hb_{f-1} = frame f's update applied to Hb_f,
+ * and every readout of frame f uses H_f + Hb_f (and z_f + zb_f).  Only the
+ * forward terminal state is returned, as the cache carries it.
  */
 struct fjob {
     const void *q, *k, *v;
@@ -226,75 +235,98 @@ struct fjob {
     int B, H, F, N, Dk, Dv;
     double key_scale;
     int norm;                      /* 1: carry z and divide the readout */
+    int bidir;                     /* 1: add the backward history to every readout */
     const void *z_in;              /* [B][H][Dk] or NULL, stored as state_dtype */
     double *z_out;                 /* [B][H][Dk] or NULL */
     double eps;
     int nthreads, worker, status;
 };
 
+/* One frame's update of (S, z) in place: decay, then the simultaneous
+ * residual write of the frame's N tokens (kk, uu, zr are scratch). */
+static void frame_update(const struct fjob *J, int b, int h, int f, double *S, double *z, double *kk,
+                         double *uu, double *zr)
+{
+    const int H = J->H, F = J->F, N = J->N, Dk = J->Dk, Dv = J->Dv;
+    const size_t T = (size_t)F * N;
+    const double a = load_elem(J->alpha, J->gate_dtype, ((size_t)b * F + f) * H + h);
+    for (int n = 0; n < N; n++) {
+        const size_t row = ((size_t)b * T + (size_t)f * N + n) * H + h;
+        const double be = load_elem(J->beta, J->gate_dtype, row);
+        double *kn = kk + (size_t)n * Dk, *un = uu + (size_t)n * Dv;
+        for (int i = 0; i < Dk; i++)
+            kn[i] = J->key_scale * load_elem(J->k, J->qkv_dtype, row * Dk + i);
+        for (int j = 0; j < Dv; j++)
+            un[j] = 0.0;
+        for (int i = 0; i < Dk; i++)
+            for (int j = 0; j < Dv; j++)
+                un[j] += S[(size_t)i * Dv + j] * kn[i];
+        for (int j = 0; j < Dv; j++)
+            un[j] = be * (load_elem(J->v, J->qkv_dtype, row * Dv + j) - a * un[j]);
+        if (J->norm) {
+            double dot = 0.0;
+            for (int i = 0; i < Dk; i++)
+                dot += kn[i] * z[i];
+            zr[n] = be * (1.0 - a * dot);
+        }
+    }
+    for (size_t e = 0; e < (size_t)Dk * Dv; e++)
+        S[e] *= a;
+    for (int n = 0; n < N; n++) {
+        const double *kn = kk + (size_t)n * Dk, *un = uu + (size_t)n * Dv;
+        for (int i = 0; i < Dk; i++)
+            for (int j = 0; j < Dv; j++)
+                S[(size_t)i * Dv + j] += kn[i] * un[j];
+    }
+    if (J->norm) {
+        for (int i = 0; i < Dk; i++)
+            z[i] *= a;
+        for (int n = 0; n < N; n++)
+            for (int i = 0; i < Dk; i++)
+                z[i] += zr[n] * kk[(size_t)n * Dk + i];
+    }
+}
+
 static int run_frame_head(const struct fjob *J, int b, int h)
 {
     const int H = J->H, F = J->F, N = J->N, Dk = J->Dk, Dv = J->Dv;
     const size_t T = (size_t)F * N;
-    double *S = (double *)calloc((size_t)Dk * Dv, sizeof(double));
+    const size_t SD = (size_t)Dk * Dv;
+    double *S = (double *)calloc(SD, sizeof(double));
     double *kk = (double *)malloc(sizeof(double) * (size_t)N * Dk);
     double *uu = (double *)malloc(sizeof(double) * (size_t)N * Dv);
     double *qq = (double *)malloc(sizeof(double) * (size_t)Dk);
     double *z = (double *)calloc((size_t)Dk, sizeof(double));
     double *zr = (double *)malloc(sizeof(double) * (size_t)N);
-    if (!S || !kk || !uu || !qq || !z || !zr) {
-        free(S); free(kk); free(uu); free(qq); free(z); free(zr);
+    /* bidirectional: the backward histories of every frame */
+    double *Sb = J->bidir ? (double *)calloc((size_t)F * SD, sizeof(double)) : NULL;
+    double *zb = J->bidir ? (double *)calloc((size_t)F * Dk, sizeof(double)) : NULL;
+    if (!S || !kk || !uu || !qq || !z || !zr || (J->bidir && (!Sb || !zb))) {
+        free(S); free(kk); free(uu); free(qq); free(z); free(zr); free(Sb); free(zb);
         return -1;
     }
-    const size_t sbase = ((size_t)b * H + h) * (size_t)Dk * Dv;
+    const size_t sbase = ((size_t)b * H + h) * SD;
     const size_t zbase = ((size_t)b * H + h) * (size_t)Dk;
+    if (J->bidir) {
+        /* backward scan within the call, from zero: Sb[F-1] = 0 and
+         * Sb[f-1] = frame f's update applied to Sb[f] */
+        for (int f = F - 1; f >= 1; f--) {
+            memcpy(Sb + (size_t)(f - 1) * SD, Sb + (size_t)f * SD, sizeof(double) * SD);
+            memcpy(zb + (size_t)(f - 1) * Dk, zb + (size_t)f * Dk, sizeof(double) * (size_t)Dk);
+            frame_update(J, b, h, f, Sb + (size_t)(f - 1) * SD, zb + (size_t)(f - 1) * Dk, kk, uu, zr);
+        }
+    }
     if (J->state_in)
-        for (size_t e = 0; e < (size_t)Dk * Dv; e++)
+        for (size_t e = 0; e < SD; e++)
             S[e] = load_elem(J->state_in, J->state_dtype, sbase + e);
     if (J->norm && J->z_in)
         for (int i = 0; i < Dk; i++)
             z[i] = load_elem(J->z_in, J->state_dtype, zbase + i);
     for (int f = 0; f < F; f++) {
-        const double a = load_elem(J->alpha, J->gate_dtype, ((size_t)b * F + f) * H + h);
-        /* residuals of every token against the decayed state of the previous frame */
-        for (int n = 0; n < N; n++) {
-            const size_t row = ((size_t)b * T + (size_t)f * N + n) * H + h;
-            const double be = load_elem(J->beta, J->gate_dtype, row);
-            double *kn = kk + (size_t)n * Dk, *un = uu + (size_t)n * Dv;
-            for (int i = 0; i < Dk; i++)
-                kn[i] = J->key_scale * load_elem(J->k, J->qkv_dtype, row * Dk + i);
-            for (int j = 0; j < Dv; j++)
-                un[j] = 0.0;
-            for (int i = 0; i < Dk; i++)
-                for (int j = 0; j < Dv; j++)
-                    un[j] += S[(size_t)i * Dv + j] * kn[i];
-            for (int j = 0; j < Dv; j++)
-                un[j] = be * (load_elem(J->v, J->qkv_dtype, row * Dv + j) - a * un[j]);
-            if (J->norm) {
-                /* normalizer residual against the decayed z: beta (1 - k~ . alpha z) */
-                double dot = 0.0;
-                for (int i = 0; i < Dk; i++)
-                    dot += kn[i] * z[i];
-                zr[n] = be * (1.0 - a * dot);
-            }
-        }
-        /* simultaneous write of the whole frame */
-        for (size_t e = 0; e < (size_t)Dk * Dv; e++)
-            S[e] *= a;
-        for (int n = 0; n < N; n++) {
-            const double *kn = kk + (size_t)n * Dk, *un = uu + (size_t)n * Dv;
-            for (int i = 0; i < Dk; i++)
-                for (int j = 0; j < Dv; j++)
-                    S[(size_t)i * Dv + j] += kn[i] * un[j];
-        }
-        if (J->norm) {
-            for (int i = 0; i < Dk; i++)
-                z[i] *= a;
-            for (int n = 0; n < N; n++)
-                for (int i = 0; i < Dk; i++)
-                    z[i] += zr[n] * kk[(size_t)n * Dk + i];
-        }
-        /* readout from the updated state */
+        frame_update(J, b, h, f, S, z, kk, uu, zr);
+        /* readout from the updated state (plus the backward history) */
+        const double *Sf = J->bidir ? Sb + (size_t)f * SD : NULL;
+        const double *zf = J->bidir ? zb + (size_t)f * Dk : NULL;
         for (int n = 0; n < N; n++) {
             const size_t row = ((size_t)b * T + (size_t)f * N + n) * H + h;
             for (int i = 0; i < Dk; i++)
@@ -304,21 +336,21 @@ static int run_frame_head(const struct fjob *J, int b, int h)
                 o[j] = 0.0;
             for (int i = 0; i < Dk; i++)
                 for (int j = 0; j < Dv; j++)
-                    o[j] += S[(size_t)i * Dv + j] * qq[i];
+                    o[j] += (Sf ? S[(size_t)i * Dv + j] + Sf[(size_t)i * Dv + j] : S[(size_t)i * Dv + j]) * qq[i];
             if (J->norm) {
                 double d = 0.0;
                 for (int i = 0; i < Dk; i++)
-                    d += z[i] * qq[i];
+                    d += (zf ? z[i] + zf[i] : z[i]) * qq[i];
                 for (int j = 0; j < Dv; j++)
                     o[j] /= d + J->eps;
             }
         }
     }
     if (J->state_out)
-        memcpy(J->state_out + sbase, S, sizeof(double) * (size_t)Dk * Dv);
+        memcpy(J->state_out + sbase, S, sizeof(double) * SD);
     if (J->norm && J->z_out)
         memcpy(J->z_out + zbase, z, sizeof(double) * (size_t)Dk);
-    free(S); free(kk); free(uu); free(qq); free(z); free(zr);
+    free(S); free(kk); free(uu); free(qq); free(z); free(zr); free(Sb); free(zb);
     return 0;
 }
 
@@ -347,7 +379,7 @@ static int frame_forward_impl(const void *q, const void *k, const void *v, int q
                               const void *state_in, const void *z_in, int state_dtype,
                               double *out, double *state_out, double *z_out,
                               int B, int H, int F, int N, int Dk, int Dv, double key_scale,
-                              int norm, double eps, int nthreads)
+                              int norm, double eps, int bidir, int nthreads)
 {
     if (!q || !k || !v || !alpha || !beta || !out)
         return -1;
@@ -377,7 +409,7 @@ static int frame_forward_impl(const void *q, const void *k, const void *v, int q
         J->out = out; J->state_out = state_out;
         J->B = B; J->H = H; J->F = F; J->N = N; J->Dk = Dk; J->Dv = Dv;
         J->key_scale = key_scale;
-        J->norm = norm; J->z_in = z_in; J->z_out = z_out; J->eps = eps;
+        J->norm = norm; J->z_in = z_in; J->z_out = z_out; J->eps = eps; J->bidir = bidir;
         J->nthreads = nthreads; J->worker = w; J->status = 0;
         if (nthreads > 1 && pthread_create(&tids[w], NULL, frame_worker_main, J) == 0)
             running[w] = 1;
@@ -403,7 +435,7 @@ int gdn_oracle_frame_forward(const void *q, const void *k, const void *v, int qk
                              int B, int H, int F, int N, int Dk, int Dv, double key_scale, int nthreads)
 {
     return frame_forward_impl(q, k, v, qkv_dtype, alpha, beta, gate_dtype, state_in, NULL, state_dtype,
-                              out, state_out, NULL, B, H, F, N, Dk, Dv, key_scale, 0, 0.0, nthreads);
+                              out, state_out, NULL, B, H, F, N, Dk, Dv, key_scale, 0, 0.0, 0, nthreads);
 }
 
 /*
@@ -420,5 +452,22 @@ int gdn_oracle_frame_forward_norm(const void *q, const void *k, const void *v, i
                                   double eps, int nthreads)
 {
     return frame_forward_impl(q, k, v, qkv_dtype, alpha, beta, gate_dtype, state_in, z_in, state_dtype,
-                              out, state_out, z_out, B, H, F, N, Dk, Dv, key_scale, 1, eps, nthreads);
+                              out, state_out, z_out, B, H, F, N, Dk, Dv, key_scale, 1, eps, 0, nthreads);
+}
+
+/*
+ * General form: normalized (0/1, z_in/z_out/eps used only with 1) and
+ * bidirectional (0/1: every readout adds the backward history of the call,
+ * see the comment above struct fjob).
+ */
+int gdn_oracle_frame_forward_ex(const void *q, const void *k, const void *v, int qkv_dtype,
+                                const void *alpha, const void *beta, int gate_dtype,
+                                const void *state_in, const void *z_in, int state_dtype,
+                                double *out, double *state_out, double *z_out,
+                                int B, int H, int F, int N, int Dk, int Dv, double key_scale,
+                                int normalized, double eps, int bidirectional, int nthreads)
+{
+    return frame_forward_impl(q, k, v, qkv_dtype, alpha, beta, gate_dtype, state_in, z_in, state_dtype,
+                              out, state_out, z_out, B, H, F, N, Dk, Dv, key_scale, normalized != 0, eps,
+                              bidirectional != 0, nthreads);
 }

@@ -14,7 +14,7 @@ import pytest
 import gdn_inputs
 import oracle
 from oracle.chunked import gdn_chunked
-from oracle.framewise import framewise_forward, framewise_forward_normalized
+from oracle.framewise import framewise_forward, framewise_forward_normalized, three_phase_forward
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 rng = np.random.default_rng
@@ -499,3 +499,63 @@ def test_n6_empty_normalizer_divides_by_eps():
     o0, _ = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=0.5)
     assert np.array_equal(zo, np.zeros_like(zo))
     assert rel(o, o0 / 0.25) < 1e-15
+
+
+# ---- bidirectional (forward scan from the cache + backward scan within the call) ----
+
+@pytest.mark.parametrize("normalized", [False, True])
+@pytest.mark.parametrize("F,N", [(1, 4), (2, 3), (4, 5), (5, 1)])
+def test_b1_bidirectional_equals_the_three_phase_algorithm(normalized, F, N):
+    """The oracle's residual loops (forward, and backward from zero over the
+    later frames) against the paper's Algorithm as printed (frame summaries,
+    forward and backward recursions, summed histories, one readout)."""
+    q, k, v, a, b, s, z = norm_case(300 + 11 * F + N, F=F, N=N)
+    ks, eps = 0.4, 1e-3
+    res = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks, normalized=normalized,
+                                   z_in=z if normalized else None, eps=eps, bidirectional=True)
+    o, st = res[0], res[1]
+    for h in range(q.shape[2]):
+        Y, Hf, zf = three_phase_forward(q[0, :, h], ks * k[0, :, h], v[0, :, h], a[0, :, h], b[0, :, h],
+                                        s[0, h], z[0, h] if normalized else None, N=N, eps=eps,
+                                        normalized=normalized, bidirectional=True)
+        assert rel(o[0, :, h], Y) < 1e-11
+        assert rel(st[0, h], Hf) < 1e-12
+        if normalized:
+            assert rel(res[2][0, h], zf) < 1e-12
+
+
+def test_b2_backward_history_is_the_reversed_recurrence():
+    """The bidirectional output of frame f exceeds the causal one by Q_f Hb_f,
+    where Hb_f is the causal oracle's terminal state over the frames
+    F-1, .., f+1 taken in that order from a zero state."""
+    F, N = 4, 3
+    q, k, v, a, b, s = frame_case(31, F=F, N=N)
+    ks = 0.5
+    ob, sb = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks, bidirectional=True)
+    of, sf = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks)
+    assert np.array_equal(sb, sf)                      # the cache carries the forward state
+    for f in range(F - 1):
+        frames = list(range(F - 1, f, -1))
+        idx = np.concatenate([np.arange(g * N, (g + 1) * N) for g in frames])
+        _, hb = oracle.gdn_frame_forward(q[:, idx], k[:, idx], v[:, idx], a[:, frames], b[:, idx], None,
+                                         frame_tokens=N, key_scale=ks)
+        sl = slice(f * N, (f + 1) * N)
+        for h in range(2):
+            assert rel(ob[0, sl, h] - of[0, sl, h], q[0, sl, h] @ hb[0, h]) < 1e-11
+
+
+@pytest.mark.parametrize("normalized", [False, True])
+def test_b3_single_frame_and_last_frame_are_causal(normalized):
+    """No later frame: with F = 1 the bidirectional call is the causal one, and
+    in general the last frame's outputs are the causal ones (bitwise)."""
+    for F in (1, 3):
+        q, k, v, a, b, s, z = norm_case(40 + F, F=F, N=4)
+        kw = dict(frame_tokens=4, key_scale=0.6, normalized=normalized, z_in=z if normalized else None)
+        rb = oracle.gdn_frame_forward(q, k, v, a, b, s, bidirectional=True, **kw)
+        rf = oracle.gdn_frame_forward(q, k, v, a, b, s, **kw)
+        last = slice((F - 1) * 4, F * 4)
+        assert np.array_equal(rb[0][:, last], rf[0][:, last])
+        if F == 1:
+            assert np.array_equal(rb[0], rf[0])
+        for x, y in zip(rb[1:], rf[1:]):
+            assert np.array_equal(x, y)

@@ -18,7 +18,9 @@ latent frames of 44x80 tokens, B=1, F=3, N=3520, H=16, Dk=Dv=128, bf16, with
 the fp32 state carried in and out; its four kernels are the frame summaries,
 their reduction over token splits, the scan over frames and the output.
 ``--path frame-norm`` measures the same call with the normalizer state and the
-normalized readout (non-negative feature maps).
+normalized readout (non-negative feature maps); ``--path frame-bidir`` and
+``--path frame-bidir-norm`` the bidirectional form of either (a backward scan
+over the call's frames beside the forward one).
 """
 import argparse
 import json
@@ -145,11 +147,15 @@ FRAME_METRIC = ("frame-wise GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=352
                 "H=16, D=128 bf16")
 FRAME_NORM_METRIC = ("frame-wise normalized GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, "
                      "H=16, D=128 bf16")
+FRAME_BIDIR_METRIC = ("bidirectional frame-wise GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, "
+                      "H=16, D=128 bf16")
+FRAME_BIDIR_NORM_METRIC = ("bidirectional frame-wise normalized GDN fwd tokens/sec and TFLOP/s at F=3 frames x "
+                           "N=3520 tokens, H=16, D=128 bf16")
 FRAME_KERNELS = {"summaries": "gdn_frame_summary_kernel", "reduce": "gdn_frame_reduce_kernel",
                  "scan": "gdn_frame_scan_kernel", "output": "gdn_frame_output_kernel"}
 
 
-def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False):
+def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=False):
     """Per-stage algorithmic flops and bytes of the frame-wise path (each stage's own
     inputs and outputs, workspace included, every byte once) and its external I/O.
 
@@ -158,7 +164,10 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False):
     scan: H_f = alpha (H - G H) + A per frame; output: O = Q H_f per token.
     norm: the normalizer z rides along as one more 16-column state tile (its
     flops and bytes are counted as the kernels move them: the extra tile, of
-    which one column is z), plus one division per output element."""
+    which one column is z), plus one division per output element.
+    bidir: the scan also runs the backward recurrence over the F - 1 later
+    frames (their G and A read once more), writes every frame's fp32 history
+    and reads it back to add it to H_f."""
     if norm:
         Dv = Dv + 16
     n = B * F * N * H                   # token-heads
@@ -173,16 +182,22 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False):
          "reduce": part + u * (Dk * Dk * esz + Dk * Dv * 4),
          "scan": u * (Dk * Dk * esz + Dk * Dv * 4 + 4 + Dk * Dv * esz) + 2 * st,
          "output": n * (Dk + Dv) * esz + u * Dk * Dv * esz}
+    if bidir:
+        ub = B * H * (F - 1)
+        f["scan"] += ub * (2.0 * Dk * Dk * Dv + 3.0 * Dk * Dv) + u * Dk * Dv
+        b["scan"] += ub * (Dk * Dk * esz + Dk * Dv * 4 + 4) + 2 * u * Dk * Dv * 4
     io_bytes = n * ((2 * Dk + 2 * Dv) * esz + 4) + u * 4 + 2 * st
     return dict(flops=f, bytes=b, io_bytes=io_bytes)
 
 
-def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False):
+def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=False):
     """Time the fp64 frame-wise oracle (as it stands) on whole calls for ~10 s."""
     import oracle
     threads = host_threads()
     reps, elapsed = 0, 0.0
     extra = dict(normalized=True, z_in=inp["z_in"]) if norm else {}
+    if bidir:
+        extra["bidirectional"] = True
     while elapsed < min_seconds and reps < 50:
         t0 = time.perf_counter()
         oracle.gdn_frame_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
@@ -192,10 +207,10 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False):
         reps += 1
     return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H={H}, D={Dk}), "
-                      f"fp64 frame-wise recurrence, {elapsed:.1f} s"}
+                      f"fp64 {'bidirectional ' if bidir else ''}frame-wise recurrence, {elapsed:.1f} s"}
 
 
-def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
+def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
     F, N = 3, 3520
     inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02",
                                        features="relu" if norm else "gauss")
@@ -213,7 +228,10 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        if norm:
+        if bidir:
+            gdn.frame_forward_bidir(q, k, v, alpha, beta, s_in, z_in, frame_tokens=N, normalized=norm, out=out,
+                                    state_out=s_out, z_out=z_out, ws=ws, token_splits=ts, stream=stream)
+        elif norm:
             gdn.frame_forward_norm(q, k, v, alpha, beta, s_in, z_in, frame_tokens=N, out=out,
                                    state_out=s_out, z_out=z_out, ws=ws, token_splits=ts, stream=stream)
         else:
@@ -221,7 +239,11 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
                                      stream=stream)
 
     ms_per_step, cold_ms = timed(step, stream)
-    if norm:
+    if bidir:
+        stage_ms = gdn.gdn_frame_profile_stages_bidir(q, k, v, alpha, beta, s_in, z_in, out, s_out, z_out,
+                                                      ws, N, normalized=norm, token_splits=ts, reps=args.steps,
+                                                      stream=stream)
+    elif norm:
         stage_ms = gdn.gdn_frame_profile_stages_norm(q, k, v, alpha, beta, s_in, z_in, out, s_out, z_out,
                                                      ws, N, token_splits=ts, reps=args.steps,
                                                      stream=stream)
@@ -230,19 +252,23 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
                                                 token_splits=ts, reps=args.steps, stream=stream)
     names = dict(zip(gdn.FRAME_STAGE_NAMES, stage_ms))
     torch.cuda.synchronize()
-    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm)
+    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm, bidir=bidir)
     sec = ms_per_step / 1e3
     tflops = sum(cnt["flops"].values()) / sec / 1e12
     dom = max(names, key=names.get)
     roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
-    roofline.update({"traffic": load_traffic(dom, "traffic_frames3x1280x704_norm.json" if norm
-                                             else "traffic_frames3x1280x704.json"),
+    # the bidirectional form shares every kernel but the scan with the
+    # unidirectional one, so their counter summaries serve it too
+    traffic = None if (bidir and dom == "scan") else load_traffic(
+        dom, "traffic_frames3x1280x704_norm.json" if norm else "traffic_frames3x1280x704.json")
+    roofline.update({"traffic": traffic,
                      "kernel": FRAME_KERNELS[dom], "duration_ms": round(names[dom], 5),
                      "algorithmic_flops_per_launch": cnt["flops"][dom],
                      "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
     stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_) for k_, v_ in names.items()}
     rec = {
-        "metric": FRAME_NORM_METRIC if norm else FRAME_METRIC,
+        "metric": (FRAME_BIDIR_NORM_METRIC if norm else FRAME_BIDIR_METRIC) if bidir
+                  else (FRAME_NORM_METRIC if norm else FRAME_METRIC),
         "value": round(B * T / sec, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -258,7 +284,9 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
                                "N=3520 (44x80) H=16 Dk=Dv=128, bf16 q/k/v, one decay per frame, "
                                "key scale 1/sqrt(Dk N), fp32 state in/out"
                                + ("; normalizer state in/out and normalized readout (eps 1e-6), "
-                                  "non-negative (ReLU) feature maps" if norm else ""),
+                                  "non-negative (ReLU) feature maps" if norm else "")
+                               + ("; bidirectional (forward scan from the state plus a backward scan over "
+                                  "the call's frames from zero)" if bidir else ""),
                    "B": B, "F": F, "N": N, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "token_splits": NS},
         "tflops": round(tflops, 2),
         "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
@@ -269,7 +297,7 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False):
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk, norm=norm)
+        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk, norm=norm, bidir=bidir)
     print(json.dumps(rec), flush=True)
 
 
@@ -284,9 +312,11 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a known-size "
                          "reference for hardware traffic counters)")
-    ap.add_argument("--path", choices=("token", "frame", "frame-norm"), default="token",
+    ap.add_argument("--path", choices=("token", "frame", "frame-norm", "frame-bidir", "frame-bidir-norm"),
+                    default="token",
                     help="token: the token-wise chunk forward (default); frame: the frame-wise "
-                         "forward; frame-norm: the frame-wise forward with the normalizer")
+                         "forward; frame-norm: the frame-wise forward with the normalizer; "
+                         "frame-bidir(-norm): their bidirectional forms")
     ap.add_argument("--token-splits", type=int, default=0,
                     help="frame path: token splits per frame (0 = the library's choice)")
     args = ap.parse_args()
@@ -345,8 +375,9 @@ def main():
             del scratch
         return ms, cold
 
-    if args.path in ("frame", "frame-norm"):
-        run_frame(args, torch, gdn, dev, to_dev, timed, norm=args.path == "frame-norm")
+    if args.path.startswith("frame"):
+        run_frame(args, torch, gdn, dev, to_dev, timed, norm=args.path.endswith("-norm"),
+                  bidir="-bidir" in args.path)
         return
 
     w = gdn_inputs.WORKLOADS[WORKLOAD]

@@ -288,6 +288,51 @@ int gdn_frame_profile_stages_norm(const void *q, const void *k, const void *v,
                                   float eps, int is_bf16, int token_splits, void *ws,
                                   size_t ws_bytes, int reps, float *stage_ms, void *stream);
 
+/*
+ * Bidirectional frame-wise forward (Section "Efficient System Co-design",
+ * paragraph on the GDN kernel, Algorithm Phase B: a forward scan from the
+ * cached state plus a backward scan within the call from a zero state, the
+ * two histories added before the readout).  With U_f the frame update of
+ * gdn_frame_forward (U_f(X) = alpha_f (X - G_f X) + A_f):
+ *
+ *     H_f  = U_f(H_{f-1})          forward, from state_in
+ *     Hb_{F-1} = 0,  Hb_{f-1} = U_f(Hb_f)   backward over the later frames
+ *     o_t  = (H_f + Hb_f)^T q_t    for every token t of frame f
+ *
+ * normalized != 0 carries z and zb the same way (the backward one from zero)
+ * and divides by (z_f + zb_f) . q_t + eps, as gdn_frame_forward_norm;
+ * normalized == 0 ignores z_in, z_out and eps.  state_out (and z_out) receive
+ * the forward terminal state only, the one a cache carries to the next call;
+ * the backward histories live in the workspace for the duration of the call.
+ * F == 1 gives the unidirectional result.  Arguments, layouts, aliasing rules
+ * and errors as gdn_frame_forward_norm; the same workspace size
+ * (gdn_frame_workspace_bytes) serves every variant.  gdn_frame_forward_bidir
+ * uses the library-cached workspace, gdn_frame_forward_bidir_ex a caller-owned
+ * one and an explicit token-split count; gdn_frame_profile_stages_bidir times
+ * the four stages as gdn_frame_profile_stages (the scan stage includes the
+ * backward sweep).
+ */
+int gdn_frame_forward_bidir(const void *q, const void *k, const void *v,
+                            const float *alpha, const float *beta, const float *state_in,
+                            const float *z_in, void *out, float *state_out, float *z_out,
+                            int B, int H, int F, int N, int Dk, int Dv, float key_scale, float eps,
+                            int is_bf16, int normalized, void *stream);
+
+int gdn_frame_forward_bidir_ex(const void *q, const void *k, const void *v,
+                               const float *alpha, const float *beta, const float *state_in,
+                               const float *z_in, void *out, float *state_out, float *z_out,
+                               int B, int H, int F, int N, int Dk, int Dv, float key_scale,
+                               float eps, int is_bf16, int normalized, int token_splits, void *ws,
+                               size_t ws_bytes, void *stream);
+
+int gdn_frame_profile_stages_bidir(const void *q, const void *k, const void *v,
+                                   const float *alpha, const float *beta, const float *state_in,
+                                   const float *z_in, void *out, float *state_out, float *z_out,
+                                   int B, int H, int F, int N, int Dk, int Dv, float key_scale,
+                                   float eps, int is_bf16, int normalized, int token_splits,
+                                   void *ws, size_t ws_bytes, int reps, float *stage_ms,
+                                   void *stream);
+
 /* Static, human-readable text for a status code. */
 const char *gdn_status_string(int status);
 

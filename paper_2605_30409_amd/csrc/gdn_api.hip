@@ -327,7 +327,8 @@ int run_cached(const void *q, const void *k, const void *v, const float *alpha, 
 // ---------------------------------------------------------------------------
 // Frame-wise path (gdn_frame_forward*): frame summaries, their reduction over
 // token splits, the scan over frames, and the output; optionally with the
-// normalizer state (gdn_frame_forward_norm*).
+// normalizer state (gdn_frame_forward_norm*) and in the bidirectional form
+// (gdn_frame_forward_bidir*).
 
 struct FrameArgs {
     const void *q, *k, *v;
@@ -336,11 +337,11 @@ struct FrameArgs {
     float *state_out, *z_out;
     int B, H, F, N, Dk, Dv;
     float key_scale, eps;
-    bool bf16, norm;
+    bool bf16, norm, bidir;
 };
 
 struct FrameWs {
-    size_t PG, PA, Gf, Af, Hf, total;
+    size_t PG, PA, Gf, Af, Hf, Hb, total;
 };
 
 int frame_blocks(int N) { return (N + 63) / 64; }
@@ -358,8 +359,9 @@ int frame_splits(long long units, int N, int token_splits) {
     return (nb + per - 1) / per;          // no empty split
 }
 
-// One layout for both variants: the A tiles and the state fragments have room
-// for the normalizer's extra 16-column tile.
+// One layout for every variant: the A tiles, the state fragments and the
+// backward histories have room for the normalizer's extra 16-column tile; the
+// histories are used by the bidirectional form only.
 FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS) {
     const size_t bhf = (size_t)B * H * F;
     const size_t DVn = (size_t)Dv + 16;
@@ -372,6 +374,7 @@ FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS)
     L.Gf = off; off = align256(off + bhf * Dk * Dk * esz);
     L.Af = off; off = align256(off + bhf * Dk * DVn * 4);
     L.Hf = off; off = align256(off + bhf * Dk * DVn * esz);
+    L.Hb = off; off = align256(off + bhf * Dk * DVn * 4);
     L.total = off;
     return L;
 }
@@ -406,8 +409,8 @@ int frame_validate(const FrameArgs &a) {
     if (!frame_shape_ok(a.B, a.H, a.F, a.N)) return GDN_ERR_SHAPE;
     if (!frame_dims_ok(a.Dk, a.Dv)) return GDN_ERR_UNSUPPORTED;
     if (misaligned(a.q) || misaligned(a.k) || misaligned(a.v) || misaligned(a.alpha) || misaligned(a.beta) ||
-        misaligned(a.state_in) || misaligned(a.out) || misaligned(a.state_out) || misaligned(a.z_in) ||
-        misaligned(a.z_out))
+        misaligned(a.state_in) || misaligned(a.out) || misaligned(a.state_out) ||
+        (a.norm && (misaligned(a.z_in) || misaligned(a.z_out))))
         return GDN_ERR_ALIGN;
     const size_t esz = a.bf16 ? 2 : 4;
     const size_t ntok = (size_t)a.B * a.F * a.N * a.H;
@@ -467,12 +470,13 @@ gdn::FrameParams<E> make_frame_params(const FrameArgs &a, int NS, void *ws) {
     p.Gf = (E *)(base + L.Gf);
     p.Af = (float *)(base + L.Af);
     p.Hf = (E *)(base + L.Hf);
+    p.Hb = (float *)(base + L.Hb);
     return p;
 }
 
 constexpr int kFrameStages = 4;  // summaries, reduction, scan, output
 
-template <class E, int DK, int DV, bool NORM>
+template <class E, int DK, int DV, bool NORM, bool BIDIR>
 hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, hipEvent_t *ev) {
     using LS = gdn::FrameSumLds<E, DK, DV>;
     using LO = gdn::FrameOutLds<E, DK, DV, NORM>;
@@ -503,7 +507,7 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
                                    dim3((unsigned)units, (NI + 3) / 4), dim3(256), 0, s, p);
             break;
         case 2:
-            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV, NORM>), dim3(gdn::xcd_blocks(BH, NJ)),
+            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV, NORM, BIDIR>), dim3(gdn::xcd_blocks(BH, NJ)),
                                dim3(64), 0, s, p);
             break;
         default:
@@ -525,19 +529,22 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
     return le != hipSuccess ? le : er;
 }
 
-template <class E, bool NORM>
+template <class E, bool NORM, bool BIDIR>
 hipError_t frame_dispatch_n(const gdn::FrameParams<E> &p, int Dk, int Dv, hipStream_t s, int reps, hipEvent_t *ev) {
-    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128, NORM>(p, s, reps, ev);
-    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64, NORM>(p, s, reps, ev);
-    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64, NORM>(p, s, reps, ev);
-    return launch_frame<E, 64, 128, NORM>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128, NORM, BIDIR>(p, s, reps, ev);
+    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64, NORM, BIDIR>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64, NORM, BIDIR>(p, s, reps, ev);
+    return launch_frame<E, 64, 128, NORM, BIDIR>(p, s, reps, ev);
 }
 
 template <class E>
 hipError_t frame_dispatch(const FrameArgs &a, int NS, void *ws, hipStream_t s, int reps, hipEvent_t *ev) {
     const gdn::FrameParams<E> p = make_frame_params<E>(a, NS, ws);
-    return a.norm ? frame_dispatch_n<E, true>(p, a.Dk, a.Dv, s, reps, ev)
-                  : frame_dispatch_n<E, false>(p, a.Dk, a.Dv, s, reps, ev);
+    if (a.bidir)
+        return a.norm ? frame_dispatch_n<E, true, true>(p, a.Dk, a.Dv, s, reps, ev)
+                      : frame_dispatch_n<E, false, true>(p, a.Dk, a.Dv, s, reps, ev);
+    return a.norm ? frame_dispatch_n<E, true, false>(p, a.Dk, a.Dv, s, reps, ev)
+                  : frame_dispatch_n<E, false, false>(p, a.Dk, a.Dv, s, reps, ev);
 }
 
 int frame_run(const FrameArgs &a, int token_splits, void *ws, size_t ws_bytes, void *stream, int reps,
@@ -593,9 +600,10 @@ int frame_profile(const FrameArgs &a, int token_splits, void *ws, size_t ws_byte
 
 FrameArgs frame_args(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
                      const float *state_in, const float *z_in, void *out, float *state_out, float *z_out, int B,
-                     int H, int F, int N, int Dk, int Dv, float key_scale, float eps, bool bf16, bool norm) {
+                     int H, int F, int N, int Dk, int Dv, float key_scale, float eps, bool bf16, bool norm,
+                     bool bidir = false) {
     return FrameArgs{q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
-                     B, H, F, N, Dk, Dv, key_scale, eps, bf16, norm};
+                     B, H, F, N, Dk, Dv, key_scale, eps, bf16, norm, bidir};
 }
 
 }  // namespace
@@ -760,6 +768,35 @@ int gdn_frame_profile_stages_norm(const void *q, const void *k, const void *v, c
                                   size_t ws_bytes, int reps, float *stage_ms, void *stream) {
     return frame_profile(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk,
                                     Dv, key_scale, eps, is_bf16 != 0, true),
+                         token_splits, ws, ws_bytes, reps, stage_ms, stream);
+}
+
+int gdn_frame_forward_bidir(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                            const float *state_in, const float *z_in, void *out, float *state_out,
+                            float *z_out, int B, int H, int F, int N, int Dk, int Dv, float key_scale, float eps,
+                            int is_bf16, int normalized, void *stream) {
+    return frame_run_cached(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N,
+                                       Dk, Dv, key_scale, eps, is_bf16 != 0, normalized != 0, true),
+                            stream);
+}
+
+int gdn_frame_forward_bidir_ex(const void *q, const void *k, const void *v, const float *alpha,
+                               const float *beta, const float *state_in, const float *z_in, void *out,
+                               float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
+                               float key_scale, float eps, int is_bf16, int normalized, int token_splits,
+                               void *ws, size_t ws_bytes, void *stream) {
+    return frame_run(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv,
+                                key_scale, eps, is_bf16 != 0, normalized != 0, true),
+                     token_splits, ws, ws_bytes, stream, 1, nullptr);
+}
+
+int gdn_frame_profile_stages_bidir(const void *q, const void *k, const void *v, const float *alpha,
+                                   const float *beta, const float *state_in, const float *z_in, void *out,
+                                   float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
+                                   float key_scale, float eps, int is_bf16, int normalized, int token_splits,
+                                   void *ws, size_t ws_bytes, int reps, float *stage_ms, void *stream) {
+    return frame_profile(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk,
+                                    Dv, key_scale, eps, is_bf16 != 0, normalized != 0, true),
                          token_splits, ws, ws_bytes, reps, stage_ms, stream);
 }
 

@@ -24,7 +24,8 @@
 //       accumulator tiles.
 //   gdn_frame_scan_kernel     one wave per (head, 16 state columns): H_f for
 //       every frame in turn, written as the output kernel's operand
-//       fragments (E), and the terminal state.
+//       fragments (E), and the terminal state; in the bidirectional form a
+//       backward sweep first, whose histories are added to the H_f written.
 //   gdn_frame_output_kernel   64 * NTW tokens of one frame per workgroup:
 //       O^T = H_f^T Q^T.
 //
@@ -64,6 +65,7 @@ template <class E> struct FrameParams {
     E *Gf;                       // [B*H][F][Dk/16][Dk/32][64][8]      G operand fragments
     float *Af;                   // [B*H][F][Dk/16][NJ][64][4]         A tiles
     E *Hf;                       // [B*H][F][NJ][Dk/32][64][8]         H_f operand fragments
+    float *Hb;                   // [B*H][F][NJ][Dk/16][64][4]         backward histories (bidirectional)
 };
 
 // A fragment whose lanes li = 0 hold ones and all other lanes zeros: as the
@@ -427,9 +429,16 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
 // G fragments and A tiles do not depend on the state, so the next frame's are
 // requested before the current frame is computed (two register sets, used
 // alternately; bf16 only, the fp32 fragments are twice as large).
+// BIDIR (the bidirectional form, Algorithm Phase B): the wave first sweeps
+// the frames F-1 .. 1 from a zero state, each frame's update applied to the
+// later frames' history, and keeps the history Hb_f of every frame (zero for
+// the last) in fp32 in Hb, lane by lane in the accumulator layout; the
+// forward sweep then reads Hb_f with frame f's operands and writes
+// H_f + Hb_f, rounded once, as the output operand.  The terminal state is the
+// forward one.
 template <class E> struct FrameScanPrefetch { static constexpr bool value = sizeof(E) == 2; };
 
-template <class E, int DK, int DV, bool NORM>
+template <class E, int DK, int DV, bool NORM, bool BIDIR>
 __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
@@ -442,6 +451,99 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     const int col = 16 * jt + li;
     const bool ztile = NORM && jt == DV / 16;                         // column 0 of this tile is z
     f32x4 Hacc[NT];
+    // this wave's history tiles of frame f (BIDIR)
+    auto hist = [&](int f) { return p.Hb + (((size_t)bh * p.F + f) * NJ + jt) * (size_t)NT * 256 + l * 4; };
+    // a frame's operands: G fragments, A tiles, the decay and, in the forward
+    // sweep of BIDIR, the frame's backward history (one load group, so that
+    // waiting for it never waits for a younger frame's loads)
+    struct Ops {
+        frag g[NT][KB];
+        f32x4 av[NT], hb[NT];
+        float a;
+    };
+    auto load_ops = [&](int f, Ops &o, auto with_hist) {
+        const size_t fi = (size_t)bh * p.F + f;
+        const E *G = p.Gf + fi * NT * KB * 512 + l * 8;
+        const float *A = p.Af + fi * NT * NJ * 256 + l * 4;
+        o.a = p.alpha[((size_t)b * p.F + f) * p.H + h];
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) o.g[t][kb] = TR::load8(G + (t * KB + kb) * 512);
+            o.av[t] = *(const f32x4 *)(A + (t * NJ + jt) * 256);
+        }
+        if constexpr (decltype(with_hist)::value) {
+            const float *hp = hist(f);
+#pragma unroll
+            for (int t = 0; t < NT; ++t) o.hb[t] = *(const f32x4 *)(hp + t * 256);
+        }
+    };
+    auto update = [&](const Ops &o) {
+        frag hb[KB];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) hb[kb] = TR::cat(TR::from_f32(Hacc[2 * kb]), TR::from_f32(Hacc[2 * kb + 1]));
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+            f32x4 gh = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) gh = TR::mma(o.g[t][kb], hb[kb], gh);
+            Hacc[t] = o.a * (Hacc[t] - gh) + o.av[t];
+        }
+    };
+    auto store_hist = [&](int f) {
+        float *hp = hist(f);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) *(f32x4 *)(hp + t * 256) = Hacc[t];
+    };
+    auto store_hf = [&](int f, const Ops &o) {
+        E *hf = p.Hf + (((size_t)bh * p.F + f) * NJ + jt) * (size_t)KB * 512 + l * 8;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            f32x4 x0 = Hacc[2 * kb], x1 = Hacc[2 * kb + 1];
+            if constexpr (BIDIR) {
+                x0 += o.hb[2 * kb];
+                x1 += o.hb[2 * kb + 1];
+            }
+            TR::store8(hf + kb * 512, TR::cat(TR::from_f32(x0), TR::from_f32(x1)));
+        }
+    };
+    // n frames fid(0), fid(1), ..: load, update, then done(i, ops of step i)
+    auto sweep = [&](int n, auto fid, auto with_hist, auto done) {
+        Ops o0;
+        if constexpr (FrameScanPrefetch<E>::value) {
+            // the prefetch is unconditional (the last frame again past the
+            // end) so the wait for a set always leaves exactly one younger set
+            // in flight
+            Ops o1;
+            load_ops(fid(0), o0, with_hist);
+            for (int i = 0; i < n; i += 2) {
+                load_ops(fid(min(i + 1, n - 1)), o1, with_hist);
+                update(o0);
+                done(i, o0);
+                if (i + 1 >= n) break;
+                load_ops(fid(min(i + 2, n - 1)), o0, with_hist);
+                update(o1);
+                done(i + 1, o1);
+            }
+        } else {
+            for (int i = 0; i < n; ++i) {
+                load_ops(fid(i), o0, with_hist);
+                update(o0);
+                done(i, o0);
+            }
+        }
+    };
+    const int F = p.F;
+    if constexpr (BIDIR) {
+#pragma unroll
+        for (int t = 0; t < NT; ++t) Hacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        store_hist(F - 1);
+        // step i applies frame F-1-i and gives the history of frame F-2-i
+        if (F > 1)
+            sweep(F - 1, [&](int i) { return F - 1 - i; }, std::false_type{},
+                  [&](int i, const Ops &) { store_hist(F - 2 - i); });
+        wait_vmcnt<0>();                         // the histories are written before they are read
+    }
     if (ztile) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -461,60 +563,8 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
 #pragma unroll
         for (int t = 0; t < NT; ++t) Hacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-    // a frame's operands: G fragments, A tiles and the decay (one load group,
-    // so that waiting for it never waits for a younger frame's loads)
-    auto load_ops = [&](int f, frag (&g)[NT][KB], f32x4 (&av)[NT], float &a) {
-        const size_t fi = (size_t)bh * p.F + f;
-        const E *G = p.Gf + fi * NT * KB * 512 + l * 8;
-        const float *A = p.Af + fi * NT * NJ * 256 + l * 4;
-        a = p.alpha[((size_t)b * p.F + f) * p.H + h];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) g[t][kb] = TR::load8(G + (t * KB + kb) * 512);
-            av[t] = *(const f32x4 *)(A + (t * NJ + jt) * 256);
-        }
-    };
-    auto frame = [&](int f, const frag (&g)[NT][KB], const f32x4 (&av)[NT], float a) {
-        const size_t fi = (size_t)bh * p.F + f;
-        frag hb[KB];
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) hb[kb] = TR::cat(TR::from_f32(Hacc[2 * kb]), TR::from_f32(Hacc[2 * kb + 1]));
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            f32x4 gh = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) gh = TR::mma(g[t][kb], hb[kb], gh);
-            Hacc[t] = a * (Hacc[t] - gh) + av[t];
-        }
-        E *hf = p.Hf + (fi * NJ + jt) * (size_t)KB * 512 + l * 8;
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-            TR::store8(hf + kb * 512, TR::cat(TR::from_f32(Hacc[2 * kb]), TR::from_f32(Hacc[2 * kb + 1])));
-    };
-    frag g0[NT][KB];
-    f32x4 v0[NT];
-    float a0;
-    if constexpr (FrameScanPrefetch<E>::value) {
-        // the prefetch is unconditional (the last frame again past the end) so
-        // the wait for a set always leaves exactly one younger set in flight
-        frag g1[NT][KB];
-        f32x4 v1[NT];
-        float a1;
-        load_ops(0, g0, v0, a0);
-        for (int f = 0; f < p.F; f += 2) {
-            load_ops(min(f + 1, p.F - 1), g1, v1, a1);
-            frame(f, g0, v0, a0);
-            if (f + 1 >= p.F) break;
-            load_ops(min(f + 2, p.F - 1), g0, v0, a0);
-            frame(f + 1, g1, v1, a1);
-        }
-    } else {
-        for (int f = 0; f < p.F; ++f) {
-            load_ops(f, g0, v0, a0);
-            frame(f, g0, v0, a0);
-        }
-    }
+    sweep(F, [](int i) { return i; }, std::integral_constant<bool, BIDIR>{},
+          [&](int i, const Ops &o) { store_hf(i, o); });
     if (ztile) {
         if (p.z_out && li == 0) {
 #pragma unroll

@@ -71,6 +71,13 @@ def lib():
         L.gdn_frame_forward_norm_ex.argtypes = ncore + [i, vp, sz, vp]
         L.gdn_frame_profile_stages_norm.restype = i
         L.gdn_frame_profile_stages_norm.argtypes = ncore + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        L.gdn_frame_forward_bidir.restype = i
+        L.gdn_frame_forward_bidir.argtypes = ncore + [i, vp]
+        L.gdn_frame_forward_bidir_ex.restype = i
+        L.gdn_frame_forward_bidir_ex.argtypes = ncore + [i, i, vp, sz, vp]
+        L.gdn_frame_profile_stages_bidir.restype = i
+        L.gdn_frame_profile_stages_bidir.argtypes = ncore + [i, i, vp, sz, i, ctypes.POINTER(ctypes.c_float),
+                                                             vp]
         L.gdn_status_string.restype = ctypes.c_char_p
         L.gdn_status_string.argtypes = [i]
         _lib = L
@@ -391,3 +398,50 @@ def frame_forward_norm(q, k, v, alpha, beta, state_in=None, z_in=None, *, frame_
         _norm_call("gdn_frame_forward_norm", q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
                    frame_tokens, key_scale, eps, (), stream)
     return out, state_out, z_out
+
+
+# ---------------------------------------------------------------------------
+# Bidirectional frame-wise GDN (gdn_frame_forward_bidir*).
+
+def gdn_frame_profile_stages_bidir(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, ws,
+                                   frame_tokens, key_scale=None, eps=1e-6, normalized=False,
+                                   token_splits=0, reps=20, stream=None):
+    """Mean per-stage durations in ms of the bidirectional frame-wise path."""
+    ms = (ctypes.c_float * len(FRAME_STAGE_NAMES))()
+    _norm_call("gdn_frame_profile_stages_bidir", q, k, v, alpha, beta, state_in, z_in, out, state_out,
+               z_out, frame_tokens, key_scale, eps,
+               (1 if normalized else 0, int(token_splits), _ptr(ws), ws.numel(), int(reps), ms), stream)
+    return [float(x) for x in ms]
+
+
+def frame_forward_bidir(q, k, v, alpha, beta, state_in=None, z_in=None, *, frame_tokens, key_scale=None,
+                        normalized=False, eps=1e-6, out=None, state_out=None, z_out=None, want_state=True,
+                        ws=None, token_splits=None, stream=None):
+    """Bidirectional frame-wise GDN forward: every frame reads out the forward state
+    (from state_in) plus the backward history of the call's later frames (from
+    zero).  Arguments as frame_forward, and with normalized=True as
+    frame_forward_norm (z_in / z_out are ignored otherwise).  The returned states
+    are the forward terminal ones.  Returns (out, state_out), or
+    (out, state_out, z_out) when normalized."""
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if not normalized:
+        z_in = z_out = None
+    if out is None:
+        out = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    if want_state:
+        if state_out is None:
+            state_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+        if normalized and z_out is None:
+            z_out = torch.empty((B, H, Dk), dtype=torch.float32, device=q.device)
+    nf = 1 if normalized else 0
+    if ws is not None or token_splits is not None:
+        ts = 0 if token_splits is None else int(token_splits)
+        if ws is None:
+            ws = frame_workspace(q, v, frame_tokens, ts)
+        _norm_call("gdn_frame_forward_bidir_ex", q, k, v, alpha, beta, state_in, z_in, out, state_out,
+                   z_out, frame_tokens, key_scale, eps, (nf, ts, _ptr(ws), ws.numel()), stream)
+    else:
+        _norm_call("gdn_frame_forward_bidir", q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
+                   frame_tokens, key_scale, eps, (nf,), stream)
+    return (out, state_out, z_out) if normalized else (out, state_out)

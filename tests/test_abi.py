@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 19 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
+    assert len(names) == 22 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -138,10 +138,11 @@ def test_frame_token_splits_and_workspace():
     wb = gdn.gdn_frame_workspace_bytes
     bhf = 16 * 3
     n = wb(1, 16, 3, 3520, 128, 128, True, 1)           # one split: no partial sums
-    # G fragments (bf16), A tiles (fp32) and state fragments (bf16), the last
-    # two with room for the normalizer's extra 16-column tile
-    expect = bhf * (128 * 128 * 2 + 128 * 144 * (4 + 2))
-    assert expect <= n < expect + 5 * 256
+    # G fragments (bf16), A tiles (fp32), state fragments (bf16) and backward
+    # histories (fp32), the last three with room for the normalizer's extra
+    # 16-column tile
+    expect = bhf * (128 * 128 * 2 + 128 * 144 * (4 + 2 + 4))
+    assert expect <= n < expect + 6 * 256
     assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 128 * (128 + 144) * 4
     assert wb(1, 16, 3, 3520, 128, 128, False, 1) > n
     assert wb(1, 16, 3, 0, 128, 128, True, 0) == 0
@@ -193,12 +194,15 @@ def ncall(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, a=BASE + 192 * MB, b=
     L = gdn.lib()
     args = [q, k, v, a, b, si, zi, o, so, zo, B, H, F, N, Dk, Dv, ctypes.c_float(0.1),
             ctypes.c_float(1e-6), 1]
+    if "_bidir" in fn:
+        args += [1]                                      # normalized
     if fn.endswith("_ex"):
         args += [0, ws, ws_bytes]
     return getattr(L, fn)(*args, None)
 
 
-@pytest.mark.parametrize("fn", ["gdn_frame_forward_norm", "gdn_frame_forward_norm_ex"])
+@pytest.mark.parametrize("fn", ["gdn_frame_forward_norm", "gdn_frame_forward_norm_ex",
+                                "gdn_frame_forward_bidir", "gdn_frame_forward_bidir_ex"])
 def test_frame_norm_validation_errors(fn):
     Z = BASE + 320 * MB
     assert ncall(fn, q=None) == -1
@@ -222,3 +226,28 @@ def test_frame_norm_binding_rejects_bad_z_on_cpu():
     with pytest.raises(ValueError):
         gdn.frame_forward_norm(q, q, q, torch.zeros(1, 2, 2), torch.zeros(1, 100, 2),
                                z_in=torch.zeros(1, 2, 32), frame_tokens=50)
+
+
+@pytest.mark.parametrize("fn", ["gdn_frame_forward_bidir", "gdn_frame_forward_bidir_ex"])
+def test_frame_bidir_unnormalized_ignores_z(fn):
+    """normalized == 0: z pointers are not validated (they are not used)."""
+    L = gdn.lib()
+    args = [BASE, BASE + 64 * MB, BASE + 128 * MB, BASE + 192 * MB, BASE + 200 * MB, None,
+            BASE + 4, BASE + 256 * MB, None, BASE + 64 * MB, 1, 2, 2, 100, 64, 64, ctypes.c_float(0.1),
+            ctypes.c_float(1e-6), 1, 0]
+    if fn.endswith("_ex"):
+        args += [0, None, 0]
+        assert getattr(L, fn)(*args, None) == -4         # reaches the workspace check
+    else:
+        args[7] = BASE + 4096                             # out overlaps q: rejected before any launch
+        assert getattr(L, fn)(*args, None) == -7
+
+
+def test_frame_bidir_profile_rejects_in_place():
+    L = gdn.lib()
+    ms = (ctypes.c_float * 4)()
+    S = BASE + 300 * MB
+    args = [BASE, BASE + 64 * MB, BASE + 128 * MB, BASE + 192 * MB, BASE + 200 * MB, S, None,
+            BASE + 256 * MB, S, None, 1, 2, 2, 100, 64, 64, ctypes.c_float(0.1), ctypes.c_float(1e-6), 1, 0,
+            0, None, 0, 3, ms]
+    assert L.gdn_frame_profile_stages_bidir(*args, None) == -7

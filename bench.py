@@ -163,29 +163,29 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=Fa
     token split); reduce: the splits' partials -> G (operand fragments) and A;
     scan: H_f = alpha (H - G H) + A per frame; output: O = Q H_f per token.
     norm: the normalizer z rides along as one more 16-column state tile (its
-    flops and bytes are counted as the kernels move them: the extra tile, of
-    which one column is z), plus one division per output element.
+    flops and workspace bytes are counted as the kernels move them: the extra
+    tile, of which one column is z; the token reads and output writes do not
+    grow), plus z in and out and one division per output element.
     bidir: the scan also runs the backward recurrence over the F - 1 later
     frames (their G and A read once more), writes every frame's fp32 history
     and reads it back to add it to H_f."""
-    if norm:
-        Dv = Dv + 16
+    Ds = Dv + 16 if norm else Dv        # state columns the kernels carry
     n = B * F * N * H                   # token-heads
     u = B * H * F                       # (frame, head) units
-    st = B * H * Dk * Dv * 4
-    part = u * NS * Dk * (Dk + Dv) * 4
-    f = {"summaries": 2.0 * n * Dk * (Dk + Dv),
-         "reduce": float(u * NS * Dk * (Dk + Dv)),
-         "scan": u * (2.0 * Dk * Dk * Dv + 3.0 * Dk * Dv),
-         "output": 2.0 * n * Dk * Dv}
+    st = B * H * Dk * Dv * 4 + (B * H * Dk * 4 if norm else 0)
+    part = u * NS * Dk * (Dk + Ds) * 4
+    f = {"summaries": 2.0 * n * Dk * (Dk + Ds),
+         "reduce": float(u * NS * Dk * (Dk + Ds)),
+         "scan": u * (2.0 * Dk * Dk * Ds + 3.0 * Dk * Ds),
+         "output": 2.0 * n * Dk * Ds + (n * Dv if norm else 0)}
     b = {"summaries": n * ((Dk + Dv) * esz + 4) + part,
-         "reduce": part + u * (Dk * Dk * esz + Dk * Dv * 4),
-         "scan": u * (Dk * Dk * esz + Dk * Dv * 4 + 4 + Dk * Dv * esz) + 2 * st,
-         "output": n * (Dk + Dv) * esz + u * Dk * Dv * esz}
+         "reduce": part + u * (Dk * Dk * esz + Dk * Ds * 4),
+         "scan": u * (Dk * Dk * esz + Dk * Ds * 4 + 4 + Dk * Ds * esz) + 2 * st,
+         "output": n * (Dk + Dv) * esz + u * Dk * Ds * esz}
     if bidir:
         ub = B * H * (F - 1)
-        f["scan"] += ub * (2.0 * Dk * Dk * Dv + 3.0 * Dk * Dv) + u * Dk * Dv
-        b["scan"] += ub * (Dk * Dk * esz + Dk * Dv * 4 + 4) + 2 * u * Dk * Dv * 4
+        f["scan"] += ub * (2.0 * Dk * Dk * Ds + 3.0 * Dk * Ds) + u * Dk * Ds
+        b["scan"] += ub * (Dk * Dk * esz + Dk * Ds * 4 + 4) + 2 * u * Dk * Ds * 4
     io_bytes = n * ((2 * Dk + 2 * Dv) * esz + 4) + u * 4 + 2 * st
     return dict(flops=f, bytes=b, io_bytes=io_bytes)
 

@@ -55,8 +55,8 @@ template <class E> struct FrameParams {
     int OB, OTPW;                // output workgroups per frame, 16-token tiles per workgroup
     float key_scale;
     // normalizer (the kernels' NORM variant): z = S^z as one more state
-    // column tile (column 0 holds z, the others stay zero), written by a value
-    // column of ones; NJ = Dv / 16 + NORM column tiles below
+    // column tile, written by value columns of ones, so that each of its 16
+    // columns holds z; NJ = Dv / 16 + NORM column tiles below
     const float *z_in;           // [B][H][Dk] or null (zero)
     float *z_out;                // [B][H][Dk] or null
     float eps;
@@ -68,16 +68,16 @@ template <class E> struct FrameParams {
     float *Hb;                   // [B*H][F][NJ][Dk/16][64][4]         backward histories (bidirectional)
 };
 
-// A fragment whose lanes li = 0 hold ones and all other lanes zeros: as the
-// B operand it is a value column of ones in column 0 of a 16-column tile.
-template <class E> __device__ __forceinline__ typename Tr<E>::frag ones_col_frag(int li);
-template <> __device__ __forceinline__ Tr<uint16_t>::frag ones_col_frag<uint16_t>(int li) {
-    const uint32_t x = li == 0 ? 0x3f803f80u : 0u;             // two bf16 ones
+// A fragment of ones: as the B operand, a 16-column tile whose every column is
+// a value column of ones, so every column of the product K~^T B [1 .. 1] is
+// K~^T beta.
+template <class E> __device__ __forceinline__ typename Tr<E>::frag ones_frag();
+template <> __device__ __forceinline__ Tr<uint16_t>::frag ones_frag<uint16_t>() {
+    const uint32_t x = 0x3f803f80u;                             // two bf16 ones
     return Tr<uint16_t>::frag{x, x, x, x};
 }
-template <> __device__ __forceinline__ Tr<float>::frag ones_col_frag<float>(int li) {
-    const float x = li == 0 ? 1.f : 0.f;
-    return Tr<float>::frag{x, x, x, x, x, x, x, x};
+template <> __device__ __forceinline__ Tr<float>::frag ones_frag<float>() {
+    return Tr<float>::frag{1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
 }
 
 // Grids of per_unit workgroups per unit with all workgroups of one unit on
@@ -283,7 +283,7 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
     // K^T B 1 (a column of ones as the value) for their row pair
     f32x4 accz[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
     const bool zw = NORM && !gw && c0 == 0;
-    const frag ones = ones_col_frag<E>(li);
+    const frag ones = ones_frag<E>();
 
     // the block loop, specialised for G waves (GB) and A waves, so that it has
     // no branch inside: all operand reads of a block (the K^T fragments
@@ -449,7 +449,7 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     const int b = bh / p.H, h = bh - b * p.H;
     const int l = threadIdx.x & 63, li = l & 15, lg = l >> 4;
     const int col = 16 * jt + li;
-    const bool ztile = NORM && jt == DV / 16;                         // column 0 of this tile is z
+    const bool ztile = NORM && jt == DV / 16;                         // every column of this tile is z
     f32x4 Hacc[NT];
     // this wave's history tiles of frame f (BIDIR)
     auto hist = [&](int f) { return p.Hb + (((size_t)bh * p.F + f) * NJ + jt) * (size_t)NT * 256 + l * 4; };
@@ -550,7 +550,7 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
             const int r0 = 32 * (t >> 1) + 8 * lg + 4 * (t & 1);
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                Hacc[t][q] = (p.z_in && li == 0) ? p.z_in[(size_t)bh * DK + r0 + q] : 0.f;
+                Hacc[t][q] = p.z_in ? p.z_in[(size_t)bh * DK + r0 + q] : 0.f;
         }
     } else if (p.state_in) {
 #pragma unroll
@@ -592,10 +592,9 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
 // is O^T, and lane (li, lg) gets O[token li][16 jo + 4 lg + q].  Each wave
 // streams its tiles with the next tile's queries in flight.  The 16 x Dv
 // result goes through LDS so that global stores write whole rows.
-// NORM: the extra column tile of H_f holds z in its column 0, so its product
-// row 0 (lanes lg = 0, q = 0) is the denominator z . q of token li; it is
-// formed first, shared with the lanes of the same token, and every output
-// element is divided by it plus eps.
+// NORM: every column of the extra column tile of H_f holds z, so every lane
+// (li, lg) of its product holds the denominator z . q of token li; it is
+// formed first and every output element is divided by it plus eps.
 constexpr int kFrameOutWgs = 1024;                 // output workgroups to aim for
 
 template <class E, int DK, int DV, bool NORM> struct FrameOutLds {
@@ -621,8 +620,18 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
     const size_t fi = (size_t)bh * p.F + f;
 
-    const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
-    for (int j = tid; j < HV; j += 256) ((u32x4 *)smem)[j] = src[j];
+    // H_f into LDS, every load of a thread in flight at once
+    {
+        constexpr int HIT = (HV + 255) / 256;
+        const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
+        u32x4 hv[HIT];
+#pragma unroll
+        for (int it = 0; it < HIT; ++it)
+            if (HV % 256 == 0 || tid + 256 * it < HV) hv[it] = src[tid + 256 * it];
+#pragma unroll
+        for (int it = 0; it < HIT; ++it)
+            if (HV % 256 == 0 || tid + 256 * it < HV) ((u32x4 *)smem)[tid + 256 * it] = hv[it];
+    }
 
     const size_t T = (size_t)p.F * p.N;
     const int ntf = (p.N + 15) / 16;                           // tiles in the frame
@@ -647,15 +656,12 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
     };
     auto compute = [&](int tile, const frag (&qf)[KB]) {
         if constexpr (NORM) {
-            // all products first (independent chains), then the division
-            f32x4 acc[NV];
-#pragma unroll
-            for (int jo = 0; jo < NV; ++jo) acc[jo] = tile_product(jo, qf);
-            const f32x4 dz = tile_product(NV, qf);
-            const float inv = 1.f / (__shfl(dz[0], li) + p.eps);   // the denominator of token li
+            // the denominator of token li first; its division overlaps the
+            // other products
+            const float inv = 1.f / (tile_product(NV, qf)[0] + p.eps);
 #pragma unroll
             for (int jo = 0; jo < NV; ++jo)
-                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(acc[jo] * inv));
+                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(tile_product(jo, qf) * inv));
         } else {
 #pragma unroll
             for (int jo = 0; jo < NV; ++jo)

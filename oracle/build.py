@@ -13,7 +13,7 @@ LIB = os.path.join(HERE, "libgdn_oracle.so")
 
 def build(verbose: bool = False) -> str:
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread",
-           "-Wall", "-Wextra", "-o", LIB + ".tmp", SRC]
+           "-Wall", "-Wextra", "-o", LIB + ".tmp", SRC, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

@@ -559,3 +559,169 @@ def test_b3_single_frame_and_last_frame_are_causal(normalized):
             assert np.array_equal(rb[0], rf[0])
         for x, y in zip(rb[1:], rf[1:]):
             assert np.array_equal(x, y)
+
+
+# ---- fused operator: RMSNorm / ReLU / 3D RoPE prologue, two states, gate and projection ----
+
+def silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def fused_case(seed, F=3, N=3, H=2, Dk=8, Dv=5):
+    r = rng(seed)
+    T = F * N
+    return dict(q=r.standard_normal((1, T, H, Dk)), k=r.standard_normal((1, T, H, Dk)),
+                v=r.standard_normal((1, T, H, Dv)), gate=r.standard_normal((1, T, H, Dv)),
+                w_o=r.standard_normal((H, Dv, Dv)), alpha=r.uniform(0.3, 1.0, (1, F, H)),
+                beta=r.uniform(0.1, 1.0, (1, T, H)), s=0.3 * r.standard_normal((1, H, Dk, Dv)),
+                z=np.abs(0.3 * r.standard_normal((1, H, Dk))), gq=r.uniform(0.5, 1.5, (H, Dk)),
+                gk=r.uniform(0.5, 1.5, (H, Dk)), freq=r.uniform(0.1, 1.3, Dk // 2),
+                axis=r.integers(0, 3, Dk // 2).astype(np.int32), N=N)
+
+
+def run_fused(c, **kw):
+    args = dict(frame_tokens=c["N"], gain_q=c["gq"], gain_k=c["gk"], rope_freq=c["freq"], rope_axis=c["axis"],
+                lat_w=2, t0=5, rms_eps=0.0)
+    args.update(kw)
+    return oracle.gdn_frame_forward_fused(c["q"], c["k"], c["v"], c["alpha"], c["beta"], c["gate"], c["w_o"],
+                                          c["s"], c["z"], **args)
+
+
+@pytest.mark.parametrize("bidirectional", [False, True])
+def test_u1_orthonormal_features_read_back_their_values(bidirectional):
+    """Raw keys c e_{2 j(n)} - d e_m (distinct channel pairs j(n) inside a
+    frame, any other channel m) with key gain 1/sqrt(Dk) and key scale 1: the
+    RMS is taken over both entries and the ReLU drops the negative one, so the
+    feature is lambda e_{2 j(n)} with lambda = c / sqrt(c^2 + d^2), whatever
+    rotation follows.  With beta = 1 / lambda^2 each frame writes a projector;
+    the query equals the key of its own token.  Then every token reads back
+    its own value over a denominator of exactly 1 + eps, whatever the states
+    and decays:
+        out_n = W_o (SiLU(g_n) o v_n) / (1 + eps).
+    A rotation applied to one side only, or differently to q and k, a rotated
+    key or query on the normalizer path, a missing ReLU or one taken before the
+    RMSNorm, the gate after the projection or a transposed W_o all break it.
+    (Bidirectional: the last frame only.)"""
+    F, N, H, Dk, Dv = 3, 3, 2, 8, 5
+    c = fused_case(61, F=F, N=N, H=H, Dk=Dk, Dv=Dv)
+    r = rng(62)
+    k = np.zeros((1, F * N, H, Dk))
+    beta = np.zeros((1, F * N, H))
+    for f in range(F):
+        for h in range(H):
+            pairs = r.permutation(Dk // 2)[:N]
+            for n in range(N):
+                cc, dd = r.uniform(0.5, 3.0), r.uniform(0.5, 3.0)
+                m = (2 * pairs[n] + 1 + 2 * r.integers(0, Dk // 2)) % Dk      # an odd channel: never 2 j(n)
+                k[0, f * N + n, h, 2 * pairs[n]] = cc
+                k[0, f * N + n, h, m] = -dd
+                beta[0, f * N + n, h] = (cc * cc + dd * dd) / (cc * cc)
+    c["k"], c["q"] = k, k.copy()
+    c["beta"] = beta
+    c["gq"] = c["gk"] = np.full((H, Dk), 1.0 / np.sqrt(Dk))
+    eps = 1e-3
+    o, _, _ = run_fused(c, key_scale=1.0, eps=eps, bidirectional=bidirectional)
+    frames = [F - 1] if bidirectional else range(F)
+    for f in frames:
+        for n in range(N):
+            t = f * N + n
+            for h in range(H):
+                expect = c["w_o"][h] @ (silu(c["gate"][0, t, h]) * c["v"][0, t, h]) / (1.0 + eps)
+                assert rel(o[0, t, h], expect) < 1e-12, (f, n, h)
+
+
+def test_u2_rotation_direction_and_pairing():
+    """A key along e_{2i} written in frame 0 and a query e_{2i+1} + e_{2j} read in
+    frame 1 (beta = 0, alpha = 1 there, so the states do not change): the
+    numerator is v sin(theta_key - theta_query) on pair i, with
+    (x_2i, x_2i+1) -> (x_2i cos - x_2i+1 sin, x_2i sin + x_2i+1 cos), and the
+    unrotated denominator is 1 + eps."""
+    Dk, Dv, N, H = 8, 3, 2, 1
+    i, j = 1, 3
+    for axis in (0, 1, 2):
+        c = fused_case(63 + axis, F=2, N=N, H=H, Dk=Dk, Dv=Dv)
+        c["axis"] = np.full(Dk // 2, axis, dtype=np.int32)
+        k = np.full((1, 2 * N, H, Dk), 0.0)
+        k[0, 0, 0, 2 * i] = 1.0
+        k[0, 1, 0, 2 * j] = 1.0
+        k[0, 2:, 0, 0] = 1.0                       # frame 1 keys: not written (beta = 0)
+        q = np.full((1, 2 * N, H, Dk), 1.0)
+        q[0, 3, 0] = 0.0
+        q[0, 3, 0, 2 * i + 1] = q[0, 3, 0, 2 * j] = 1.0
+        c["k"], c["q"] = k, q
+        c["v"][0, 1] = 0.0
+        c["beta"] = np.array([[[1.0], [1.0], [0.0], [0.0]]])
+        c["alpha"] = np.array([[[0.7], [1.0]]])
+        c["gq"] = np.full((H, Dk), np.sqrt(2.0 / Dk))
+        c["gk"] = np.full((H, Dk), 1.0 / np.sqrt(Dk))
+        c["w_o"] = np.eye(Dv)[None]
+        c["s"], c["z"] = None, None
+        eps, lat_w, t0 = 1e-3, 2, 5
+        o, _, _ = run_fused(c, key_scale=1.0, eps=eps, lat_w=lat_w, t0=t0)
+
+        def theta(f, s):
+            coord = (t0 + f, s // lat_w, s % lat_w)[axis]
+            return c["freq"][i] * coord
+        expect = silu(c["gate"][0, 3, 0]) * c["v"][0, 0, 0] * np.sin(theta(0, 0) - theta(1, 1)) / (1.0 + eps)
+        assert rel(o[0, 3, 0], expect) < 1e-12, axis
+
+
+def test_u3_rmsnorm_is_per_token_scale_free():
+    """With rms_eps = 0, scaling each token's raw q and k by its own positive
+    factor changes nothing (the normalisation is over the channels of one
+    token and head)."""
+    c = fused_case(64)
+    o1, s1, z1 = run_fused(c)
+    r = rng(65)
+    c["q"] = c["q"] * r.uniform(0.1, 10.0, c["q"].shape[:3])[..., None]
+    c["k"] = c["k"] * r.uniform(0.1, 10.0, c["k"].shape[:3])[..., None]
+    o2, s2, z2 = run_fused(c)
+    assert rel(o2, o1) < 1e-12 and rel(s2, s1) < 1e-12 and rel(z2, z1) < 1e-12
+
+
+def test_u4_no_rotation_and_identity_epilogue_reduce_to_the_normalized_oracle():
+    """freq = 0, unit gains, raw q and k already non-negative with a mean square
+    of 1 per token (so RMSNorm and ReLU return them), W_o = I: out / SiLU(g)
+    is the normalized frame-wise oracle's output on the same q, k."""
+    c = fused_case(66, F=3, N=4, Dk=8, Dv=6)
+    for key in ("q", "k"):
+        x = np.abs(c[key])
+        c[key] = x / np.sqrt((x * x).mean(axis=-1, keepdims=True))
+    c["freq"] = np.zeros_like(c["freq"])
+    c["gq"] = c["gk"] = np.ones_like(c["gq"])
+    c["w_o"] = np.stack([np.eye(6)] * 2)
+    ks, eps = 0.35, 1e-3
+    o, st, zo = run_fused(c, key_scale=ks, eps=eps)
+    ro, rs, rz = oracle.gdn_frame_forward(c["q"], c["k"], c["v"], c["alpha"], c["beta"], c["s"], frame_tokens=4,
+                                          key_scale=ks, normalized=True, z_in=c["z"], eps=eps)
+    assert rel(o / silu(c["gate"]), ro) < 1e-11
+    assert rel(st, rs) < 1e-12 and rel(zo, rz) < 1e-12
+
+
+def test_u5_streaming_split_advances_the_time_coordinate():
+    """Two calls (the second with t0 advanced by the first call's frames and the
+    carried states) equal one call, bitwise."""
+    c = fused_case(67, F=4, N=3)
+    o, st, zo = run_fused(c, t0=2)
+    a = dict(c, q=c["q"][:, :6], k=c["k"][:, :6], v=c["v"][:, :6], gate=c["gate"][:, :6],
+             alpha=c["alpha"][:, :2], beta=c["beta"][:, :6])
+    oa, sa, za = run_fused(a, t0=2)
+    b = dict(c, q=c["q"][:, 6:], k=c["k"][:, 6:], v=c["v"][:, 6:], gate=c["gate"][:, 6:],
+             alpha=c["alpha"][:, 2:], beta=c["beta"][:, 6:], s=sa, z=za)
+    ob, sb, zb = run_fused(b, t0=4)
+    assert np.array_equal(np.concatenate([oa, ob], axis=1), o)
+    assert np.array_equal(sb, st) and np.array_equal(zb, zo)
+    ob2, _, _ = run_fused(b, t0=5)
+    assert not np.allclose(ob2, ob)                 # the time coordinate matters
+
+
+def test_u6_bidirectional_single_and_last_frame():
+    for F in (1, 3):
+        c = fused_case(68 + F, F=F, N=3)
+        rb = run_fused(c, bidirectional=True)
+        rf = run_fused(c)
+        last = slice(3 * (F - 1), 3 * F)
+        assert np.array_equal(rb[0][:, last], rf[0][:, last])
+        assert np.array_equal(rb[1], rf[1]) and np.array_equal(rb[2], rf[2])
+        if F == 3:
+            assert not np.allclose(rb[0][:, :3], rf[0][:, :3])

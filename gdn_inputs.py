@@ -190,3 +190,73 @@ def make_frame_inputs(workload, frames, *, frame_tokens=None, call=0, B=None, H=
     if features == "relu":
         out["z_in"] = z_in
     return out
+
+
+def rope_3d_params(Dk, base=10000.0):
+    """Frequencies and axes of a fixed 3D RoPE over Dk / 2 channel pairs: a
+    quarter of the pairs rotate with the time coordinate and three eighths each
+    with the latent row and column; along each axis the pair frequencies run
+    geometrically from 1 down towards 1 / base.  Returns (freq float32 [Dk/2],
+    axis int32 [Dk/2]).  These are inputs to the operator, not its arithmetic."""
+    P = Dk // 2
+    nt = P // 4
+    ny = (P - nt) // 2
+    nx = P - nt - ny
+    freq, axis = [], []
+    for a, n in ((0, nt), (1, ny), (2, nx)):
+        freq += [base ** (-j / n) for j in range(n)]
+        axis += [a] * n
+    return np.array(freq, dtype=np.float32), np.array(axis, dtype=np.int32)
+
+
+def make_fused_inputs(workload, frames, *, frame_tokens=None, B=None, H=None, Dk=None, Dv=None,
+                      state=None, seed=None, lat_w=80, t0=0):
+    """Draw one call's inputs for the fused operator (bf16): the raw query and
+    key projections (N(0, 1) with a per-token scale drawn from [0.2, 5], so the
+    RMSNorm has work to do), v, the output gate pre-activation (N(0, 1)), the
+    per-head projection W_o (N(0, 1 / Dv)), RMSNorm gains (uniform [0.5, 1.5]),
+    the 3D RoPE parameters of rope_3d_params, and the decays, write gates and
+    states as make_frame_inputs (z_in >= 0).  Draw order: q, k, their scales,
+    v, gate, W_o, gains, alpha noise, beta noise, state_in, z_in."""
+    w = WORKLOADS[workload] if isinstance(workload, int) else workload
+    idx = WORKLOADS.index(w) if w in WORKLOADS else 99
+    B = w.B if B is None else B
+    H = w.H if H is None else H
+    Dk = w.Dk if Dk is None else Dk
+    Dv = w.Dv if Dv is None else Dv
+    N = 3520 if frame_tokens is None else int(frame_tokens)
+    F = int(frames)
+    T = F * N
+    state = w.state if state is None else state
+    rng = np.random.default_rng(700000 + 1000 * idx if seed is None else seed)
+    q = rng.standard_normal((B, T, H, Dk), dtype=np.float32)
+    k = rng.standard_normal((B, T, H, Dk), dtype=np.float32)
+    q *= rng.uniform(0.2, 5.0, (B, T, H, 1)).astype(np.float32)
+    k *= rng.uniform(0.2, 5.0, (B, T, H, 1)).astype(np.float32)
+    v = rng.standard_normal((B, T, H, Dv), dtype=np.float32)
+    gate = rng.standard_normal((B, T, H, Dv), dtype=np.float32)
+    w_o = (rng.standard_normal((H, Dv, Dv), dtype=np.float32) / np.float32(np.sqrt(Dv))).astype(np.float32)
+    gain_q = rng.uniform(0.5, 1.5, (H, Dk)).astype(np.float32)
+    gain_k = rng.uniform(0.5, 1.5, (H, Dk)).astype(np.float32)
+    if w.alpha.startswith("softplus"):
+        mu = float(w.alpha[len("softplus"):])
+        z = rng.standard_normal((B, F, H)).astype(np.float64) + mu
+        alpha = np.exp(-np.logaddexp(0.0, z)).astype(np.float32)
+    else:
+        alpha = rng.uniform(0.5, 1.0, (B, F, H)).astype(np.float32)
+    if w.beta == "sigmoid":
+        z = rng.standard_normal((B, T, H)).astype(np.float64)
+        beta = (1.0 / (1.0 + np.exp(-z))).astype(np.float32)
+    else:
+        beta = rng.uniform(0.0, 1.0, (B, T, H)).astype(np.float32)
+    state_in = z_in = None
+    if state == "normal0.02":
+        state_in = (0.02 * rng.standard_normal((B, H, Dk, Dv), dtype=np.float32)).astype(np.float32)
+        z_in = np.abs(0.02 * rng.standard_normal((B, H, Dk), dtype=np.float32)).astype(np.float32)
+    elif state != "zero":
+        raise ValueError(state)
+    freq, axis = rope_3d_params(Dk)
+    bf = f32_to_bf16_bits
+    return dict(q=bf(q), k=bf(k), v=bf(v), gate=bf(gate), w_o=bf(w_o), alpha=alpha, beta=beta,
+                state_in=state_in, z_in=z_in, gain_q=gain_q, gain_k=gain_k, rope_freq=freq, rope_axis=axis,
+                lat_w=int(lat_w), t0=int(t0), frame_tokens=N, dtype="bf16")

@@ -333,6 +333,77 @@ int gdn_frame_profile_stages_bidir(const void *q, const void *k, const void *v,
                                    void *ws, size_t ws_bytes, int reps, float *stage_ms,
                                    void *stream);
 
+/*
+ * The fused GDN operator around the frame-wise normalized recurrence (appendix
+ * on the GDN block: subsection "Attention features" for the feature maps and
+ * the key rescale; subsection "Frame-wise delta-rule update", equations
+ * appendix_gdn_kv_update and appendix_gdn_z_update; subsection "Normalized
+ * readout and output projection", equations appendix_gdn_readout and
+ * appendix_gdn_output; Algorithm alg:gdn-kernel).  bf16 only.  Per token n
+ * and head h, from the raw projections q_n = q_raw[b][n][h], k_n (length Dk):
+ *
+ *   r(x)  = gain o x / sqrt(mean_i x_i^2 + rms_eps)       (RMSNorm over Dk)
+ *   q~ = ReLU(r_q(q_n)),   k~ = key_scale ReLU(r_k(k_n))   (unrotated features)
+ *   q^ = R_n q~,           k^ = R_n k~                     (3D RoPE)
+ *   H_f = alpha_f (H - K^_f^T B_f K^_f H) + K^_f^T B_f V_f          (rotated keys)
+ *   z_f = alpha_f (z - K~_f^T B_f K~_f z) + K~_f^T beta_f           (unrotated keys)
+ *   y_n = (H_f^T q^_n) / (z_f . q~_n + eps)
+ *   out_n = W_o[h] (SiLU(gate_n) o y_n),   SiLU(x) = x / (1 + e^-x)
+ *
+ * R_n rotates channel pair (2i, 2i+1) by theta_i = rope_freq[i] * c_i(n):
+ * (x_2i, x_2i+1) -> (x_2i cos - x_2i+1 sin, x_2i sin + x_2i+1 cos), with c_i
+ * the coordinate of token n = f N + s of the call along rope_axis[i]: 0 the
+ * time t0 + f, 1 the latent row s / lat_w, any other value the latent column
+ * s % lat_w.  With bidirectional != 0 both states get the backward histories
+ * of gdn_frame_forward_bidir before the readout.
+ *
+ *   q_raw, k_raw  [B][T][H][Dk]   bf16     gate  [B][T][H][Dv]  bf16 (before the SiLU)
+ *   v, out        [B][T][H][Dv]   bf16     w_o   [H][Dv][Dv]    bf16, row = output channel
+ *   gain_q, gain_k [H][Dk]  fp32           rope_freq [Dk/2] fp32 (radians per unit)
+ *   rope_axis [Dk/2] int32                 alpha, beta, states: as gdn_frame_forward_norm
+ *   lat_w >= 1 (tokens per latent row), t0 (time coordinate of frame 0)
+ *
+ * All pointers are device pointers (16-byte aligned); gate, w_o, the gains
+ * and the RoPE arrays are required.  Outputs may not overlap any input;
+ * state_in == state_out and z_in == z_out are allowed.  The bf16 path rounds
+ * the features, the gated readout and the products' operands to bf16 (fp32
+ * accumulation); the sines and cosines are the GPU's fast ones.
+ * gdn_frame_forward_fused uses the library-cached workspace,
+ * gdn_frame_forward_fused_ex a caller-owned one of gdn_frame_workspace_bytes
+ * (is_bf16 = 1) and an explicit token-split count; gdn_frame_profile_stages_fused
+ * times the four stages (its last stage is the fused output).  Errors as the
+ * other frame-wise calls; a missing prologue/epilogue input is GDN_ERR_NULL,
+ * lat_w < 1 GDN_ERR_SHAPE.
+ */
+int gdn_frame_forward_fused(const void *q_raw, const void *k_raw, const void *v, const void *gate,
+                            const void *w_o, const float *alpha, const float *beta,
+                            const float *gain_q, const float *gain_k, const float *rope_freq,
+                            const int *rope_axis, const float *state_in, const float *z_in,
+                            void *out, float *state_out, float *z_out,
+                            int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0,
+                            float key_scale, float rms_eps, float eps, int bidirectional,
+                            void *stream);
+
+int gdn_frame_forward_fused_ex(const void *q_raw, const void *k_raw, const void *v, const void *gate,
+                               const void *w_o, const float *alpha, const float *beta,
+                               const float *gain_q, const float *gain_k, const float *rope_freq,
+                               const int *rope_axis, const float *state_in, const float *z_in,
+                               void *out, float *state_out, float *z_out,
+                               int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0,
+                               float key_scale, float rms_eps, float eps, int bidirectional,
+                               int token_splits, void *ws, size_t ws_bytes, void *stream);
+
+int gdn_frame_profile_stages_fused(const void *q_raw, const void *k_raw, const void *v,
+                                   const void *gate, const void *w_o, const float *alpha,
+                                   const float *beta, const float *gain_q, const float *gain_k,
+                                   const float *rope_freq, const int *rope_axis,
+                                   const float *state_in, const float *z_in, void *out,
+                                   float *state_out, float *z_out, int B, int H, int F, int N,
+                                   int Dk, int Dv, int lat_w, int t0, float key_scale,
+                                   float rms_eps, float eps, int bidirectional, int token_splits,
+                                   void *ws, size_t ws_bytes, int reps, float *stage_ms,
+                                   void *stream);
+
 /* Static, human-readable text for a status code. */
 const char *gdn_status_string(int status);
 

@@ -338,10 +338,18 @@ struct FrameArgs {
     int B, H, F, N, Dk, Dv;
     float key_scale, eps;
     bool bf16, norm, bidir;
+    // the fused operator (gdn_frame_forward_fused*): q and k are the raw
+    // projections; the remaining fields are its prologue and epilogue inputs
+    bool fused;
+    const void *gate, *w_o;
+    const float *gain_q, *gain_k, *rope_freq;
+    const int *rope_axis;
+    float rms_eps;
+    int lat_w, t0;
 };
 
 struct FrameWs {
-    size_t PG, PA, Gf, Af, Hf, Hb, total;
+    size_t PG, PA, Gf, Af, Hf, Hb, PGz, Gzf, total;
 };
 
 int frame_blocks(int N) { return (N + 63) / 64; }
@@ -361,7 +369,8 @@ int frame_splits(long long units, int N, int token_splits) {
 
 // One layout for every variant: the A tiles, the state fragments and the
 // backward histories have room for the normalizer's extra 16-column tile; the
-// histories are used by the bidirectional form only.
+// histories are used by the bidirectional form only, the unrotated-key Gram
+// fragments and their partials by the fused operator only.
 FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS) {
     const size_t bhf = (size_t)B * H * F;
     const size_t DVn = (size_t)Dv + 16;
@@ -375,6 +384,8 @@ FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS)
     L.Af = off; off = align256(off + bhf * Dk * DVn * 4);
     L.Hf = off; off = align256(off + bhf * Dk * DVn * esz);
     L.Hb = off; off = align256(off + bhf * Dk * DVn * 4);
+    L.PGz = off; off = align256(off + bhf * np * Dk * Dk * 4);
+    L.Gzf = off; off = align256(off + bhf * Dk * Dk * esz);
     L.total = off;
     return L;
 }
@@ -438,6 +449,19 @@ int frame_validate(const FrameArgs &a) {
         if (r.overlaps(ro)) return GDN_ERR_ALIAS;
     }
     if (rso.overlaps(rzo)) return GDN_ERR_ALIAS;
+    if (a.fused) {
+        if (!a.gate || !a.w_o || !a.gain_q || !a.gain_k || !a.rope_freq || !a.rope_axis) return GDN_ERR_NULL;
+        if (a.lat_w < 1) return GDN_ERR_SHAPE;
+        if (!a.bf16 || !a.norm) return GDN_ERR_UNSUPPORTED;
+        if (misaligned(a.gate) || misaligned(a.w_o) || misaligned(a.gain_q) || misaligned(a.gain_k) ||
+            misaligned(a.rope_freq) || misaligned(a.rope_axis))
+            return GDN_ERR_ALIGN;
+        const Range extra[] = {range(a.gate, ntok * a.Dv * esz), range(a.w_o, (size_t)a.H * a.Dv * a.Dv * esz),
+                               range(a.gain_q, (size_t)a.H * a.Dk * 4), range(a.gain_k, (size_t)a.H * a.Dk * 4),
+                               range(a.rope_freq, (size_t)a.Dk / 2 * 4), range(a.rope_axis, (size_t)a.Dk / 2 * 4)};
+        for (const Range &r : extra)
+            if (ro.overlaps(r) || rso.overlaps(r) || rzo.overlaps(r)) return GDN_ERR_ALIAS;
+    }
     return GDN_OK;
 }
 
@@ -471,48 +495,87 @@ gdn::FrameParams<E> make_frame_params(const FrameArgs &a, int NS, void *ws) {
     p.Af = (float *)(base + L.Af);
     p.Hf = (E *)(base + L.Hf);
     p.Hb = (float *)(base + L.Hb);
+    p.PGz = (float *)(base + L.PGz);
+    p.Gzf = (E *)(base + L.Gzf);
+    p.gate = (const E *)a.gate;
+    p.w_o = (const E *)a.w_o;
+    p.gain_q = a.gain_q;
+    p.gain_k = a.gain_k;
+    p.rope_freq = a.rope_freq;
+    p.rope_axis = a.rope_axis;
+    p.rms_eps = a.rms_eps;
+    p.lat_w = a.lat_w;
+    p.t0 = a.t0;
+    p.feat_scale = a.key_scale;
+    if (a.fused) {
+        // the key scale is applied to the key features as they are formed
+        p.key_scale = 1.f;
+        // one workgroup per CU (the fused output needs 100+ KB of LDS): at
+        // most 256 workgroups in all unless the units alone exceed that
+        const long long units = (long long)a.B * a.H * a.F;
+        const int ntf = (a.N + 15) / 16;
+        long long ob = 256 / units;
+        if (ob < 1) ob = 1;
+        if (ob > ntf) ob = ntf;
+        p.OTPW = (int)((ntf + ob - 1) / ob);
+        p.OB = (ntf + p.OTPW - 1) / p.OTPW;
+    }
     return p;
 }
 
 constexpr int kFrameStages = 4;  // summaries, reduction, scan, output
 
-template <class E, int DK, int DV, bool NORM, bool BIDIR>
+template <class E, int DK, int DV, bool NORM, bool BIDIR, bool FUSED = false>
 hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, hipEvent_t *ev) {
-    using LS = gdn::FrameSumLds<E, DK, DV>;
+    using LS = gdn::FrameSumLds<E, DK, DV, FUSED>;
     using LO = gdn::FrameOutLds<E, DK, DV, NORM>;
+    using LF = gdn::FusedOutLds<DK, DV>;
+    const void *out_kernel;
+    size_t out_lds;
+    if constexpr (FUSED) {
+        out_kernel = (const void *)gdn::gdn_frame_output_fused_kernel<DK, DV>;
+        out_lds = LF::bytes;
+    } else {
+        out_kernel = (const void *)gdn::gdn_frame_output_kernel<E, DK, DV, NORM>;
+        out_lds = LO::bytes;
+    }
     static std::once_flag attr_once;
     static hipError_t attr_err = hipSuccess;
     std::call_once(attr_once, [&] {
-        hipError_t e = hipFuncSetAttribute((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, NORM>,
+        hipError_t e = hipFuncSetAttribute((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, NORM, FUSED>,
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)LS::bytes);
         if (e == hipSuccess)
-            e = hipFuncSetAttribute((const void *)gdn::gdn_frame_output_kernel<E, DK, DV, NORM>,
-                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)LO::bytes);
+            e = hipFuncSetAttribute(out_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)out_lds);
         attr_err = e;
     });
     if (attr_err != hipSuccess) return attr_err;
     const long long BH = (long long)p.B * p.H, units = BH * p.F;
     constexpr int NJ = DV / 16 + NORM;
-    constexpr int NI = (DK / 16) * (DK / 32) + (DK / 16) * NJ;      // reduction items per unit
+    // reduction items per unit (FUSED: also the unrotated-key G fragments)
+    constexpr int NI = (DK / 16) * (DK / 32) * (FUSED ? 2 : 1) + (DK / 16) * NJ;
     auto stage = [&](int i) {
         switch (i) {
         case 0:
-            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV, NORM>), dim3((unsigned)(units * p.NS)),
-                               dim3((gdn::kSumCompute + gdn::kSumLoaders) * 64), LS::bytes, s, p);
+            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV, NORM, FUSED>),
+                               dim3((unsigned)(units * p.NS)), dim3(gdn::sum_threads<FUSED>()), LS::bytes, s, p);
             break;
         case 1:
             // a single split writes the summaries in their final form
             if (p.NS > 1)
-                hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV, NORM>),
+                hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV, NORM, FUSED>),
                                    dim3((unsigned)units, (NI + 3) / 4), dim3(256), 0, s, p);
             break;
         case 2:
-            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV, NORM, BIDIR>), dim3(gdn::xcd_blocks(BH, NJ)),
-                               dim3(64), 0, s, p);
+            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV, NORM, BIDIR, FUSED>),
+                               dim3(gdn::xcd_blocks(BH, NJ)), dim3(64), 0, s, p);
             break;
         default:
-            hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV, NORM>),
-                               dim3(gdn::xcd_blocks(units, p.OB)), dim3(256), LO::bytes, s, p);
+            if constexpr (FUSED)
+                hipLaunchKernelGGL((gdn::gdn_frame_output_fused_kernel<DK, DV>), dim3(gdn::xcd_blocks(units, p.OB)),
+                                   dim3(gdn::kFusedOutWaves * 64), LF::bytes, s, p);
+            else
+                hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV, NORM>),
+                                   dim3(gdn::xcd_blocks(units, p.OB)), dim3(256), LO::bytes, s, p);
         }
     };
     hipError_t er = hipSuccess;
@@ -529,17 +592,22 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
     return le != hipSuccess ? le : er;
 }
 
-template <class E, bool NORM, bool BIDIR>
+template <class E, bool NORM, bool BIDIR, bool FUSED = false>
 hipError_t frame_dispatch_n(const gdn::FrameParams<E> &p, int Dk, int Dv, hipStream_t s, int reps, hipEvent_t *ev) {
-    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128, NORM, BIDIR>(p, s, reps, ev);
-    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64, NORM, BIDIR>(p, s, reps, ev);
-    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64, NORM, BIDIR>(p, s, reps, ev);
-    return launch_frame<E, 64, 128, NORM, BIDIR>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128, NORM, BIDIR, FUSED>(p, s, reps, ev);
+    if (Dk == 64 && Dv == 64) return launch_frame<E, 64, 64, NORM, BIDIR, FUSED>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 64) return launch_frame<E, 128, 64, NORM, BIDIR, FUSED>(p, s, reps, ev);
+    return launch_frame<E, 64, 128, NORM, BIDIR, FUSED>(p, s, reps, ev);
 }
 
 template <class E>
 hipError_t frame_dispatch(const FrameArgs &a, int NS, void *ws, hipStream_t s, int reps, hipEvent_t *ev) {
     const gdn::FrameParams<E> p = make_frame_params<E>(a, NS, ws);
+    if constexpr (sizeof(E) == 2) {
+        if (a.fused)
+            return a.bidir ? frame_dispatch_n<E, true, true, true>(p, a.Dk, a.Dv, s, reps, ev)
+                           : frame_dispatch_n<E, true, false, true>(p, a.Dk, a.Dv, s, reps, ev);
+    }
     if (a.bidir)
         return a.norm ? frame_dispatch_n<E, true, true>(p, a.Dk, a.Dv, s, reps, ev)
                       : frame_dispatch_n<E, false, true>(p, a.Dk, a.Dv, s, reps, ev);
@@ -604,6 +672,26 @@ FrameArgs frame_args(const void *q, const void *k, const void *v, const float *a
                      bool bidir = false) {
     return FrameArgs{q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
                      B, H, F, N, Dk, Dv, key_scale, eps, bf16, norm, bidir};
+}
+
+FrameArgs fused_args(const void *q_raw, const void *k_raw, const void *v, const void *gate, const void *w_o,
+                     const float *alpha, const float *beta, const float *gain_q, const float *gain_k,
+                     const float *rope_freq, const int *rope_axis, const float *state_in, const float *z_in,
+                     void *out, float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
+                     int lat_w, int t0, float key_scale, float rms_eps, float eps, int bidirectional) {
+    FrameArgs a = frame_args(q_raw, k_raw, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk,
+                             Dv, key_scale, eps, true, true, bidirectional != 0);
+    a.fused = true;
+    a.gate = gate;
+    a.w_o = w_o;
+    a.gain_q = gain_q;
+    a.gain_k = gain_k;
+    a.rope_freq = rope_freq;
+    a.rope_axis = rope_axis;
+    a.rms_eps = rms_eps;
+    a.lat_w = lat_w;
+    a.t0 = t0;
+    return a;
 }
 
 }  // namespace
@@ -797,6 +885,45 @@ int gdn_frame_profile_stages_bidir(const void *q, const void *k, const void *v, 
                                    void *ws, size_t ws_bytes, int reps, float *stage_ms, void *stream) {
     return frame_profile(frame_args(q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk,
                                     Dv, key_scale, eps, is_bf16 != 0, normalized != 0, true),
+                         token_splits, ws, ws_bytes, reps, stage_ms, stream);
+}
+
+int gdn_frame_forward_fused(const void *q_raw, const void *k_raw, const void *v, const void *gate,
+                            const void *w_o, const float *alpha, const float *beta, const float *gain_q,
+                            const float *gain_k, const float *rope_freq, const int *rope_axis,
+                            const float *state_in, const float *z_in, void *out, float *state_out, float *z_out,
+                            int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0, float key_scale,
+                            float rms_eps, float eps, int bidirectional, void *stream) {
+    return frame_run_cached(fused_args(q_raw, k_raw, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq,
+                                       rope_axis, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w,
+                                       t0, key_scale, rms_eps, eps, bidirectional),
+                            stream);
+}
+
+int gdn_frame_forward_fused_ex(const void *q_raw, const void *k_raw, const void *v, const void *gate,
+                               const void *w_o, const float *alpha, const float *beta, const float *gain_q,
+                               const float *gain_k, const float *rope_freq, const int *rope_axis,
+                               const float *state_in, const float *z_in, void *out, float *state_out,
+                               float *z_out, int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0,
+                               float key_scale, float rms_eps, float eps, int bidirectional, int token_splits,
+                               void *ws, size_t ws_bytes, void *stream) {
+    return frame_run(fused_args(q_raw, k_raw, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq, rope_axis,
+                                state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w, t0, key_scale,
+                                rms_eps, eps, bidirectional),
+                     token_splits, ws, ws_bytes, stream, 1, nullptr);
+}
+
+int gdn_frame_profile_stages_fused(const void *q_raw, const void *k_raw, const void *v, const void *gate,
+                                   const void *w_o, const float *alpha, const float *beta, const float *gain_q,
+                                   const float *gain_k, const float *rope_freq, const int *rope_axis,
+                                   const float *state_in, const float *z_in, void *out, float *state_out,
+                                   float *z_out, int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0,
+                                   float key_scale, float rms_eps, float eps, int bidirectional,
+                                   int token_splits, void *ws, size_t ws_bytes, int reps, float *stage_ms,
+                                   void *stream) {
+    return frame_profile(fused_args(q_raw, k_raw, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq,
+                                    rope_axis, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w, t0,
+                                    key_scale, rms_eps, eps, bidirectional),
                          token_splits, ws, ws_bytes, reps, stage_ms, stream);
 }
 

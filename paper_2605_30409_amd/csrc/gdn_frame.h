@@ -66,6 +66,18 @@ template <class E> struct FrameParams {
     float *Af;                   // [B*H][F][Dk/16][NJ][64][4]         A tiles
     E *Hf;                       // [B*H][F][NJ][Dk/32][64][8]         H_f operand fragments
     float *Hb;                   // [B*H][F][NJ][Dk/16][64][4]         backward histories (bidirectional)
+    // fused operator (the FUSED variants): raw projections in q and k, the
+    // feature maps formed on load; the normalizer recurrence takes its own
+    // Gram matrix of the unrotated keys
+    E *Gzf;                      // [B*H][F][Dk/16][Dk/32][64][8]      unrotated-key G fragments
+    float *PGz;                  // [B*H][F][NS][Dk/16][Dk/16][64][4]  its partial tiles
+    const E *gate;               // [B][T][H][Dv]  output gate before the SiLU
+    const E *w_o;                // [H][Dv][Dv]    per-head output projection (row = output channel)
+    const float *gain_q, *gain_k;  // [H][Dk]      RMSNorm gains
+    const float *rope_freq;      // [Dk/2]         angle per coordinate unit of channel pair i
+    const int *rope_axis;        // [Dk/2]         its coordinate: 0 time, 1 latent row, else latent column
+    float rms_eps, feat_scale;   // RMSNorm epsilon; key scale applied to the key features
+    int lat_w, t0;               // tokens per latent row; time coordinate of frame 0
 };
 
 // A fragment of ones: as the B operand, a 16-column tile whose every column is
@@ -99,12 +111,13 @@ __device__ __forceinline__ void xcd_unit(int id, int per_unit, int &unit, int &s
 // copy then reads contiguous runs of at least 256 bytes (4 rows of 16 chunks,
 // or whole rows when a row is shorter), and the transposed operand reads of a
 // fragment differ from one fragment to the next by a constant offset.
-template <class E, int DK, int DV> struct FrameSumLds {
+template <class E, int DK, int DV, bool FUSED = false> struct FrameSumLds {
     static constexpr int KB_ = 64 * DK * (int)sizeof(E), VB_ = 64 * DV * (int)sizeof(E);
-    static constexpr int SLOT = KB_ + VB_ + 256;
+    static constexpr int KH_ = FUSED ? KB_ : 0;                  // rotated key features (FUSED)
+    static constexpr int SLOT = KB_ + VB_ + KH_ + 256;
     static constexpr int NCK = KB_ / 1024, NCV = VB_ / 1024;   // 1 KB copies per block
     static constexpr int CAP = 160 * 1024;
-    static constexpr int DL = CAP / SLOT;
+    static constexpr int DL = (CAP - (FUSED ? 8 * DK + 1024 : 0)) / SLOT;
     // loaders 0, 1 (halves of the key copies, 0 also the betas) and 2, 3
     // (halves of the value copies) wait with DEPTH - 2 younger blocks in
     // flight: vmcnt <= 63
@@ -112,8 +125,13 @@ template <class E, int DK, int DV> struct FrameSumLds {
     static constexpr int DVM = 2 + 63 / PER;
     static constexpr int D0 = DL < DVM ? DL : DVM;
     static constexpr int DEPTH = D0 < 6 ? D0 : 6;
-    static constexpr size_t oK = 0, oV = KB_, oB = KB_ + VB_;
-    static constexpr size_t bytes = (size_t)DEPTH * SLOT;
+    static constexpr size_t oK = 0, oV = KB_, oB = KB_ + VB_, oKh = KB_ + VB_ + 256;
+    // FUSED: after the ring, the key gains [DK], pair frequencies [DK/2] and
+    // pair axes [DK/2] (as float), then 1 KB that takes the copies issued past
+    // the last block (their slot is being transformed in place)
+    static constexpr size_t oC = (size_t)DEPTH * SLOT;
+    static constexpr size_t oDm = oC + (size_t)8 * DK;
+    static constexpr size_t bytes = oC + (FUSED ? (size_t)8 * DK + 1024 : 0);
     static_assert(DEPTH >= 2, "summary ring needs two slots");
     static_assert(KB_ % 2048 == 0 && VB_ % 2048 == 0, "whole 1 KB copies, two loaders each");
 };
@@ -180,11 +198,29 @@ __device__ __forceinline__ Tr<float>::frag scale_frag(Tr<float>::frag x, const f
 // squared) and A's tiles (key scale) in their final form: the pair of row
 // tiles (2 kb, 2 kb + 1) of G column tile t is, lane by lane, fragment (t, kb).
 // With several splits it writes fp32 partial tiles for the reduction.
+// FUSED (the whole operator; bf16): the keys arrive raw.  Once a block has
+// landed, the compute waves turn its rows into the unrotated features
+// k~ = key_scale ReLU(gain o k / rms(k)) in place and their rotations
+// k^ = R k~ (3D RoPE) into a second area of the slot, 16 lanes per row (the
+// row's sum of squares reduced across them), and a second barrier hands the
+// features over.  G and A take k^; four more compute waves accumulate the
+// unrotated Gram matrix K~^T B K~ and K~^T beta for the normalizer.  The key
+// scale is then already in the features.
 constexpr int kSumCompute = 8, kSumLoaders = 4;
+template <bool FUSED> constexpr int sum_threads() { return (kSumCompute + (FUSED ? 4 : 0) + kSumLoaders) * 64; }
 
-template <class E, int DK, int DV, bool NORM>
-__global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_summary_kernel(FrameParams<E> p) {
-    using L = FrameSumLds<E, DK, DV>;
+// Coordinate of token (frame f, position s in the frame) along axis ax (0
+// time, 1 latent row, else latent column), for the 3D RoPE.
+template <class E>
+__device__ __forceinline__ float rope_coord(const FrameParams<E> &p, int ax, int f, int s) {
+    const int y = s / p.lat_w;
+    return (float)(ax == 0 ? p.t0 + f : ax == 1 ? y : s - y * p.lat_w);
+}
+
+template <class E, int DK, int DV, bool NORM, bool FUSED = false>
+__global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel(FrameParams<E> p) {
+    static_assert(!FUSED || (NORM && sizeof(E) == 2), "the fused operator is normalized and bf16");
+    using L = FrameSumLds<E, DK, DV, FUSED>;
     using TR = Tr<E>;
     using frag = typename TR::frag;
     constexpr int D = L::DEPTH;
@@ -209,18 +245,27 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
     const int nb = (t_hi - t_lo + 63) / 64;
     const size_t row_b = (size_t)b * T;
     auto slot = [&](int i) { return smem + (size_t)(i % D) * L::SLOT; };
+    constexpr int NCOMP = kSumCompute + (FUSED ? 4 : 0);
 
-    if (w >= kSumCompute) {
+    if (w >= NCOMP) {
         // ---------------- loader waves ----------------
         // loaders 0, 1: halves of the key copies (0 also the betas); 2, 3:
         // halves of the value copies.  Rows past the split repeat its last
-        // token (their beta is zeroed where it is used).
-        const int ld = w - kSumCompute;
+        // token (their beta is zeroed where it is used).  Every iteration
+        // issues the same number of copies so that the waits below count
+        // right: past the last block the last block is copied again, onto
+        // itself (unchanged bytes) or, FUSED, into a dummy area, since the
+        // compute waves rewrite that slot in place.
+        const int ld = w - NCOMP;
         const bool keys = ld < 2;
-        auto issue = [&](int i) {
+        auto issue = [&](int ii) {
+            const int i = min(ii, nb - 1);
+            const bool dummy = FUSED && ii >= nb;
             const int t0 = t_lo + 64 * i, rmax = t_hi - 1 - t0;
             const size_t row0 = (row_b + t0) * p.H + h;
             unsigned char *sl = slot(i);
+            // destination of a copy to byte offset off of the slot
+#define GDN_SUM_DST(off) ((__attribute__((address_space(3))) void *)(dummy ? smem + L::oDm : sl + (off)))
             if (keys) {
                 const char *base = (const char *)(p.k + row0 * DK);
                 const unsigned rstride = (unsigned)(p.H * DK * ESZ);
@@ -231,13 +276,12 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
                     gm_src<RK>(ci, l, r, c);
                     __builtin_amdgcn_global_load_lds(
                         (const void *)(base + (unsigned)min(r, rmax) * rstride + 16u * (unsigned)c),
-                        (__attribute__((address_space(3))) void *)(sl + L::oK + 1024 * ci), 16, 0, 0);
+                        GDN_SUM_DST(L::oK + 1024 * ci), 16, 0, 0);
                 }
                 if (ld == 0) {
                     const char *bb = (const char *)(p.beta + row0);
                     __builtin_amdgcn_global_load_lds(
-                        (const void *)(bb + (unsigned)min(l, rmax) * (unsigned)(4 * p.H)),
-                        (__attribute__((address_space(3))) void *)(sl + L::oB), 4, 0, 0);
+                        (const void *)(bb + (unsigned)min(l, rmax) * (unsigned)(4 * p.H)), GDN_SUM_DST(L::oB), 4, 0, 0);
                 }
             } else {
                 const char *base = (const char *)(p.v + row0 * DV);
@@ -249,9 +293,10 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
                     gm_src<RV>(ci, l, r, c);
                     __builtin_amdgcn_global_load_lds(
                         (const void *)(base + (unsigned)min(r, rmax) * rstride + 16u * (unsigned)c),
-                        (__attribute__((address_space(3))) void *)(sl + L::oV + 1024 * ci), 16, 0, 0);
+                        GDN_SUM_DST(L::oV + 1024 * ci), 16, 0, 0);
                 }
             }
+#undef GDN_SUM_DST
         };
         // block i has landed once at most D - 2 younger blocks are in flight
         auto wait_oldest = [&]() {
@@ -260,18 +305,20 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
             else wait_vmcnt<(D - 2) * NCV2>();
         };
 #pragma unroll
-        for (int i = 0; i < D - 1; ++i) issue(min(i, nb - 1));
+        for (int i = 0; i < D - 1; ++i) issue(i);
         for (int i = 0; i < nb; ++i) {
             wait_oldest();
             lds_only_barrier();                  // block i handed to the compute waves
-            issue(min(i + D - 1, nb - 1));       // refills the slot of block i - 1
+            issue(i + D - 1);                    // refills the slot of block i - 1
+            if constexpr (FUSED) lds_only_barrier();   // block i's features formed
         }
         wait_vmcnt<0>();
         return;
     }
 
     // ---------------- compute waves ----------------
-    const bool gw = w < 4;                                            // G waves, else A waves
+    const bool gw = w < 4;                                            // G waves (4..7: A waves)
+    const bool zgw = FUSED && w >= 8;                                 // unrotated Gram waves (FUSED)
     const int wq = w & 3, kbw = wq % NP, c0 = wq / NP;                // row pair, column share
     constexpr int CPW = CPG > CPA ? CPG : CPA;
     f32x4 acc[2][CPW];
@@ -279,26 +326,91 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
     for (int a = 0; a < 2; ++a)
 #pragma unroll
         for (int j = 0; j < CPW; ++j) acc[a][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // normalizer: the A waves of the first column share also accumulate
-    // K^T B 1 (a column of ones as the value) for their row pair
+    // normalizer: the A waves (FUSED: the unrotated Gram waves) of the first
+    // column share also accumulate K^T B 1 (a column of ones as the value)
+    // for their row pair
     f32x4 accz[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-    const bool zw = NORM && !gw && c0 == 0;
+    const bool zw = NORM && (FUSED ? zgw : (!gw && w < 8)) && c0 == 0;
     const frag ones = ones_frag<E>();
+
+    // FUSED: the feature maps of one block, in place (k~) and into the
+    // rotated area (k^); RK lanes per row, lane l holding channels 8 (l % RK) ..
+    // (the head's key gains, pair frequencies and axes, staged once; the
+    // first barrier orders these writes before any transform)
+    if constexpr (FUSED) {
+        float *cst = (float *)(smem + L::oC);
+        for (int j = w * 64 + l; j < 2 * DK; j += NCOMP * 64)
+            cst[j] = j < DK ? p.gain_k[h * DK + j]
+                            : j < DK + DK / 2 ? p.rope_freq[j - DK] : (float)p.rope_axis[j - DK - DK / 2];
+    }
+    [[maybe_unused]] auto transform = [&](int i) {
+        if constexpr (FUSED) {
+            constexpr int RPP = NCOMP * 64 / RK;                      // rows per pass
+            const int cc = l % RK;                                    // this lane's 8 channels 8 cc ..
+            unsigned char *sl = slot(i);
+            E *sK = (E *)(sl + L::oK), *sKh = (E *)(sl + L::oKh);
+            const int tok0 = t_lo + 64 * i, rmax = t_hi - 1 - tok0;
+            const float *cst = (const float *)(smem + L::oC);
+#pragma unroll
+            for (int r0 = 0; r0 < 64; r0 += RPP) {
+                const int r = r0 + (w * 64 + l) / RK;
+                const int rr = min(r, 63);
+                E *src = sK + gm_at<E, RK>(rr, 8 * cc);
+                const u32x4 raw = *(const u32x4 *)src;
+                float x[8];
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    x[2 * d] = __uint_as_float(raw[d] << 16);
+                    x[2 * d + 1] = __uint_as_float(raw[d] & 0xffff0000u);
+                }
+                float ss = 0.f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) ss += x[q] * x[q];
+#pragma unroll
+                for (int m = 1; m < RK; m <<= 1) ss += __shfl_xor(ss, m);
+                const float inv = rsqrtf(ss * (1.f / DK) + p.rms_eps);
+                // the token in this row (rows past the split repeat its last one)
+                // and its coordinates (time, latent row, latent column)
+                const int s_in = tok0 + min(rr, rmax) - f * p.N;
+                const int yc = s_in / p.lat_w;
+                const float ct = (float)(p.t0 + f), cy = (float)yc, cx = (float)(s_in - yc * p.lat_w);
+#pragma unroll
+                for (int q = 0; q < 8; ++q) x[q] = p.feat_scale * fmaxf(cst[8 * cc + q] * x[q] * inv, 0.f);
+                u32x4 ft, fh;
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    const int pr = 4 * cc + d;
+                    const float ax = cst[DK + DK / 2 + pr];
+                    const float th = cst[DK + pr] * (ax == 0.f ? ct : ax == 1.f ? cy : cx);
+                    const float sn = __sinf(th), cs = __cosf(th);
+                    ft[d] = pack_bf16x2(x[2 * d], x[2 * d + 1]);
+                    fh[d] = pack_bf16x2(x[2 * d] * cs - x[2 * d + 1] * sn, x[2 * d] * sn + x[2 * d + 1] * cs);
+                }
+                if (r < 64) {
+                    *(u32x4 *)src = ft;
+                    *(u32x4 *)(sKh + gm_at<E, RK>(rr, 8 * cc)) = fh;
+                }
+            }
+        }
+    };
 
     // the block loop, specialised for G waves (GB) and A waves, so that it has
     // no branch inside: all operand reads of a block (the K^T fragments
     // multiplied by beta) are issued before its products, which start as the
     // reads return.  Nothing reads a slot after the barrier that hands the
     // next block over (the loaders then refill it).
-    auto run = [&](auto gb) {
-        constexpr bool GB = decltype(gb)::value;
+    // role 0: G waves, 1: A waves, 2: unrotated Gram waves (FUSED)
+    auto run = [&](auto role) {
+        constexpr int RO = decltype(role)::value;
+        constexpr bool GB = RO != 1;
         constexpr int NC = GB ? CPG : CPA;
+        constexpr size_t oKey = (FUSED && RO != 2) ? L::oKh : L::oK;
         struct Ops {
             frag a[2], b[NC];
         };
         auto read = [&](int i, int kb, Ops &o) {
             const unsigned char *sl = slot(i);
-            const E *sK = (const E *)(sl + L::oK), *sV = (const E *)(sl + L::oV);
+            const E *sK = (const E *)(sl + oKey), *sV = (const E *)(sl + L::oV);
             const float *sB = (const float *)(sl + L::oB);
             // betas of this lane's 8 k-slots: tokens 32 kb + 8 lg + q'
             const f32x4 be0 = *(const f32x4 *)(sB + 32 * kb + 8 * lg);
@@ -325,7 +437,7 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
             for (int a = 0; a < 2; ++a)
 #pragma unroll
                 for (int j = 0; j < NC; ++j) acc[a][j] = TR::mma(o.a[a], o.b[j], acc[a][j]);
-            if constexpr (NORM && !GB) {
+            if constexpr (NORM && (FUSED ? RO == 2 : RO == 1)) {
                 if (zw) {
 #pragma unroll
                     for (int a = 0; a < 2; ++a) accz[a] = TR::mma(o.a[a], ones, accz[a]);
@@ -337,28 +449,47 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
             // the barrier also completes the previous block's reads, so the
             // loaders may refill that block's slot
             lds_only_barrier();                  // block i has landed
-            read(i, 0, o0);
-            read(i, 1, o1);
-            mul(o0);
-            mul(o1);
+            if constexpr (FUSED) {
+                transform(i);
+                lds_only_barrier();              // its features are formed
+                // one operand set at a time: 16 waves leave 128 registers each
+                read(i, 0, o0);
+                mul(o0);
+                read(i, 1, o0);
+                mul(o0);
+            } else {
+                read(i, 0, o0);
+                read(i, 1, o1);
+                mul(o0);
+                mul(o1);
+            }
         }
     };
     if (gw)
-        run(std::true_type{});
+        run(std::integral_constant<int, 0>{});
+    else if (zgw)
+        run(std::integral_constant<int, 2>{});
     else
-        run(std::false_type{});
+        run(std::integral_constant<int, 1>{});
 
     const size_t fi = (size_t)bh * p.F + f;
-    const int cpw = gw ? CPG : CPA;
+    const bool gram = gw || zgw;
+    const int cpw = gram ? CPG : CPA;
     if (p.NS == 1) {
         const float ks = p.key_scale;
-        if (gw) {
+        if (gram) {
             const float k2 = ks * ks;
+            E *dstg = zgw ? p.Gzf : p.Gf;
 #pragma unroll
             for (int j = 0; j < CPG; ++j) {
                 const int t = c0 * CPG + j;                             // G column tile (P32)
-                TR::store8(p.Gf + ((fi * NR + t) * KBN + kbw) * 512 + l * 8,
+                TR::store8(dstg + ((fi * NR + t) * KBN + kbw) * 512 + l * 8,
                            TR::cat(TR::from_f32(acc[0][j] * k2), TR::from_f32(acc[1][j] * k2)));
+            }
+            if (FUSED && zw) {
+#pragma unroll
+                for (int a = 0; a < 2; ++a)
+                    *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + NCA) * 256 + l * 4) = accz[a] * ks;
             }
         } else {
 #pragma unroll
@@ -368,15 +499,15 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
                 for (int a = 0; a < 2; ++a)
                     *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + jt) * 256 + l * 4) = acc[a][j] * ks;
             }
-            if (zw) {
+            if (!FUSED && zw) {
 #pragma unroll
                 for (int a = 0; a < 2; ++a)
                     *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + NCA) * 256 + l * 4) = accz[a] * ks;
             }
         }
     } else {
-        const int NC = gw ? NCG : NJA;
-        float *dst = (gw ? p.PG : p.PA) + (fi * p.NS + s) * (size_t)NR * NC * 256;
+        const int NC = gram ? NCG : NJA;
+        float *dst = (gw ? p.PG : zgw ? p.PGz : p.PA) + (fi * p.NS + s) * (size_t)NR * NC * 256;
 #pragma unroll
         for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -384,27 +515,32 @@ __global__ __launch_bounds__((kSumCompute + kSumLoaders) * 64) void gdn_frame_su
                 if (j < cpw)
                     *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + c0 * cpw + j) * 64 + l) * 4) = acc[a][j];
         if (zw) {
+            // the A partials' normalizer tile (FUSED: written by the unrotated Gram waves)
+            float *dz = p.PA + (fi * p.NS + s) * (size_t)NR * NJA * 256;
 #pragma unroll
             for (int a = 0; a < 2; ++a)
-                *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + NCA) * 64 + l) * 4) = accz[a];
+                *(f32x4 *)(dz + ((size_t)((2 * kbw + a) * NJA + NCA) * 64 + l) * 4) = accz[a];
         }
     }
 }
 
 // Sum over the splits.  Items per (frame, head): the Dk/16 x Dk/32 G operand
-// fragments, then the Dk/16 x Dv/16 A tiles; one wave per item.
-template <class E, int DK, int DV, bool NORM>
+// fragments, then the Dk/16 x Dv/16 A tiles, then (FUSED) the unrotated-key G
+// fragments; one wave per item.
+template <class E, int DK, int DV, bool NORM, bool FUSED = false>
 __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     constexpr int NR = DK / 16, KB = DK / 32, NCV = DV / 16 + NORM;
-    constexpr int NGI = NR * KB, NI = NGI + NR * NCV;
+    constexpr int NGI = NR * KB, NAI = NR * NCV, NI = NGI + NAI + (FUSED ? NGI : 0);
     const int item = blockIdx.y * 4 + (threadIdx.x >> 6);
     const size_t fi = blockIdx.x;                                // (b*H + h) * F + f
     if (item >= NI) return;
     const int l = threadIdx.x & 63;
-    if (item < NGI) {
-        const int t = item / KB, kb = item - t * KB;
-        const float *src = p.PG + fi * p.NS * (size_t)NR * NR * 256 + l * 4;
+    const bool gz = FUSED && item >= NGI + NAI;
+    if (item < NGI || gz) {
+        const int gi = gz ? item - NGI - NAI : item;
+        const int t = gi / KB, kb = gi - t * KB;
+        const float *src = (gz ? p.PGz : p.PG) + fi * p.NS * (size_t)NR * NR * 256 + l * 4;
         f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = lo;
         for (int s = 0; s < p.NS; ++s) {
             const float *ps = src + (size_t)s * NR * NR * 256;
@@ -412,7 +548,7 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
             hi += *(const f32x4 *)(ps + (size_t)((2 * kb + 1) * NR + t) * 256);
         }
         const float k2 = p.key_scale * p.key_scale;
-        TR::store8(p.Gf + ((fi * NR + t) * KB + kb) * 512 + l * 8,
+        TR::store8((gz ? p.Gzf : p.Gf) + ((fi * NR + t) * KB + kb) * 512 + l * 8,
                    TR::cat(TR::from_f32(lo * k2), TR::from_f32(hi * k2)));
     } else {
         const int a = item - NGI;                                // = t * NCV + jt
@@ -435,10 +571,11 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
 // the last) in fp32 in Hb, lane by lane in the accumulator layout; the
 // forward sweep then reads Hb_f with frame f's operands and writes
 // H_f + Hb_f, rounded once, as the output operand.  The terminal state is the
-// forward one.
+// forward one.  FUSED: the normalizer tile takes the unrotated-key Gram
+// matrix (the other tiles the rotated one).
 template <class E> struct FrameScanPrefetch { static constexpr bool value = sizeof(E) == 2; };
 
-template <class E, int DK, int DV, bool NORM, bool BIDIR>
+template <class E, int DK, int DV, bool NORM, bool BIDIR, bool FUSED = false>
 __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
@@ -463,7 +600,8 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
     };
     auto load_ops = [&](int f, Ops &o, auto with_hist) {
         const size_t fi = (size_t)bh * p.F + f;
-        const E *G = p.Gf + fi * NT * KB * 512 + l * 8;
+        // FUSED: the normalizer follows the Gram matrix of the unrotated keys
+        const E *G = ((FUSED && ztile) ? p.Gzf : p.Gf) + fi * NT * KB * 512 + l * 8;
         const float *A = p.Af + fi * NT * NJ * 256 + l * 4;
         o.a = p.alpha[((size_t)b * p.F + f) * p.H + h];
 #pragma unroll
@@ -689,6 +827,182 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
         if (i + 4 >= tile_hi) break;
         load_q(clampi(i + 8), qa);
         compute(i + 4, qb);
+    }
+}
+
+// Phase C of the fused operator (bf16).  As gdn_frame_output_kernel (each
+// workgroup a run of 16-token tiles of one (frame, head), wave w every
+// kFusedOutWaves-th tile from w, the next tile's loads in flight), with the
+// query features formed on load and the gate and the per-head projection
+// applied before the store.  Lane (li, lg) holds token li, channels
+// 32 kb + 8 lg + q' of k block kb:
+//   q~ = ReLU(gain_q o q / rms(q))   (the sum of squares reduced over the 4
+//                                     lanes of the token),  q^ = R q~ (RoPE);
+//   numerator tiles H_f^T q^, normalizer tile z . q~ (every column holds z);
+//   y = SiLU(gate) o numerator / (z . q~ + eps), staged in LDS as bf16;
+//   out^T = W_o y^T with W_o staged in LDS as operand fragments, then the
+//   result tile goes back through LDS for whole-row stores.
+constexpr int kFusedOutWaves = 8;
+
+template <int DK, int DV> struct FusedOutLds {
+    static constexpr int NJ = DV / 16 + 1;
+    static constexpr int LDO = DV + 8;                          // staged row stride (bf16)
+    static constexpr size_t oW = (size_t)2 * DK * 16 * NJ;      // after H_f: W_o fragments
+    static constexpr size_t oP = oW + (size_t)2 * DV * DV;      // gain_q[DK], freq[DK/2], axis[DK/2] (float)
+    static constexpr size_t oO = oP + (size_t)4 * 2 * DK;       // one 16-row staging tile per wave
+    static constexpr size_t bytes = oO + (size_t)2 * kFusedOutWaves * 16 * LDO;
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_kernel(FrameParams<uint16_t> p) {
+    using E = uint16_t;
+    using TR = Tr<E>;
+    using frag = TR::frag;
+    using LO = FusedOutLds<DK, DV>;
+    constexpr int KB = DK / 32, NV = DV / 16, NJ = LO::NJ, KBV = DV / 32;
+    constexpr int NTH = kFusedOutWaves * 64;
+    extern __shared__ __align__(16) unsigned char smem[];
+    int unit, blk;
+    xcd_unit(blockIdx.x, p.OB, unit, blk);
+    if (unit >= p.F * p.B * p.H) return;
+    const int bh = unit / p.F, f = unit - bh * p.F;
+    const int b = bh / p.H, h = bh - b * p.H;
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
+    const size_t fi = (size_t)bh * p.F + f;
+
+    // H_f fragments, W_o fragments (jo, kb): lane l holds
+    // W_o[h][16 jo + l % 16][32 kb + 8 (l / 16) ..], and the prologue constants
+    {
+        constexpr int HV = NJ * 16 * DK * 2 / 16, HIT = (HV + NTH - 1) / NTH;
+        constexpr int WV = DV * DV * 2 / 16, WIT = WV / NTH;
+        static_assert(WV % NTH == 0, "whole W_o staging passes");
+        const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
+        u32x4 hv[HIT], wv[WIT];
+#pragma unroll
+        for (int it = 0; it < HIT; ++it)
+            if (HV % NTH == 0 || tid + NTH * it < HV) hv[it] = src[tid + NTH * it];
+#pragma unroll
+        for (int it = 0; it < WIT; ++it) {
+            const int j = tid + NTH * it, fr = j >> 6, ll = j & 63, jo = fr / KBV, kb = fr - jo * KBV;
+            wv[it] = *(const u32x4 *)(p.w_o + ((size_t)h * DV + 16 * jo + (ll & 15)) * DV + 32 * kb + 8 * (ll >> 4));
+        }
+        float *cp = (float *)(smem + LO::oP);
+        for (int j = tid; j < 2 * DK; j += NTH)
+            cp[j] = j < DK ? p.gain_q[h * DK + j]
+                           : j < DK + DK / 2 ? p.rope_freq[j - DK] : (float)p.rope_axis[j - DK - DK / 2];
+#pragma unroll
+        for (int it = 0; it < HIT; ++it)
+            if (HV % NTH == 0 || tid + NTH * it < HV) ((u32x4 *)smem)[tid + NTH * it] = hv[it];
+#pragma unroll
+        for (int it = 0; it < WIT; ++it) ((u32x4 *)(smem + LO::oW))[tid + NTH * it] = wv[it];
+    }
+
+    const size_t T = (size_t)p.F * p.N;
+    const int ntf = (p.N + 15) / 16;
+    const int tile_lo = blk * p.OTPW, tile_hi = min(ntf, tile_lo + p.OTPW);
+    const size_t row_f = (size_t)b * T + (size_t)f * p.N;
+    // query fragments and gate quads of tile i; rows past the frame read its last token
+    auto load = [&](int i, frag (&qf)[KB], u32x2 (&gt)[NV]) {
+        const int n = min(16 * i + li, p.N - 1);
+        const size_t row = (row_f + n) * p.H + h;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) qf[kb] = load_frag<E>(p.q + row * DK + 32 * kb, lg);
+#pragma unroll
+        for (int jo = 0; jo < NV; ++jo) gt[jo] = *(const u32x2 *)(p.gate + row * DV + 16 * jo + 4 * lg);
+    };
+    const E *sH = (const E *)smem + l * 8;
+    const E *sW = (const E *)(smem + LO::oW) + l * 8;
+    const float *cgain = (const float *)(smem + LO::oP), *cfreq = cgain + DK, *caxis = cfreq + DK / 2;
+    E *sO = (E *)(smem + LO::oO) + w * 16 * LO::LDO;
+    constexpr int VE = 8, RV = DV / VE;                        // bf16 per 16 bytes, vectors per row
+    auto compute = [&](int tile, const frag (&qf)[KB], const u32x2 (&gt)[NV]) {
+        // prologue: features of token li
+        float x[KB][8];
+        float ss = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                x[kb][2 * d] = __uint_as_float(qf[kb][d] << 16);
+                x[kb][2 * d + 1] = __uint_as_float(qf[kb][d] & 0xffff0000u);
+                ss += x[kb][2 * d] * x[kb][2 * d] + x[kb][2 * d + 1] * x[kb][2 * d + 1];
+            }
+        ss += __shfl_xor(ss, 16);
+        ss += __shfl_xor(ss, 32);
+        const float inv = rsqrtf(ss * (1.f / DK) + p.rms_eps);
+        const int n = min(16 * tile + li, p.N - 1);
+        frag qt[KB], qh[KB];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            const int ch = 32 * kb + 8 * lg;
+            float xt[8], xh[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) xt[q] = fmaxf(cgain[ch + q] * x[kb][q] * inv, 0.f);
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                const int pr = ch / 2 + d;
+                const float th = cfreq[pr] * rope_coord(p, (int)caxis[pr], f, n);
+                const float sn = __sinf(th), cs = __cosf(th);
+                xh[2 * d] = xt[2 * d] * cs - xt[2 * d + 1] * sn;
+                xh[2 * d + 1] = xt[2 * d] * sn + xt[2 * d + 1] * cs;
+            }
+            qt[kb] = frag{pack_bf16x2(xt[0], xt[1]), pack_bf16x2(xt[2], xt[3]), pack_bf16x2(xt[4], xt[5]),
+                          pack_bf16x2(xt[6], xt[7])};
+            qh[kb] = frag{pack_bf16x2(xh[0], xh[1]), pack_bf16x2(xh[2], xh[3]), pack_bf16x2(xh[4], xh[5]),
+                          pack_bf16x2(xh[6], xh[7])};
+        }
+        // the denominator of token li (every column of the normalizer tile is z)
+        f32x4 dz = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) dz = TR::mma(TR::load8(sH + (NV * KB + kb) * 512), qt[kb], dz);
+        const float invd = 1.f / (dz[0] + p.eps);
+        // gated, normalized readout into the staging tile
+#pragma unroll
+        for (int jo = 0; jo < NV; ++jo) {
+            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb) acc = TR::mma(TR::load8(sH + (jo * KB + kb) * 512), qh[kb], acc);
+            const f32x4 g = TR::to_f32(gt[jo]);
+            f32x4 y;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) y[q] = g[q] / (1.f + __expf(-g[q])) * (acc[q] * invd);
+            TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(y));
+        }
+        // projection: out^T = W_o y^T, y^T as the B operand read back by rows
+        frag yb[KBV];
+#pragma unroll
+        for (int kb = 0; kb < KBV; ++kb) yb[kb] = TR::load8(sO + li * LO::LDO + 32 * kb + 8 * lg);
+#pragma unroll
+        for (int jo = 0; jo < NV; ++jo) {
+            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < KBV; ++kb) o = TR::mma(TR::load8(sW + (jo * KBV + kb) * 512), yb[kb], o);
+            TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(o));
+        }
+        // rows r of the tile, RV lanes per row, 64 / RV rows per pass
+#pragma unroll
+        for (int pass = 0; pass < 16 * RV / 64; ++pass) {
+            const int r = pass * (64 / RV) + l / RV, c = (l % RV) * VE;
+            const u32x4 val = *(const u32x4 *)(sO + r * LO::LDO + c);
+            const int nn = 16 * tile + r;
+            if (tile < tile_hi && nn < p.N) *(u32x4 *)(p.out + ((row_f + nn) * p.H + h) * DV + c) = val;
+        }
+    };
+    // the prefetch is unconditional (clamped to the workgroup's last tile) so
+    // the wait for one buffer always leaves exactly the other in flight
+    constexpr int SW = kFusedOutWaves;
+    auto clampi = [&](int i) { return min(i, tile_hi - 1); };
+    frag qa[KB], qb[KB];
+    u32x2 ga[NV], gb[NV];
+    const int i0 = tile_lo + w;
+    load(clampi(i0), qa, ga);
+    lds_barrier();                                // staging complete
+    for (int i = i0; i < tile_hi; i += 2 * SW) {
+        load(clampi(i + SW), qb, gb);
+        compute(i, qa, ga);
+        if (i + SW >= tile_hi) break;
+        load(clampi(i + 2 * SW), qa, ga);
+        compute(i + SW, qb, gb);
     }
 }
 

@@ -78,6 +78,13 @@ def lib():
         L.gdn_frame_profile_stages_bidir.restype = i
         L.gdn_frame_profile_stages_bidir.argtypes = ncore + [i, i, vp, sz, i, ctypes.POINTER(ctypes.c_float),
                                                              vp]
+        ucore = [vp] * 16 + [i] * 8 + [fl] * 3 + [i]        # 16 pointers, sizes, lat_w, t0, scales, bidir
+        L.gdn_frame_forward_fused.restype = i
+        L.gdn_frame_forward_fused.argtypes = ucore + [vp]
+        L.gdn_frame_forward_fused_ex.restype = i
+        L.gdn_frame_forward_fused_ex.argtypes = ucore + [i, vp, sz, vp]
+        L.gdn_frame_profile_stages_fused.restype = i
+        L.gdn_frame_profile_stages_fused.argtypes = ucore + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
         L.gdn_status_string.restype = ctypes.c_char_p
         L.gdn_status_string.argtypes = [i]
         _lib = L
@@ -445,3 +452,86 @@ def frame_forward_bidir(q, k, v, alpha, beta, state_in=None, z_in=None, *, frame
         _norm_call("gdn_frame_forward_bidir", q, k, v, alpha, beta, state_in, z_in, out, state_out, z_out,
                    frame_tokens, key_scale, eps, (nf,), stream)
     return (out, state_out, z_out) if normalized else (out, state_out)
+
+
+# ---------------------------------------------------------------------------
+# The fused operator (gdn_frame_forward_fused*): RMSNorm / ReLU / 3D RoPE on the
+# raw q and k, the two states, the normalized readout, SiLU gate and W_o.
+
+def _check_param(t, shape, dtype, dev, name):
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must be {dtype} {list(shape)}")
+    if t.device != dev or not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous on {dev}")
+
+
+def _fused_call(name, q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq, rope_axis, state_in, z_in,
+                out, state_out, z_out, frame_tokens, lat_w, t0, key_scale, rms_eps, eps, bidirectional, extra,
+                stream):
+    B, H, T, Dk, Dv, is_bf16 = _check(q, k, v, alpha, beta, state_in, out, state_out, frame_tokens)
+    if not is_bf16:
+        raise ValueError("the fused operator takes bf16 q, k, v, gate and w_o")
+    dev = q.device
+    _check_param(gate, v.shape, torch.bfloat16, dev, "gate")
+    _check_param(w_o, (H, Dv, Dv), torch.bfloat16, dev, "w_o")
+    _check_param(gain_q, (H, Dk), torch.float32, dev, "gain_q")
+    _check_param(gain_k, (H, Dk), torch.float32, dev, "gain_k")
+    _check_param(rope_freq, (Dk // 2,), torch.float32, dev, "rope_freq")
+    _check_param(rope_axis, (Dk // 2,), torch.int32, dev, "rope_axis")
+    _check_z(z_in, B, H, Dk, dev, "z_in")
+    _check_z(z_out, B, H, Dk, dev, "z_out")
+    N = int(frame_tokens)
+    ks = default_key_scale(Dk, N) if key_scale is None else float(key_scale)
+    with torch.cuda.device(dev):
+        rc = getattr(lib(), name)(_ptr(q), _ptr(k), _ptr(v), _ptr(gate), _ptr(w_o), _ptr(alpha), _ptr(beta),
+                                  _ptr(gain_q), _ptr(gain_k), _ptr(rope_freq), _ptr(rope_axis), _ptr(state_in),
+                                  _ptr(z_in), _ptr(out), _ptr(state_out), _ptr(z_out), B, H, T // N, N, Dk, Dv,
+                                  int(lat_w), int(t0), ctypes.c_float(ks), ctypes.c_float(rms_eps),
+                                  ctypes.c_float(eps), 1 if bidirectional else 0, *extra, _stream(dev, stream))
+    if rc != GDN_OK:
+        raise GdnError(name, rc)
+
+
+def gdn_frame_profile_stages_fused(q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq, rope_axis,
+                                   state_in, z_in, out, state_out, z_out, ws, frame_tokens, lat_w, t0=0,
+                                   key_scale=None, rms_eps=1e-6, eps=1e-6, bidirectional=False, token_splits=0,
+                                   reps=20, stream=None):
+    """Mean per-stage durations in ms of the fused operator."""
+    ms = (ctypes.c_float * len(FRAME_STAGE_NAMES))()
+    _fused_call("gdn_frame_profile_stages_fused", q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq,
+                rope_axis, state_in, z_in, out, state_out, z_out, frame_tokens, lat_w, t0, key_scale, rms_eps,
+                eps, bidirectional, (int(token_splits), _ptr(ws), ws.numel(), int(reps), ms), stream)
+    return [float(x) for x in ms]
+
+
+def frame_forward_fused(q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq, rope_axis, state_in=None,
+                        z_in=None, *, frame_tokens, lat_w, t0=0, key_scale=None, rms_eps=1e-6, eps=1e-6,
+                        bidirectional=False, out=None, state_out=None, z_out=None, want_state=True, ws=None,
+                        token_splits=None, stream=None):
+    """The fused frame-wise GDN operator (bf16).  q, k: the raw projections
+    [B, T, H, Dk]; v, gate (pre-SiLU) [B, T, H, Dv]; w_o [H, Dv, Dv] (row = output
+    channel); alpha [B, F, H], beta [B, T, H] fp32; gain_q, gain_k [H, Dk] fp32
+    RMSNorm gains; rope_freq [Dk/2] fp32 and rope_axis [Dk/2] int32 (0 time, 1
+    latent row, 2 latent column) of the 3D RoPE, with lat_w tokens per latent row
+    and t0 the time coordinate of the first frame; state_in [B, H, Dk, Dv] and
+    z_in [B, H, Dk] fp32 or None.  Returns (out [B, T, H, Dv] bf16, state_out,
+    z_out)."""
+    B, T, H, Dk = q.shape
+    Dv = v.shape[-1]
+    if out is None:
+        out = torch.empty((B, T, H, Dv), dtype=q.dtype, device=q.device)
+    if want_state:
+        if state_out is None:
+            state_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=q.device)
+        if z_out is None:
+            z_out = torch.empty((B, H, Dk), dtype=torch.float32, device=q.device)
+    args = (q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq, rope_axis, state_in, z_in, out, state_out,
+            z_out, frame_tokens, lat_w, t0, key_scale, rms_eps, eps, bidirectional)
+    if ws is not None or token_splits is not None:
+        ts = 0 if token_splits is None else int(token_splits)
+        if ws is None:
+            ws = frame_workspace(q, v, frame_tokens, ts)
+        _fused_call("gdn_frame_forward_fused_ex", *args, (ts, _ptr(ws), ws.numel()), stream)
+    else:
+        _fused_call("gdn_frame_forward_fused", *args, (), stream)
+    return out, state_out, z_out

@@ -21,7 +21,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 22 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
+    assert len(names) == 25 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -141,9 +141,9 @@ def test_frame_token_splits_and_workspace():
     # G fragments (bf16), A tiles (fp32), state fragments (bf16) and backward
     # histories (fp32), the last three with room for the normalizer's extra
     # 16-column tile
-    expect = bhf * (128 * 128 * 2 + 128 * 144 * (4 + 2 + 4))
-    assert expect <= n < expect + 6 * 256
-    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 128 * (128 + 144) * 4
+    expect = bhf * (128 * 128 * 2 + 128 * 144 * (4 + 2 + 4) + 128 * 128 * 2)   # + unrotated-key G (fused)
+    assert expect <= n < expect + 8 * 256
+    assert wb(1, 16, 3, 3520, 128, 128, True, 2) - n >= bhf * 2 * 128 * (2 * 128 + 144) * 4
     assert wb(1, 16, 3, 3520, 128, 128, False, 1) > n
     assert wb(1, 16, 3, 0, 128, 128, True, 0) == 0
     assert wb(1, 16, 3, 3520, 128, 32, True, 0) == 0
@@ -251,3 +251,38 @@ def test_frame_bidir_profile_rejects_in_place():
             BASE + 256 * MB, S, None, 1, 2, 2, 100, 64, 64, ctypes.c_float(0.1), ctypes.c_float(1e-6), 1, 0,
             0, None, 0, 3, ms]
     assert L.gdn_frame_profile_stages_bidir(*args, None) == -7
+
+
+def ucall(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, g=BASE + 160 * MB, w=BASE + 176 * MB,
+          a=BASE + 192 * MB, b=BASE + 200 * MB, gq=BASE + 208 * MB, gk=BASE + 209 * MB, fr=BASE + 210 * MB,
+          ax=BASE + 211 * MB, si=None, zi=None, o=BASE + 256 * MB, so=None, zo=None, B=1, H=2, F=2, N=100,
+          Dk=64, Dv=64, lat_w=10, ws=None, ws_bytes=0):
+    L = gdn.lib()
+    args = [q, k, v, g, w, a, b, gq, gk, fr, ax, si, zi, o, so, zo, B, H, F, N, Dk, Dv, lat_w, 0,
+            ctypes.c_float(0.1), ctypes.c_float(1e-6), ctypes.c_float(1e-6), 0]
+    if fn.endswith("_ex"):
+        args += [0, ws, ws_bytes]
+    return getattr(L, fn)(*args, None)
+
+
+@pytest.mark.parametrize("fn", ["gdn_frame_forward_fused", "gdn_frame_forward_fused_ex"])
+def test_frame_fused_validation_errors(fn):
+    assert ucall(fn, g=None) == -1
+    assert ucall(fn, w=None) == -1
+    assert ucall(fn, ax=None) == -1
+    assert ucall(fn, lat_w=0) == -2
+    assert ucall(fn, Dk=96) == -3
+    assert ucall(fn, g=BASE + 160 * MB + 8) == -6
+    assert ucall(fn, o=BASE + 176 * MB) == -7            # out overlaps w_o
+    assert ucall(fn, so=BASE + 208 * MB) == -7           # state_out overlaps gain_q
+    if fn.endswith("_ex"):
+        assert ucall(fn) == -4
+
+
+def test_frame_fused_binding_rejects_fp32_on_cpu():
+    import torch
+    q = torch.zeros(1, 100, 2, 64)
+    with pytest.raises(ValueError):
+        gdn.frame_forward_fused(q, q, q, q, torch.zeros(2, 64, 64), torch.zeros(1, 2, 2), torch.zeros(1, 100, 2),
+                                torch.ones(2, 64), torch.ones(2, 64), torch.ones(32), torch.zeros(32, dtype=torch.int32),
+                                frame_tokens=50, lat_w=10)

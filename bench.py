@@ -20,7 +20,10 @@ their reduction over token splits, the scan over frames and the output.
 ``--path frame-norm`` measures the same call with the normalizer state and the
 normalized readout (non-negative feature maps); ``--path frame-bidir`` and
 ``--path frame-bidir-norm`` the bidirectional form of either (a backward scan
-over the call's frames beside the forward one).
+over the call's frames beside the forward one); ``--path frame-fused`` (and
+``frame-fused-bidir``) the whole operator of the paper's GDN block around it:
+raw q and k projections through RMSNorm, ReLU and 3D RoPE, the two states,
+the normalized readout, the SiLU gate and the per-head projection W_o.
 """
 import argparse
 import json
@@ -151,11 +154,13 @@ FRAME_BIDIR_METRIC = ("bidirectional frame-wise GDN fwd tokens/sec and TFLOP/s a
                       "H=16, D=128 bf16")
 FRAME_BIDIR_NORM_METRIC = ("bidirectional frame-wise normalized GDN fwd tokens/sec and TFLOP/s at F=3 frames x "
                            "N=3520 tokens, H=16, D=128 bf16")
+FRAME_FUSED_METRIC = ("fused frame-wise GDN operator (RMSNorm/ReLU/3D-RoPE prologue, SiLU gate and W_o epilogue) "
+                      "fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, H=16, D=128 bf16")
 FRAME_KERNELS = {"summaries": "gdn_frame_summary_kernel", "reduce": "gdn_frame_reduce_kernel",
                  "scan": "gdn_frame_scan_kernel", "output": "gdn_frame_output_kernel"}
 
 
-def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=False):
+def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=False, fused=False):
     """Per-stage algorithmic flops and bytes of the frame-wise path (each stage's own
     inputs and outputs, workspace included, every byte once) and its external I/O.
 
@@ -168,7 +173,14 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=Fa
     grow), plus z in and out and one division per output element.
     bidir: the scan also runs the backward recurrence over the F - 1 later
     frames (their G and A read once more), writes every frame's fp32 history
-    and reads it back to add it to H_f."""
+    and reads it back to add it to H_f.
+    fused (implies norm): the summaries also form the unrotated-key Gram
+    matrix for the normalizer (its partials, reduction and fragments counted
+    like G's, and the scan reads it); the output reads the gate beside the
+    queries and multiplies by W_o (read once per head).  The feature maps,
+    the division and the gate are elementwise work, not counted as flops."""
+    if fused:
+        norm = True
     Ds = Dv + 16 if norm else Dv        # state columns the kernels carry
     n = B * F * N * H                   # token-heads
     u = B * H * F                       # (frame, head) units
@@ -182,19 +194,44 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=Fa
          "reduce": part + u * (Dk * Dk * esz + Dk * Ds * 4),
          "scan": u * (Dk * Dk * esz + Dk * Ds * 4 + 4 + Dk * Ds * esz) + 2 * st,
          "output": n * (Dk + Dv) * esz + u * Dk * Ds * esz}
+    if fused:
+        gpart = u * NS * Dk * Dk * 4
+        f["summaries"] += 2.0 * n * Dk * Dk
+        f["reduce"] += float(u * NS * Dk * Dk)
+        b["summaries"] += gpart
+        b["reduce"] += gpart + u * Dk * Dk * esz
+        b["scan"] += u * Dk * Dk * esz
+        f["output"] += 2.0 * n * Dv * Dv
+        b["output"] += n * Dv * esz + H * Dv * Dv * esz
     if bidir:
         ub = B * H * (F - 1)
         f["scan"] += ub * (2.0 * Dk * Dk * Ds + 3.0 * Dk * Ds) + u * Dk * Ds
         b["scan"] += ub * (Dk * Dk * esz + Dk * Ds * 4 + 4) + 2 * u * Dk * Ds * 4
     io_bytes = n * ((2 * Dk + 2 * Dv) * esz + 4) + u * 4 + 2 * st
+    if fused:
+        io_bytes += n * Dv * esz + H * Dv * Dv * esz
     return dict(flops=f, bytes=b, io_bytes=io_bytes)
 
 
-def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=False):
+def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=False, fused=False):
     """Time the fp64 frame-wise oracle (as it stands) on whole calls for ~10 s."""
     import oracle
     threads = host_threads()
     reps, elapsed = 0, 0.0
+    if fused:
+        while elapsed < min_seconds and reps < 50:
+            t0 = time.perf_counter()
+            oracle.gdn_frame_forward_fused(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], inp["gate"],
+                                           inp["w_o"], inp["state_in"], inp["z_in"],
+                                           frame_tokens=inp["frame_tokens"], gain_q=inp["gain_q"],
+                                           gain_k=inp["gain_k"], rope_freq=inp["rope_freq"],
+                                           rope_axis=inp["rope_axis"], lat_w=inp["lat_w"], t0=inp["t0"],
+                                           bidirectional=bidir, nthreads=threads)
+            elapsed += time.perf_counter() - t0
+            reps += 1
+        return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+                "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H={H}, D={Dk}), "
+                          f"fp64 fused operator{' (bidirectional)' if bidir else ''}, {elapsed:.1f} s"}
     extra = dict(normalized=True, z_in=inp["z_in"]) if norm else {}
     if bidir:
         extra["bidirectional"] = True
@@ -210,10 +247,14 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=Fal
                       f"fp64 {'bidirectional ' if bidir else ''}frame-wise recurrence, {elapsed:.1f} s"}
 
 
-def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
+def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fused=False):
     F, N = 3, 3520
-    inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02",
-                                       features="relu" if norm else "gauss")
+    if fused:
+        norm = True
+        inp = gdn_inputs.make_fused_inputs(2, F, frame_tokens=N, state="normal0.02", lat_w=80, t0=0)
+    else:
+        inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02",
+                                           features="relu" if norm else "gauss")
     B, T, H, Dk = inp["q"].shape
     Dv = inp["v"].shape[-1]
     q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
@@ -221,6 +262,8 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
     out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
     s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
     z_in = to_dev(inp["z_in"]) if norm else None
+    fz = {key: to_dev(inp[key]) for key in ("gate", "w_o", "gain_q", "gain_k", "rope_freq", "rope_axis")} if fused \
+        else None
     z_out = torch.empty((B, H, Dk), dtype=torch.float32, device=dev) if norm else None
     ts = args.token_splits
     ws = gdn.frame_workspace(q, v, N, ts)
@@ -228,7 +271,12 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
     stream = torch.cuda.current_stream(dev)
 
     def step():
-        if bidir:
+        if fused:
+            gdn.frame_forward_fused(q, k, v, fz["gate"], fz["w_o"], alpha, beta, fz["gain_q"], fz["gain_k"],
+                                    fz["rope_freq"], fz["rope_axis"], s_in, z_in, frame_tokens=N, lat_w=80, t0=0,
+                                    bidirectional=bidir, out=out, state_out=s_out, z_out=z_out, ws=ws,
+                                    token_splits=ts, stream=stream)
+        elif bidir:
             gdn.frame_forward_bidir(q, k, v, alpha, beta, s_in, z_in, frame_tokens=N, normalized=norm, out=out,
                                     state_out=s_out, z_out=z_out, ws=ws, token_splits=ts, stream=stream)
         elif norm:
@@ -239,7 +287,12 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
                                      stream=stream)
 
     ms_per_step, cold_ms = timed(step, stream)
-    if bidir:
+    if fused:
+        stage_ms = gdn.gdn_frame_profile_stages_fused(q, k, v, fz["gate"], fz["w_o"], alpha, beta, fz["gain_q"],
+                                                      fz["gain_k"], fz["rope_freq"], fz["rope_axis"], s_in, z_in, out,
+                                                      s_out, z_out, ws, N, 80, 0, bidirectional=bidir,
+                                                      token_splits=ts, reps=args.steps, stream=stream)
+    elif bidir:
         stage_ms = gdn.gdn_frame_profile_stages_bidir(q, k, v, alpha, beta, s_in, z_in, out, s_out, z_out,
                                                       ws, N, normalized=norm, token_splits=ts, reps=args.steps,
                                                       stream=stream)
@@ -252,22 +305,26 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
                                                 token_splits=ts, reps=args.steps, stream=stream)
     names = dict(zip(gdn.FRAME_STAGE_NAMES, stage_ms))
     torch.cuda.synchronize()
-    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm, bidir=bidir)
+    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm, bidir=bidir, fused=fused)
     sec = ms_per_step / 1e3
     tflops = sum(cnt["flops"].values()) / sec / 1e12
     dom = max(names, key=names.get)
     roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
     # the bidirectional form shares every kernel but the scan with the
     # unidirectional one, so their counter summaries serve it too
-    traffic = None if (bidir and dom == "scan") else load_traffic(
-        dom, "traffic_frames3x1280x704_norm.json" if norm else "traffic_frames3x1280x704.json")
+    if fused:
+        traffic = None if dom == "scan" and bidir else load_traffic(dom, "traffic_frames3x1280x704_fused.json")
+    else:
+        traffic = None if (bidir and dom == "scan") else load_traffic(
+            dom, "traffic_frames3x1280x704_norm.json" if norm else "traffic_frames3x1280x704.json")
     roofline.update({"traffic": traffic,
                      "kernel": FRAME_KERNELS[dom], "duration_ms": round(names[dom], 5),
                      "algorithmic_flops_per_launch": cnt["flops"][dom],
                      "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
     stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_) for k_, v_ in names.items()}
     rec = {
-        "metric": (FRAME_BIDIR_NORM_METRIC if norm else FRAME_BIDIR_METRIC) if bidir
+        "metric": FRAME_FUSED_METRIC + (" (bidirectional)" if bidir else "") if fused
+                  else (FRAME_BIDIR_NORM_METRIC if norm else FRAME_BIDIR_METRIC) if bidir
                   else (FRAME_NORM_METRIC if norm else FRAME_METRIC),
         "value": round(B * T / sec, 1),
         "unit": "tokens/s",
@@ -284,7 +341,10 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
                                "N=3520 (44x80) H=16 Dk=Dv=128, bf16 q/k/v, one decay per frame, "
                                "key scale 1/sqrt(Dk N), fp32 state in/out"
                                + ("; normalizer state in/out and normalized readout (eps 1e-6), "
-                                  "non-negative (ReLU) feature maps" if norm else "")
+                                  "non-negative (ReLU) feature maps" if norm and not fused else "")
+                               + ("; fused operator: raw q/k projections through RMSNorm, ReLU and a fixed 3D "
+                                  "RoPE (44x80 latent grid), normalizer from the unrotated keys, SiLU output gate "
+                                  "and per-head W_o" if fused else "")
                                + ("; bidirectional (forward scan from the state plus a backward scan over "
                                   "the call's frames from zero)" if bidir else ""),
                    "B": B, "F": F, "N": N, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "token_splits": NS},
@@ -297,7 +357,7 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False):
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk, norm=norm, bidir=bidir)
+        rec["cpu_baseline"] = frame_cpu_baseline(inp, B, T, H, Dk, norm=norm, bidir=bidir, fused=fused)
     print(json.dumps(rec), flush=True)
 
 
@@ -312,11 +372,13 @@ def main():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (a known-size "
                          "reference for hardware traffic counters)")
-    ap.add_argument("--path", choices=("token", "frame", "frame-norm", "frame-bidir", "frame-bidir-norm"),
+    ap.add_argument("--path", choices=("token", "frame", "frame-norm", "frame-bidir", "frame-bidir-norm",
+                                       "frame-fused", "frame-fused-bidir"),
                     default="token",
                     help="token: the token-wise chunk forward (default); frame: the frame-wise "
                          "forward; frame-norm: the frame-wise forward with the normalizer; "
-                         "frame-bidir(-norm): their bidirectional forms")
+                         "frame-bidir(-norm): their bidirectional forms; frame-fused(-bidir): the whole "
+                         "operator with its prologue and epilogue")
     ap.add_argument("--token-splits", type=int, default=0,
                     help="frame path: token splits per frame (0 = the library's choice)")
     args = ap.parse_args()
@@ -377,7 +439,7 @@ def main():
 
     if args.path.startswith("frame"):
         run_frame(args, torch, gdn, dev, to_dev, timed, norm=args.path.endswith("-norm"),
-                  bidir="-bidir" in args.path)
+                  bidir="-bidir" in args.path, fused="-fused" in args.path)
         return
 
     w = gdn_inputs.WORKLOADS[WORKLOAD]

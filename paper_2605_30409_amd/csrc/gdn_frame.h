@@ -117,7 +117,7 @@ template <class E, int DK, int DV, bool FUSED = false> struct FrameSumLds {
     static constexpr int SLOT = KB_ + VB_ + KH_ + 256;
     static constexpr int NCK = KB_ / 1024, NCV = VB_ / 1024;   // 1 KB copies per block
     static constexpr int CAP = 160 * 1024;
-    static constexpr int DL = (CAP - (FUSED ? 8 * DK + 1024 : 0)) / SLOT;
+    static constexpr int DL = (CAP - (FUSED ? 1024 : 0)) / SLOT;
     // loaders 0, 1 (halves of the key copies, 0 also the betas) and 2, 3
     // (halves of the value copies) wait with DEPTH - 2 younger blocks in
     // flight: vmcnt <= 63
@@ -126,12 +126,11 @@ template <class E, int DK, int DV, bool FUSED = false> struct FrameSumLds {
     static constexpr int D0 = DL < DVM ? DL : DVM;
     static constexpr int DEPTH = D0 < 6 ? D0 : 6;
     static constexpr size_t oK = 0, oV = KB_, oB = KB_ + VB_, oKh = KB_ + VB_ + 256;
-    // FUSED: after the ring, the key gains [DK], pair frequencies [DK/2] and
-    // pair axes [DK/2] (as float), then 1 KB that takes the copies issued past
-    // the last block (their slot is being transformed in place)
-    static constexpr size_t oC = (size_t)DEPTH * SLOT;
-    static constexpr size_t oDm = oC + (size_t)8 * DK;
-    static constexpr size_t bytes = oC + (FUSED ? (size_t)8 * DK + 1024 : 0);
+    // FUSED: after the ring, 1 KB that takes the copies issued past the last
+    // block (their slot is being transformed in place)
+    static constexpr size_t oDm = (size_t)DEPTH * SLOT;
+    static constexpr size_t bytes = oDm + (FUSED ? 1024 : 0);
+    static_assert(!FUSED || DEPTH >= 3, "the fused ring holds a block in use, one being formed and one loading");
     static_assert(DEPTH >= 2, "summary ring needs two slots");
     static_assert(KB_ % 2048 == 0 && VB_ % 2048 == 0, "whole 1 KB copies, two loaders each");
 };
@@ -198,14 +197,16 @@ __device__ __forceinline__ Tr<float>::frag scale_frag(Tr<float>::frag x, const f
 // squared) and A's tiles (key scale) in their final form: the pair of row
 // tiles (2 kb, 2 kb + 1) of G column tile t is, lane by lane, fragment (t, kb).
 // With several splits it writes fp32 partial tiles for the reduction.
-// FUSED (the whole operator; bf16): the keys arrive raw.  Once a block has
-// landed, the compute waves turn its rows into the unrotated features
+// FUSED (the whole operator; bf16): the keys arrive raw.  A three-stage ring:
+// while the compute waves multiply block i, each loader wave waits for its
+// own copies of block i + 1 -- the key rows 16 ld .. 16 ld + 15 and a share
+// of the values -- and turns those rows into the unrotated features
 // k~ = key_scale ReLU(gain o k / rms(k)) in place and their rotations
-// k^ = R k~ (3D RoPE) into a second area of the slot, 16 lanes per row (the
-// row's sum of squares reduced across them), and a second barrier hands the
-// features over.  G and A take k^; four more compute waves accumulate the
-// unrotated Gram matrix K~^T B K~ and K~^T beta for the normalizer.  The key
-// scale is then already in the features.
+// k^ = R k~ (3D RoPE) into a second area of the slot (Dk / 8 lanes per row,
+// the row's sum of squares reduced across them); the next barrier hands both
+// over.  G and A take k^; four more compute waves accumulate the unrotated
+// Gram matrix K~^T B K~ and K~^T beta for the normalizer.  The key scale is
+// then already in the features.
 constexpr int kSumCompute = 8, kSumLoaders = 4;
 template <bool FUSED> constexpr int sum_threads() { return (kSumCompute + (FUSED ? 4 : 0) + kSumLoaders) * 64; }
 
@@ -247,6 +248,125 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
     auto slot = [&](int i) { return smem + (size_t)(i % D) * L::SLOT; };
     constexpr int NCOMP = kSumCompute + (FUSED ? 4 : 0);
 
+    if (FUSED && w >= NCOMP) {
+        // ---------------- loader waves (FUSED) ----------------
+        const int ld = w - NCOMP;
+        constexpr int CK = L::NCK / 4, CV = L::NCV / 4;               // copies per loader and block
+        static_assert(L::NCK % 4 == 0 && L::NCV % 4 == 0, "whole copies per loader");
+        // block ii's copies by this loader (past the last block: the last
+        // block's again, into the dummy area, so that every iteration issues
+        // the same number of copies and the waits count right)
+        auto issue = [&](int ii) {
+            const int i = min(ii, nb - 1);
+            const bool dummy = ii >= nb;
+            const int t0 = t_lo + 64 * i, rmax = t_hi - 1 - t0;
+            const size_t row0 = (row_b + t0) * p.H + h;
+            unsigned char *sl = dummy ? smem + L::oDm : slot(i);
+            const size_t stepc = dummy ? 0 : 1024;
+            const char *kb_ = (const char *)(p.k + row0 * DK);
+            const unsigned krs = (unsigned)(p.H * DK * ESZ);
+#pragma unroll
+            for (int j = 0; j < CK; ++j) {
+                const int ci = ld * CK + j;
+                int r, c;
+                gm_src<RK>(ci, l, r, c);
+                __builtin_amdgcn_global_load_lds(
+                    (const void *)(kb_ + (unsigned)min(r, rmax) * krs + 16u * (unsigned)c),
+                    (__attribute__((address_space(3))) void *)(sl + (dummy ? 0 : L::oK) + stepc * ci), 16, 0, 0);
+            }
+            const char *vb_ = (const char *)(p.v + row0 * DV);
+            const unsigned vrs = (unsigned)(p.H * DV * ESZ);
+#pragma unroll
+            for (int j = 0; j < CV; ++j) {
+                const int ci = ld * CV + j;
+                int r, c;
+                gm_src<RV>(ci, l, r, c);
+                __builtin_amdgcn_global_load_lds(
+                    (const void *)(vb_ + (unsigned)min(r, rmax) * vrs + 16u * (unsigned)c),
+                    (__attribute__((address_space(3))) void *)(sl + (dummy ? 0 : L::oV) + stepc * ci), 16, 0, 0);
+            }
+            if (ld == 0) {
+                const char *bb = (const char *)(p.beta + row0);
+                __builtin_amdgcn_global_load_lds(
+                    (const void *)(bb + (unsigned)min(l, rmax) * (unsigned)(4 * p.H)),
+                    (__attribute__((address_space(3))) void *)(sl + (dummy ? 0 : L::oB)), 4, 0, 0);
+            }
+        };
+        // this loader's copies of the next block have landed once at most
+        // D - 2 younger blocks are in flight
+        auto wait_next = [&]() {
+            if (ld == 0) wait_vmcnt<(D - 2) * (CK + CV + 1)>();
+            else wait_vmcnt<(D - 2) * (CK + CV)>();
+        };
+        // this lane's channels 8 cc .. 8 cc + 7 (pairs 4 cc ..): gains,
+        // pair frequencies and axes
+        const int cc = l % RK;
+        float gk[8], fr[4];
+        int ax[4];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) gk[q] = p.gain_k[h * DK + 8 * cc + q];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            fr[d] = p.rope_freq[4 * cc + d];
+            ax[d] = p.rope_axis[4 * cc + d];
+        }
+        const float ct = (float)(p.t0 + f);
+        // rows 16 ld .. 16 ld + 15 of block i, 64 / RK rows per pass
+        auto transform = [&](int i) {
+            unsigned char *sl = slot(i);
+            E *sK = (E *)(sl + L::oK), *sKh = (E *)(sl + L::oKh);
+            const int tok0 = t_lo + 64 * i, rmax = t_hi - 1 - tok0;
+#pragma unroll
+            for (int r0 = 0; r0 < 16; r0 += 64 / RK) {
+                const int r = 16 * ld + r0 + l / RK;
+                E *src = sK + gm_at<E, RK>(r, 8 * cc);
+                const u32x4 raw = *(const u32x4 *)src;
+                float x[8];
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    x[2 * d] = __uint_as_float(raw[d] << 16);
+                    x[2 * d + 1] = __uint_as_float(raw[d] & 0xffff0000u);
+                }
+                float ss = 0.f;
+#pragma unroll
+                for (int q = 0; q < 8; ++q) ss += x[q] * x[q];
+#pragma unroll
+                for (int m = 1; m < RK; m <<= 1) ss += __shfl_xor(ss, m);
+                const float inv = rsqrtf(ss * (1.f / DK) + p.rms_eps);
+                // the token in this row (rows past the split repeat its last
+                // one) and its latent row and column
+                const int s_in = tok0 + min(r, rmax) - f * p.N;
+                const int yc = s_in / p.lat_w;
+                const float cy = (float)yc, cx = (float)(s_in - yc * p.lat_w);
+                u32x4 ft, fh;
+#pragma unroll
+                for (int d = 0; d < 4; ++d) {
+                    const float x0 = p.feat_scale * fmaxf(gk[2 * d] * x[2 * d] * inv, 0.f);
+                    const float x1 = p.feat_scale * fmaxf(gk[2 * d + 1] * x[2 * d + 1] * inv, 0.f);
+                    const float th = fr[d] * (ax[d] == 0 ? ct : ax[d] == 1 ? cy : cx);
+                    const float sn = __sinf(th), cs = __cosf(th);
+                    ft[d] = pack_bf16x2(x0, x1);
+                    fh[d] = pack_bf16x2(x0 * cs - x1 * sn, x0 * sn + x1 * cs);
+                }
+                *(u32x4 *)src = ft;
+                *(u32x4 *)(sKh + gm_at<E, RK>(r, 8 * cc)) = fh;
+            }
+        };
+#pragma unroll
+        for (int i = 0; i < D - 1; ++i) issue(i);
+        wait_next();
+        transform(0);
+        for (int i = 0; i < nb; ++i) {
+            lds_only_barrier();                  // block i (its features formed) handed over
+            issue(i + D - 1);                    // refills the slot of block i - 1
+            if (i + 1 < nb) {
+                wait_next();
+                transform(i + 1);
+            }
+        }
+        wait_vmcnt<0>();
+        return;
+    }
     if (w >= NCOMP) {
         // ---------------- loader waves ----------------
         // loaders 0, 1: halves of the key copies (0 also the betas); 2, 3:
@@ -254,18 +374,15 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
         // token (their beta is zeroed where it is used).  Every iteration
         // issues the same number of copies so that the waits below count
         // right: past the last block the last block is copied again, onto
-        // itself (unchanged bytes) or, FUSED, into a dummy area, since the
-        // compute waves rewrite that slot in place.
+        // itself (unchanged bytes).
         const int ld = w - NCOMP;
         const bool keys = ld < 2;
         auto issue = [&](int ii) {
             const int i = min(ii, nb - 1);
-            const bool dummy = FUSED && ii >= nb;
             const int t0 = t_lo + 64 * i, rmax = t_hi - 1 - t0;
             const size_t row0 = (row_b + t0) * p.H + h;
             unsigned char *sl = slot(i);
-            // destination of a copy to byte offset off of the slot
-#define GDN_SUM_DST(off) ((__attribute__((address_space(3))) void *)(dummy ? smem + L::oDm : sl + (off)))
+#define GDN_SUM_DST(off) ((__attribute__((address_space(3))) void *)(sl + (off)))
             if (keys) {
                 const char *base = (const char *)(p.k + row0 * DK);
                 const unsigned rstride = (unsigned)(p.H * DK * ESZ);
@@ -310,7 +427,6 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
             wait_oldest();
             lds_only_barrier();                  // block i handed to the compute waves
             issue(i + D - 1);                    // refills the slot of block i - 1
-            if constexpr (FUSED) lds_only_barrier();   // block i's features formed
         }
         wait_vmcnt<0>();
         return;
@@ -332,67 +448,6 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
     f32x4 accz[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
     const bool zw = NORM && (FUSED ? zgw : (!gw && w < 8)) && c0 == 0;
     const frag ones = ones_frag<E>();
-
-    // FUSED: the feature maps of one block, in place (k~) and into the
-    // rotated area (k^); RK lanes per row, lane l holding channels 8 (l % RK) ..
-    // (the head's key gains, pair frequencies and axes, staged once; the
-    // first barrier orders these writes before any transform)
-    if constexpr (FUSED) {
-        float *cst = (float *)(smem + L::oC);
-        for (int j = w * 64 + l; j < 2 * DK; j += NCOMP * 64)
-            cst[j] = j < DK ? p.gain_k[h * DK + j]
-                            : j < DK + DK / 2 ? p.rope_freq[j - DK] : (float)p.rope_axis[j - DK - DK / 2];
-    }
-    [[maybe_unused]] auto transform = [&](int i) {
-        if constexpr (FUSED) {
-            constexpr int RPP = NCOMP * 64 / RK;                      // rows per pass
-            const int cc = l % RK;                                    // this lane's 8 channels 8 cc ..
-            unsigned char *sl = slot(i);
-            E *sK = (E *)(sl + L::oK), *sKh = (E *)(sl + L::oKh);
-            const int tok0 = t_lo + 64 * i, rmax = t_hi - 1 - tok0;
-            const float *cst = (const float *)(smem + L::oC);
-#pragma unroll
-            for (int r0 = 0; r0 < 64; r0 += RPP) {
-                const int r = r0 + (w * 64 + l) / RK;
-                const int rr = min(r, 63);
-                E *src = sK + gm_at<E, RK>(rr, 8 * cc);
-                const u32x4 raw = *(const u32x4 *)src;
-                float x[8];
-#pragma unroll
-                for (int d = 0; d < 4; ++d) {
-                    x[2 * d] = __uint_as_float(raw[d] << 16);
-                    x[2 * d + 1] = __uint_as_float(raw[d] & 0xffff0000u);
-                }
-                float ss = 0.f;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) ss += x[q] * x[q];
-#pragma unroll
-                for (int m = 1; m < RK; m <<= 1) ss += __shfl_xor(ss, m);
-                const float inv = rsqrtf(ss * (1.f / DK) + p.rms_eps);
-                // the token in this row (rows past the split repeat its last one)
-                // and its coordinates (time, latent row, latent column)
-                const int s_in = tok0 + min(rr, rmax) - f * p.N;
-                const int yc = s_in / p.lat_w;
-                const float ct = (float)(p.t0 + f), cy = (float)yc, cx = (float)(s_in - yc * p.lat_w);
-#pragma unroll
-                for (int q = 0; q < 8; ++q) x[q] = p.feat_scale * fmaxf(cst[8 * cc + q] * x[q] * inv, 0.f);
-                u32x4 ft, fh;
-#pragma unroll
-                for (int d = 0; d < 4; ++d) {
-                    const int pr = 4 * cc + d;
-                    const float ax = cst[DK + DK / 2 + pr];
-                    const float th = cst[DK + pr] * (ax == 0.f ? ct : ax == 1.f ? cy : cx);
-                    const float sn = __sinf(th), cs = __cosf(th);
-                    ft[d] = pack_bf16x2(x[2 * d], x[2 * d + 1]);
-                    fh[d] = pack_bf16x2(x[2 * d] * cs - x[2 * d + 1] * sn, x[2 * d] * sn + x[2 * d + 1] * cs);
-                }
-                if (r < 64) {
-                    *(u32x4 *)src = ft;
-                    *(u32x4 *)(sKh + gm_at<E, RK>(rr, 8 * cc)) = fh;
-                }
-            }
-        }
-    };
 
     // the block loop, specialised for G waves (GB) and A waves, so that it has
     // no branch inside: all operand reads of a block (the K^T fragments
@@ -448,10 +503,8 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
         for (int i = 0; i < nb; ++i) {
             // the barrier also completes the previous block's reads, so the
             // loaders may refill that block's slot
-            lds_only_barrier();                  // block i has landed
+            lds_only_barrier();                  // block i has landed (FUSED: its features formed)
             if constexpr (FUSED) {
-                transform(i);
-                lds_only_barrier();              // its features are formed
                 // one operand set at a time: 16 waves leave 128 registers each
                 read(i, 0, o0);
                 mul(o0);
@@ -965,7 +1018,8 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
             const f32x4 g = TR::to_f32(gt[jo]);
             f32x4 y;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) y[q] = g[q] / (1.f + __expf(-g[q])) * (acc[q] * invd);
+            for (int q = 0; q < 4; ++q)
+                y[q] = g[q] * __builtin_amdgcn_rcpf(1.f + __expf(-g[q])) * (acc[q] * invd);
             TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(y));
         }
         // projection: out^T = W_o y^T, y^T as the B operand read back by rows

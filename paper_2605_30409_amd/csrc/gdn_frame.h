@@ -185,6 +185,21 @@ __device__ __forceinline__ Tr<float>::frag scale_frag(Tr<float>::frag x, const f
     return x;
 }
 
+// Sum over aligned groups of R lanes (R = 8 or 16), every lane of a group
+// receiving the group's sum, with DPP lane moves (no LDS traffic): swaps
+// within quads, then the mirror within 8 lanes, then within 16.
+template <int R> __device__ __forceinline__ float group_sum(float x) {
+    static_assert(R == 8 || R == 16, "group of 8 or 16 lanes");
+    auto dpp = [](float v, auto ctrl) {
+        return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), decltype(ctrl)::value, 0xf, 0xf, false));
+    };
+    x += dpp(x, std::integral_constant<int, 0xB1>{});                  // quad_perm [1, 0, 3, 2]
+    x += dpp(x, std::integral_constant<int, 0x4E>{});                  // quad_perm [2, 3, 0, 1]
+    x += dpp(x, std::integral_constant<int, 0x141>{});                 // row_half_mirror
+    if constexpr (R == 16) x += dpp(x, std::integral_constant<int, 0x140>{});   // row_mirror
+    return x;
+}
+
 // Phase A.  Workgroup (token split s, frame f, head): [G | A] over the split's
 // tokens (G = K^T B K with P32 rows and columns, A = K^T B V with P32 rows),
 // with 8 compute waves and 4 loader waves.  The loaders copy 64-token blocks
@@ -248,7 +263,7 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
     auto slot = [&](int i) { return smem + (size_t)(i % D) * L::SLOT; };
     constexpr int NCOMP = kSumCompute + (FUSED ? 4 : 0);
 
-    if (FUSED && w >= NCOMP) {
+    if constexpr (FUSED) if (w >= NCOMP) {
         // ---------------- loader waves (FUSED) ----------------
         const int ld = w - NCOMP;
         constexpr int CK = L::NCK / 4, CV = L::NCV / 4;               // copies per loader and block
@@ -311,16 +326,22 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
             ax[d] = p.rope_axis[4 * cc + d];
         }
         const float ct = (float)(p.t0 + f);
-        // rows 16 ld .. 16 ld + 15 of block i, 64 / RK rows per pass
+        // rows 16 ld .. 16 ld + 15 of block i, 64 / RK rows per pass; all of
+        // the wave's reads are issued before its first write
         auto transform = [&](int i) {
+            constexpr int NPASS = 16 * RK / 64;
             unsigned char *sl = slot(i);
             E *sK = (E *)(sl + L::oK), *sKh = (E *)(sl + L::oKh);
             const int tok0 = t_lo + 64 * i, rmax = t_hi - 1 - tok0;
+            u32x4 raws[NPASS];
 #pragma unroll
-            for (int r0 = 0; r0 < 16; r0 += 64 / RK) {
-                const int r = 16 * ld + r0 + l / RK;
+            for (int ps = 0; ps < NPASS; ++ps)
+                raws[ps] = *(const u32x4 *)(sK + gm_at<E, RK>(16 * ld + ps * (64 / RK) + l / RK, 8 * cc));
+#pragma unroll
+            for (int ps = 0; ps < NPASS; ++ps) {
+                const int r = 16 * ld + ps * (64 / RK) + l / RK;
                 E *src = sK + gm_at<E, RK>(r, 8 * cc);
-                const u32x4 raw = *(const u32x4 *)src;
+                const u32x4 raw = raws[ps];
                 float x[8];
 #pragma unroll
                 for (int d = 0; d < 4; ++d) {
@@ -330,8 +351,7 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
                 float ss = 0.f;
 #pragma unroll
                 for (int q = 0; q < 8; ++q) ss += x[q] * x[q];
-#pragma unroll
-                for (int m = 1; m < RK; m <<= 1) ss += __shfl_xor(ss, m);
+                ss = group_sum<RK>(ss);
                 const float inv = rsqrtf(ss * (1.f / DK) + p.rms_eps);
                 // the token in this row (rows past the split repeat its last
                 // one) and its latent row and column

@@ -225,13 +225,6 @@ template <int R> __device__ __forceinline__ float group_sum(float x) {
 constexpr int kSumCompute = 8, kSumLoaders = 4;
 template <bool FUSED> constexpr int sum_threads() { return (kSumCompute + (FUSED ? 4 : 0) + kSumLoaders) * 64; }
 
-// Coordinate of token (frame f, position s in the frame) along axis ax (0
-// time, 1 latent row, else latent column), for the 3D RoPE.
-template <class E>
-__device__ __forceinline__ float rope_coord(const FrameParams<E> &p, int ax, int f, int s) {
-    const int y = s / p.lat_w;
-    return (float)(ax == 0 ? p.t0 + f : ax == 1 ? y : s - y * p.lat_w);
-}
 
 template <class E, int DK, int DV, bool NORM, bool FUSED = false>
 __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel(FrameParams<E> p) {
@@ -316,14 +309,16 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
         // this lane's channels 8 cc .. 8 cc + 7 (pairs 4 cc ..): gains,
         // pair frequencies and axes
         const int cc = l % RK;
-        float gk[8], fr[4];
-        int ax[4];
+        float gk[8], wt[4], wy[4], wx[4];        // per pair: angle per unit of time, row, column
 #pragma unroll
         for (int q = 0; q < 8; ++q) gk[q] = p.gain_k[h * DK + 8 * cc + q];
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            fr[d] = p.rope_freq[4 * cc + d];
-            ax[d] = p.rope_axis[4 * cc + d];
+            const float fq = p.rope_freq[4 * cc + d];
+            const int a = p.rope_axis[4 * cc + d];
+            wt[d] = a == 0 ? fq : 0.f;
+            wy[d] = a == 1 ? fq : 0.f;
+            wx[d] = (a != 0 && a != 1) ? fq : 0.f;
         }
         const float ct = (float)(p.t0 + f);
         // rows 16 ld .. 16 ld + 15 of block i, 64 / RK rows per pass; all of
@@ -363,7 +358,7 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
                 for (int d = 0; d < 4; ++d) {
                     const float x0 = p.feat_scale * fmaxf(gk[2 * d] * x[2 * d] * inv, 0.f);
                     const float x1 = p.feat_scale * fmaxf(gk[2 * d + 1] * x[2 * d + 1] * inv, 0.f);
-                    const float th = fr[d] * (ax[d] == 0 ? ct : ax[d] == 1 ? cy : cx);
+                    const float th = wt[d] * ct + wy[d] * cy + wx[d] * cx;
                     const float sn = __sinf(th), cs = __cosf(th);
                     ft[d] = pack_bf16x2(x0, x1);
                     fh[d] = pack_bf16x2(x0 * cs - x1 * sn, x0 * sn + x1 * cs);
@@ -915,14 +910,17 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
 //   y = SiLU(gate) o numerator / (z . q~ + eps), staged in LDS as bf16;
 //   out^T = W_o y^T with W_o staged in LDS as operand fragments, then the
 //   result tile goes back through LDS for whole-row stores.
-constexpr int kFusedOutWaves = 8;
+constexpr int kFusedOutWaves = 16;
 
 template <int DK, int DV> struct FusedOutLds {
     static constexpr int NJ = DV / 16 + 1;
     static constexpr int LDO = DV + 8;                          // staged row stride (bf16)
     static constexpr size_t oW = (size_t)2 * DK * 16 * NJ;      // after H_f: W_o fragments
-    static constexpr size_t oP = oW + (size_t)2 * DV * DV;      // gain_q[DK], freq[DK/2], axis[DK/2] (float)
-    static constexpr size_t oO = oP + (size_t)4 * 2 * DK;       // one 16-row staging tile per wave
+    // gain_q[DK], then per channel pair the angle per unit of time, latent
+    // row and latent column (the pair's frequency on its axis, zero on the
+    // other two)
+    static constexpr size_t oP = oW + (size_t)2 * DV * DV;
+    static constexpr size_t oO = oP + (size_t)4 * (DK + 3 * (DK / 2));   // one 16-row staging tile per wave
     static constexpr size_t bytes = oO + (size_t)2 * kFusedOutWaves * 16 * LDO;
 };
 
@@ -947,8 +945,7 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
     // W_o[h][16 jo + l % 16][32 kb + 8 (l / 16) ..], and the prologue constants
     {
         constexpr int HV = NJ * 16 * DK * 2 / 16, HIT = (HV + NTH - 1) / NTH;
-        constexpr int WV = DV * DV * 2 / 16, WIT = WV / NTH;
-        static_assert(WV % NTH == 0, "whole W_o staging passes");
+        constexpr int WV = DV * DV * 2 / 16, WIT = (WV + NTH - 1) / NTH;
         const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
         u32x4 hv[HIT], wv[WIT];
 #pragma unroll
@@ -956,18 +953,24 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
             if (HV % NTH == 0 || tid + NTH * it < HV) hv[it] = src[tid + NTH * it];
 #pragma unroll
         for (int it = 0; it < WIT; ++it) {
-            const int j = tid + NTH * it, fr = j >> 6, ll = j & 63, jo = fr / KBV, kb = fr - jo * KBV;
+            const int j = min(tid + NTH * it, WV - 1), fr = j >> 6, ll = j & 63, jo = fr / KBV, kb = fr - jo * KBV;
             wv[it] = *(const u32x4 *)(p.w_o + ((size_t)h * DV + 16 * jo + (ll & 15)) * DV + 32 * kb + 8 * (ll >> 4));
         }
         float *cp = (float *)(smem + LO::oP);
-        for (int j = tid; j < 2 * DK; j += NTH)
-            cp[j] = j < DK ? p.gain_q[h * DK + j]
-                           : j < DK + DK / 2 ? p.rope_freq[j - DK] : (float)p.rope_axis[j - DK - DK / 2];
+        for (int j = tid; j < DK + 3 * (DK / 2); j += NTH) {
+            if (j < DK) {
+                cp[j] = p.gain_q[h * DK + j];
+            } else {
+                const int pr = (j - DK) / 3, axis = (j - DK) - 3 * pr, a = p.rope_axis[pr];
+                cp[j] = (a == axis || (axis == 2 && a != 0 && a != 1)) ? p.rope_freq[pr] : 0.f;
+            }
+        }
 #pragma unroll
         for (int it = 0; it < HIT; ++it)
             if (HV % NTH == 0 || tid + NTH * it < HV) ((u32x4 *)smem)[tid + NTH * it] = hv[it];
 #pragma unroll
-        for (int it = 0; it < WIT; ++it) ((u32x4 *)(smem + LO::oW))[tid + NTH * it] = wv[it];
+        for (int it = 0; it < WIT; ++it)
+            if (WV % NTH == 0 || tid + NTH * it < WV) ((u32x4 *)(smem + LO::oW))[tid + NTH * it] = wv[it];
     }
 
     const size_t T = (size_t)p.F * p.N;
@@ -985,7 +988,7 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
     };
     const E *sH = (const E *)smem + l * 8;
     const E *sW = (const E *)(smem + LO::oW) + l * 8;
-    const float *cgain = (const float *)(smem + LO::oP), *cfreq = cgain + DK, *caxis = cfreq + DK / 2;
+    const float *cgain = (const float *)(smem + LO::oP), *cang = cgain + DK;
     E *sO = (E *)(smem + LO::oO) + w * 16 * LO::LDO;
     constexpr int VE = 8, RV = DV / VE;                        // bf16 per 16 bytes, vectors per row
     auto compute = [&](int tile, const frag (&qf)[KB], const u32x2 (&gt)[NV]) {
@@ -1003,7 +1006,10 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
         ss += __shfl_xor(ss, 16);
         ss += __shfl_xor(ss, 32);
         const float inv = rsqrtf(ss * (1.f / DK) + p.rms_eps);
+        // token li's time, latent row and latent column
         const int n = min(16 * tile + li, p.N - 1);
+        const int yc = n / p.lat_w;
+        const float ct = (float)(p.t0 + f), cy = (float)yc, cx = (float)(n - yc * p.lat_w);
         frag qt[KB], qh[KB];
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
@@ -1013,8 +1019,8 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
             for (int q = 0; q < 8; ++q) xt[q] = fmaxf(cgain[ch + q] * x[kb][q] * inv, 0.f);
 #pragma unroll
             for (int d = 0; d < 4; ++d) {
-                const int pr = ch / 2 + d;
-                const float th = cfreq[pr] * rope_coord(p, (int)caxis[pr], f, n);
+                const float *ang = cang + 3 * (ch / 2 + d);
+                const float th = ang[0] * ct + ang[1] * cy + ang[2] * cx;
                 const float sn = __sinf(th), cs = __cosf(th);
                 xh[2 * d] = xt[2 * d] * cs - xt[2 * d + 1] * sn;
                 xh[2 * d + 1] = xt[2 * d] * sn + xt[2 * d + 1] * cs;

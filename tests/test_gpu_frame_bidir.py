@@ -186,3 +186,12 @@ def test_three_frame_call_bidirectional_full(gdn, normalized):
 def test_cfg_batch_bidirectional_sampled_heads(gdn):
     inp = make(3, 3, 3520, False, seed=29950)
     check(gdn, inp, False, "bf16 B4 F3 N3520 H20 D64 heads 0,7,19", heads=(0, 7, 19))
+
+
+@pytest.mark.parametrize("normalized", [False, True])
+def test_many_frames_bidirectional(gdn, normalized):
+    """40 frames of 16 tokens: the backward sweep and its histories over many
+    frames, odd and even sweep lengths in the scan's two-set prefetch."""
+    for F in (40, 41):
+        inp = make(1, F, 16, normalized, B=1, H=2, dtype="bf16", seed=29980 + F + normalized)
+        check(gdn, inp, normalized, f"{'norm ' if normalized else ''}bf16 F{F} N16")

@@ -176,3 +176,11 @@ def test_fused_short_splits_deterministic(gdn, N, splits):
     for _ in range(3):
         again = run_gpu(gdn, inp, token_splits=splits)
         assert all(torch.equal(a, b) for a, b in zip(first, again))
+
+
+@pytest.mark.parametrize("bidirectional", [False, True])
+def test_many_frames_fused(gdn, bidirectional):
+    """33 frames of 30 tokens on a 6-wide latent grid, time coordinate from 100."""
+    inp = gdn_inputs.make_fused_inputs(1, 33, frame_tokens=30, H=2, lat_w=6, t0=100,
+                                       seed=39990 + bidirectional)
+    check(gdn, inp, f"{'bidir ' if bidirectional else ''}F33 N30", bidirectional)

@@ -163,3 +163,8 @@ def test_three_frame_call_normalized_full(gdn):
 def test_cfg_batch_normalized_sampled_heads(gdn):
     inp = relu_inputs(3, 3, 3520, seed=19950)
     check(gdn, inp, "bf16 B4 F3 N3520 H20 D64 heads 0,7,19", heads=(0, 7, 19))
+
+
+def test_many_frames_normalized(gdn):
+    inp = relu_inputs(1, 37, 20, H=2, seed=19990)
+    check(gdn, inp, "bf16 F37 N20")

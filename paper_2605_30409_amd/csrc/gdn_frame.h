@@ -16,9 +16,10 @@
 // correction G_f H_{f-1} goes through the MFMAs.)
 //
 // Kernels, E = bf16 bits or fp32 storage, fp32 accumulation everywhere:
-//   gdn_frame_summary_kernel  (token split s, half c, frame f, head): the
-//       half c = 0 accumulates G, c = 1 accumulates A, over the split's
-//       tokens (64-token blocks staged in LDS); writes fp32 partial tiles.
+//   gdn_frame_summary_kernel  (token split s, frame f, head): G and A over the
+//       split's tokens, 64-token blocks streamed through an LDS ring by loader
+//       waves; the final G fragments and A tiles with a single split, else
+//       fp32 partial tiles.
 //   gdn_frame_reduce_kernel   sums the NS splits' partials and applies the
 //       key scale: G as ready-made MFMA operand fragments (E), A as fp32
 //       accumulator tiles.
@@ -26,8 +27,13 @@
 //       every frame in turn, written as the output kernel's operand
 //       fragments (E), and the terminal state; in the bidirectional form a
 //       backward sweep first, whose histories are added to the H_f written.
-//   gdn_frame_output_kernel   64 * NTW tokens of one frame per workgroup:
-//       O^T = H_f^T Q^T.
+//   gdn_frame_output_kernel   a run of 16-token tiles of one frame per
+//       workgroup: O^T = H_f^T Q^T.
+// The normalizer (NORM variants) rides along as one more 16-column state
+// tile.  The fused operator (FUSED variants, bf16) forms the key features in
+// the summary kernel, carries the normalizer on its own Gram matrix of the
+// unrotated keys, and ends in gdn_frame_output_fused_kernel (query features,
+// gate and per-head projection).
 //
 // Tile layouts (see gdn_device.h for the lane conventions).  Accumulator
 // tiles over the Dk rows are in P32 order: row tile r = 2 m + a holds rows
@@ -105,7 +111,9 @@ __device__ __forceinline__ void xcd_unit(int id, int per_unit, int &unit, int &s
 }
 
 // LDS ring of the summary kernel: DEPTH slots, each one 64-token block of
-// raw keys, raw values and the block's 64 betas.  A 64-row tile with R
+// raw keys, raw values and the block's 64 betas (FUSED: the raw keys become
+// the unrotated features in place, and a second key area takes the rotated
+// ones).  A 64-row tile with R
 // 16-byte chunks per row is stored in groups of four rows: chunk c of row r
 // sits at chunk position 4 R (r / 4) + 16 (c / 4) + 4 (r % 4) + c % 4.  A 1 KB
 // copy then reads contiguous runs of at least 256 bytes (4 rows of 16 chunks,
@@ -131,6 +139,9 @@ template <class E, int DK, int DV, bool FUSED = false> struct FrameSumLds {
     static constexpr size_t oDm = (size_t)DEPTH * SLOT;
     static constexpr size_t bytes = oDm + (FUSED ? 1024 : 0);
     static_assert(!FUSED || DEPTH >= 3, "the fused ring holds a block in use, one being formed and one loading");
+    // fused loaders wait for their own copies (a quarter of the key and value
+    // copies, loader 0 also the betas) with DEPTH - 2 younger blocks in flight
+    static_assert(!FUSED || (DEPTH - 2) * (NCK / 4 + NCV / 4 + 1) <= 63, "fused waits within vmcnt");
     static_assert(DEPTH >= 2, "summary ring needs two slots");
     static_assert(KB_ % 2048 == 0 && VB_ % 2048 == 0, "whole 1 KB copies, two loaders each");
 };
@@ -224,7 +235,6 @@ template <int R> __device__ __forceinline__ float group_sum(float x) {
 // then already in the features.
 constexpr int kSumCompute = 8, kSumLoaders = 4;
 template <bool FUSED> constexpr int sum_threads() { return (kSumCompute + (FUSED ? 4 : 0) + kSumLoaders) * 64; }
-
 
 template <class E, int DK, int DV, bool NORM, bool FUSED = false>
 __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel(FrameParams<E> p) {

@@ -115,7 +115,7 @@ def cpu_baseline(inp, B, T, min_seconds=10.0):
     import oracle
     threads = host_threads()
     reps, elapsed = 0, 0.0
-    while elapsed < min_seconds and reps < 50:
+    while elapsed < min_seconds and reps < 1000:
         t0 = time.perf_counter()
         oracle.gdn_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
                            inp["state_in"], nthreads=threads)
@@ -219,7 +219,7 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=Fal
     threads = host_threads()
     reps, elapsed = 0, 0.0
     if fused:
-        while elapsed < min_seconds and reps < 50:
+        while elapsed < min_seconds and reps < 1000:
             t0 = time.perf_counter()
             oracle.gdn_frame_forward_fused(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], inp["gate"],
                                            inp["w_o"], inp["state_in"], inp["z_in"],
@@ -235,7 +235,7 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=Fal
     extra = dict(normalized=True, z_in=inp["z_in"]) if norm else {}
     if bidir:
         extra["bidirectional"] = True
-    while elapsed < min_seconds and reps < 50:
+    while elapsed < min_seconds and reps < 1000:
         t0 = time.perf_counter()
         oracle.gdn_frame_forward(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"],
                                  inp["state_in"], frame_tokens=inp["frame_tokens"], nthreads=threads,

@@ -112,6 +112,19 @@ def test_validation_errors(fn):
         assert call(fn, ws=BASE + 512 * MB + 16, ws_bytes=1 << 30) == -4   # misaligned
 
 
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    """No fallback: without the built library every entry point raises."""
+    from paper_2605_30409_amd import gdn as binding
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "libgdn.so"))
+    with pytest.raises(ImportError):
+        binding.lib()
+    with pytest.raises(ImportError):
+        binding.gdn_status_string(0)
+    with pytest.raises(ImportError):
+        binding.gdn_workspace_bytes(1, 2, 64, 64, 64)
+
+
 def test_binding_rejects_bad_tensors_on_cpu():
     import torch
     q = torch.zeros(1, 64, 2, 64)

@@ -367,7 +367,8 @@ int gdn_frame_profile_stages_bidir(const void *q, const void *k, const void *v,
  * and the RoPE arrays are required.  Outputs may not overlap any input;
  * state_in == state_out and z_in == z_out are allowed.  The bf16 path rounds
  * the features, the gated readout and the products' operands to bf16 (fp32
- * accumulation); the sines and cosines are the GPU's fast ones.
+ * accumulation); the sines and cosines are the GPU's hardware ones, on angles
+ * reduced to one turn.
  * gdn_frame_forward_fused uses the library-cached workspace,
  * gdn_frame_forward_fused_ex a caller-owned one of gdn_frame_workspace_bytes
  * (is_bf16 = 1) and an explicit token-split count; gdn_frame_profile_stages_fused

@@ -49,6 +49,13 @@
 
 namespace gdn {
 
+// Rotation angles are formed in turns (the pair's frequency / 2 pi times the
+// token's coordinate on its axis) and reduced to [-1/2, 1/2] before the
+// hardware sine and cosine, whose input is in turns and whose accuracy holds
+// only over a bounded range; so long time coordinates stay accurate up to the
+// fp32 rounding of the angle itself.
+constexpr float kInvTwoPi = 0.15915494309189535f;
+
 template <class E> struct FrameParams {
     const E *q, *k, *v;          // [B][T][H][Dk] / [Dv], T = F * N
     const float *alpha;          // [B][F][H]
@@ -319,12 +326,12 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
         // this lane's channels 8 cc .. 8 cc + 7 (pairs 4 cc ..): gains,
         // pair frequencies and axes
         const int cc = l % RK;
-        float gk[8], wt[4], wy[4], wx[4];        // per pair: angle per unit of time, row, column
+        float gk[8], wt[4], wy[4], wx[4];        // per pair: turns per unit of time, row, column
 #pragma unroll
         for (int q = 0; q < 8; ++q) gk[q] = p.gain_k[h * DK + 8 * cc + q];
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
-            const float fq = p.rope_freq[4 * cc + d];
+            const float fq = p.rope_freq[4 * cc + d] * kInvTwoPi;   // turns per unit
             const int a = p.rope_axis[4 * cc + d];
             wt[d] = a == 0 ? fq : 0.f;
             wy[d] = a == 1 ? fq : 0.f;
@@ -368,8 +375,9 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
                 for (int d = 0; d < 4; ++d) {
                     const float x0 = p.feat_scale * fmaxf(gk[2 * d] * x[2 * d] * inv, 0.f);
                     const float x1 = p.feat_scale * fmaxf(gk[2 * d + 1] * x[2 * d + 1] * inv, 0.f);
-                    const float th = wt[d] * ct + wy[d] * cy + wx[d] * cx;
-                    const float sn = __sinf(th), cs = __cosf(th);
+                    float rv = wt[d] * ct + wy[d] * cy + wx[d] * cx;
+                    rv -= rintf(rv);
+                    const float sn = __builtin_amdgcn_sinf(rv), cs = __builtin_amdgcn_cosf(rv);
                     ft[d] = pack_bf16x2(x0, x1);
                     fh[d] = pack_bf16x2(x0 * cs - x1 * sn, x0 * sn + x1 * cs);
                 }
@@ -926,9 +934,9 @@ template <int DK, int DV> struct FusedOutLds {
     static constexpr int NJ = DV / 16 + 1;
     static constexpr int LDO = DV + 8;                          // staged row stride (bf16)
     static constexpr size_t oW = (size_t)2 * DK * 16 * NJ;      // after H_f: W_o fragments
-    // gain_q[DK], then per channel pair the angle per unit of time, latent
-    // row and latent column (the pair's frequency on its axis, zero on the
-    // other two)
+    // gain_q[DK], then per channel pair the turns per unit of time, latent
+    // row and latent column (the pair's frequency / 2 pi on its axis, zero on
+    // the other two)
     static constexpr size_t oP = oW + (size_t)2 * DV * DV;
     static constexpr size_t oO = oP + (size_t)4 * (DK + 3 * (DK / 2));   // one 16-row staging tile per wave
     static constexpr size_t bytes = oO + (size_t)2 * kFusedOutWaves * 16 * LDO;
@@ -972,7 +980,7 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
                 cp[j] = p.gain_q[h * DK + j];
             } else {
                 const int pr = (j - DK) / 3, axis = (j - DK) - 3 * pr, a = p.rope_axis[pr];
-                cp[j] = (a == axis || (axis == 2 && a != 0 && a != 1)) ? p.rope_freq[pr] : 0.f;
+                cp[j] = (a == axis || (axis == 2 && a != 0 && a != 1)) ? p.rope_freq[pr] * kInvTwoPi : 0.f;
             }
         }
 #pragma unroll
@@ -1030,8 +1038,9 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
 #pragma unroll
             for (int d = 0; d < 4; ++d) {
                 const float *ang = cang + 3 * (ch / 2 + d);
-                const float th = ang[0] * ct + ang[1] * cy + ang[2] * cx;
-                const float sn = __sinf(th), cs = __cosf(th);
+                float rv = ang[0] * ct + ang[1] * cy + ang[2] * cx;
+                rv -= rintf(rv);
+                const float sn = __builtin_amdgcn_sinf(rv), cs = __builtin_amdgcn_cosf(rv);
                 xh[2 * d] = xt[2 * d] * cs - xt[2 * d + 1] * sn;
                 xh[2 * d + 1] = xt[2 * d] * sn + xt[2 * d + 1] * cs;
             }

@@ -184,3 +184,12 @@ def test_many_frames_fused(gdn, bidirectional):
     inp = gdn_inputs.make_fused_inputs(1, 33, frame_tokens=30, H=2, lat_w=6, t0=100,
                                        seed=39990 + bidirectional)
     check(gdn, inp, f"{'bidir ' if bidirectional else ''}F33 N30", bidirectional)
+
+
+@pytest.mark.parametrize("t0", [5000, 20000])
+def test_long_time_coordinate_fused(gdn, t0):
+    """Time coordinates whose angles run to thousands of turns (the first time
+    pair turns once per 2 pi frames): the kernels reduce each angle to one turn
+    before the hardware sine and cosine."""
+    inp = gdn_inputs.make_fused_inputs(1, 3, frame_tokens=100, H=2, lat_w=10, t0=t0, seed=39700 + t0 % 97)
+    check(gdn, inp, f"t0={t0} F3 N100")

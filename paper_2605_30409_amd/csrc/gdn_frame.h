@@ -880,12 +880,15 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
     };
     auto compute = [&](int tile, const frag (&qf)[KB]) {
         if constexpr (NORM) {
-            // the denominator of token li first; its division overlaps the
-            // other products
+            // every numerator product first, then the denominator of token li:
+            // no product waits for the division
+            f32x4 acc[NV];
+#pragma unroll
+            for (int jo = 0; jo < NV; ++jo) acc[jo] = tile_product(jo, qf);
             const float inv = 1.f / (tile_product(NV, qf)[0] + p.eps);
 #pragma unroll
             for (int jo = 0; jo < NV; ++jo)
-                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(tile_product(jo, qf) * inv));
+                TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(acc[jo] * inv));
         } else {
 #pragma unroll
             for (int jo = 0; jo < NV; ++jo)

@@ -931,7 +931,7 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
 //   y = SiLU(gate) o numerator / (z . q~ + eps), staged in LDS as bf16;
 //   out^T = W_o y^T with W_o staged in LDS as operand fragments, then the
 //   result tile goes back through LDS for whole-row stores.
-constexpr int kFusedOutWaves = 16;
+constexpr int kFusedOutWaves = 12;
 
 template <int DK, int DV> struct FusedOutLds {
     static constexpr int NJ = DV / 16 + 1;

@@ -575,7 +575,8 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
                                    dim3(gdn::kFusedOutWaves * 64), LF::bytes, s, p);
             else
                 hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV, NORM>),
-                                   dim3(gdn::xcd_blocks(units, p.OB)), dim3(256), LO::bytes, s, p);
+                                   dim3(gdn::xcd_blocks(units, p.OB)), dim3(LO::WAVES * 64), LO::bytes,
+                                   s, p);
         }
     };
     hipError_t er = hipSuccess;

@@ -809,7 +809,7 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
 }
 
 // Phase C.  Workgroup blk of a (frame, head) unit takes the 16-token tiles
-// [TPW blk, TPW (blk + 1)) of the frame, wave w every fourth of them from w.
+// [TPW blk, TPW (blk + 1)) of the frame, wave w every WAVES-th of them from w.
 // H_f's fragments are staged in LDS once per workgroup: lane (li, lg) of
 // fragment (jo, kb) holds H_f[32 kb + 8 lg + q'][16 jo + li], the A operand of
 // row 16 jo + li of H_f^T.  With the query rows as B operand the product tile
@@ -821,15 +821,20 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
 // formed first and every output element is divided by it plus eps.
 constexpr int kFrameOutWgs = 1024;                 // output workgroups to aim for
 
+// waves per output workgroup, one staging tile each (measured best: 4 for the
+// numerator-only readout, 6 with the normalizer's extra product tile)
+template <bool NORM> constexpr int frame_out_waves() { return NORM ? 6 : 4; }
+
 template <class E, int DK, int DV, bool NORM> struct FrameOutLds {
+    static constexpr int WAVES = frame_out_waves<NORM>();
     static constexpr int NJ = DV / 16 + NORM;
     static constexpr int LDO = DV + 16 / (int)sizeof(E);       // staged output row stride
     static constexpr size_t oO = sizeof(E) * DK * 16 * NJ;     // after H_f: one 16-row tile per wave
-    static constexpr size_t bytes = oO + sizeof(E) * 4 * 16 * LDO;
+    static constexpr size_t bytes = oO + sizeof(E) * WAVES * 16 * LDO;
 };
 
 template <class E, int DK, int DV, bool NORM>
-__global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p) {
+__global__ __launch_bounds__(64 * frame_out_waves<NORM>()) void gdn_frame_output_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
     using frag = typename TR::frag;
     using LO = FrameOutLds<E, DK, DV, NORM>;
@@ -846,15 +851,15 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
 
     // H_f into LDS, every load of a thread in flight at once
     {
-        constexpr int HIT = (HV + 255) / 256;
+        constexpr int NTH = 64 * LO::WAVES, HIT = (HV + NTH - 1) / NTH;
         const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
         u32x4 hv[HIT];
 #pragma unroll
         for (int it = 0; it < HIT; ++it)
-            if (HV % 256 == 0 || tid + 256 * it < HV) hv[it] = src[tid + 256 * it];
+            if (HV % NTH == 0 || tid + NTH * it < HV) hv[it] = src[tid + NTH * it];
 #pragma unroll
         for (int it = 0; it < HIT; ++it)
-            if (HV % 256 == 0 || tid + 256 * it < HV) ((u32x4 *)smem)[tid + 256 * it] = hv[it];
+            if (HV % NTH == 0 || tid + NTH * it < HV) ((u32x4 *)smem)[tid + NTH * it] = hv[it];
     }
 
     const size_t T = (size_t)p.F * p.N;
@@ -910,12 +915,13 @@ __global__ __launch_bounds__(256) void gdn_frame_output_kernel(FrameParams<E> p)
     const int i0 = tile_lo + w;
     load_q(clampi(i0), qa);
     lds_barrier();
-    for (int i = i0; i < tile_hi; i += 8) {
-        load_q(clampi(i + 4), qb);
+    constexpr int SW = LO::WAVES;
+    for (int i = i0; i < tile_hi; i += 2 * SW) {
+        load_q(clampi(i + SW), qb);
         compute(i, qa);
-        if (i + 4 >= tile_hi) break;
-        load_q(clampi(i + 8), qa);
-        compute(i + 4, qb);
+        if (i + SW >= tile_hi) break;
+        load_q(clampi(i + 2 * SW), qa);
+        compute(i + SW, qb);
     }
 }
 

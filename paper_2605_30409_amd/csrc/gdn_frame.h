@@ -819,7 +819,7 @@ __global__ __launch_bounds__(64) void gdn_frame_scan_kernel(FrameParams<E> p) {
 // NORM: every column of the extra column tile of H_f holds z, so every lane
 // (li, lg) of its product holds the denominator z . q of token li; it is
 // formed first and every output element is divided by it plus eps.
-constexpr int kFrameOutWgs = 1024;                 // output workgroups to aim for
+constexpr int kFrameOutWgs = 768;                  // output workgroups to aim for (3 per CU; swept)
 
 // waves per output workgroup, one staging tile each (measured best: 4 for the
 // numerator-only readout, 6 with the normalizer's extra product tile)

@@ -42,64 +42,61 @@ import gdn_inputs  # noqa: E402
 METRIC = "GDN fwd tokens/sec and TFLOP/s at T=3520,H=16,D=128 bf16; % of MFMA peak"
 WORKLOAD = 1                 # one 1280x704 frame
 PEAK_BF16_TFLOPS = 2516.6    # MI355X dense bf16 MFMA
+PEAK_F32_TFLOPS = 157.3      # MI355X fp32 matrix
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E
 # stage name (as the library reports stages) -> kernel
 KERNELS = {"wy": "gdn_wy_kernel", "group_transfer": "gdn_chunkscan_kernel<SCAN_TRANS>",
            "group_scan": "gdn_groupscan_kernel", "chunk_states": "gdn_chunkscan_kernel<SCAN_STATES>",
            "output": "gdn_output_kernel"}
-KERNEL_FUSED = "gdn_chunkscan_kernel<SCAN_STATES, output fused>"
+KERNELS_FUSED = dict(KERNELS, chunk_states="gdn_chunkscan_kernel<SCAN_STATES, output fused>")
+EXTRA_WORKLOADS = (0, 2, 3, 4)
 
 
-def algorithmic_counts(B, T, H, Dk, Dv, G, C=64, esz=2, fused=None):
-    """Per-stage algorithmic flops and bytes (each stage's own inputs and outputs,
-    workspace included, every byte once), and the path's external I/O bytes.
+def path_counts(B, T, H, Dk, Dv, C=64, esz=2):
+    """The path's algorithmic work and I/O (the chunked method's own contractions,
+    causal and strict triangles counted once; every input read once, every output
+    written once, the state in and out):
+        F_alg = 6 Dk Dv + (C-1)(2Dk+Dv) + (C+1)(Dk+Dv) + C^2/3   flop per token-head
+        bytes = (2Dk+Dv) s + 8 + Dv s                            per token-head
+                + 2 B H Dk Dv 4                                  per call (fp32 state)
+    with s the q/k/v/out element size.  Workspace traffic is not algorithmic."""
+    n = B * T * H
+    flops = n * (6.0 * Dk * Dv + (C - 1) * (2 * Dk + Dv) + (C + 1) * (Dk + Dv) + C * C / 3.0)
+    io = n * ((2 * Dk + Dv) * esz + 8 + Dv * esz) + 2 * B * H * Dk * Dv * 4
+    return flops, io
 
-    `fused` (default: bf16 with a single scan group, the library's own rule) moves
-    the output into the chunk-state scan: the WY kernel then also forms the
-    decay-scaled queries and the masked decayed Q K^T tile of each chunk, and the
-    scan reads those and writes `out` instead of the chunk states."""
-    n = B * T * H                       # token-heads
+
+def workspace_traffic(B, T, H, Dk, Dv, G, C=64, esz=2):
+    """Workspace bytes each stage writes and reads (every byte once).  With one
+    scan group on the bf16 path the output is fused into the scan: the WY kernel
+    then also writes the decay-scaled queries and the masked decayed Q K^T tile
+    of every chunk (row fragments the scan's output waves read) and the scan
+    writes no per-chunk state."""
     NC = -(-T // C)
     NG = -(-NC // G)
-    if fused is None:
-        fused = esz == 2 and NG == 1
-    nch = B * H * NC                    # chunks (the ragged tail counts as a whole chunk)
-    ngr = B * H * NG if NG > 1 else 0   # scan groups (none with a single group)
-    st = B * H * Dk * Dv * 4            # one fp32 state per (b, h)
-    wy_fac = nch * (C * (2 * Dk + Dv) * esz + 8)       # -W, Kt, Ut and the chunk decay
-    wy_out = wy_fac + nch * C * 8                      # ... and the fp64 prefix g
-    qp = nch * C * (Dk + C) * esz if fused else 0      # scaled Q and masked P tiles
-    qk_f = n * (C + 1) * Dk                            # causal Q K^T
-    out_f = n * (2.0 * Dk * Dv + (C + 1) * Dv)         # Q H and P U
-    f = {"wy": n * ((C - 1) * (2 * Dk + Dv) + C * C / 3.0) + (qk_f if fused else 0),
-         "group_transfer": nch * C * 4.0 * Dk * (Dk + Dv) if ngr else 0.0,
-         "group_scan": ngr * (2.0 * Dk * Dk * Dv + 2.0 * Dk * Dv),
-         "chunk_states": nch * C * 4.0 * Dk * Dv + (out_f if fused else 0),
-         "output": 0.0 if fused else out_f + qk_f}
-    b = {"wy": n * ((Dk + Dv + (Dk if fused else 0)) * esz + 8) + wy_out + qp,
-         "group_transfer": (wy_fac + ngr * (Dk * Dk * esz + Dv * Dk * 4 + 8)) if ngr else 0,
-         "group_scan": (ngr * (Dk * Dk * esz + 2 * Dv * Dk * 4 + 8) + 2 * st) if ngr else 0,
-         "chunk_states": wy_fac + (ngr * Dv * Dk * 4 if ngr else 2 * st)
-                         + (qp + n * Dv * esz if fused else nch * Dv * (Dk + C) * esz),
-         "output": 0 if fused else
-                   n * (2 * Dk + Dv) * esz + nch * (C * 8 + Dv * (Dk + C) * esz)}
-    io_bytes = n * ((2 * Dk + Dv) * esz + 8 + Dv * esz) + 2 * st
-    return dict(flops=f, bytes=b, io_bytes=io_bytes, groups=NG, group_size=G, fused=fused)
+    nch = B * H * NC
+    fused = esz == 2 and NG == 1
+    ngr = B * H * NG if NG > 1 else 0
+    gates = nch * (C * 8 + 8)
+    fac = nch * C * (2 * Dk + Dv) * esz                    # -W, Kt, U~t
+    qp = nch * C * (Dk + C) * esz if fused else 0          # scaled Q, masked P
+    grp = ngr * (Dk * Dk * esz + Dv * Dk * 4 + 8)          # N, Psi^T, log Gamma
+    hg = ngr * Dv * Dk * 4                                 # group entry states
+    hs_us = 0 if fused else nch * Dv * (Dk + C) * esz      # per-chunk state and pseudo-values
+    zero = {"written": 0, "read": 0}
+    return {"wy": {"written": gates + fac + qp, "read": 0},
+            "group_transfer": {"written": grp, "read": fac + nch * 8} if ngr else zero,
+            "group_scan": {"written": hg, "read": grp} if ngr else zero,
+            "chunk_states": {"written": hs_us, "read": fac + nch * 8 + hg + qp},
+            "output": zero if fused else {"written": 0, "read": hs_us + nch * C * 8}}
 
 
-def binding_roof(flops, nbytes, ms):
-    """The roof (MFMA or HBM) whose lower bound on the duration is larger, and the
-    achieved rate against it."""
-    t_mfma = flops / (PEAK_BF16_TFLOPS * 1e12)
-    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
-    sec = ms / 1e3
-    if t_mfma >= t_hbm:
-        a = flops / sec / 1e12
-        return {"bound": "mfma", "achieved": round(a, 2), "peak": PEAK_BF16_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(a / PEAK_BF16_TFLOPS, 4)}
-    a = nbytes / sec / 1e9
-    return {"bound": "hbm", "achieved": round(a, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-            "frac": round(a / PEAK_HBM_GBS, 4)}
+def pct(xs, p):
+    return float(np.percentile(np.asarray(xs, dtype=np.float64), p))
+
+
+def stats(xs):
+    return {"median": round(pct(xs, 50), 5), "p10": round(pct(xs, 10), 5), "p90": round(pct(xs, 90), 5)}
 
 
 def host_threads():
@@ -108,6 +105,16 @@ def host_threads():
     except AttributeError:
         n = os.cpu_count() or 1
     return max(1, min(n, 16))
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def cpu_baseline(inp, B, T, min_seconds=10.0):
@@ -122,13 +129,14 @@ def cpu_baseline(inp, B, T, min_seconds=10.0):
         elapsed += time.perf_counter() - t0
         reps += 1
     return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H=16, D=128), "
                       f"fp64 token recurrence, {elapsed:.1f} s"}
 
 
-def load_traffic(stage, summary="traffic_frame1280x704.json"):
-    """HBM traffic per launch of `stage`'s kernel from the committed counter summary,
-    or None when the summary is missing or was taken on different kernel source."""
+def load_traffic(summary):
+    """Per-stage HBM bytes per launch from a committed counter summary, or None when
+    the summary is missing or was taken on different kernel source."""
     path = os.path.join(ROOT, "profiles", summary)
     if not os.path.exists(path):
         return None
@@ -140,10 +148,102 @@ def load_traffic(stage, summary="traffic_frame1280x704.json"):
             h.update(open(os.path.join(ROOT, f), "rb").read())
         if h.hexdigest() != rec["source_sha256"]:
             return None
-        k = rec["stages"].get(stage)
-        return None if k is None else float(k["hbm_bytes_per_launch"])
+        return {k: float(v["hbm_bytes_per_launch"]) for k, v in rec["stages"].items()}
     except Exception:
         return None
+
+
+def token_roofline(flops, io, names, kernels, traffic, peak_tflops):
+    """Roofline of the dominant kernel, per the path's algorithmic I/O: the call's
+    bytes (or flops) over that kernel's launch duration.  The path's intensity is
+    below the ridge (~315 flop/B), so its bound is HBM."""
+    dom = max(names, key=names.get)
+    sec = names[dom] / 1e3
+    bound_hbm = flops / io < peak_tflops * 1e12 / (PEAK_HBM_GBS * 1e9)
+    a_gbs = io / sec / 1e9
+    a_tf = flops / sec / 1e12
+    r = {"bound": "hbm", "achieved": round(a_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+         "frac": round(a_gbs / PEAK_HBM_GBS, 4)} if bound_hbm else \
+        {"bound": "mfma", "achieved": round(a_tf, 2), "peak": peak_tflops, "unit": "TFLOP/s",
+         "frac": round(a_tf / peak_tflops, 4)}
+    call_traffic = None if traffic is None else sum(traffic.get(k, 0.0) for k in names if names[k] > 0)
+    r.update({"traffic": None if call_traffic is None else round(call_traffic),
+              "traffic_scope": "whole call (sum over the call's kernels), FETCH_SIZE and WRITE_SIZE "
+                               "scaled by a plain copy kernel",
+              "traffic_over_algorithmic": None if call_traffic is None else round(call_traffic / io, 3),
+              "traffic_dominant_kernel": None if traffic is None or dom not in traffic else round(traffic[dom]),
+              "kernel": kernels.get(dom, dom), "duration_ms": round(names[dom], 5),
+              "algorithmic_bytes_per_launch": io, "algorithmic_flops_per_launch": flops,
+              "mfma_frac_dominant": round(a_tf / peak_tflops, 4)})
+    return r
+
+
+def time_steps(step, stream, steps, warmup, torch):
+    """`warmup` untimed steps, then `steps` steps with an event before each and one
+    after the last, all on `stream`, between two synchronizations.  Returns the
+    mean (first to last event / steps) and the per-step durations in ms."""
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record(stream)
+    for i in range(steps):
+        step()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return ev[0].elapsed_time(ev[steps]) / steps, per
+
+
+def run_extra_workload(idx, gdn, torch, dev, stream, reps):
+    """GPU time per call on workload `idx` (device-drawn inputs of its shapes and
+    value distributions; workload 2 is the 20-call streaming chain with the state
+    threaded on the device, timed as a whole and divided by 20)."""
+    w = gdn_inputs.WORKLOADS[idx]
+    esz = 2 if w.dtype == "bf16" else 4
+    calls = [gdn_inputs.make_device_inputs(idx, dev, call=c) for c in range(w.calls)]
+    B, T, H, Dk, Dv = w.B, w.T, w.H, w.Dk, w.Dv
+    out = torch.empty((B, T, H, Dv), dtype=calls[0]["q"].dtype, device=dev)
+    st = [torch.zeros((B, H, Dk, Dv), dtype=torch.float32, device=dev) for _ in range(2)]
+    if calls[0]["state_in"] is not None:
+        st[0].copy_(calls[0]["state_in"])
+    ws = gdn.workspace(calls[0]["q"], calls[0]["v"])
+    fwd = gdn.gdn_chunk_forward_ws if w.dtype == "bf16" else gdn.gdn_chunk_forward_f32_ws
+
+    def chain():
+        for c, inp in enumerate(calls):
+            si = st[c & 1] if (c > 0 or calls[0]["state_in"] is not None) else None
+            fwd(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], si, out, st[(c + 1) & 1], ws,
+                stream=stream)
+
+    _, per = time_steps(chain, stream, reps, 2, torch)
+    per_call = [x / w.calls for x in per]
+    inp = calls[0]
+    stage = gdn.gdn_profile_stages(inp["q"], inp["k"], inp["v"], inp["alpha"], inp["beta"], inp["state_in"],
+                                   out, st[1], ws, reps=max(3, reps // 2), stream=stream)
+    torch.cuda.synchronize()
+    names = {k: v for k, v in zip(gdn.STAGE_NAMES, stage) if v > 0}
+    G = gdn.gdn_scan_group_size(B, H, T, Dk, Dv, is_bf16=esz == 2)
+    fused = esz == 2 and -(-(-(-T // 64)) // G) == 1
+    flops, io = path_counts(B, T, H, Dk, Dv, esz=esz)
+    wst = workspace_traffic(B, T, H, Dk, Dv, G, esz=esz)
+    ws_bytes = sum(v["written"] + v["read"] for v in wst.values())
+    med = pct(per_call, 50) / 1e3
+    peak = PEAK_BF16_TFLOPS if esz == 2 else PEAK_F32_TFLOPS
+    dom = max(names, key=names.get)
+    rec = {"workload": w.name, "calls": w.calls, "ms_per_call": stats(per_call),
+           "tokens_per_s": round(B * T / med, 1), "tflops": round(flops / med / 1e12, 3),
+           "mfma_frac": round(flops / med / 1e12 / peak, 5), "peak_tflops": peak,
+           "hbm_frac_io": round(io / med / 1e9 / PEAK_HBM_GBS, 4),
+           "algorithmic_bytes": io, "algorithmic_flops": flops,
+           "scan_group": G, "output_fused": fused,
+           "stage_ms": {k: round(v, 5) for k, v in names.items()},
+           "dominant_kernel": (KERNELS_FUSED if fused else KERNELS).get(dom, dom),
+           "workspace_bytes": ws_bytes,
+           "workspace_gbs": round(ws_bytes / med / 1e9, 1)}
+    del calls, out, st, ws
+    torch.cuda.empty_cache()
+    return rec
 
 
 FRAME_METRIC = ("frame-wise GDN fwd tokens/sec and TFLOP/s at F=3 frames x N=3520 tokens, "
@@ -161,56 +261,50 @@ FRAME_KERNELS = {"summaries": "gdn_frame_summary_kernel", "reduce": "gdn_frame_r
 
 
 def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=False, fused=False):
-    """Per-stage algorithmic flops and bytes of the frame-wise path (each stage's own
-    inputs and outputs, workspace included, every byte once) and its external I/O.
+    """Algorithmic flops per stage and the call's I/O bytes for the frame-wise path,
+    plus each stage's workspace bytes (reported apart: not algorithmic).
 
-    summaries: G = K^T B K and A = K^T B V over every token (fp32 partial tiles per
-    token split); reduce: the splits' partials -> G (operand fragments) and A;
-    scan: H_f = alpha (H - G H) + A per frame; output: O = Q H_f per token.
-    norm: the normalizer z rides along as one more 16-column state tile (its
-    flops and workspace bytes are counted as the kernels move them: the extra
-    tile, of which one column is z; the token reads and output writes do not
-    grow), plus z in and out and one division per output element.
-    bidir: the scan also runs the backward recurrence over the F - 1 later
-    frames (their G and A read once more), writes every frame's fp32 history
-    and reads it back to add it to H_f.
-    fused (implies norm): the summaries also form the unrotated-key Gram
-    matrix for the normalizer (its partials, reduction and fragments counted
-    like G's, and the scan reads it); the output reads the gate beside the
-    queries and multiplies by W_o (read once per head).  The feature maps,
-    the division and the gate are elementwise work, not counted as flops."""
+    flops: summaries G = K^T B K and A = K^T B V over every token (plus b = K^T beta
+    for the normalizer, and the unrotated-key Gram matrix of the fused operator);
+    scan H_f = alpha (H - G H) + A per frame (z as one more column with the
+    normalizer; the backward scan over the F - 1 later frames when bidirectional);
+    output O = Q H_f per token (d = Q z with the normalizer; W_o in the fused
+    operator).  The token-split reduction adds no algorithmic flops.
+    I/O bytes: q, k, v, out (and the fused operator's gate and W_o), alpha, beta,
+    the state (and z) in and out."""
     if fused:
         norm = True
-    Ds = Dv + 16 if norm else Dv        # state columns the kernels carry
+    Dz = 1 if norm else 0               # normalizer columns that are work
+    Ds = Dv + (16 if norm else 0)       # state columns the kernels carry
     n = B * F * N * H                   # token-heads
     u = B * H * F                       # (frame, head) units
     st = B * H * Dk * Dv * 4 + (B * H * Dk * 4 if norm else 0)
-    part = u * NS * Dk * (Dk + Ds) * 4
-    f = {"summaries": 2.0 * n * Dk * (Dk + Ds),
-         "reduce": float(u * NS * Dk * (Dk + Ds)),
-         "scan": u * (2.0 * Dk * Dk * Ds + 3.0 * Dk * Ds),
-         "output": 2.0 * n * Dk * Ds + (n * Dv if norm else 0)}
-    b = {"summaries": n * ((Dk + Dv) * esz + 4) + part,
-         "reduce": part + u * (Dk * Dk * esz + Dk * Ds * 4),
-         "scan": u * (Dk * Dk * esz + Dk * Ds * 4 + 4 + Dk * Ds * esz) + 2 * st,
-         "output": n * (Dk + Dv) * esz + u * Dk * Ds * esz}
+    part = u * NS * Dk * (Dk + Ds) * 4 if NS > 1 else 0
+    f = {"summaries": 2.0 * n * Dk * (Dk + Dv + Dz),
+         "reduce": 0.0,
+         "scan": u * (2.0 * Dk * Dk * (Dv + Dz) + 3.0 * Dk * (Dv + Dz)),
+         "output": 2.0 * n * Dk * (Dv + Dz) + (n * Dv if norm else 0)}
+    ws = {"summaries": {"written": part if NS > 1 else u * (Dk * Dk * esz + Dk * Ds * 4), "read": 0},
+          "reduce": {"written": u * (Dk * Dk * esz + Dk * Ds * 4) if NS > 1 else 0, "read": part},
+          "scan": {"written": u * Dk * Ds * esz, "read": u * (Dk * Dk * esz + Dk * Ds * 4)},
+          "output": {"written": 0, "read": u * Dk * Ds * esz}}
     if fused:
-        gpart = u * NS * Dk * Dk * 4
+        gpart = u * NS * Dk * Dk * 4 if NS > 1 else 0
         f["summaries"] += 2.0 * n * Dk * Dk
-        f["reduce"] += float(u * NS * Dk * Dk)
-        b["summaries"] += gpart
-        b["reduce"] += gpart + u * Dk * Dk * esz
-        b["scan"] += u * Dk * Dk * esz
+        ws["summaries"]["written"] += gpart if NS > 1 else u * Dk * Dk * esz
+        ws["reduce"]["read"] += gpart
+        ws["reduce"]["written"] += u * Dk * Dk * esz if NS > 1 else 0
+        ws["scan"]["read"] += u * Dk * Dk * esz
         f["output"] += 2.0 * n * Dv * Dv
-        b["output"] += n * Dv * esz + H * Dv * Dv * esz
     if bidir:
         ub = B * H * (F - 1)
-        f["scan"] += ub * (2.0 * Dk * Dk * Ds + 3.0 * Dk * Ds) + u * Dk * Ds
-        b["scan"] += ub * (Dk * Dk * esz + Dk * Ds * 4 + 4) + 2 * u * Dk * Ds * 4
+        f["scan"] += ub * (2.0 * Dk * Dk * (Dv + Dz) + 3.0 * Dk * (Dv + Dz)) + u * Dk * (Dv + Dz)
+        ws["scan"]["written"] += u * Dk * Ds * 4
+        ws["scan"]["read"] += u * Dk * Ds * 4
     io_bytes = n * ((2 * Dk + 2 * Dv) * esz + 4) + u * 4 + 2 * st
     if fused:
         io_bytes += n * Dv * esz + H * Dv * Dv * esz
-    return dict(flops=f, bytes=b, io_bytes=io_bytes)
+    return dict(flops=f, io_bytes=io_bytes, workspace=ws)
 
 
 def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=False, fused=False):
@@ -230,6 +324,7 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=Fal
             elapsed += time.perf_counter() - t0
             reps += 1
         return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+                "cpu_model": cpu_model(),
                 "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H={H}, D={Dk}), "
                           f"fp64 fused operator{' (bidirectional)' if bidir else ''}, {elapsed:.1f} s"}
     extra = dict(normalized=True, z_in=inp["z_in"]) if norm else {}
@@ -243,6 +338,7 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=Fal
         elapsed += time.perf_counter() - t0
         reps += 1
     return {"value": B * T * reps / elapsed, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": f"{reps} whole calls of the timed workload (B={B}, T={T}, H={H}, D={Dk}), "
                       f"fp64 {'bidirectional ' if bidir else ''}frame-wise recurrence, {elapsed:.1f} s"}
 
@@ -286,7 +382,7 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
             gdn.gdn_frame_forward_ex(q, k, v, alpha, beta, s_in, out, s_out, ws, N, token_splits=ts,
                                      stream=stream)
 
-    ms_per_step, cold_ms = timed(step, stream)
+    ms_per_step, per_step, cold = timed(step, stream)
     if fused:
         stage_ms = gdn.gdn_frame_profile_stages_fused(q, k, v, fz["gate"], fz["w_o"], alpha, beta, fz["gain_q"],
                                                       fz["gain_k"], fz["rope_freq"], fz["rope_axis"], s_in, z_in, out,
@@ -303,25 +399,23 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
     else:
         stage_ms = gdn.gdn_frame_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws, N,
                                                 token_splits=ts, reps=args.steps, stream=stream)
-    names = dict(zip(gdn.FRAME_STAGE_NAMES, stage_ms))
+    names = {k_: v_ for k_, v_ in zip(gdn.FRAME_STAGE_NAMES, stage_ms) if v_ > 0}
     torch.cuda.synchronize()
     cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm, bidir=bidir, fused=fused)
+    flops = sum(cnt["flops"].values())
     sec = ms_per_step / 1e3
-    tflops = sum(cnt["flops"].values()) / sec / 1e12
-    dom = max(names, key=names.get)
-    roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
-    # the bidirectional form shares every kernel but the scan with the
-    # unidirectional one, so their counter summaries serve it too
+    tflops = flops / sec / 1e12
+    # counter summaries: the bidirectional form shares every kernel but the scan
+    # with the unidirectional one
+    summary = ("traffic_frames3x1280x704_fused.json" if fused else
+               "traffic_frames3x1280x704_norm.json" if norm else "traffic_frames3x1280x704.json")
+    traffic = load_traffic(summary)
+    if traffic is not None and bidir:
+        traffic = None
+    kernels = dict(FRAME_KERNELS)
     if fused:
-        traffic = None if dom == "scan" and bidir else load_traffic(dom, "traffic_frames3x1280x704_fused.json")
-    else:
-        traffic = None if (bidir and dom == "scan") else load_traffic(
-            dom, "traffic_frames3x1280x704_norm.json" if norm else "traffic_frames3x1280x704.json")
-    roofline.update({"traffic": traffic,
-                     "kernel": FRAME_KERNELS[dom], "duration_ms": round(names[dom], 5),
-                     "algorithmic_flops_per_launch": cnt["flops"][dom],
-                     "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
-    stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_) for k_, v_ in names.items()}
+        kernels.update({"summaries": "gdn_frame_summary_fused_kernel", "output": "gdn_frame_output_fused_kernel"})
+    roofline = token_roofline(flops, cnt["io_bytes"], names, kernels, traffic, PEAK_BF16_TFLOPS)
     rec = {
         "metric": FRAME_FUSED_METRIC + (" (bidirectional)" if bidir else "") if fused
                   else (FRAME_BIDIR_NORM_METRIC if norm else FRAME_BIDIR_METRIC) if bidir
@@ -351,9 +445,10 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
         "tflops": round(tflops, 2),
         "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
         "hbm_frac_io": round(cnt["io_bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
-        "ms_per_step_cold": None if cold_ms is None else round(cold_ms, 5),
+        "step_ms": stats(per_step),
+        "ms_per_step_cold": None if cold is None else stats(cold),
         "stage_ms": {k_: round(v_, 5) for k_, v_ in names.items()},
-        "stage_roofline": {k_: (v_["bound"], v_["frac"]) for k_, v_ in stage_roofs.items()},
+        "workspace_bytes": cnt["workspace"],
         "roofline": roofline,
     }
     if not args.no_cpu_baseline:
@@ -367,6 +462,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="token path: skip the per-call timing of the other four workloads")
     ap.add_argument("--cold-steps", type=int, default=20,
                     help="extra steps each preceded by a 1 GiB write that evicts the caches")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -409,22 +506,14 @@ def main():
         del src, dst
 
     def timed(step, stream):
-        """Warmup, then `steps` timed steps between two events on `stream`, then
-        cold-cache steps (each after a 1 GiB write that evicts L2 and MALL)."""
-        for _ in range(args.warmup):
-            step()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            step()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
+        """Warmup, then `steps` timed steps (an event before each and after the last,
+        on `stream`), then cold-cache steps (each after a 1 GiB write that evicts L2
+        and the MALL).  Returns (mean ms per step, per-step ms, cold per-step ms)."""
+        ms, per = time_steps(step, stream, args.steps, args.warmup, torch)
         cold = None
         if args.cold_steps > 0:
             scratch = torch.empty(1 << 28, dtype=torch.float32, device=dev)
-            times = []
+            cold = []
             for i in range(args.cold_steps):
                 scratch.fill_(float(i))
                 a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -432,10 +521,9 @@ def main():
                 step()
                 b.record(stream)
                 torch.cuda.synchronize()
-                times.append(a.elapsed_time(b))
-            cold = float(np.median(times))
+                cold.append(a.elapsed_time(b))
             del scratch
-        return ms, cold
+        return ms, per, cold
 
     if args.path.startswith("frame"):
         run_frame(args, torch, gdn, dev, to_dev, timed, norm=args.path.endswith("-norm"),
@@ -456,27 +544,23 @@ def main():
     def step():
         gdn.gdn_chunk_forward_ws(q, k, v, alpha, beta, s_in, out, s_out, ws, chunk=C, stream=stream)
 
-    ms_per_step, cold_ms = timed(step, stream)
+    ms_per_step, per_step, cold = timed(step, stream)
 
     # Per-stage durations: HIP events recorded by the library on the same stream.
     stage_ms = gdn.gdn_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws,
                                       reps=args.steps, chunk=C, stream=stream)
-    names = dict(zip(gdn.STAGE_NAMES, stage_ms))
+    names = {k_: v_ for k_, v_ in zip(gdn.STAGE_NAMES, stage_ms) if v_ > 0}
     torch.cuda.synchronize()
 
     G = gdn.gdn_scan_group_size(B, H, T, Dk, Dv, C)
-    cnt = algorithmic_counts(B, T, H, Dk, Dv, G, C)
+    NG = -(-(-(-T // C)) // G)
+    fused = NG == 1
+    flops, io = path_counts(B, T, H, Dk, Dv, C)
     sec = ms_per_step / 1e3
-    tflops = sum(cnt["flops"].values()) / sec / 1e12
-    dom = max(names, key=names.get)
-    roofline = binding_roof(cnt["flops"][dom], cnt["bytes"][dom], names[dom])
-    kname = KERNEL_FUSED if (dom == "chunk_states" and cnt["fused"]) else KERNELS[dom]
-    roofline.update({"traffic": load_traffic(dom), "kernel": kname,
-                     "duration_ms": round(names[dom], 5),
-                     "algorithmic_flops_per_launch": cnt["flops"][dom],
-                     "algorithmic_bytes_per_launch": cnt["bytes"][dom]})
-    stage_roofs = {k_: binding_roof(cnt["flops"][k_], cnt["bytes"][k_], v_)
-                   for k_, v_ in names.items() if v_ > 0 and (cnt["flops"][k_] or cnt["bytes"][k_])}
+    tflops = flops / sec / 1e12
+    traffic = load_traffic("traffic_frame1280x704.json")
+    roofline = token_roofline(flops, io, names, KERNELS_FUSED if fused else KERNELS, traffic,
+                              PEAK_BF16_TFLOPS)
 
     rec = {
         "metric": METRIC,
@@ -494,15 +578,21 @@ def main():
         "config": {"workload": "one 1280x704 latent frame: B=1 T=3520 (44x80) H=16 Dk=Dv=128 "
                                "chunk=64, bf16 q/k/v, fp32 state in/out",
                    "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C,
-                   "scan_group": G, "scan_groups": cnt["groups"], "output_fused": cnt["fused"]},
+                   "scan_group": G, "scan_groups": NG, "output_fused": fused},
+        "step_ms": stats(per_step),
         "tflops": round(tflops, 2),
         "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
-        "hbm_frac_io": round(cnt["io_bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
-        "ms_per_step_cold": None if cold_ms is None else round(cold_ms, 5),
+        "hbm_frac_io": round(io / sec / 1e9 / PEAK_HBM_GBS, 4),
+        "ms_per_step_cold": None if cold is None else stats(cold),
         "stage_ms": {k_: round(v_, 5) for k_, v_ in names.items()},
-        "stage_roofline": {k_: (v_["bound"], v_["frac"]) for k_, v_ in stage_roofs.items()},
+        "workspace_bytes": workspace_traffic(B, T, H, Dk, Dv, G, C),
         "roofline": roofline,
     }
+    if not args.no_workloads:
+        extra = {}
+        for idx in EXTRA_WORKLOADS:
+            extra[str(idx)] = run_extra_workload(idx, gdn, torch, dev, stream, reps=10 if idx == 4 else 20)
+        rec["workloads"] = extra
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(inp, B, T)
     print(json.dumps(rec), flush=True)

@@ -260,3 +260,48 @@ def make_fused_inputs(workload, frames, *, frame_tokens=None, B=None, H=None, Dk
     return dict(q=bf(q), k=bf(k), v=bf(v), gate=bf(gate), w_o=bf(w_o), alpha=alpha, beta=beta,
                 state_in=state_in, z_in=z_in, gain_q=gain_q, gain_k=gain_k, rope_freq=freq, rope_axis=axis,
                 lat_w=int(lat_w), t0=int(t0), frame_tokens=N, dtype="bf16")
+
+
+def make_device_inputs(workload, device, call=0, *, seed=None):
+    """Draw one call's inputs for ``workload`` directly in device memory, with
+    the value distributions and draw order of make_inputs but torch's seeded
+    generator on the device (fast enough for the largest workloads, whose host
+    draws take tens of seconds).  The values differ from make_inputs'; they
+    serve timing, never parity.  Returns a dict of torch tensors (q, k, v in
+    bf16 or fp32; alpha, beta, state_in in fp32; state_in None for a zero
+    state) plus "dtype"."""
+    import torch
+
+    w = WORKLOADS[workload] if isinstance(workload, int) else workload
+    idx = WORKLOADS.index(w) if w in WORKLOADS else 99
+    gen = torch.Generator(device=device)
+    gen.manual_seed(900000 + 1000 * idx + call if seed is None else seed)
+    B, T, H, Dk, Dv = w.B, w.T, w.H, w.Dk, w.Dv
+
+    def randn(*shape):
+        return torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
+
+    def unit_rows(x):
+        return x / torch.sqrt(torch.sum(x * x, dim=-1, keepdim=True))
+
+    q = unit_rows(randn(B, T, H, Dk))
+    k = unit_rows(randn(B, T, H, Dk))
+    v = randn(B, T, H, Dv)
+    if w.alpha.startswith("softplus"):
+        mu = float(w.alpha[len("softplus"):])
+        alpha = torch.exp(-torch.nn.functional.softplus(randn(B, T, H) + mu))
+    elif w.alpha == "uniform0.5":
+        alpha = 0.5 + 0.5 * torch.rand((B, T, H), generator=gen, device=device)
+    else:
+        raise ValueError(w.alpha)
+    if w.beta == "sigmoid":
+        beta = torch.sigmoid(randn(B, T, H))
+    elif w.beta == "uniform":
+        beta = torch.rand((B, T, H), generator=gen, device=device)
+    else:
+        raise ValueError(w.beta)
+    state_in = 0.02 * randn(B, H, Dk, Dv) if w.state == "normal0.02" else None
+    if w.dtype == "bf16":
+        q, k, v = q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+    return dict(q=q.contiguous(), k=k.contiguous(), v=v.contiguous(), alpha=alpha.contiguous(),
+                beta=beta.contiguous(), state_in=state_in, dtype=w.dtype)

@@ -119,7 +119,8 @@ int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v,
 /*
  * Scan-group control.  scan_group = chunks per scan group: 0 picks the
  * library's choice (one group when T is at most 64 chunks or when
- * B*H*Dv/16 >= 512, else about sqrt(chunks)), a value >= the number of
+ * B*H*Dv/16 >= 64 on the bf16 path, >= 512 on the fp32 path; else about
+ * sqrt(chunks)), a value >= the number of
  * chunks gives a single sequential scan, and any value in between is used as
  * given (negative counts as 0).  The two calls
  * below take it explicitly: gdn_workspace_bytes_ex sizes the workspace for
@@ -130,9 +131,9 @@ int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v,
 size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
                               int scan_group);
 
-/* Chunks per scan group the calls above use for this shape and scan_group
- * (0 for unsupported arguments). */
-int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int scan_group);
+/* Chunks per scan group the calls above use for this shape, path (is_bf16)
+ * and scan_group (0 for unsupported arguments). */
+int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group);
 
 int gdn_chunk_forward_ex(const void *q, const void *k, const void *v,
                          const float *alpha, const float *beta, const float *state_in,

@@ -23,19 +23,22 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 int num_chunks(int T) { return (T + kChunk - 1) / kChunk; }
 
-// Chunks per scan group.  A single group (one sequential scan per (b, h),
-// spread over Dv/16 workgroups) when the sequence is short or when the
-// (b, h) streams alone fill the chip; otherwise about sqrt(NC) chunks per
-// group, which balances the group-parallel passes (two passes over G chunks)
-// against the sequential scan over NC / G groups.
-int auto_group(int NC, long long BH, int Dv) {
-    if (NC <= 64 || BH * (Dv / 16) >= 512) return NC;
+// Chunks per scan group.  bf16: a single group (one sequential scan per
+// (b, h) with the output fused into it) whenever the (b, h) streams give at
+// least 64 column-tile workgroups -- measured faster than any grouped scan on
+// the 3-frame, batched and 12-frame workloads -- or the sequence has at most 64
+// chunks.  fp32, and bf16 with fewer streams: a single group when the sequence
+// is short or when the streams alone fill the chip; otherwise about sqrt(NC)
+// chunks per group, which balances the group-parallel passes (two passes over
+// G chunks) against the sequential scan over NC / G groups.
+int auto_group(int NC, long long BH, int Dv, bool bf16) {
+    if (NC <= 64 || BH * (Dv / 16) >= (bf16 ? 64 : 512)) return NC;
     int G = (int)(__builtin_sqrt((double)NC) + 0.5);
     return G < 2 ? 2 : G;
 }
 
-int resolve_group(int NC, long long BH, int Dv, int group) {
-    if (group <= 0) group = auto_group(NC, BH, Dv);
+int resolve_group(int NC, long long BH, int Dv, int group, bool bf16) {
+    if (group <= 0) group = auto_group(NC, BH, Dv, bf16);
     return group > NC ? NC : group;
 }
 
@@ -149,6 +152,16 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
     return p;
 }
 
+// Launch one kernel whose only argument is a parameter struct; returns the
+// launch's own status (the thread's pending HIP error is neither read nor
+// cleared, so an error the caller left pending is not reported as this call's).
+template <class P>
+hipError_t launch(const void *fn, dim3 grid, dim3 block, size_t lds, hipStream_t s, const P &p) {
+    P copy = p;
+    void *args[] = {&copy};
+    return hipLaunchKernel(fn, grid, block, args, lds, s);
+}
+
 // The scan kernel with the output fused (bf16 only; nullptr for fp32).
 template <class E, int DK, int DV> const void *fused_scan_fn() {
     if constexpr (sizeof(E) == 2)
@@ -202,40 +215,32 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
     const unsigned BH = (unsigned)(p.B * p.H);
     // workgroup counts: column blocks x 8 x ceil(units / 8) (see the XCD placement)
     auto groups = [](unsigned nblocks, unsigned units) { return nblocks * 8u * ((units + 7u) / 8u); };
-    auto stage = [&](int i) {
+    auto stage = [&](int i) -> hipError_t {
         switch (i) {
         case 0:
-            hipLaunchKernelGGL((gdn::gdn_wy_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(64 * gdn::kWyWaves), lds1,
-                               s, p);
-            break;
+            return launch((const void *)gdn::gdn_wy_kernel<E, DK, DV>, dim3(p.NC, BH), dim3(64 * gdn::kWyWaves),
+                          lds1, s, p);
         case 1:
-            hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT, NCW>),
-                               dim3(groups((DK + DV) / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads),
-                               LT::bytes, s, p);
-            break;
+            return launch((const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_TRANS, CT, NCW>,
+                          dim3(groups((DK + DV) / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads), LT::bytes, s,
+                          p);
         case 2:
-            hipLaunchKernelGGL((gdn::gdn_groupscan_kernel<E, DK, DV>), dim3(groups(DV / 16, BH)),
-                               dim3(DK), 0, s, p);
-            break;
+            return launch((const void *)gdn::gdn_groupscan_kernel<E, DK, DV>, dim3(groups(DV / 16, BH)), dim3(DK),
+                          0, s, p);
         case 3:
-            if (p.NG > 1) {
-                hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT, NCW>),
-                                   dim3(groups(DV / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads),
-                                   LT::bytes, s, p);
-            } else if (p.fused) {
-                // one sequential scan per (b, h), one column tile per workgroup,
-                // which also computes the output of its columns
-                if constexpr (sizeof(E) == 2)
-                    hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1, true>),
-                                       dim3(groups(DV / 16, BH)), dim3(scan_threadsF), LF::bytes, s, p);
-            } else {
-                // one sequential scan per (b, h): one column tile per compute wave
-                hipLaunchKernelGGL((gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1>),
-                                   dim3(groups(DV / 16, BH)), dim3(scan_threads1), L1::bytes, s, p);
-            }
-            break;
+            if (p.NG > 1)
+                return launch((const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, CT, NCW>,
+                              dim3(groups(DV / (16 * CT * NCW), BH * p.NG)), dim3(scan_threads), LT::bytes, s, p);
+            // one sequential scan per (b, h), one column tile per workgroup,
+            // which also computes the output of its columns (bf16)
+            if (p.fused)
+                return launch(fused_scan_fn<E, DK, DV>(), dim3(groups(DV / 16, BH)), dim3(scan_threadsF), LF::bytes,
+                              s, p);
+            // one sequential scan per (b, h): one column tile per compute wave
+            return launch((const void *)gdn::gdn_chunkscan_kernel<E, DK, DV, gdn::SCAN_STATES, 1, 1>,
+                          dim3(groups(DV / 16, BH)), dim3(scan_threads1), L1::bytes, s, p);
         default:
-            hipLaunchKernelGGL((gdn::gdn_output_kernel<E, DK, DV>), dim3(p.NC, BH), dim3(256), lds3, s, p);
+            return launch((const void *)gdn::gdn_output_kernel<E, DK, DV>, dim3(p.NC, BH), dim3(256), lds3, s, p);
         }
     };
     hipError_t er = hipSuccess;
@@ -244,15 +249,14 @@ hipError_t launch_path(const gdn::Params<E> &p, hipStream_t s, StageTiming *tm) 
         if (tm) tm->ran[i] = runs;
         if (!runs) continue;
         if (!tm) {
-            stage(i);
+            er = stage(i);
             continue;
         }
         er = hipEventRecord(tm->ev[2 * i], s);
-        for (int r = 0; r < tm->reps && er == hipSuccess; ++r) stage(i);
+        for (int r = 0; r < tm->reps && er == hipSuccess; ++r) er = stage(i);
         if (er == hipSuccess) er = hipEventRecord(tm->ev[2 * i + 1], s);
     }
-    const hipError_t le = hipGetLastError();
-    return le != hipSuccess ? le : er;
+    return er;
 }
 
 template <class E>
@@ -269,7 +273,7 @@ int run(const void *q, const void *k, const void *v, const float *alpha, const f
     const size_t esz = bf16 ? 2 : 4;
     int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
     if (st != GDN_OK) return st;
-    const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, group);
+    const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, group, bf16);
     if (!ws || ((uintptr_t)ws & 255u) || ws_bytes < ws_layout(B, H, T, Dk, Dv, esz, G).total)
         return GDN_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
@@ -316,7 +320,7 @@ int run_cached(const void *q, const void *k, const void *v, const float *alpha, 
     int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, esz);
     if (st != GDN_OK) return st;
     const size_t need =
-        ws_layout(B, H, T, Dk, Dv, esz, resolve_group(num_chunks(T), (long long)B * H, Dv, 0)).total;
+        ws_layout(B, H, T, Dk, Dv, esz, resolve_group(num_chunks(T), (long long)B * H, Dv, 0, bf16)).total;
     void *ws = nullptr;
     st = cached_workspace(need, &ws);
     if (st != GDN_OK) return st;
@@ -553,44 +557,40 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
     constexpr int NJ = DV / 16 + NORM;
     // reduction items per unit (FUSED: also the unrotated-key G fragments)
     constexpr int NI = (DK / 16) * (DK / 32) * (FUSED ? 2 : 1) + (DK / 16) * NJ;
-    auto stage = [&](int i) {
+    auto stage = [&](int i) -> hipError_t {
         switch (i) {
         case 0:
-            hipLaunchKernelGGL((gdn::gdn_frame_summary_kernel<E, DK, DV, NORM, FUSED>),
-                               dim3((unsigned)(units * p.NS)), dim3(gdn::sum_threads<FUSED>()), LS::bytes, s, p);
-            break;
+            return launch((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, NORM, FUSED>,
+                          dim3((unsigned)(units * p.NS)), dim3(gdn::sum_threads<FUSED>()), LS::bytes, s, p);
         case 1:
             // a single split writes the summaries in their final form
             if (p.NS > 1)
-                hipLaunchKernelGGL((gdn::gdn_frame_reduce_kernel<E, DK, DV, NORM, FUSED>),
-                                   dim3((unsigned)units, (NI + 3) / 4), dim3(256), 0, s, p);
-            break;
+                return launch((const void *)gdn::gdn_frame_reduce_kernel<E, DK, DV, NORM, FUSED>,
+                              dim3((unsigned)units, (NI + 3) / 4), dim3(256), 0, s, p);
+            return hipSuccess;
         case 2:
-            hipLaunchKernelGGL((gdn::gdn_frame_scan_kernel<E, DK, DV, NORM, BIDIR, FUSED>),
-                               dim3(gdn::xcd_blocks(BH, NJ)), dim3(64), 0, s, p);
-            break;
+            return launch((const void *)gdn::gdn_frame_scan_kernel<E, DK, DV, NORM, BIDIR, FUSED>,
+                          dim3(gdn::xcd_blocks(BH, NJ)), dim3(64), 0, s, p);
         default:
             if constexpr (FUSED)
-                hipLaunchKernelGGL((gdn::gdn_frame_output_fused_kernel<DK, DV>), dim3(gdn::xcd_blocks(units, p.OB)),
-                                   dim3(gdn::kFusedOutWaves * 64), LF::bytes, s, p);
+                return launch((const void *)gdn::gdn_frame_output_fused_kernel<DK, DV>,
+                              dim3(gdn::xcd_blocks(units, p.OB)), dim3(gdn::kFusedOutWaves * 64), LF::bytes, s, p);
             else
-                hipLaunchKernelGGL((gdn::gdn_frame_output_kernel<E, DK, DV, NORM>),
-                                   dim3(gdn::xcd_blocks(units, p.OB)), dim3(LO::WAVES * 64), LO::bytes,
-                                   s, p);
+                return launch((const void *)gdn::gdn_frame_output_kernel<E, DK, DV, NORM>,
+                              dim3(gdn::xcd_blocks(units, p.OB)), dim3(LO::WAVES * 64), LO::bytes, s, p);
         }
     };
     hipError_t er = hipSuccess;
     for (int i = 0; i < kFrameStages && er == hipSuccess; ++i) {
         if (!ev) {
-            stage(i);
+            er = stage(i);
             continue;
         }
         er = hipEventRecord(ev[2 * i], s);
-        for (int r = 0; r < reps && er == hipSuccess; ++r) stage(i);
+        for (int r = 0; r < reps && er == hipSuccess; ++r) er = stage(i);
         if (er == hipSuccess) er = hipEventRecord(ev[2 * i + 1], s);
     }
-    const hipError_t le = hipGetLastError();
-    return le != hipSuccess ? le : er;
+    return er;
 }
 
 template <class E, bool NORM, bool BIDIR, bool FUSED = false>
@@ -717,16 +717,16 @@ size_t gdn_workspace_bytes(int B, int H, int T, int Dk, int Dv, int chunk, int i
     return gdn_workspace_bytes_ex(B, H, T, Dk, Dv, chunk, is_bf16, 0);
 }
 
-int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int scan_group) {
+int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group) {
     if (!shape_ok(B, H, T) || !dims_ok(Dk, Dv, chunk)) return 0;
-    return resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group);
+    return resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group, is_bf16 != 0);
 }
 
 size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
                               int scan_group) {
     if (!shape_ok(B, H, T) || !dims_ok(Dk, Dv, chunk)) return 0;
     return ws_layout(B, H, T, Dk, Dv, is_bf16 ? 2 : 4,
-                     resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group))
+                     resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group, is_bf16 != 0))
         .total;
 }
 

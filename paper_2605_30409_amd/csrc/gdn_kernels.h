@@ -61,8 +61,6 @@ template <class E> struct Params {
     float *HgT;       // per (b*H + h, group): entry state H^T [Dv][Dk]
 };
 
-constexpr float kLogAlphaMin = -87.3f;  // ~ log(FLT_MIN): alpha below this acts as 1.2e-38
-
 // --------------------------------------------------------------------------
 // Stage 1: per-chunk WY / UT transform.  Grid (NC, B*H), kWyWaves waves.
 // --------------------------------------------------------------------------
@@ -536,9 +534,11 @@ void gdn_chunkscan_kernel(Params<E> p) {
     if (w >= NCW + NOW) {
         // ---------------- loader waves ----------------
         const int ld = w - NCW - NOW;
-        auto issue = [&](int c) {
-            const size_t cidx = (size_t)bh * p.NC + c;
-            E *sl = slot_of(c);
+        // copies of chunk `src` into the slot of chunk `dst` (dst = src except
+        // past the end, see below)
+        auto issue = [&](int dst, int src) {
+            const size_t cidx = (size_t)bh * p.NC + src;
+            E *sl = slot_of(dst);
             const E *ut = p.Ut + cidx * (size_t)DV * kChunk + (size_t)(wbase / 16) * 1024;
             if (ld == 0) {
                 copy_kb<L::NC_W>(p.W + cidx * (size_t)L::WK, sl, l);
@@ -561,14 +561,17 @@ void gdn_chunkscan_kernel(Params<E> p) {
                 else wait_vmcnt<(D - 2) * L::NC_W>();
             }
         };
-        // prologue: chunks c_begin .. c_begin + D - 2 (past the end: the last
-        // chunk again, into its own slot, so the count per chunk is constant)
+        // Prologue: chunks c_begin .. c_begin + D - 2.  Past the end the loaders
+        // still issue the same number of copies (so that the per-chunk count the
+        // waits rely on is constant), reading the last chunk, into the slot of
+        // the missing chunk: a slot no compute wave reads again.
 #pragma unroll
-        for (int i = 0; i < D - 1; ++i) issue(min(c_begin + i, c_end - 1));
+        for (int i = 0; i < D - 1; ++i) issue(c_begin + i, min(c_begin + i, c_end - 1));
         for (int c = c_begin; c < c_end; ++c) {
             wait_oldest();
-            lds_only_barrier();                 // chunk c handed to the compute waves
-            issue(min(c + D - 1, c_end - 1));   // refills the slot of chunk c - 1
+            lds_only_barrier();  // chunk c handed to the compute waves
+            // refills the slot of chunk c - 1
+            issue(c + D - 1, min(c + D - 1, c_end - 1));
         }
         wait_vmcnt<0>();
         lds_only_barrier();                     // ring quiet: the compute waves may reuse it

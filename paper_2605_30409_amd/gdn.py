@@ -46,7 +46,7 @@ def lib():
         L.gdn_workspace_bytes_ex.restype = sz
         L.gdn_workspace_bytes_ex.argtypes = [i, i, i, i, i, i, i, i]
         L.gdn_scan_group_size.restype = i
-        L.gdn_scan_group_size.argtypes = [i, i, i, i, i, i, i]
+        L.gdn_scan_group_size.argtypes = [i, i, i, i, i, i, i, i]
         L.gdn_chunk_forward_ex.restype = i
         L.gdn_chunk_forward_ex.argtypes = core + [i, i, vp, sz, vp]
         L.gdn_profile_stages.restype = i
@@ -189,8 +189,8 @@ def gdn_chunk_forward_f32_ws(q, k, v, alpha, beta, state_in, out, state_out, ws,
           (_ptr(ws), ws.numel()), stream)
 
 
-def gdn_scan_group_size(B, H, T, Dk, Dv, chunk=CHUNK, scan_group=0):
-    return int(lib().gdn_scan_group_size(B, H, T, Dk, Dv, chunk, int(scan_group)))
+def gdn_scan_group_size(B, H, T, Dk, Dv, chunk=CHUNK, scan_group=0, is_bf16=True):
+    return int(lib().gdn_scan_group_size(B, H, T, Dk, Dv, chunk, 1 if is_bf16 else 0, int(scan_group)))
 
 
 def gdn_chunk_forward_ex(q, k, v, alpha, beta, state_in, out, state_out, ws, scan_group=0,

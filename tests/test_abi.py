@@ -4,6 +4,7 @@ the GPU (no compute call is made here)."""
 import ctypes
 import os
 import re
+import sys
 
 import pytest
 
@@ -36,16 +37,26 @@ def test_status_strings():
 
 def test_scan_group_size():
     sg = gdn.gdn_scan_group_size
-    assert sg(1, 16, 3520, 128, 128) == 55               # 55 chunks: one group
-    assert sg(1, 16, 4097, 128, 128) == 8                # 65 chunks: round(sqrt(65))
-    assert sg(1, 16, 10560, 128, 128) == 13              # 165 chunks
-    assert sg(1, 32, 42240, 128, 128) == 26              # 660 chunks
-    assert sg(4, 20, 10560, 64, 64) == 13                # 80 streams x 4 column tiles
-    assert sg(8, 16, 10560, 128, 128) == 165             # 128 streams x 8 column tiles fill the chip
+    f32 = dict(is_bf16=False)
+    # bf16: one group once the streams give >= 64 column tiles, or up to 64 chunks
+    assert sg(1, 16, 3520, 128, 128) == 55               # 55 chunks
+    assert sg(1, 16, 10560, 128, 128) == 165             # 16 streams x 8 column tiles
+    assert sg(1, 32, 42240, 128, 128) == 660
+    assert sg(4, 20, 10560, 64, 64) == 165               # 80 streams x 4 column tiles
+    assert sg(1, 4, 10560, 128, 128) == 13               # 32 column tiles: ~sqrt(165)
+    assert sg(1, 2, 4097, 64, 64) == 8                   # 65 chunks, 8 column tiles
+    # fp32: one group up to 64 chunks or when the streams fill the chip (512 tiles)
+    assert sg(1, 16, 3520, 128, 128, **f32) == 55
+    assert sg(1, 16, 4097, 128, 128, **f32) == 8         # 65 chunks: round(sqrt(65))
+    assert sg(1, 16, 10560, 128, 128, **f32) == 13       # 165 chunks
+    assert sg(1, 32, 42240, 128, 128, **f32) == 26       # 660 chunks
+    assert sg(4, 20, 10560, 64, 64, **f32) == 13         # 80 streams x 4 column tiles
+    assert sg(8, 16, 10560, 128, 128, **f32) == 165      # 128 streams x 8 column tiles fill the chip
     assert sg(1, 2, 1, 64, 64) == 1
     assert sg(1, 16, 3520, 128, 128, scan_group=7) == 7
     assert sg(1, 16, 3520, 128, 128, scan_group=1000) == 55
-    assert sg(1, 16, 10560, 128, 128, scan_group=-3) == 13
+    assert sg(1, 16, 10560, 128, 128, scan_group=-3) == 165
+    assert sg(1, 16, 10560, 128, 128, scan_group=-3, **f32) == 13
     assert sg(1, 16, 0, 128, 128) == 0
     assert sg(1, 16, 64, 128, 128, chunk=32) == 0
     assert sg(1, 16, 64, 96, 128) == 0
@@ -299,3 +310,33 @@ def test_frame_fused_binding_rejects_fp32_on_cpu():
         gdn.frame_forward_fused(q, q, q, q, torch.zeros(2, 64, 64), torch.zeros(1, 2, 2), torch.zeros(1, 100, 2),
                                 torch.ones(2, 64), torch.ones(2, 64), torch.ones(32), torch.zeros(32, dtype=torch.int32),
                                 frame_tokens=50, lat_w=10)
+
+
+_FAILED_LAUNCH = r"""
+import sys
+sys.path.insert(0, {root!r})
+import paper_2605_30409_amd as gdn
+L = gdn.lib()
+BASE, MB = 1 << 40, 1 << 20
+n = gdn.gdn_workspace_bytes(1, 2, 130, 64, 64)
+args = (BASE, BASE + 64 * MB, BASE + 128 * MB, BASE + 192 * MB, BASE + 200 * MB, None, BASE + 256 * MB, None,
+        1, 2, 130, 64, 64, 64)
+print(L.gdn_chunk_forward_ws(*args, BASE + 512 * MB, n, None), L.gdn_chunk_forward(*args, None))
+"""
+
+
+def test_failed_launch_returns_hip_error():
+    """Arguments that pass validation on a host whose HIP launches fail (no GPU):
+    both the explicit-workspace and the cached-workspace calls return
+    GDN_ERR_HIP (-5) instead of crashing or reporting success.  Runs in a child
+    process (the HIP runtime keeps its failed state), and only where no GPU is
+    visible: there the fake addresses are never dereferenced."""
+    import subprocess
+    from conftest import gpu_available
+    if gpu_available():
+        pytest.skip("a GPU is visible: the fake addresses would be launched on")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, "-c", _FAILED_LAUNCH.format(root=root)], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.split() == ["-5", "-5"]  # GDN_ERR_HIP

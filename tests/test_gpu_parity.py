@@ -119,15 +119,14 @@ def test_workload3_batched_fast_forget(gdn):
 
 
 def test_workload4_long_context(gdn):
-    # The oracle runs on 4 of the 32 heads (independent streams), every token.
-    check(gdn, gdn_inputs.make_inputs(4), "workload 4 (T42240 H32), heads 0,9,22,31",
-          heads=[0, 9, 22, 31])
+    # every head and every token (the fp64 oracle takes a few seconds on 16 threads)
+    check(gdn, gdn_inputs.make_inputs(4), "workload 4 (T42240 H32), all heads")
 
 
 def test_workload2_streaming_20_calls(gdn):
-    """20 calls with the fp32 state threaded on the device; oracle on 2 heads."""
+    """20 calls with the fp32 state threaded on the device; every head."""
     torch = torch_mod()
-    heads = [0, 11]
+    heads = list(range(16))
     st_dev = None
     ref_state = None
     worst_o = worst_s = 0.0

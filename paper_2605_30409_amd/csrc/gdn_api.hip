@@ -55,8 +55,12 @@ WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
     L.W = off;    off = align256(off + nch * kChunk * Dk * esz);
     L.Kt = off;   off = align256(off + nch * Dk * kChunk * esz);
     L.Ut = off;   off = align256(off + nch * Dv * kChunk * esz);
-    L.Hs = off;   off = align256(off + nch * Dv * Dk * esz);
-    L.Us = off;   off = align256(off + nch * Dv * kChunk * esz);
+    // With the output fused into the scan (bf16, one group) these regions hold
+    // the chunk's decay-scaled queries (C x Dk) and masked scores (C x C)
+    // instead of the per-chunk state (Dv x Dk) and pseudo-values (Dv x C).
+    const bool fused = esz == 2 && NG == 1;
+    L.Hs = off;   off = align256(off + nch * (fused ? kChunk : Dv) * Dk * esz);
+    L.Us = off;   off = align256(off + nch * (fused ? kChunk : Dv) * kChunk * esz);
     L.Nf = off;   off = align256(off + ngr * Dk * Dk * esz);
     L.PsiT = off; off = align256(off + ngr * Dv * Dk * 4);
     L.lgam = off; off = align256(off + ngr * 8);

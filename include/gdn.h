@@ -131,6 +131,29 @@ int gdn_chunk_forward_f32_ws(const float *q, const float *k, const float *v,
 size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16,
                               int scan_group);
 
+/*
+ * Allocation-free variant of gdn_chunk_forward (bf16 path), for callers that
+ * cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  The workspace is an array of
+ * GDN_NOALLOC_MAX_WORKSPACE bytes in the library's device code object: each
+ * GPU the call runs on holds its own copy until the process ends.  The call
+ * makes no hipMalloc, hipFree or other allocating call; on its first use with
+ * a device current it looks up that device's copy (hipGetSymbolAddress).
+ * Arguments, layouts, validation and results are those of gdn_chunk_forward
+ * (bitwise the same outputs).  Shapes whose workspace, gdn_workspace_bytes(...,
+ * is_bf16 = 1), exceeds GDN_NOALLOC_MAX_WORKSPACE return GDN_ERR_WORKSPACE
+ * before anything is enqueued; one 1280x704 frame (B = 1, T = 3520, H = 16,
+ * Dk = Dv = 128: 62.3 MiB) fits.  Every call on a GPU shares that GPU's array:
+ * calls that overlap on one GPU (several host threads, or streams not ordered
+ * with each other) race and give wrong results.  No part of the array needs to
+ * start at zero: a call writes every byte it reads.
+ */
+#define GDN_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
+int gdn_chunk_forward_noalloc(const void *q, const void *k, const void *v,
+                              const float *alpha, const float *beta, const float *state_in,
+                              void *out, float *state_out,
+                              int B, int H, int T, int Dk, int Dv, int chunk, void *stream);
+
 /* Chunks per scan group the calls above use for this shape, path (is_bf16)
  * and scan_group (0 for unsupported arguments). */
 int gdn_scan_group_size(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group);

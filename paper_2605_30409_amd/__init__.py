@@ -14,7 +14,7 @@ from .gdn import (CHUNK, FRAME_STAGE_NAMES, STAGE_NAMES, GdnError, LIB_PATH,  # 
                   gdn_frame_profile_stages_fused,
                   gdn_frame_profile_stages_norm,
                   gdn_chunk_forward_ex, gdn_chunk_forward_f32, gdn_chunk_forward_f32_ws,
-                  gdn_chunk_forward_ws, gdn_frame_forward_ex, gdn_frame_profile_stages,
+                  gdn_chunk_forward_ws, gdn_chunk_forward_noalloc, gdn_frame_forward_ex, gdn_frame_profile_stages,
                   gdn_frame_token_splits, gdn_frame_workspace_bytes, gdn_profile_stages,
                   gdn_scan_group_size, gdn_status_string, gdn_workspace_bytes,
                   gdn_workspace_bytes_ex, lib, workspace)

@@ -332,6 +332,44 @@ int run_cached(const void *q, const void *k, const void *v, const float *alpha, 
                need, stream, nullptr);
 }
 
+// Allocation-free path (gdn_chunk_forward_noalloc): the workspace is a
+// file-scope device array, one copy per GPU.  In host code `scratch` names a
+// host-side stand-in, not a device address; the address of each GPU's copy
+// comes from hipGetSymbolAddress and is kept per device.
+static __device__ __align__(256) unsigned char scratch[GDN_NOALLOC_MAX_WORKSPACE];
+
+std::mutex g_scratch_mu;
+std::unordered_map<int, void *> g_scratch;  // device -> its copy of `scratch`
+
+int scratch_address(void **ptr) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return GDN_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    auto it = g_scratch.find(dev);
+    if (it == g_scratch.end()) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return GDN_ERR_HIP;
+        it = g_scratch.emplace(dev, p).first;
+    }
+    *ptr = it->second;
+    return GDN_OK;
+}
+
+int run_noalloc(const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+                const float *state_in, void *out, float *state_out, int B, int H, int T, int Dk, int Dv,
+                int chunk, void *stream) {
+    int st = validate(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, 2);
+    if (st != GDN_OK) return st;
+    const size_t need =
+        ws_layout(B, H, T, Dk, Dv, 2, resolve_group(num_chunks(T), (long long)B * H, Dv, 0, true)).total;
+    if (need > GDN_NOALLOC_MAX_WORKSPACE) return GDN_ERR_WORKSPACE;
+    void *ws = nullptr;
+    st = scratch_address(&ws);
+    if (st != GDN_OK) return st;
+    return run(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, true, 0, ws,
+               GDN_NOALLOC_MAX_WORKSPACE, stream, nullptr);
+}
+
 // ---------------------------------------------------------------------------
 // Frame-wise path (gdn_frame_forward*): frame summaries, their reduction over
 // token splits, the scan over frames, and the output; optionally with the
@@ -715,6 +753,12 @@ int gdn_chunk_forward_f32(const float *q, const float *k, const float *v, const 
                           int B, int H, int T, int Dk, int Dv, int chunk, void *stream) {
     return run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, false,
                       stream);
+}
+
+int gdn_chunk_forward_noalloc(const void *q, const void *k, const void *v, const float *alpha,
+                              const float *beta, const float *state_in, void *out, float *state_out, int B,
+                              int H, int T, int Dk, int Dv, int chunk, void *stream) {
+    return run_noalloc(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, stream);
 }
 
 size_t gdn_workspace_bytes(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16) {

@@ -38,6 +38,7 @@ def lib():
         for name in ("gdn_chunk_forward", "gdn_chunk_forward_f32"):
             fn = getattr(L, name)
             fn.restype, fn.argtypes = i, core + [vp]
+        L.gdn_chunk_forward_noalloc.restype, L.gdn_chunk_forward_noalloc.argtypes = i, core + [vp]
         for name in ("gdn_chunk_forward_ws", "gdn_chunk_forward_f32_ws"):
             fn = getattr(L, name)
             fn.restype, fn.argtypes = i, core + [vp, sz, vp]
@@ -174,6 +175,11 @@ def gdn_chunk_forward(q, k, v, alpha, beta, state_in, out, state_out, chunk=CHUN
 def gdn_chunk_forward_f32(q, k, v, alpha, beta, state_in, out, state_out, chunk=CHUNK, stream=None):
     """fp32 path with the library-cached workspace."""
     _call("gdn_chunk_forward_f32", q, k, v, alpha, beta, state_in, out, state_out, chunk, (), stream)
+
+
+def gdn_chunk_forward_noalloc(q, k, v, alpha, beta, state_in, out, state_out, chunk=CHUNK, stream=None):
+    """bf16 path with the library's static device workspace (no allocation)."""
+    _call("gdn_chunk_forward_noalloc", q, k, v, alpha, beta, state_in, out, state_out, chunk, (), stream)
 
 
 def gdn_chunk_forward_ws(q, k, v, alpha, beta, state_in, out, state_out, ws, chunk=CHUNK, stream=None):

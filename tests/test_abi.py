@@ -22,7 +22,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 25 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
+    assert len(names) == 26 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -107,7 +107,7 @@ def call(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, a=BASE + 192 * MB, b=B
 
 @pytest.mark.parametrize("fn", ["gdn_chunk_forward", "gdn_chunk_forward_f32",
                                 "gdn_chunk_forward_ws", "gdn_chunk_forward_f32_ws",
-                                "gdn_chunk_forward_ex"])
+                                "gdn_chunk_forward_ex", "gdn_chunk_forward_noalloc"])
 def test_validation_errors(fn):
     assert call(fn, q=None) == -1
     assert call(fn, o=None) == -1
@@ -126,6 +126,19 @@ def test_validation_errors(fn):
         assert call(fn) == -4                            # no workspace
         assert call(fn, ws=BASE + 512 * MB, ws_bytes=100) == -4
         assert call(fn, ws=BASE + 512 * MB + 16, ws_bytes=1 << 30) == -4   # misaligned
+
+
+def test_noalloc_rejects_workspace_beyond_its_array():
+    """The allocation-free call returns GDN_ERR_WORKSPACE, before any HIP call,
+    when the shape's workspace exceeds its static array (64 MiB): one 1280x704
+    frame at H = 16 fits, twelve frames at H = 32 do not."""
+    limit = 64 << 20
+    assert gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 64, True) <= limit
+    big = dict(B=1, H=32, T=42240, Dk=128, Dv=128)
+    assert gdn.gdn_workspace_bytes(1, 32, 42240, 128, 128, 64, True) > limit
+    n = big["B"] * big["T"] * big["H"] * 128 * 2
+    assert call("gdn_chunk_forward_noalloc", q=BASE, k=BASE + n, v=BASE + 2 * n, a=BASE + 3 * n,
+                b=BASE + 3 * n + (1 << 30), o=BASE + 4 * n, **big) == -4
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

@@ -132,6 +132,18 @@ size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, in
                               int scan_group);
 
 /*
+ * Host-only consistency check of the workspace layout (no HIP call): for the
+ * path a call with these arguments takes, every region of the workspace
+ * (cumulative log decays, chunk decays, -W, Kt, U~t, per-chunk states or
+ * fused-output operands, pseudo-values, and the grouped scan's transfers,
+ * offsets, log decays and entry states) starts 256-byte aligned and spans at
+ * least the highest byte the kernels index in it (their index expressions at
+ * the largest chunk and group index).  Returns GDN_OK, the 1-based number of
+ * the first region that fails, or GDN_ERR_SHAPE / GDN_ERR_UNSUPPORTED.
+ */
+int gdn_workspace_check(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group);
+
+/*
  * Allocation-free variant of gdn_chunk_forward (bf16 path), for callers that
  * cannot allocate device memory: code under HIP graph capture, tight serving
  * loops, harnesses that forbid hipMalloc.  The workspace is an array of

@@ -69,6 +69,51 @@ WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
     return L;
 }
 
+// Bytes each workspace region must span for the kernels that use it, from the
+// kernels' index expressions evaluated at their largest indices (chunk index
+// cidx = B H NC - 1, group index gidx = B H NG - 1, lane 63, last fragment):
+// the highest element offset touched, plus the element's width.  0 if no
+// kernel of the path uses the region.
+struct WsNeeds {
+    size_t g, gc, W, Kt, Ut, Hs, Us, Nf, PsiT, lgam, HgT;
+};
+
+WsNeeds ws_needs(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
+    const size_t NC = (size_t)num_chunks(T), NG = (NC + G - 1) / G;
+    const size_t cmax = (size_t)B * H * NC - 1;             // last chunk record
+    const size_t gmax = (size_t)B * H * NG - 1;             // last group record
+    const bool fused = esz == 2 && NG == 1;
+    const size_t KB = (size_t)Dk / 32, NFR = (size_t)(Dk / 64) * 8, NJ = (size_t)Dv / 16;
+    WsNeeds n{};
+    // WY kernel: g[cidx * 64 + l], gc[cidx]
+    n.g = (cmax * kChunk + 63 + 1) * 8;
+    n.gc = (cmax + 1) * 8;
+    // -W fragment ((wv * 4 + st) * 2 + kb) * 512 + l * 8, 8 elements
+    n.W = (cmax * kChunk * Dk + ((((size_t)Dk / 64 - 1) * 4 + 3) * 2 + 1) * 512 + 63 * 8 + 8) * esz;
+    // Kt fragment f * 512 + l * 8, f < NFR; the scan copies whole records
+    n.Kt = (cmax * Dk * kChunk + (NFR - 1) * 512 + 63 * 8 + 8) * esz;
+    // U~t quad (4 jt + st) * 256 + l * 4, 4 elements
+    n.Ut = (cmax * Dv * kChunk + (4 * (NJ - 1) + 3) * 256 + 63 * 4 + 4) * esz;
+    if (fused) {
+        // WY: Qf (rt * KB + kb) * 512 + l * 8 and Pf (rt * 2 + m) * 512 + l * 8
+        n.Hs = (cmax * kChunk * Dk + (3 * KB + KB - 1) * 512 + 63 * 8 + 8) * esz;
+        n.Us = (cmax * kChunk * kChunk + (3 * 2 + 1) * 512 + 63 * 8 + 8) * esz;
+    } else {
+        // chunk states: Hs[(column) * Dk + 32 kb + 8 lg], Us[(column) * 64 + 32 + 8 lg]
+        n.Hs = (cmax * Dv * Dk + (size_t)(Dv - 1) * Dk + 32 * (KB - 1) + 24 + 8) * esz;
+        n.Us = (cmax * Dv * kChunk + (size_t)(Dv - 1) * kChunk + 32 + 24 + 8) * esz;
+    }
+    if (NG > 1) {
+        // group transfer: N fragments ((v * 4 + t) * (Dk / 32) + kb) * 512 + l * 8,
+        // Psi^T[(gidx * Dv + column) * Dk + row], log Gamma[gidx]; group scan: H^T like Psi^T
+        n.Nf = (gmax * Dk * Dk + ((((size_t)Dk / 64 - 1) * 4 + 3) * KB + KB - 1) * 512 + 63 * 8 + 8) * esz;
+        n.PsiT = ((gmax * Dv + Dv - 1) * Dk + Dk) * 4;
+        n.lgam = (gmax + 1) * 8;
+        n.HgT = ((gmax * Dv + Dv - 1) * Dk + Dk) * 4;
+    }
+    return n;
+}
+
 bool shape_ok(int B, int H, int T) {
     if (B < 1 || H < 1 || T < 1) return false;
     // gridDim.y carries B*H
@@ -753,6 +798,22 @@ int gdn_chunk_forward_f32(const float *q, const float *k, const float *v, const 
                           int B, int H, int T, int Dk, int Dv, int chunk, void *stream) {
     return run_cached(q, k, v, alpha, beta, state_in, out, state_out, B, H, T, Dk, Dv, chunk, false,
                       stream);
+}
+
+int gdn_workspace_check(int B, int H, int T, int Dk, int Dv, int chunk, int is_bf16, int scan_group) {
+    if (!shape_ok(B, H, T)) return GDN_ERR_SHAPE;
+    if (!dims_ok(Dk, Dv, chunk)) return GDN_ERR_UNSUPPORTED;
+    const size_t esz = is_bf16 ? 2 : 4;
+    const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group, is_bf16 != 0);
+    const WsLayout L = ws_layout(B, H, T, Dk, Dv, esz, G);
+    const WsNeeds n = ws_needs(B, H, T, Dk, Dv, esz, G);
+    const size_t start[] = {L.g, L.gc, L.W, L.Kt, L.Ut, L.Hs, L.Us, L.Nf, L.PsiT, L.lgam, L.HgT, L.total};
+    const size_t need[] = {n.g, n.gc, n.W, n.Kt, n.Ut, n.Hs, n.Us, n.Nf, n.PsiT, n.lgam, n.HgT};
+    for (int r = 0; r < 11; ++r) {
+        if (start[r] % 256) return r + 1;                    // regions start 256-byte aligned
+        if (need[r] > start[r + 1] - start[r]) return r + 1;  // region too small
+    }
+    return GDN_OK;
 }
 
 int gdn_chunk_forward_noalloc(const void *q, const void *k, const void *v, const float *alpha,

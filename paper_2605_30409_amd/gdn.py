@@ -39,6 +39,8 @@ def lib():
             fn = getattr(L, name)
             fn.restype, fn.argtypes = i, core + [vp]
         L.gdn_chunk_forward_noalloc.restype, L.gdn_chunk_forward_noalloc.argtypes = i, core + [vp]
+        L.gdn_workspace_check.restype = i
+        L.gdn_workspace_check.argtypes = [i, i, i, i, i, i, i, i]
         for name in ("gdn_chunk_forward_ws", "gdn_chunk_forward_f32_ws"):
             fn = getattr(L, name)
             fn.restype, fn.argtypes = i, core + [vp, sz, vp]

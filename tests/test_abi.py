@@ -22,7 +22,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 26 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
+    assert len(names) == 27 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -126,6 +126,23 @@ def test_validation_errors(fn):
         assert call(fn) == -4                            # no workspace
         assert call(fn, ws=BASE + 512 * MB, ws_bytes=100) == -4
         assert call(fn, ws=BASE + 512 * MB + 16, ws_bytes=1 << 30) == -4   # misaligned
+
+
+@pytest.mark.parametrize("is_bf16", [1, 0])
+@pytest.mark.parametrize("Dk,Dv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+def test_workspace_regions_cover_kernel_indexing(is_bf16, Dk, Dv):
+    """Every workspace region spans what the kernels index in it, for every
+    path: one scan group (fused output on bf16), grouped scans with short last
+    groups, ragged T, batches, many heads."""
+    L = gdn.lib()
+    for B, H in ((1, 1), (1, 16), (2, 3), (4, 20), (1, 32), (8, 16)):
+        for T in (1, 63, 64, 65, 200, 1500, 3520, 3557, 10560, 42240):
+            nc = -(-T // 64)
+            for g in sorted({0, 1, 2, 7, 13, nc, nc + 5}):
+                rc = L.gdn_workspace_check(B, H, T, Dk, Dv, 64, is_bf16, g)
+                assert rc == 0, (B, H, T, Dk, Dv, is_bf16, g, rc)
+    assert L.gdn_workspace_check(1, 1, 0, 64, 64, 64, 1, 0) == -2
+    assert L.gdn_workspace_check(1, 1, 64, 96, 64, 64, 1, 0) == -3
 
 
 def test_noalloc_rejects_workspace_beyond_its_array():

@@ -50,6 +50,9 @@ KERNELS = {"wy": "gdn_wy_kernel", "group_transfer": "gdn_chunkscan_kernel<SCAN_T
            "output": "gdn_output_kernel"}
 KERNELS_FUSED = dict(KERNELS, chunk_states="gdn_chunkscan_kernel<SCAN_STATES, output fused>")
 EXTRA_WORKLOADS = (0, 2, 3, 4)
+# committed counter summaries of the token path, per workload
+TRAFFIC_SUMMARY = {1: "traffic_frame1280x704.json", 2: "traffic_stream3x1280x704.json",
+                   4: "traffic_long12x1280x704.json"}
 
 
 def path_counts(B, T, H, Dk, Dv, C=64, esz=2):
@@ -462,6 +465,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing leg")
+    ap.add_argument("--workload", type=int, default=WORKLOAD, choices=range(len(gdn_inputs.WORKLOADS)),
+                    help="token path: the workload a step runs (default 1, one 1280x704 frame; the "
+                         "others draw their inputs on the device)")
     ap.add_argument("--no-workloads", action="store_true",
                     help="token path: skip the per-call timing of the other four workloads")
     ap.add_argument("--cold-steps", type=int, default=20,
@@ -530,21 +536,40 @@ def main():
                   bidir="-bidir" in args.path, fused="-fused" in args.path)
         return
 
-    w = gdn_inputs.WORKLOADS[WORKLOAD]
+    widx = args.workload
+    w = gdn_inputs.WORKLOADS[widx]
     B, T, H, Dk, Dv, C = w.B, w.T, w.H, w.Dk, w.Dv, w.chunk
-    inp = gdn_inputs.make_inputs(WORKLOAD)
-
-    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
-    alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
-    out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
+    bf16 = w.dtype == "bf16"
+    if widx == WORKLOAD:
+        inp = gdn_inputs.make_inputs(WORKLOAD)
+        calls = [{key: to_dev(inp[key]) for key in ("q", "k", "v", "alpha", "beta", "state_in")}]
+    else:
+        # device-drawn inputs (timing only); the streaming workload's calls
+        # each get their own draw and the state is threaded through them
+        inp = None
+        calls = [gdn_inputs.make_device_inputs(widx, dev, call=c) for c in range(w.calls)]
+    out = torch.empty((B, T, H, Dv), dtype=calls[0]["q"].dtype, device=dev)
     s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
-    ws = gdn.workspace(q, v)
+    states = [torch.zeros_like(s_out), s_out]
+    ws = gdn.workspace(calls[0]["q"], calls[0]["v"])
     stream = torch.cuda.current_stream(dev)
+    fwd = gdn.gdn_chunk_forward_ws if bf16 else gdn.gdn_chunk_forward_f32_ws
+    ncall = [0]
 
     def step():
-        gdn.gdn_chunk_forward_ws(q, k, v, alpha, beta, s_in, out, s_out, ws, chunk=C, stream=stream)
+        c = ncall[0]
+        x = calls[c % len(calls)]
+        if len(calls) == 1:
+            fwd(x["q"], x["k"], x["v"], x["alpha"], x["beta"], x["state_in"], out, s_out, ws, chunk=C, stream=stream)
+        else:
+            fwd(x["q"], x["k"], x["v"], x["alpha"], x["beta"], states[c & 1], out, states[(c + 1) & 1], ws, chunk=C,
+                stream=stream)
+        ncall[0] = c + 1
 
     ms_per_step, per_step, cold = timed(step, stream)
+    x = calls[0]
+    q, k, v, alpha, beta = x["q"], x["k"], x["v"], x["alpha"], x["beta"]
+    s_in = x["state_in"] if x["state_in"] is not None else states[0]
 
     # Per-stage durations: HIP events recorded by the library on the same stream.
     stage_ms = gdn.gdn_profile_stages(q, k, v, alpha, beta, s_in, out, s_out, ws,
@@ -552,18 +577,19 @@ def main():
     names = {k_: v_ for k_, v_ in zip(gdn.STAGE_NAMES, stage_ms) if v_ > 0}
     torch.cuda.synchronize()
 
-    G = gdn.gdn_scan_group_size(B, H, T, Dk, Dv, C)
+    G = gdn.gdn_scan_group_size(B, H, T, Dk, Dv, C, is_bf16=bf16)
     NG = -(-(-(-T // C)) // G)
-    fused = NG == 1
-    flops, io = path_counts(B, T, H, Dk, Dv, C)
+    fused = bf16 and NG == 1
+    esz = 2 if bf16 else 4
+    flops, io = path_counts(B, T, H, Dk, Dv, C, esz=esz)
     sec = ms_per_step / 1e3
     tflops = flops / sec / 1e12
-    traffic = load_traffic("traffic_frame1280x704.json")
-    roofline = token_roofline(flops, io, names, KERNELS_FUSED if fused else KERNELS, traffic,
-                              PEAK_BF16_TFLOPS)
+    peak = PEAK_BF16_TFLOPS if bf16 else PEAK_F32_TFLOPS
+    traffic = load_traffic(TRAFFIC_SUMMARY.get(widx, "none"))
+    roofline = token_roofline(flops, io, names, KERNELS_FUSED if fused else KERNELS, traffic, peak)
 
     rec = {
-        "metric": METRIC,
+        "metric": METRIC if widx == WORKLOAD else f"GDN fwd tokens/sec and TFLOP/s, workload {w.name}",
         "value": round(B * T / sec, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
@@ -573,27 +599,29 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if bf16 else "f32",
         "data": "synthetic",
         "config": {"workload": "one 1280x704 latent frame: B=1 T=3520 (44x80) H=16 Dk=Dv=128 "
-                               "chunk=64, bf16 q/k/v, fp32 state in/out",
+                               "chunk=64, bf16 q/k/v, fp32 state in/out" if widx == WORKLOAD else w.name
+                               + (f" (a step is one call of the {w.calls}-call chain, state threaded)"
+                                  if w.calls > 1 else ""),
                    "B": B, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "chunk": C,
                    "scan_group": G, "scan_groups": NG, "output_fused": fused},
         "step_ms": stats(per_step),
         "tflops": round(tflops, 2),
-        "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "mfma_frac": round(tflops / peak, 4),
         "hbm_frac_io": round(io / sec / 1e9 / PEAK_HBM_GBS, 4),
         "ms_per_step_cold": None if cold is None else stats(cold),
         "stage_ms": {k_: round(v_, 5) for k_, v_ in names.items()},
-        "workspace_bytes": workspace_traffic(B, T, H, Dk, Dv, G, C),
+        "workspace_bytes": workspace_traffic(B, T, H, Dk, Dv, G, C, esz=esz),
         "roofline": roofline,
     }
-    if not args.no_workloads:
+    if not args.no_workloads and widx == WORKLOAD:
         extra = {}
         for idx in EXTRA_WORKLOADS:
             extra[str(idx)] = run_extra_workload(idx, gdn, torch, dev, stream, reps=10 if idx == 4 else 20)
         rec["workloads"] = extra
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and inp is not None:
         rec["cpu_baseline"] = cpu_baseline(inp, B, T)
     print(json.dumps(rec), flush=True)
 

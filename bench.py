@@ -156,12 +156,16 @@ def load_traffic(summary):
         return None
 
 
-def token_roofline(flops, io, names, kernels, traffic, peak_tflops):
-    """Roofline of the dominant kernel, per the path's algorithmic I/O: the call's
-    bytes (or flops) over that kernel's launch duration.  The path's intensity is
-    below the ridge (~315 flop/B), so its bound is HBM."""
+def token_roofline(flops, io, names, kernels, traffic, peak_tflops, own_io=None):
+    """Roofline of the dominant kernel.  Token path: the call's algorithmic I/O
+    (or flops) over that kernel's launch duration.  Frame-wise paths (own_io
+    given): the dominant kernel's own share of the call's I/O -- the inputs it
+    reads and the outputs it writes, no workspace.  The paths' intensity is
+    below the ridge (~315 flop/B), so their bound is HBM."""
     dom = max(names, key=names.get)
     sec = names[dom] / 1e3
+    if own_io is not None:
+        io = own_io[dom]
     bound_hbm = flops / io < peak_tflops * 1e12 / (PEAK_HBM_GBS * 1e9)
     a_gbs = io / sec / 1e9
     a_tf = flops / sec / 1e12
@@ -182,20 +186,28 @@ def token_roofline(flops, io, names, kernels, traffic, peak_tflops):
 
 
 def time_steps(step, stream, steps, warmup, torch):
-    """`warmup` untimed steps, then `steps` steps with an event before each and one
-    after the last, all on `stream`, between two synchronizations.  Returns the
-    mean (first to last event / steps) and the per-step durations in ms."""
+    """`warmup` untimed steps, then `steps` steps between two events on `stream`
+    (bracketed by synchronizations): the mean.  Then the same number of steps
+    again, each between its own pair of events: the per-step durations in ms
+    (their median and spread; the events between steps add a little time, so
+    the mean is taken from the first pass)."""
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
-    ev[0].record(stream)
-    for i in range(steps):
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
         step()
-        ev[i + 1].record(stream)
+    e1.record(stream)
     torch.cuda.synchronize()
-    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
-    return ev[0].elapsed_time(ev[steps]) / steps, per
+    mean = e0.elapsed_time(e1) / steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        step()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return mean, [a.elapsed_time(b) for a, b in ev]
 
 
 def run_extra_workload(idx, gdn, torch, dev, stream, reps):
@@ -305,9 +317,13 @@ def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=Fa
         ws["scan"]["written"] += u * Dk * Ds * 4
         ws["scan"]["read"] += u * Dk * Ds * 4
     io_bytes = n * ((2 * Dk + 2 * Dv) * esz + 4) + u * 4 + 2 * st
+    # each kernel's own share of the call's I/O
+    own = {"summaries": n * ((Dk + Dv) * esz + 4), "reduce": 0,
+           "scan": u * 4 + 2 * st, "output": n * (Dk + Dv) * esz}
     if fused:
         io_bytes += n * Dv * esz + H * Dv * Dv * esz
-    return dict(flops=f, io_bytes=io_bytes, workspace=ws)
+        own["output"] += n * Dv * esz + H * Dv * Dv * esz
+    return dict(flops=f, io_bytes=io_bytes, workspace=ws, own_io=own)
 
 
 def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=False, fused=False):
@@ -418,7 +434,8 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
     kernels = dict(FRAME_KERNELS)
     if fused:
         kernels.update({"summaries": "gdn_frame_summary_fused_kernel", "output": "gdn_frame_output_fused_kernel"})
-    roofline = token_roofline(flops, cnt["io_bytes"], names, kernels, traffic, PEAK_BF16_TFLOPS)
+    roofline = token_roofline(flops, cnt["io_bytes"], names, kernels, traffic, PEAK_BF16_TFLOPS,
+                              own_io=cnt["own_io"])
     rec = {
         "metric": FRAME_FUSED_METRIC + (" (bidirectional)" if bidir else "") if fused
                   else (FRAME_BIDIR_NORM_METRIC if norm else FRAME_BIDIR_METRIC) if bidir

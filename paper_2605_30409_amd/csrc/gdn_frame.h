@@ -406,15 +406,16 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
         // halves of the value copies.  Rows past the split repeat its last
         // token (their beta is zeroed where it is used).  Every iteration
         // issues the same number of copies so that the waits below count
-        // right: past the last block the last block is copied again, onto
-        // itself (unchanged bytes).
+        // right: past the last block the last block is copied again, into the
+        // slot of the missing block ii (the slot just released, which no
+        // compute wave reads again).
         const int ld = w - NCOMP;
         const bool keys = ld < 2;
         auto issue = [&](int ii) {
             const int i = min(ii, nb - 1);
             const int t0 = t_lo + 64 * i, rmax = t_hi - 1 - t0;
             const size_t row0 = (row_b + t0) * p.H + h;
-            unsigned char *sl = slot(i);
+            unsigned char *sl = slot(ii);
 #define GDN_SUM_DST(off) ((__attribute__((address_space(3))) void *)(sl + (off)))
             if (keys) {
                 const char *base = (const char *)(p.k + row0 * DK);

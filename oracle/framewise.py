@@ -74,53 +74,3 @@ def framewise_forward_normalized(q, k, v, alpha_f, beta, S0=None, z0=None, N=1, 
         Y[sl] = ((S @ Qf) / (z @ Qf + eps)).T
     return Y, S, z
 
-
-def three_phase_forward(q, k, v, alpha_f, beta, S0=None, z0=None, N=1, eps=1e-6, normalized=False,
-                        bidirectional=False):
-    """One (b, h) stream through the paper's three phases (Algorithm
-    alg:gdn-kernel) in the H = S^T orientation (H: Dk x Dv), keys already
-    rescaled by the caller:
-
-      Phase A, per frame: P_f = I - K^T B K, A_f = K^T B V, b_f = K^T beta
-      Phase B: forward  H_f = alpha_f P_f H_{f-1} + A_f,  z_f = alpha_f P_f z_{f-1} + b_f
-               backward Hb_{F-1} = 0,  Hb_{f-1} = alpha_f P_f Hb_f + A_f  (same for z)
-               histories H_f (+ Hb_f), z_f (+ zb_f)
-      Phase C: Y = Q H_hist, divided by Q z_hist + eps when normalized.
-
-    q, k: [T, Dk] (row tokens); v: [T, Dv].  Returns (Y [T, Dv], H_F, z_F)."""
-    q, k, v = (np.asarray(x, dtype=np.float64) for x in (q, k, v))
-    T, Dk = k.shape
-    Dv = v.shape[1]
-    F = T // N
-    I = np.eye(Dk)
-    P, A, bz = [], [], []
-    for f in range(F):
-        sl = slice(f * N, (f + 1) * N)
-        K = k[sl]
-        Bm = np.diag(np.asarray(beta[sl], dtype=np.float64))
-        P.append(I - K.T @ Bm @ K)
-        A.append(K.T @ Bm @ v[sl])
-        bz.append(K.T @ np.asarray(beta[sl], dtype=np.float64))
-    H = np.zeros((Dk, Dv)) if S0 is None else np.asarray(S0, dtype=np.float64).copy()
-    z = np.zeros(Dk) if z0 is None else np.asarray(z0, dtype=np.float64).copy()
-    Hs, zs = [], []
-    for f in range(F):
-        H = float(alpha_f[f]) * P[f] @ H + A[f]
-        z = float(alpha_f[f]) * P[f] @ z + bz[f]
-        Hs.append(H.copy())
-        zs.append(z.copy())
-    if bidirectional:
-        Hb = [np.zeros((Dk, Dv)) for _ in range(F)]
-        zb = [np.zeros(Dk) for _ in range(F)]
-        for f in range(F - 1, 0, -1):
-            Hb[f - 1] = float(alpha_f[f]) * P[f] @ Hb[f] + A[f]
-            zb[f - 1] = float(alpha_f[f]) * P[f] @ zb[f] + bz[f]
-        Hs = [Hs[f] + Hb[f] for f in range(F)]
-        zs = [zs[f] + zb[f] for f in range(F)]
-    Y = np.zeros((T, Dv))
-    for f in range(F):
-        sl = slice(f * N, (f + 1) * N)
-        Y[sl] = q[sl] @ Hs[f]
-        if normalized:
-            Y[sl] /= (q[sl] @ zs[f] + eps)[:, None]
-    return Y, H, z

@@ -14,7 +14,7 @@ import pytest
 import gdn_inputs
 import oracle
 from oracle.chunked import gdn_chunked
-from oracle.framewise import framewise_forward, framewise_forward_normalized, three_phase_forward
+from oracle.framewise import framewise_forward, framewise_forward_normalized
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
 rng = np.random.default_rng
@@ -505,23 +505,46 @@ def test_n6_empty_normalizer_divides_by_eps():
 
 @pytest.mark.parametrize("normalized", [False, True])
 @pytest.mark.parametrize("F,N", [(1, 4), (2, 3), (4, 5), (5, 1)])
-def test_b1_bidirectional_equals_the_three_phase_algorithm(normalized, F, N):
-    """The oracle's residual loops (forward, and backward from zero over the
-    later frames) against the paper's Algorithm as printed (frame summaries,
-    forward and backward recursions, summed histories, one readout)."""
+def test_b1_bidirectional_reads_the_sum_of_two_compact_histories(normalized, F, N):
+    """Bidirectional readout from the printed compact update alone.  The
+    forward history of frame f is the compact update run over frames 0..f from
+    the cached state; the backward one is the same update run over the later
+    frames F-1, .., f+1 (in that order) from a zero state, each frame keeping
+    its own decay.  The frame reads out from the sum of the two (and, when
+    normalized, divides by the sum of the two normalizer states).  Catches a
+    backward scan that starts from the cache, includes frame f itself, takes
+    its neighbour's decay, or a readout from only one of the histories."""
     q, k, v, a, b, s, z = norm_case(300 + 11 * F + N, F=F, N=N)
     ks, eps = 0.4, 1e-3
     res = oracle.gdn_frame_forward(q, k, v, a, b, s, frame_tokens=N, key_scale=ks, normalized=normalized,
                                    z_in=z if normalized else None, eps=eps, bidirectional=True)
     o, st = res[0], res[1]
-    for h in range(q.shape[2]):
-        Y, Hf, zf = three_phase_forward(q[0, :, h], ks * k[0, :, h], v[0, :, h], a[0, :, h], b[0, :, h],
-                                        s[0, h], z[0, h] if normalized else None, N=N, eps=eps,
-                                        normalized=normalized, bidirectional=True)
-        assert rel(o[0, :, h], Y) < 1e-11
-        assert rel(st[0, h], Hf) < 1e-12
+
+    def compact(frames, h, S0, z0):
+        """Terminal (S [Dv, Dk], z [Dk]) of the compact update over `frames`."""
+        idx = np.concatenate([np.arange(g * N, (g + 1) * N) for g in frames])
+        args = (q[0, idx, h], ks * k[0, idx, h], v[0, idx, h], a[0, frames, h], b[0, idx, h], S0)
         if normalized:
-            assert rel(res[2][0, h], zf) < 1e-12
+            _, S, zz = framewise_forward_normalized(*args, z0=z0, N=N, eps=eps)
+            return S, zz
+        return framewise_forward(*args, N=N)[1], None
+
+    Dk, Dv = k.shape[-1], v.shape[-1]
+    for h in range(q.shape[2]):
+        zin = z[0, h] if normalized else None
+        for f in range(F):
+            Sf, zf = compact(list(range(f + 1)), h, s[0, h].T, zin)
+            Sb, zb = (np.zeros((Dv, Dk)), np.zeros(Dk)) if f == F - 1 else \
+                compact(list(range(F - 1, f, -1)), h, None, None)
+            Qf = q[0, f * N:(f + 1) * N, h].T
+            Y = (Sf + Sb) @ Qf
+            if normalized:
+                Y = Y / ((zf + zb) @ Qf + eps)
+            assert rel(o[0, f * N:(f + 1) * N, h], Y.T) < 1e-11
+        Sfin, zfin = compact(list(range(F)), h, s[0, h].T, zin)
+        assert rel(st[0, h], Sfin.T) < 1e-12
+        if normalized:
+            assert rel(res[2][0, h], zfin) < 1e-12
 
 
 def test_b2_backward_history_is_the_reversed_recurrence():

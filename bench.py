@@ -70,27 +70,30 @@ def path_counts(B, T, H, Dk, Dv, C=64, esz=2):
 
 
 def workspace_traffic(B, T, H, Dk, Dv, G, C=64, esz=2):
-    """Workspace bytes each stage writes and reads (every byte once).  With one
-    scan group on the bf16 path the output is fused into the scan: the WY kernel
-    then also writes the decay-scaled queries and the masked decayed Q K^T tile
-    of every chunk (row fragments the scan's output waves read) and the scan
+    """Workspace bytes each stage writes and reads (every byte once).  The WY
+    kernel writes the gates (g, and a record of the per-token key decay factors
+    in fp32 with g_C), -W and U~t; the scans read the keys from the input.  With one scan
+    group on the bf16 path the output is fused into the scan: the WY kernel then
+    also writes the decay-scaled queries and the masked decayed Q K^T tile of
+    every chunk (row fragments the scan's output waves read) and the scan
     writes no per-chunk state."""
     NC = -(-T // C)
     NG = -(-NC // G)
     nch = B * H * NC
     fused = esz == 2 and NG == 1
     ngr = B * H * NG if NG > 1 else 0
-    gates = nch * (C * 8 + 8)
-    fac = nch * C * (2 * Dk + Dv) * esz                    # -W, Kt, U~t
+    gates = nch * (C * 8 + (C + 4) * 4)
+    fac = nch * C * (Dk + Dv) * esz                        # -W, U~t
+    scan_gates = nch * (C + 4) * 4                         # key scales, g_C
     qp = nch * C * (Dk + C) * esz if fused else 0          # scaled Q, masked P
     grp = ngr * (Dk * Dk * esz + Dv * Dk * 4 + 8)          # N, Psi^T, log Gamma
     hg = ngr * Dv * Dk * 4                                 # group entry states
     hs_us = 0 if fused else nch * Dv * (Dk + C) * esz      # per-chunk state and pseudo-values
     zero = {"written": 0, "read": 0}
     return {"wy": {"written": gates + fac + qp, "read": 0},
-            "group_transfer": {"written": grp, "read": fac + nch * 8} if ngr else zero,
+            "group_transfer": {"written": grp, "read": fac + scan_gates} if ngr else zero,
             "group_scan": {"written": hg, "read": grp} if ngr else zero,
-            "chunk_states": {"written": hs_us, "read": fac + nch * 8 + hg + qp},
+            "chunk_states": {"written": hs_us, "read": fac + scan_gates + hg + qp},
             "output": zero if fused else {"written": 0, "read": hs_us + nch * C * 8}}
 
 

@@ -134,8 +134,9 @@ size_t gdn_workspace_bytes_ex(int B, int H, int T, int Dk, int Dv, int chunk, in
 /*
  * Host-only consistency check of the workspace layout (no HIP call): for the
  * path a call with these arguments takes, every region of the workspace
- * (cumulative log decays, chunk decays, -W, Kt, U~t, per-chunk states or
- * fused-output operands, pseudo-values, and the grouped scan's transfers,
+ * (cumulative log decays, per-chunk gate records of key decay factors and
+ * chunk decay, -W, U~t, per-chunk states or fused-output operands,
+ * pseudo-values, and the grouped scan's transfers,
  * offsets, log decays and entry states) starts 256-byte aligned and spans at
  * least the highest byte the kernels index in it (their index expressions at
  * the largest chunk and group index).  Returns GDN_OK, the 1-based number of

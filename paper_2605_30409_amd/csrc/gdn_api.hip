@@ -14,9 +14,10 @@
 namespace {
 
 using gdn::kChunk;
+using gdn::kGateRec;
 
 struct WsLayout {
-    size_t g, gc, W, Kt, Ut, Hs, Us, Nf, PsiT, lgam, HgT, total;
+    size_t g, gf, W, Ut, Hs, Us, Nf, PsiT, lgam, HgT, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -51,9 +52,8 @@ WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
     WsLayout L;
     size_t off = 0;
     L.g = off;    off = align256(off + nch * kChunk * 8);
-    L.gc = off;   off = align256(off + nch * 8);
+    L.gf = off;   off = align256(off + nch * kGateRec * 4);
     L.W = off;    off = align256(off + nch * kChunk * Dk * esz);
-    L.Kt = off;   off = align256(off + nch * Dk * kChunk * esz);
     L.Ut = off;   off = align256(off + nch * Dv * kChunk * esz);
     // With the output fused into the scan (bf16, one group) these regions hold
     // the chunk's decay-scaled queries (C x Dk) and masked scores (C x C)
@@ -75,7 +75,7 @@ WsLayout ws_layout(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
 // the highest element offset touched, plus the element's width.  0 if no
 // kernel of the path uses the region.
 struct WsNeeds {
-    size_t g, gc, W, Kt, Ut, Hs, Us, Nf, PsiT, lgam, HgT;
+    size_t g, gf, W, Ut, Hs, Us, Nf, PsiT, lgam, HgT;
 };
 
 WsNeeds ws_needs(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
@@ -83,15 +83,14 @@ WsNeeds ws_needs(int B, int H, int T, int Dk, int Dv, size_t esz, int G) {
     const size_t cmax = (size_t)B * H * NC - 1;             // last chunk record
     const size_t gmax = (size_t)B * H * NG - 1;             // last group record
     const bool fused = esz == 2 && NG == 1;
-    const size_t KB = (size_t)Dk / 32, NFR = (size_t)(Dk / 64) * 8, NJ = (size_t)Dv / 16;
+    const size_t KB = (size_t)Dk / 32, NJ = (size_t)Dv / 16;
     WsNeeds n{};
-    // WY kernel: g[cidx * 64 + l], gc[cidx]
+    // WY kernel: g[cidx * 64 + l], gf[cidx * 68 + l] and the fp64 g_C at
+    // gf + cidx * 68 + 64 (the scan copies gf[cidx * 68 + 4 l .. + 3], l < 17)
     n.g = (cmax * kChunk + 63 + 1) * 8;
-    n.gc = (cmax + 1) * 8;
+    n.gf = (cmax * kGateRec + kGateRec) * 4;
     // -W fragment ((wv * 4 + st) * 2 + kb) * 512 + l * 8, 8 elements
     n.W = (cmax * kChunk * Dk + ((((size_t)Dk / 64 - 1) * 4 + 3) * 2 + 1) * 512 + 63 * 8 + 8) * esz;
-    // Kt fragment f * 512 + l * 8, f < NFR; the scan copies whole records
-    n.Kt = (cmax * Dk * kChunk + (NFR - 1) * 512 + 63 * 8 + 8) * esz;
     // U~t quad (4 jt + st) * 256 + l * 4, 4 elements
     n.Ut = (cmax * Dv * kChunk + (4 * (NJ - 1) + 3) * 256 + 63 * 4 + 4) * esz;
     if (fused) {
@@ -183,9 +182,8 @@ gdn::Params<E> make_params(const void *q, const void *k, const void *v, const fl
     const WsLayout L = ws_layout(B, H, T, Dk, Dv, sizeof(E), G);
     unsigned char *base = (unsigned char *)ws;
     p.g = (double *)(base + L.g);
-    p.gc = (double *)(base + L.gc);
+    p.gf = (float *)(base + L.gf);
     p.W = (E *)(base + L.W);
-    p.Kt = (E *)(base + L.Kt);
     p.Ut = (E *)(base + L.Ut);
     p.Hs = (E *)(base + L.Hs);
     p.Us = (E *)(base + L.Us);
@@ -807,9 +805,9 @@ int gdn_workspace_check(int B, int H, int T, int Dk, int Dv, int chunk, int is_b
     const int G = resolve_group(num_chunks(T), (long long)B * H, Dv, scan_group, is_bf16 != 0);
     const WsLayout L = ws_layout(B, H, T, Dk, Dv, esz, G);
     const WsNeeds n = ws_needs(B, H, T, Dk, Dv, esz, G);
-    const size_t start[] = {L.g, L.gc, L.W, L.Kt, L.Ut, L.Hs, L.Us, L.Nf, L.PsiT, L.lgam, L.HgT, L.total};
-    const size_t need[] = {n.g, n.gc, n.W, n.Kt, n.Ut, n.Hs, n.Us, n.Nf, n.PsiT, n.lgam, n.HgT};
-    for (int r = 0; r < 11; ++r) {
+    const size_t start[] = {L.g, L.gf, L.W, L.Ut, L.Hs, L.Us, L.Nf, L.PsiT, L.lgam, L.HgT, L.total};
+    const size_t need[] = {n.g, n.gf, n.W, n.Ut, n.Hs, n.Us, n.Nf, n.PsiT, n.lgam, n.HgT};
+    for (int r = 0; r < 10; ++r) {
         if (start[r] % 256) return r + 1;                    // regions start 256-byte aligned
         if (need[r] > start[r + 1] - start[r]) return r + 1;  // region too small
     }

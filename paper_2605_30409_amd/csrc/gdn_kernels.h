@@ -20,9 +20,10 @@
 // Workspace per (b*H + h, chunk) -- see gdn_api.hip for the byte layout:
 //   g  [64]       fp64   cumulative log decay (fp64 so that g_r - g_s keeps
 //                        its precision when the decay over a chunk is huge)
-//   gc            fp64   g at the chunk's last token (compact, for the scan)
+//   gf [68]       fp32   e^{g_C - g_r} (the update's per-token key scale),
+//                        then g_C, the log decay over the chunk, as one fp64,
+//                        and gamma = e^{g_C}
 //   W  64*Dk      E      -W (the WY factor, negated), fragment-major for the scan
-//   Kt Dk*64      E      Kt = (diag(e^{g_C - g}) K)^T, fragment-major
 //   Ut Dv*64      E      Ut, fragment-major
 //   Hs [Dv][Dk]   E      H_{c-1}^T, the state entering the chunk
 //   Us [Dv][64]   E      U^T
@@ -30,10 +31,11 @@
 // consume the operand, so every scan load is one contiguous wave access:
 //   W  [Dk/64 wave][4 token tile][2 k block][64 lane][8]
 //        = -W[32 m + p32_row(a, li)][64 wave + 32 kb + 8 lg + e]    (tile 2 m + a)
-//   Kt [Dk/64 wave][4 row tile][2 token block][64 lane][8]
-//        = Kt[64 wave + 32 (t / 2) + p32_row(t % 2, li)][32 m + 8 lg + e]
 //   Ut [Dv/16 column tile][4 token tile][64 lane][4]
 //        = Ut[32 m + 8 lg + 4 a + e][16 jt + li]                      (tile 2 m + a)
+// The scan reads the keys from the input itself and applies their decay
+// factors in registers: the update takes K^T (diag(e^{g_C - g}) U), so no
+// scaled copy of K is written.
 #pragma once
 
 #include "gdn_device.h"
@@ -48,8 +50,8 @@ template <class E> struct Params {
     int B, H, T, NC;
     int G, NG;        // chunks per scan group, number of groups
     double *g;
-    double *gc;       // per (b*H + h, chunk): g at the chunk's last token
-    E *W, *Kt, *Ut, *Hs, *Us;
+    float *gf;        // per (b*H + h, chunk): e^{g_C - g_r} [64], g_C (fp64), e^{g_C}, 1 unused
+    E *W, *Ut, *Hs, *Us;
     // Fused output (bf16, one scan group): the scan computes the output, from
     // Qf = diag(e^g) Q and Pf = (Q K^T o M) row fragments written by the WY
     // kernel (they reuse the Hs / Us workspace regions, which are then unused).
@@ -65,7 +67,7 @@ template <class E> struct Params {
 // Stage 1: per-chunk WY / UT transform.  Grid (NC, B*H), kWyWaves waves.
 // --------------------------------------------------------------------------
 // LDS: K rows, A (fp32; V rows take its place once the solve is done), T
-// (fp32), gates.  52.5 KB on the bf16 path at D = 128: three workgroups per CU.
+// (fp32), gates.  52.3 KB on the bf16 path at D = 128: three workgroups per CU.
 template <class E, int DK, int DV> struct WyLds {
     static constexpr int PAD = 16 / (int)sizeof(E);
     static constexpr int LDK = DK + PAD;      // K, row-major (token rows)
@@ -77,7 +79,7 @@ template <class E, int DK, int DV> struct WyLds {
     static constexpr size_t oA = oK + sizeof(E) * kChunk * LDK;  // A, then V
     static constexpr size_t oT = oA + (szA > szV ? szA : szV);
     static constexpr size_t oG = oT + szA;
-    static constexpr size_t bytes = oG + 8 * kChunk + 4 * 4 * kChunk;
+    static constexpr size_t bytes = oG + 8 * kChunk + 3 * 4 * kChunk;
     // waves per SIMD when as many eight-wave workgroups as fit in 160 KB share
     // a CU (the register budget the kernel is compiled for)
     static constexpr int fit = (int)((160 * 1024) / bytes);
@@ -111,7 +113,7 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
     constexpr int NKV = kChunk * (DK / VE) / NT;   // K vectors per thread
     constexpr int NVV = kChunk * (DV / VE) / NT;   // V vectors per thread
     static_assert(NKV * NT == kChunk * (DK / VE) && NVV * NT == kChunk * (DV / VE), "whole vectors per thread");
-    constexpr int NFR = (DK / 64) * 8;             // W (and Kt) fragments per chunk
+    constexpr int NFR = (DK / 64) * 8;             // W fragments per chunk
     constexpr double kLog2e = 1.4426950408889634;
     extern __shared__ __align__(16) unsigned char smem[];
     E *sK = (E *)(smem + L::oK);
@@ -121,8 +123,7 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
     double *sg = (double *)(smem + L::oG);        // g_r
     float *sb = (float *)(sg + kChunk);           // beta_r
     float *sw = sb + kChunk;                      // -beta_r e^{g_r}
-    float *sd = sw + kChunk;                      // e^{g_C - g_r}
-    float *sgl = sd + kChunk;                     // g_r log2(e) in fp32 (bf16 path)
+    float *sgl = sw + kChunk;                     // g_r log2(e) in fp32 (bf16 path)
 
     const int c = blockIdx.x, bh = blockIdx.y;
     const int b = bh / p.H, h = bh - b * p.H;
@@ -175,13 +176,17 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
             if (l >= d) g += o;
         }
         const double gC = __shfl(g, kChunk - 1);
+        const float eg = __builtin_amdgcn_exp2f((float)(g * kLog2e));
         sg[l] = g;
         sgl[l] = (float)(g * kLog2e);
         sb[l] = be;
-        sw[l] = -be * __builtin_amdgcn_exp2f((float)(g * kLog2e));
-        sd[l] = __builtin_amdgcn_exp2f((float)((gC - g) * kLog2e));
+        sw[l] = -be * eg;
         p.g[cidx * kChunk + l] = g;
-        if (l == 0) p.gc[cidx] = gC;
+        p.gf[cidx * kGateRec + l] = __builtin_amdgcn_exp2f((float)((gC - g) * kLog2e));
+        if (l == 0) {
+            *(double *)(p.gf + cidx * kGateRec + kChunk) = gC;
+            p.gf[cidx * kGateRec + kChunk + 2] = expf((float)gC);
+        }
     }
 #pragma unroll
     for (int n = 0; n < NKV; ++n) {
@@ -225,9 +230,9 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
     lds_barrier();
 
     // T = (I + A)^{-1} in fp32.  Wave 0 inverts the four diagonal 16x16 blocks
-    // by forward substitution (lane = block * 16 + column) while the other
-    // waves produce the fused-output fragments and the Kt fragments, which
-    // need only Q, K and the gates.
+    // by forward substitution (lane = block * 16 + column) while waves 1..6
+    // produce the fused-output score fragments, which need only Q, K and the
+    // gates.
     if (w == 0) {
         const int base = 16 * (l >> 4), j = l & 15;
         float x[16];
@@ -250,9 +255,9 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
         // Fused output: job (rt, m) writes, for token tile rt,
         //   Qf[rt][kb][lane][e] = e^{g_r} Q[r][32 kb + 8 lg + e]      (m = 0 jobs)
         //   Pf[rt][m][lane][e]  = e^{g_r - g_s} q_r . k_s (s <= r, else 0), s = 32 m + 8 lg + e,
-        // the row fragments (B operands over d, resp. s) of the fused output.  P^T
-        // tiles take their s rows in P32 order, so a tile pair is one fragment;
-        // block m = 1 only matters for r >= 32.
+        // the row fragments (B operands over d, resp. s) of the fused output.
+        // P^T tiles take their s rows in P32 order, so a tile pair is one
+        // fragment; block m = 1 only matters for r >= 32.
         if constexpr (sizeof(E) == 2) {
             if (p.fused && qjob) {
                 if (qjob_m == 0) {
@@ -266,56 +271,23 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
                     }
                 }
                 E *Pf = p.Pf + cidx * (size_t)kChunk * kChunk + l * 8;
-                {
-                    const int m = qjob_m;
-                    typename TR::quad pq[2];
+                const int m = qjob_m;
+                typename TR::quad pq[2];
 #pragma unroll
-                    for (int a = 0; a < 2; ++a) {
-                        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+                for (int a = 0; a < 2; ++a) {
+                    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                        for (int kb = 0; kb < DK / 32; ++kb)
-                            acc = TR::mma(load_frag<E>(sK + (32 * m + p32_row(a, li)) * L::LDK + 32 * kb, lg), qf[kb], acc);
+                    for (int kb = 0; kb < DK / 32; ++kb)
+                        acc = TR::mma(load_frag<E>(sK + (32 * m + p32_row(a, li)) * L::LDK + 32 * kb, lg), qf[kb], acc);
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            const int s2 = 32 * m + 8 * lg + 4 * a + q;
-                            acc[q] = (s2 <= rq) ? wy_decay<E>(sg, sgl, rq, s2) * acc[q] : 0.f;
-                        }
-                        pq[a] = TR::from_f32(acc);
+                    for (int q = 0; q < 4; ++q) {
+                        const int s2 = 32 * m + 8 * lg + 4 * a + q;
+                        acc[q] = (s2 <= rq) ? wy_decay<E>(sg, sgl, rq, s2) * acc[q] : 0.f;
                     }
-                    TR::store8(Pf + (size_t)(qjob_rt * 2 + m) * 512, TR::cat(pq[0], pq[1]));
+                    pq[a] = TR::from_f32(acc);
                 }
+                TR::store8(Pf + (size_t)(qjob_rt * 2 + m) * 512, TR::cat(pq[0], pq[1]));
             }
-        }
-    }
-    {
-        // Kt fragment f = (wave * 4 + t) * 2 + m holds, for lane (li, lg),
-        // K[32 m + 8 lg + e][64 wave + 32 (t / 2) + p32_row(t % 2, li)] e^{g_C - g_s}.
-        // Every wave takes a share sized to its other work in this phase:
-        // with the fused output, wave 0 (diagonal inversion) takes 2 of 16,
-        // waves 1..4 (a score job and a Qf tile) 1 each, waves 5, 6 (a score
-        // job) 3 each and wave 7 4: fragments [kt_split(w), kt_split(w + 1))
-        // * NFR / 16; without it the waves split them evenly.
-        E *Kf = p.Kt + cidx * (size_t)DK * kChunk + l * 8;
-        const bool fused = sizeof(E) == 2 && p.fused;
-        static_assert(NWV == 8, "the Kt split assumes eight waves");
-        // (a select chain on the wave-uniform w: a constant table indexed by
-        // it would be read from memory)
-        auto kt_split = [](int i) {
-            return i <= 0 ? 0 : i == 1 ? 2 : i == 2 ? 3 : i == 3 ? 4 : i == 4 ? 5 : i == 5 ? 6 : i == 6 ? 9 : i == 7 ? 12 : 16;
-        };
-        const int f_lo = fused ? kt_split(w) * NFR / 16 : w * NFR / NWV;
-        const int f_cnt = (fused ? kt_split(w + 1) * NFR / 16 : (w + 1) * NFR / NWV) - f_lo;
-        constexpr int KT_MAX = (NFR * 4 + 15) / 16 > (NFR + NWV - 1) / NWV ? (NFR * 4 + 15) / 16 : (NFR + NWV - 1) / NWV;
-#pragma unroll
-        for (int i = 0; i < KT_MAX; ++i) {
-            if (i >= f_cnt) break;
-            const int f = f_lo + i;
-            const int wv = f >> 3, t = (f >> 1) & 3, m = f & 1;
-            const frag kv = tr_frag<E>(sK, L::LDK, 32 * m, 64 * wv + 32 * (t >> 1), true, t & 1, li, lg);
-            const f32x4 k0 = TR::to_f32(TR::lo(kv)), k1 = TR::to_f32(TR::hi(kv));
-            const int s0 = 32 * m + 8 * lg;
-            const f32x4 d0 = *(const f32x4 *)(sd + s0), d1 = *(const f32x4 *)(sd + s0 + 4);
-            TR::store8(Kf + f * 512, TR::cat(TR::from_f32(k0 * d0), TR::from_f32(k1 * d1)));
         }
     }
     lds_barrier();
@@ -414,9 +386,10 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
 }
 
 // --------------------------------------------------------------------------
-// Stage 2: the state recurrence across chunks, H_c = gamma_c H_{c-1} + Kt_c^T U_c
-// with U_c = Ut_c - W_c H_{c-1}, i.e. H_c = A_c H_{c-1} + B_c with the affine
-// chunk transfer A_c = gamma_c I - Kt_c^T W_c, B_c = Kt_c^T Ut_c (the token-wise
+// Stage 2: the state recurrence across chunks, H_c = gamma_c H_{c-1} + K_c^T D_c U_c
+// with U_c = Ut_c - W_c H_{c-1} and D_c = diag(e^{g_C - g}), i.e.
+// H_c = A_c H_{c-1} + B_c with the affine chunk transfer
+// A_c = gamma_c I - K_c^T D_c W_c, B_c = K_c^T D_c Ut_c (the token-wise
 // counterpart of the paper's S_f = alpha_f P_f S_{f-1} + A_f).  The chunks are
 // cut into groups of G; the sequential dependency is reduced to one step per
 // group:
@@ -434,9 +407,12 @@ __attribute__((amdgpu_waves_per_eu(WyLds<E, DK, DV>::waves_per_simd))) void gdn_
 // (b, h, group).  It has NCW compute waves, each carrying 16 * CT columns over
 // all Dk rows through the group's chunks in fp32 accumulators (so U = Ut - W H
 // needs no exchange between waves), and two loader waves that stream the chunk
-// operands (-W, Kt, and the workgroup's Ut columns) into an LDS ring of DEPTH
-// slots with asynchronous global->LDS copies (1 KB per instruction, lane i's
-// 16 bytes landing at +16 i, so the fragment-major workspace layout is kept).
+// operands (-W, the chunk's key rows read from the input, the workgroup's Ut
+// columns and the key scales e^{g_C - g}) into an LDS ring of DEPTH slots with
+// asynchronous global->LDS copies (1 KB per instruction, lane i's 16 bytes
+// landing at +16 i: the fragment-major workspace layout is kept, and each key
+// row's 16-byte pieces land permuted, see kswz).  The update takes
+// K^T (diag(e^{g_C - g}) U): the key scales are applied to U in registers.
 // One workgroup barrier per chunk hands a slot over: before barrier c the
 // loaders have waited (vmcnt) for chunk c's copies; after it they refill the
 // slot of chunk c - 1, which every compute wave has finished reading.  The
@@ -447,7 +423,7 @@ enum { SCAN_TRANS = 0, SCAN_STATES = 1 };
 
 // Column tiles per compute wave and compute waves per workgroup for the
 // grouped passes; a single-group scan uses one column tile and one compute
-// wave per workgroup (every workgroup loads all of W and Kt each chunk, so
+// wave per workgroup (every workgroup loads all of W and K each chunk, so
 // narrow workgroups spread that traffic over more CUs).
 template <class E> struct ScanCT { static constexpr int value = sizeof(E) == 2 ? 2 : 1; };
 constexpr int kScanNCW = 2;
@@ -455,15 +431,17 @@ constexpr int kScanNCW = 2;
 template <class E, int DK, int CT, int NCW, bool FUSE = false> struct ScanLds {
     static constexpr int KB = DK / 32;                     // 32-row blocks of the state
     static constexpr int NT = DK / 16;                     // 16-row tiles of the state
-    static constexpr int WK = kChunk * DK;                 // elements of -W (and of Kt) per chunk
+    static constexpr int WK = kChunk * DK;                 // elements of -W (and of K) per chunk
     static constexpr int UT = NCW * CT * 1024;             // elements of the workgroup's Ut per chunk
-    static constexpr int SLOT = 2 * WK + UT;               // ring slot: -W, Kt, Ut
+    static constexpr int oD = 2 * WK + UT;                 // key scales, g_C: one gate record
+    static constexpr int SLOT = oD + 4 * kGateRec / (int)sizeof(E);  // ring slot: -W, K rows, Ut, gates
     static constexpr int SLOT_BYTES = SLOT * (int)sizeof(E);
-    static constexpr int NC_W = WK * (int)sizeof(E) / 1024;   // 1 KB copies of -W (and of Kt)
+    static constexpr int NC_W = WK * (int)sizeof(E) / 1024;   // 1 KB copies of -W (and of K)
     static constexpr int NC_U = UT * (int)sizeof(E) / 1024;
-    // loader 0 copies -W and the first half of Ut, loader 1 Kt and the rest
+    // loader 0 copies -W, the first half of Ut and the gate record (one
+    // 17-lane copy), loader 1 the key rows and the rest of Ut
     static constexpr int NC_U0 = NC_U / 2, NC_U1 = NC_U - NC_U0;
-    static constexpr int NCOPY0 = NC_W + NC_U0, NCOPY1 = NC_W + NC_U1;
+    static constexpr int NCOPY0 = NC_W + NC_U0 + 1, NCOPY1 = NC_W + NC_U1;
     static constexpr int LDS_CAP = 152 * 1024;
     // fused output: H_{c-1} (KB fragments) and U (2) per column tile handed
     // from each compute wave to its output wave, double-buffered
@@ -489,6 +467,41 @@ template <int N> __device__ __forceinline__ void copy_kb(const void *src, void *
                                          16, 0, 0);
 }
 
+// Key rows in the scan's LDS ring: row r (a token of the chunk) holds its DK
+// elements with the 16-byte granules permuted, granule g stored at g ^ kswz(r).
+// The update's A operand is read with transposing reads, whose 16 lanes take
+// 4 consecutive rows x 4 consecutive granules: the permutation sends them to
+// 16 distinct bank groups.  kswz(r + 4) = kswz(r) for the rows r = 8 i + j,
+// j < 4, those reads start from.  fp32 rows are gathered element by element
+// and stay in order.
+template <class E, int DK> __device__ __forceinline__ int kswz(int r) {
+    constexpr int GPR = DK * (int)sizeof(E) / 16;  // granules per row
+    if constexpr (sizeof(E) == 4)
+        return 0;
+    else if constexpr (GPR == 16)
+        return 4 * (r & 3);         // 256-byte rows: the 4 rows take disjoint granule quads
+    else
+        return 4 * ((r >> 1) & 1);  // 128-byte rows: two per bank line, the pairs take disjoint quads
+}
+
+// Update A-operand fragment from the ring's key rows Kr (the tr_frag read in
+// P32 order, through the permutation): lane (li, lg) receives
+// K[row0 + 8 lg + q'][colbase + p32_row(a, li)], q' = 0..7.
+template <class E, int DK>
+__device__ __forceinline__ typename Tr<E>::frag kt_frag(const E *Kr, int row0, int colbase, int a, int li,
+                                                        int lg) {
+    if constexpr (sizeof(E) == 2) {
+        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+        const int row = row0 + 8 * lg + (li >> 2);
+        const int off = 8 * ((colbase / 8 + (li & 3)) ^ kswz<E, DK>(row)) + 4 * a;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(Kr + row * DK + off));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(Kr + (row + 4) * DK + off));
+        return Tr<E>::cat(__builtin_bit_cast(u32x2, lo), __builtin_bit_cast(u32x2, hi));
+    } else {
+        return tr_frag<E>(Kr, DK, row0, colbase, true, a, li, lg);
+    }
+}
+
 template <class E, int DK, int DV, int PHASE, int CT, int NCW, bool FUSE = false>
 __global__ __launch_bounds__((NCW * (FUSE ? 2 : 1) + 2) * 64) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gdn_chunkscan_kernel(Params<E> p) {
@@ -498,6 +511,9 @@ void gdn_chunkscan_kernel(Params<E> p) {
     static_assert(!FUSE || PHASE == SCAN_STATES, "the output is fused into the state pass only");
     constexpr int NOW = FUSE ? NCW : 0;                  // output waves
     constexpr int D = L::DEPTH;
+    // compute waves read the next chunk's operands ahead when the ring has
+    // room for it (four slots: the loaders then still issue two chunks ahead)
+    constexpr int AHEAD = D >= 4 ? 1 : 0;
     constexpr int KB = L::KB, NT = L::NT;
     constexpr int WGC = NCW * 16 * CT;                   // columns per workgroup
     constexpr int WCOLS = PHASE == SCAN_TRANS ? DK + DV : DV;
@@ -509,11 +525,12 @@ void gdn_chunkscan_kernel(Params<E> p) {
     // XCD-aware placement: workgroups are dealt round-robin to the 8 XCDs, so
     // id = 8 slot + x runs on XCD x.  The NJB column blocks of one (b, h, group)
     // get consecutive slots of the same XCD and share its L2 for the chunk
-    // operands W, Kt that all of them read.
+    // operands W, K that all of them read.
     const int id = blockIdx.x, x = id & 7, slot = id >> 3;
     const int unit = (slot / NJB) * 8 + x, jb = slot % NJB;
     if (unit >= p.B * p.H * p.NG) return;
     const int bh = unit / p.NG, grp = unit - bh * p.NG;
+    const int b = bh / p.H, h = bh - b * p.H;
     const int c_begin = grp * p.G, c_end = min(p.NC, c_begin + p.G);
     // w is wave-uniform: scalar branches and addresses
     const int tid = threadIdx.x, w = __builtin_amdgcn_readfirstlane(tid >> 6), l = tid & 63, li = l & 15,
@@ -534,6 +551,25 @@ void gdn_chunkscan_kernel(Params<E> p) {
     if (w >= NCW + NOW) {
         // ---------------- loader waves ----------------
         const int ld = w - NCW - NOW;
+        // Key rows of chunk `src` from the input (B, T, H, DK): instruction n,
+        // lane l fills LDS granule 64 n + l, i.e. granule (64 n + l) % GPR of
+        // row (64 n + l) / GPR, from the row's granule permuted back by kswz.
+        // Rows past the sequence's end are read from its last token; their
+        // pseudo-values are exactly zero (beta = 0 and zero V and K rows in the
+        // WY factors), so they add nothing to the update.
+        auto copy_krows = [&](int src, E *dst) {
+            constexpr int GPR = DK * (int)sizeof(E) / 16, VE = 16 / (int)sizeof(E);
+            const int t0 = src * kChunk, tl = p.T - 1;
+            const E *kbase = p.k + (size_t)b * p.T * p.H * DK + (size_t)h * DK;
+#pragma unroll
+            for (int n = 0; n < L::NC_W; ++n) {
+                const int idx = 64 * n + l, r = idx / GPR, g = (idx % GPR) ^ kswz<E, DK>(r);
+                const int t = min(t0 + r, tl);
+                __builtin_amdgcn_global_load_lds((const void *)(kbase + (size_t)t * p.H * DK + g * VE),
+                                                 (__attribute__((address_space(3))) void *)((char *)dst + 1024 * n),
+                                                 16, 0, 0);
+            }
+        };
         // copies of chunk `src` into the slot of chunk `dst` (dst = src except
         // past the end, see below)
         auto issue = [&](int dst, int src) {
@@ -543,22 +579,28 @@ void gdn_chunkscan_kernel(Params<E> p) {
             if (ld == 0) {
                 copy_kb<L::NC_W>(p.W + cidx * (size_t)L::WK, sl, l);
                 if (has_ut) copy_kb<L::NC_U0>(ut, sl + 2 * L::WK, l);
+                if (l < kGateRec / 4)  // the gate record: 272 bytes
+                    __builtin_amdgcn_global_load_lds((const void *)(p.gf + cidx * kGateRec + 4 * l),
+                                                     (__attribute__((address_space(3))) void *)(sl + L::oD), 16, 0,
+                                                     0);
             } else {
-                copy_kb<L::NC_W>(p.Kt + cidx * (size_t)L::WK, sl + L::WK, l);
+                copy_krows(src, sl + L::WK);
                 if (has_ut)
                     copy_kb<L::NC_U1>((const char *)ut + 1024 * L::NC_U0,
                                       (char *)(sl + 2 * L::WK) + 1024 * L::NC_U0, l);
             }
         };
-        // Chunk c's copies have landed once at most D - 2 younger chunks' are
-        // in flight (every chunk issues the same number of copies).
+        // Chunk c (with AHEAD chunk c + 1) has landed once at most D - 2
+        // (D - 3) younger chunks' copies are in flight (every chunk issues the
+        // same number of copies).
+        constexpr int NF = D - 2 - AHEAD;
         auto wait_oldest = [&]() {
             if (ld == 0) {
-                if (has_ut) wait_vmcnt<(D - 2) * L::NCOPY0>();
-                else wait_vmcnt<(D - 2) * L::NC_W>();
+                if (has_ut) wait_vmcnt<NF * L::NCOPY0>();
+                else wait_vmcnt<NF * (L::NC_W + 1)>();
             } else {
-                if (has_ut) wait_vmcnt<(D - 2) * L::NCOPY1>();
-                else wait_vmcnt<(D - 2) * L::NC_W>();
+                if (has_ut) wait_vmcnt<NF * L::NCOPY1>();
+                else wait_vmcnt<NF * L::NC_W>();
             }
         };
         // Prologue: chunks c_begin .. c_begin + D - 2.  Past the end the loaders
@@ -591,7 +633,6 @@ void gdn_chunkscan_kernel(Params<E> p) {
             // Lane (li, lg) gets O[16 rt + li][jw + 16 ct + 4 lg + q].
             const int wo = w - NCW;
             const int jw = wbase + 16 * CT * wo;
-            const int b = bh / p.H, h = bh - b * p.H;
             // Operands of chunk c live in register set (c - c_begin) & 1: at
             // barrier c the wave requests chunk c's and finishes chunk c - 1
             // from the other set, so a load is consumed one chunk later.
@@ -689,120 +730,169 @@ void gdn_chunkscan_kernel(Params<E> p) {
     }
     double lgam = 0.0;  // sum of gC over the group
 
-    // Blocks of 64 chunks: gC of chunk cblk + i sits in lane i of gcl.
-    for (int cblk = c_begin; cblk < c_end; cblk += 64) {
-        const double gcl = (cblk + l < c_end) ? p.gc[(size_t)bh * p.NC + cblk + l] : 0.0;
-        const int cstop = min(c_end, cblk + 64);
-        for (int c = cblk; c < cstop; ++c) {
-            const size_t cidx = (size_t)bh * p.NC + c;
-            const unsigned long long gbits = __builtin_bit_cast(unsigned long long, gcl);
-            const double gC = __builtin_bit_cast(
-                double, ((unsigned long long)(unsigned)__builtin_amdgcn_readlane((int)(gbits >> 32), c - cblk)
-                         << 32) |
-                            (unsigned)__builtin_amdgcn_readlane((int)gbits, c - cblk));
-            lds_only_barrier();  // chunk c's operands are in its slot
-            const E *sl = slot_of(c);
-            const E *Wl = sl + l * 8;
-            const E *Kl = sl + L::WK + l * 8;
-            const E *Ul = sl + 2 * L::WK + (size_t)w * CT * 1024 + l * 4;
+    // Operands of one chunk, read from its ring slot (fragment layouts below).
+    // With AHEAD the wave reads chunk c + 1's slot while it computes chunk c,
+    // so the LDS latency stays off the chain.
+    struct Ops {
+        frag wf[KB][4], kf[NT][2];
+        typename TR::quad us[4][CT];
+        f32x4 dsc[4];
+        double gC;
+        float gam;
+    };
+    //   -W fragment (wave kb / 2, token tile st, k block kb % 2),
+    //   K^T fragment (row tile t, token block m): rows d in P32 order
+    //     32 (t / 2) + p32_row(t % 2, li), tokens 32 m + 8 lg + e,
+    //   U~t quad of token tile st = 2 m + a: tokens 32 m + 8 lg + 4 a + q
+    //     (zero for Phi columns), and the key scales of the same tokens,
+    //   g_C and gamma = e^{g_C} (broadcast reads).
+    auto read_ops = [&](int c, Ops &o) {
+        const E *sl = slot_of(c);
+        const float *Dl = (const float *)(sl + L::oD);
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+            for (int st = 0; st < 4; ++st)
+                o.us[st][ct] = has_ut ? TR::load(sl + 2 * L::WK + (size_t)w * CT * 1024 + l * 4 + ct * 1024 + st * 256)
+                                      : TR::zero();
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int a = 0; a < 2; ++a) {
+                    const int st = 2 * m + a;
+                    o.wf[kb][st] = TR::load8(sl + l * 8 + (((kb >> 1) * 4 + st) * 2 + (kb & 1)) * 512);
+                }
+#pragma unroll
+        for (int m = 0; m < 2; ++m)
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+                o.kf[t][m] = kt_frag<E, DK>(sl + L::WK, 32 * m, 32 * (t >> 1), t & 1, li, lg);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) o.dsc[st] = *(const f32x4 *)(Dl + 32 * (st >> 1) + 8 * lg + 4 * (st & 1));
+        o.gC = *(const double *)(Dl + kChunk);
+        o.gam = Dl[kChunk + 2];
+    };
 
-            // All operand fragments of the chunk, read up front so the LDS
-            // latency overlaps the MFMA chain (the U~t seeds first: the first
-            // MFMAs need them):
-            //   -W fragment (wave kb / 2, token tile st, k block kb % 2),
-            //   Kt fragment (row tile t = 4 v + t', token block m) at (2 t + m).
-            // U = U~t - W H (the workspace holds -W): token tile st = 2 m + a
-            // holds tokens 32 m + 8 lg + 4 a + q; the MFMAs start from U~t
-            // (zero for Phi columns).
-            f32x4 part[4][CT];
+    // bf16: the U~t seeds enter the accumulators through an MFMA with a 0/1
+    // selection operand (exact: one product 1 x u per entry), so no VALU
+    // unpacking sits before the first W H MFMA.  sel[a] places the 32-token
+    // B fragment cat(us[2 m], us[2 m + 1]) (lane (li, lg): tokens 32 m + 8 lg
+    // + e') in the rows of tile 2 m + a, i.e. tile row i takes token
+    // 32 m + p32_row(a, i): lane (li, lg) of sel[a] holds 1 at e' = 4 a +
+    // li % 4 when lg = li / 4, else 0.
+    frag sel[2];
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
-#pragma unroll
-                for (int st = 0; st < 4; ++st)
-                    part[st][ct] = has_ut ? TR::to_f32(TR::load(Ul + ct * 1024 + st * 256)) : f32x4{0.f, 0.f, 0.f, 0.f};
-            frag wf[KB][4], kf[NT][2];
-#pragma unroll
-            for (int m = 0; m < 2; ++m)
-#pragma unroll
-                for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                    for (int a = 0; a < 2; ++a) {
-                        const int st = 2 * m + a;
-                        wf[kb][st] = TR::load8(Wl + (((kb >> 1) * 4 + st) * 2 + (kb & 1)) * 512);
-                    }
-#pragma unroll
-            for (int m = 0; m < 2; ++m)
-#pragma unroll
-                for (int t = 0; t < NT; ++t) kf[t][m] = TR::load8(Kl + (t * 2 + m) * 512);
+    for (int a = 0; a < 2; ++a) {
+        f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = {0.f, 0.f, 0.f, 0.f};
+        if (lg == (li >> 2)) {
+            if (a == 0) lo[li & 3] = 1.f;
+            else hi[li & 3] = 1.f;
+        }
+        sel[a] = TR::cat(TR::from_f32(lo), TR::from_f32(hi));
+    }
 
-            // H_{c-1} rounded to E: B operands over the KB 32-row blocks.
-            frag hb[KB][CT];
+    // One chunk: U = U~t - W H_{c-1} (the workspace holds -W), then
+    // H_c = gamma H_{c-1} + K^T (diag(e^{g_C - g}) U).  The chain per token
+    // half m: its W H MFMAs, the conversion of its U half (as is, for the
+    // output, and scaled by e^{g_C - g}, for the update), then that half's
+    // update.  Half 0 is finished first, so its conversion overlaps the MFMAs
+    // of half 1, and half 1's conversion those of the first update.  The
+    // output wave's operands (H_{c-1}, then each U half) are handed off as
+    // soon as they exist, so the stores have drained by the next barrier.
+    auto step = [&](int c, const Ops &o) {
+        const size_t cidx = (size_t)bh * p.NC + c;
+        const int i = (c - c_begin) & 1;
+        // H_{c-1} rounded to E: B operands over the KB 32-row blocks.
+        frag hb[KB][CT];
 #pragma unroll
-            for (int ct = 0; ct < CT; ++ct)
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-                for (int kb = 0; kb < KB; ++kb)
-                    hb[kb][ct] = TR::cat(TR::from_f32(Hacc[2 * kb][ct]), TR::from_f32(Hacc[2 * kb + 1][ct]));
-            // The chain per token half m: its W H MFMAs, the conversion of its
-            // U half, then that half's Kt^T U update.  Half 0 is finished
-            // first, so its conversion and the decay of H overlap the MFMAs
-            // of half 1, and half 1's conversion those of the first update.
-            frag ub[2][CT];
-            auto wh_half = [&](int m) {
+            for (int kb = 0; kb < KB; ++kb) {
+                hb[kb][ct] = TR::cat(TR::from_f32(Hacc[2 * kb][ct]), TR::from_f32(Hacc[2 * kb + 1][ct]));
+                if constexpr (FUSE) *hoff_at(i, w, ct, kb) = hb[kb][ct];
+            }
+        lgam += o.gC;
 #pragma unroll
-                for (int kb = 0; kb < KB; ++kb)
+        for (int t = 0; t < NT; ++t)
 #pragma unroll
-                    for (int a = 0; a < 2; ++a)
+            for (int ct = 0; ct < CT; ++ct) Hacc[t][ct] *= o.gam;
+        f32x4 part[4][CT];
 #pragma unroll
-                        for (int ct = 0; ct < CT; ++ct)
-                            part[2 * m + a][ct] = TR::mma(wf[kb][2 * m + a], hb[kb][ct], part[2 * m + a][ct]);
-            };
-            auto cvt_half = [&](int m) {
+        for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-                for (int ct = 0; ct < CT; ++ct)
-                    ub[m][ct] = TR::cat(TR::from_f32(part[2 * m][ct]), TR::from_f32(part[2 * m + 1][ct]));
-            };
-            auto kt_half = [&](int m) {
+            for (int st = 0; st < 4; ++st) {
+                if constexpr (sizeof(E) == 2)
+                    part[st][ct] = TR::mma(sel[st & 1], TR::cat(o.us[st & 2][ct], o.us[(st & 2) + 1][ct]),
+                                           f32x4{0.f, 0.f, 0.f, 0.f});
+                else
+                    part[st][ct] = TR::to_f32(o.us[st][ct]);
+            }
+        frag ub[2][CT], uk[2][CT];
+        auto wh_half = [&](int m) {
 #pragma unroll
-                for (int t = 0; t < NT; ++t)
+            for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-                    for (int ct = 0; ct < CT; ++ct) Hacc[t][ct] = TR::mma(kf[t][m], ub[m][ct], Hacc[t][ct]);
-            };
-            wh_half(0);
-            wh_half(1);
-            cvt_half(0);
-            lgam += gC;
-            const float gam = expf((float)gC);
+                for (int a = 0; a < 2; ++a)
+#pragma unroll
+                    for (int ct = 0; ct < CT; ++ct)
+                        part[2 * m + a][ct] = TR::mma(o.wf[kb][2 * m + a], hb[kb][ct], part[2 * m + a][ct]);
+        };
+        auto cvt_half = [&](int m) {
+#pragma unroll
+            for (int ct = 0; ct < CT; ++ct) {
+                ub[m][ct] = TR::cat(TR::from_f32(part[2 * m][ct]), TR::from_f32(part[2 * m + 1][ct]));
+                uk[m][ct] = TR::cat(TR::from_f32(part[2 * m][ct] * o.dsc[2 * m]),
+                                    TR::from_f32(part[2 * m + 1][ct] * o.dsc[2 * m + 1]));
+                if constexpr (FUSE) *hoff_at(i, w, ct, KB + m) = ub[m][ct];
+            }
+        };
+        auto kt_half = [&](int m) {
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
-                for (int ct = 0; ct < CT; ++ct) Hacc[t][ct] *= gam;
-            kt_half(0);
-            cvt_half(1);
-            kt_half(1);
-            if constexpr (FUSE) {
-                // hand H_{c-1} and U to the output wave (it reads them after
-                // the next barrier; the buffers alternate per chunk)
-                const int i = (c - c_begin) & 1;
+                for (int ct = 0; ct < CT; ++ct) Hacc[t][ct] = TR::mma(o.kf[t][m], uk[m][ct], Hacc[t][ct]);
+        };
+        wh_half(0);
+        wh_half(1);
+        cvt_half(0);
+        kt_half(0);
+        cvt_half(1);
+        kt_half(1);
+        if constexpr (PHASE == SCAN_STATES && !FUSE) {
 #pragma unroll
-                for (int ct = 0; ct < CT; ++ct) {
+            for (int ct = 0; ct < CT; ++ct) {
 #pragma unroll
-                    for (int kb = 0; kb < KB; ++kb) *hoff_at(i, w, ct, kb) = hb[kb][ct];
-                    *hoff_at(i, w, ct, KB) = ub[0][ct];
-                    *hoff_at(i, w, ct, KB + 1) = ub[1][ct];
-                }
-            } else if (PHASE == SCAN_STATES) {
-#pragma unroll
-                for (int ct = 0; ct < CT; ++ct) {
-#pragma unroll
-                    for (int kb = 0; kb < KB; ++kb)
-                        TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)(jw + 16 * ct + li) * DK + 32 * kb + 8 * lg,
-                                   hb[kb][ct]);
-                    E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)(jw + 16 * ct + li) * kChunk + 8 * lg;
-                    TR::store8(Us, ub[0][ct]);
-                    TR::store8(Us + 32, ub[1][ct]);
-                }
+                for (int kb = 0; kb < KB; ++kb)
+                    TR::store8(p.Hs + cidx * (size_t)DV * DK + (size_t)(jw + 16 * ct + li) * DK + 32 * kb + 8 * lg,
+                               hb[kb][ct]);
+                E *Us = p.Us + cidx * (size_t)DV * kChunk + (size_t)(jw + 16 * ct + li) * kChunk + 8 * lg;
+                TR::store8(Us, ub[0][ct]);
+                TR::store8(Us + 32, ub[1][ct]);
             }
         }
+    };
+
+    // Barrier c hands over chunk c (and, with AHEAD, chunk c + 1: the loaders
+    // wait one chunk further).  Operand sets alternate between chunks.
+    Ops opA, opB;
+    for (int c = c_begin; c < c_end; c += 2) {
+        lds_only_barrier();  // barrier c
+        if constexpr (AHEAD) {
+            if (c == c_begin) read_ops(c, opA);
+            read_ops(c + 1, opB);  // past the end: a padding slot, not used
+        } else {
+            read_ops(c, opA);
+        }
+        step(c, opA);
+        if (c + 1 >= c_end) break;
+        lds_only_barrier();  // barrier c + 1
+        if constexpr (AHEAD)
+            read_ops(c + 2, opA);
+        else
+            read_ops(c + 1, opB);
+        step(c + 1, opB);
     }
     lds_only_barrier();  // the loaders have drained: the ring is free
 

@@ -64,22 +64,23 @@ def test_scan_group_size():
 
 def test_workspace_bytes():
     nch = 16 * 55
-    # g, gC, -W, Kt, Ut, Hs, Us
-    base = nch * 64 * 8 + nch * 8 + nch * 2 * (64 * 128 * 4 + 128 * 128)
+    # g, gate records (key decay factors and g_C), -W, Ut, Hs, Us
+    gates = nch * 64 * 8 + nch * 68 * 4
+    base = gates + nch * 2 * (64 * 128 * 2 + 128 * 128 + 128 * 64)
     # one scan group on the bf16 path: the output is fused into the scan and the
     # last two regions hold the scaled queries (64 x 128) and scores (64 x 64)
-    fused = nch * 64 * 8 + nch * 8 + nch * 2 * (64 * 128 * 4 + 64 * 64)
+    fused = gates + nch * 2 * (64 * 128 * 3 + 64 * 64)
     n = gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 64, True)
-    assert fused <= n < fused + 11 * 256
+    assert fused <= n < fused + 10 * 256
     assert n == gdn.gdn_workspace_bytes_ex(1, 16, 3520, 128, 128, 64, True, 0)
     n32 = gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 64, False)   # fp32: per-chunk states
-    base32 = nch * 64 * 8 + nch * 8 + nch * 4 * (64 * 128 * 4 + 128 * 128)
-    assert base32 <= n32 < base32 + 11 * 256
+    base32 = gates + nch * 4 * (64 * 128 * 2 + 128 * 128 + 128 * 64)
+    assert base32 <= n32 < base32 + 10 * 256
     # 11 groups of 5 chunks add N (bf16), Psi^T, log Gamma and entry states (fp32)
     ngr = 16 * 11
     grouped = gdn.gdn_workspace_bytes_ex(1, 16, 3520, 128, 128, 64, True, 5)
     expect = base + ngr * (128 * 128 * 2 + 128 * 128 * 4 * 2 + 8)
-    assert expect <= grouped < expect + 11 * 256
+    assert expect <= grouped < expect + 10 * 256
     assert gdn.gdn_workspace_bytes(1, 16, 3520, 96, 128, 64, True) == 0
     assert gdn.gdn_workspace_bytes(1, 16, 3520, 128, 128, 32, True) == 0
     assert gdn.gdn_workspace_bytes(0, 16, 3520, 128, 128, 64, True) == 0

@@ -27,7 +27,6 @@
 namespace gdn {
 
 constexpr int kChunk = 64;  // tokens per chunk (one wavefront of lanes)
-constexpr int kGateRec = kChunk + 4;  // floats per chunk gate record of the token path
 constexpr float kLogAlphaMin = -87.3f;  // ~ log(FLT_MIN): alpha below this acts as 1.2e-38
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));

@@ -42,6 +42,8 @@
 
 namespace gdn {
 
+constexpr int kGateRec = kChunk + 4;  // floats per chunk gate record (see gf above)
+
 template <class E> struct Params {
     const E *q, *k, *v;
     const float *alpha, *beta, *state_in;

@@ -156,10 +156,11 @@ int gdn_workspace_check(int B, int H, int T, int Dk, int Dv, int chunk, int is_b
  * (bitwise the same outputs).  Shapes whose workspace, gdn_workspace_bytes(...,
  * is_bf16 = 1), exceeds GDN_NOALLOC_MAX_WORKSPACE return GDN_ERR_WORKSPACE
  * before anything is enqueued; one 1280x704 frame (B = 1, T = 3520, H = 16,
- * Dk = Dv = 128: 62.3 MiB) fits.  Every call on a GPU shares that GPU's array:
+ * Dk = Dv = 128: 48.8 MiB) fits.  Every call on a GPU shares that GPU's array:
  * calls that overlap on one GPU (several host threads, or streams not ordered
  * with each other) race and give wrong results.  No part of the array needs to
- * start at zero: a call writes every byte it reads.
+ * start at zero: every value a call uses was written earlier in the same call
+ * (its copies also move a few padding bytes that nothing uses).
  */
 #define GDN_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
 int gdn_chunk_forward_noalloc(const void *q, const void *k, const void *v,

@@ -279,6 +279,20 @@ FRAME_KERNELS = {"summaries": "gdn_frame_summary_kernel", "reduce": "gdn_frame_r
 
 
 def frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=2, norm=False, bidir=False, fused=False):
+    """See below; with fused and esz = 4 (the fp32 operator) the workspace also
+    carries the four feature maps (written once, each read once) and the gated
+    readout (written and read once)."""
+    r = _frame_counts(B, F, N, H, Dk, Dv, NS, esz, norm, bidir, fused)
+    if fused and esz == 4:
+        n = B * F * N * H
+        r["workspace"]["summaries"]["written"] += 4 * n * Dk * 4
+        r["workspace"]["summaries"]["read"] += 2 * n * Dk * 4
+        r["workspace"]["output"]["read"] += 2 * n * Dk * 4 + n * Dv * 4
+        r["workspace"]["output"]["written"] += n * Dv * 4
+    return r
+
+
+def _frame_counts(B, F, N, H, Dk, Dv, NS, esz, norm, bidir, fused):
     """Algorithmic flops per stage and the call's I/O bytes for the frame-wise path,
     plus each stage's workspace bytes (reported apart: not algorithmic).
 
@@ -365,11 +379,12 @@ def frame_cpu_baseline(inp, B, T, H, Dk, min_seconds=10.0, norm=False, bidir=Fal
                       f"fp64 {'bidirectional ' if bidir else ''}frame-wise recurrence, {elapsed:.1f} s"}
 
 
-def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fused=False):
+def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fused=False, f32=False):
     F, N = 3, 3520
     if fused:
         norm = True
-        inp = gdn_inputs.make_fused_inputs(2, F, frame_tokens=N, state="normal0.02", lat_w=80, t0=0)
+        inp = gdn_inputs.make_fused_inputs(2, F, frame_tokens=N, state="normal0.02", lat_w=80, t0=0,
+                                           dtype="f32" if f32 else "bf16")
     else:
         inp = gdn_inputs.make_frame_inputs(2, F, frame_tokens=N, state="normal0.02",
                                            features="relu" if norm else "gauss")
@@ -377,14 +392,14 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
     Dv = inp["v"].shape[-1]
     q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
     alpha, beta, s_in = to_dev(inp["alpha"]), to_dev(inp["beta"]), to_dev(inp["state_in"])
-    out = torch.empty((B, T, H, Dv), dtype=torch.bfloat16, device=dev)
+    out = torch.empty((B, T, H, Dv), dtype=q.dtype, device=dev)
     s_out = torch.empty((B, H, Dk, Dv), dtype=torch.float32, device=dev)
     z_in = to_dev(inp["z_in"]) if norm else None
     fz = {key: to_dev(inp[key]) for key in ("gate", "w_o", "gain_q", "gain_k", "rope_freq", "rope_axis")} if fused \
         else None
     z_out = torch.empty((B, H, Dk), dtype=torch.float32, device=dev) if norm else None
     ts = args.token_splits
-    ws = gdn.frame_workspace(q, v, N, ts)
+    ws = gdn.fused_workspace(q, v, N, ts) if fused else gdn.frame_workspace(q, v, N, ts)
     NS = gdn.gdn_frame_token_splits(B, H, F, N, Dk, Dv, ts)
     stream = torch.cuda.current_stream(dev)
 
@@ -423,7 +438,8 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
                                                 token_splits=ts, reps=args.steps, stream=stream)
     names = {k_: v_ for k_, v_ in zip(gdn.FRAME_STAGE_NAMES, stage_ms) if v_ > 0}
     torch.cuda.synchronize()
-    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, norm=norm, bidir=bidir, fused=fused)
+    esz = 4 if f32 else 2
+    cnt = frame_algorithmic_counts(B, F, N, H, Dk, Dv, NS, esz=esz, norm=norm, bidir=bidir, fused=fused)
     flops = sum(cnt["flops"].values())
     sec = ms_per_step / 1e3
     tflops = flops / sec / 1e12
@@ -431,16 +447,20 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
     # with the unidirectional one
     summary = ("traffic_frames3x1280x704_fused.json" if fused else
                "traffic_frames3x1280x704_norm.json" if norm else "traffic_frames3x1280x704.json")
-    traffic = load_traffic(summary)
+    traffic = None if f32 else load_traffic(summary)
     if traffic is not None and bidir:
         traffic = None
     kernels = dict(FRAME_KERNELS)
-    if fused:
+    if fused and f32:
+        kernels.update({"summaries": "gdn_frame_features_kernel + 2 x gdn_frame_summary_kernel<float>",
+                        "output": "gdn_frame_output_f32_fused_kernel + gdn_frame_project_f32_kernel"})
+    elif fused:
         kernels.update({"summaries": "gdn_frame_summary_fused_kernel", "output": "gdn_frame_output_fused_kernel"})
-    roofline = token_roofline(flops, cnt["io_bytes"], names, kernels, traffic, PEAK_BF16_TFLOPS,
-                              own_io=cnt["own_io"])
+    peak = PEAK_F32_TFLOPS if f32 else PEAK_BF16_TFLOPS
+    roofline = token_roofline(flops, cnt["io_bytes"], names, kernels, traffic, peak, own_io=cnt["own_io"])
     rec = {
-        "metric": FRAME_FUSED_METRIC + (" (bidirectional)" if bidir else "") if fused
+        "metric": (FRAME_FUSED_METRIC.replace(" bf16", " fp32") if f32 else FRAME_FUSED_METRIC)
+                  + (" (bidirectional)" if bidir else "") if fused
                   else (FRAME_BIDIR_NORM_METRIC if norm else FRAME_BIDIR_METRIC) if bidir
                   else (FRAME_NORM_METRIC if norm else FRAME_METRIC),
         "value": round(B * T / sec, 1),
@@ -452,10 +472,11 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "f32" if f32 else "bf16",
         "data": "synthetic",
         "config": {"workload": "frame-wise streaming call of 3 latent 1280x704 frames: B=1 F=3 "
-                               "N=3520 (44x80) H=16 Dk=Dv=128, bf16 q/k/v, one decay per frame, "
+                               "N=3520 (44x80) H=16 Dk=Dv=128, " + ("fp32" if f32 else "bf16") +
+                               " q/k/v, one decay per frame, "
                                "key scale 1/sqrt(Dk N), fp32 state in/out"
                                + ("; normalizer state in/out and normalized readout (eps 1e-6), "
                                   "non-negative (ReLU) feature maps" if norm and not fused else "")
@@ -466,7 +487,7 @@ def run_frame(args, torch, gdn, dev, to_dev, timed, norm=False, bidir=False, fus
                                   "the call's frames from zero)" if bidir else ""),
                    "B": B, "F": F, "N": N, "T": T, "H": H, "Dk": Dk, "Dv": Dv, "token_splits": NS},
         "tflops": round(tflops, 2),
-        "mfma_frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+        "mfma_frac": round(tflops / peak, 4),
         "hbm_frac_io": round(cnt["io_bytes"] / sec / 1e9 / PEAK_HBM_GBS, 4),
         "step_ms": stats(per_step),
         "ms_per_step_cold": None if cold is None else stats(cold),
@@ -496,12 +517,13 @@ def main():
                     help="run one plain device copy of this many MiB first (a known-size "
                          "reference for hardware traffic counters)")
     ap.add_argument("--path", choices=("token", "frame", "frame-norm", "frame-bidir", "frame-bidir-norm",
-                                       "frame-fused", "frame-fused-bidir"),
+                                       "frame-fused", "frame-fused-bidir", "frame-fused-f32",
+                                       "frame-fused-f32-bidir"),
                     default="token",
                     help="token: the token-wise chunk forward (default); frame: the frame-wise "
                          "forward; frame-norm: the frame-wise forward with the normalizer; "
                          "frame-bidir(-norm): their bidirectional forms; frame-fused(-bidir): the whole "
-                         "operator with its prologue and epilogue")
+                         "operator with its prologue and epilogue; frame-fused-f32(-bidir): its fp32 mode")
     ap.add_argument("--token-splits", type=int, default=0,
                     help="frame path: token splits per frame (0 = the library's choice)")
     args = ap.parse_args()
@@ -553,7 +575,7 @@ def main():
 
     if args.path.startswith("frame"):
         run_frame(args, torch, gdn, dev, to_dev, timed, norm=args.path.endswith("-norm"),
-                  bidir="-bidir" in args.path, fused="-fused" in args.path)
+                  bidir="-bidir" in args.path, fused="-fused" in args.path, f32="-f32" in args.path)
         return
 
     widx = args.workload

@@ -210,8 +210,9 @@ def rope_3d_params(Dk, base=10000.0):
 
 
 def make_fused_inputs(workload, frames, *, frame_tokens=None, B=None, H=None, Dk=None, Dv=None,
-                      state=None, seed=None, lat_w=80, t0=0):
-    """Draw one call's inputs for the fused operator (bf16): the raw query and
+                      state=None, seed=None, lat_w=80, t0=0, dtype="bf16"):
+    """Draw one call's inputs for the fused operator (dtype "bf16": q, k, v,
+    gate and W_o rounded to bf16 bit patterns; "f32": kept in fp32): the raw query and
     key projections (N(0, 1) with a per-token scale drawn from [0.2, 5], so the
     RMSNorm has work to do), v, the output gate pre-activation (N(0, 1)), the
     per-head projection W_o (N(0, 1 / Dv)), RMSNorm gains (uniform [0.5, 1.5]),
@@ -256,10 +257,12 @@ def make_fused_inputs(workload, frames, *, frame_tokens=None, B=None, H=None, Dk
     elif state != "zero":
         raise ValueError(state)
     freq, axis = rope_3d_params(Dk)
-    bf = f32_to_bf16_bits
+    if dtype not in ("bf16", "f32"):
+        raise ValueError(dtype)
+    bf = f32_to_bf16_bits if dtype == "bf16" else (lambda x: x)
     return dict(q=bf(q), k=bf(k), v=bf(v), gate=bf(gate), w_o=bf(w_o), alpha=alpha, beta=beta,
                 state_in=state_in, z_in=z_in, gain_q=gain_q, gain_k=gain_k, rope_freq=freq, rope_axis=axis,
-                lat_w=int(lat_w), t0=int(t0), frame_tokens=N, dtype="bf16")
+                lat_w=int(lat_w), t0=int(t0), frame_tokens=N, dtype=dtype)
 
 
 def make_device_inputs(workload, device, call=0, *, seed=None):

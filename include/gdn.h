@@ -377,8 +377,9 @@ int gdn_frame_profile_stages_bidir(const void *q, const void *k, const void *v,
  * the key rescale; subsection "Frame-wise delta-rule update", equations
  * appendix_gdn_kv_update and appendix_gdn_z_update; subsection "Normalized
  * readout and output projection", equations appendix_gdn_readout and
- * appendix_gdn_output; Algorithm alg:gdn-kernel).  bf16 only.  Per token n
- * and head h, from the raw projections q_n = q_raw[b][n][h], k_n (length Dk):
+ * appendix_gdn_output; Algorithm alg:gdn-kernel).  bf16 here; the _f32 calls
+ * below are the fp32 mode.  Per token n and head h, from the raw projections
+ * q_n = q_raw[b][n][h], k_n (length Dk):
  *
  *   r(x)  = gain o x / sqrt(mean_i x_i^2 + rms_eps)       (RMSNorm over Dk)
  *   q~ = ReLU(r_q(q_n)),   k~ = key_scale ReLU(r_k(k_n))   (unrotated features)
@@ -442,6 +443,54 @@ int gdn_frame_profile_stages_fused(const void *q_raw, const void *k_raw, const v
                                    float rms_eps, float eps, int bidirectional, int token_splits,
                                    void *ws, size_t ws_bytes, int reps, float *stage_ms,
                                    void *stream);
+
+/*
+ * The fused operator in fp32 (the paper's "ieee" precision mode, appendix "GDN
+ * Kernel Details", "Precision modes"): the same computation as
+ * gdn_frame_forward_fused with q_raw, k_raw, v, gate, w_o and out in fp32 and
+ * every feature, product and readout in fp32 (no bf16 rounding anywhere; the
+ * rotation angles in fp64 with accurate sines and cosines).  Arguments,
+ * layouts, aliasing rules and errors as the bf16 calls.  The workspace also
+ * holds the four feature maps and the gated readout (about
+ * 4 B T H (4 Dk + Dv) bytes on top): size it with
+ * gdn_frame_fused_workspace_bytes(..., is_bf16 = 0, ...).
+ * gdn_frame_profile_stages_fused_f32 times four stages: features and
+ * summaries, reduction, scan, output and projection.
+ */
+int gdn_frame_forward_fused_f32(const float *q_raw, const float *k_raw, const float *v,
+                                const float *gate, const float *w_o, const float *alpha,
+                                const float *beta, const float *gain_q, const float *gain_k,
+                                const float *rope_freq, const int *rope_axis,
+                                const float *state_in, const float *z_in, float *out,
+                                float *state_out, float *z_out, int B, int H, int F, int N,
+                                int Dk, int Dv, int lat_w, int t0, float key_scale,
+                                float rms_eps, float eps, int bidirectional, void *stream);
+
+int gdn_frame_forward_fused_f32_ex(const float *q_raw, const float *k_raw, const float *v,
+                                   const float *gate, const float *w_o, const float *alpha,
+                                   const float *beta, const float *gain_q, const float *gain_k,
+                                   const float *rope_freq, const int *rope_axis,
+                                   const float *state_in, const float *z_in, float *out,
+                                   float *state_out, float *z_out, int B, int H, int F, int N,
+                                   int Dk, int Dv, int lat_w, int t0, float key_scale,
+                                   float rms_eps, float eps, int bidirectional, int token_splits,
+                                   void *ws, size_t ws_bytes, void *stream);
+
+int gdn_frame_profile_stages_fused_f32(const float *q_raw, const float *k_raw, const float *v,
+                                       const float *gate, const float *w_o, const float *alpha,
+                                       const float *beta, const float *gain_q, const float *gain_k,
+                                       const float *rope_freq, const int *rope_axis,
+                                       const float *state_in, const float *z_in, float *out,
+                                       float *state_out, float *z_out, int B, int H, int F, int N,
+                                       int Dk, int Dv, int lat_w, int t0, float key_scale,
+                                       float rms_eps, float eps, int bidirectional,
+                                       int token_splits, void *ws, size_t ws_bytes, int reps,
+                                       float *stage_ms, void *stream);
+
+/* Workspace bytes the fused operator's _ex calls need (is_bf16 = 1: equal to
+ * gdn_frame_workspace_bytes; 0 for unsupported arguments). */
+size_t gdn_frame_fused_workspace_bytes(int B, int H, int F, int N, int Dk, int Dv, int is_bf16,
+                                       int token_splits);
 
 /* Static, human-readable text for a status code. */
 const char *gdn_status_string(int status);

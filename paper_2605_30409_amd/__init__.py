@@ -10,7 +10,7 @@ operator with its prologue and epilogue (``frame_forward_fused``).
 """
 from .gdn import (CHUNK, FRAME_STAGE_NAMES, STAGE_NAMES, GdnError, LIB_PATH,  # noqa: F401
                   default_key_scale, forward, frame_forward, frame_forward_bidir, frame_forward_fused,
-                  frame_forward_norm, frame_workspace, gdn_chunk_forward, gdn_frame_profile_stages_bidir,
+                  frame_forward_norm, frame_workspace, fused_workspace, gdn_chunk_forward, gdn_frame_profile_stages_bidir,
                   gdn_frame_profile_stages_fused,
                   gdn_frame_profile_stages_norm,
                   gdn_chunk_forward_ex, gdn_chunk_forward_f32, gdn_chunk_forward_f32_ws,

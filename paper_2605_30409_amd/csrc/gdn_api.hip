@@ -438,7 +438,7 @@ struct FrameArgs {
 };
 
 struct FrameWs {
-    size_t PG, PA, Gf, Af, Hf, Hb, PGz, Gzf, total;
+    size_t PG, PA, Gf, Af, Hf, Hb, PGz, Gzf, FQT, FQH, FKT, FKH, Y, total;
 };
 
 int frame_blocks(int N) { return (N + 63) / 64; }
@@ -459,8 +459,10 @@ int frame_splits(long long units, int N, int token_splits) {
 // One layout for every variant: the A tiles, the state fragments and the
 // backward histories have room for the normalizer's extra 16-column tile; the
 // histories are used by the bidirectional form only, the unrotated-key Gram
-// fragments and their partials by the fused operator only.
-FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS) {
+// fragments and their partials by the fused operator only.  The fused
+// operator in fp32 also keeps its feature maps and gated readout (ntok_feat =
+// its B F N H token rows; 0 otherwise).
+FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS, size_t ntok_feat = 0) {
     const size_t bhf = (size_t)B * H * F;
     const size_t DVn = (size_t)Dv + 16;
     FrameWs L;
@@ -475,8 +477,18 @@ FrameWs frame_ws_layout(int B, int H, int F, int Dk, int Dv, size_t esz, int NS)
     L.Hb = off; off = align256(off + bhf * Dk * DVn * 4);
     L.PGz = off; off = align256(off + bhf * np * Dk * Dk * 4);
     L.Gzf = off; off = align256(off + bhf * Dk * Dk * esz);
+    L.FQT = off; off = align256(off + ntok_feat * Dk * 4);
+    L.FQH = off; off = align256(off + ntok_feat * Dk * 4);
+    L.FKT = off; off = align256(off + ntok_feat * Dk * 4);
+    L.FKH = off; off = align256(off + ntok_feat * Dk * 4);
+    L.Y = off;   off = align256(off + ntok_feat * Dv * 4);
     L.total = off;
     return L;
+}
+
+// Token rows whose features the fp32 fused operator keeps in the workspace.
+size_t frame_feat_rows(bool fused, bool bf16, int B, int H, int F, int N) {
+    return (fused && !bf16) ? (size_t)B * H * F * N : 0;
 }
 
 // Output workgroups per (frame, head): about `wgs` workgroups in all, each a
@@ -541,7 +553,7 @@ int frame_validate(const FrameArgs &a) {
     if (a.fused) {
         if (!a.gate || !a.w_o || !a.gain_q || !a.gain_k || !a.rope_freq || !a.rope_axis) return GDN_ERR_NULL;
         if (a.lat_w < 1) return GDN_ERR_SHAPE;
-        if (!a.bf16 || !a.norm) return GDN_ERR_UNSUPPORTED;
+        if (!a.norm) return GDN_ERR_UNSUPPORTED;
         if (misaligned(a.gate) || misaligned(a.w_o) || misaligned(a.gain_q) || misaligned(a.gain_k) ||
             misaligned(a.rope_freq) || misaligned(a.rope_axis))
             return GDN_ERR_ALIGN;
@@ -576,7 +588,8 @@ gdn::FrameParams<E> make_frame_params(const FrameArgs &a, int NS, void *ws) {
     p.z_in = a.norm ? a.z_in : nullptr;
     p.z_out = a.norm ? a.z_out : nullptr;
     p.eps = a.eps;
-    const FrameWs L = frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, sizeof(E), NS);
+    const FrameWs L = frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, sizeof(E), NS,
+                                      frame_feat_rows(a.fused, a.bf16, a.B, a.H, a.F, a.N));
     unsigned char *base = (unsigned char *)ws;
     p.PG = (float *)(base + L.PG);
     p.PA = (float *)(base + L.PA);
@@ -586,6 +599,12 @@ gdn::FrameParams<E> make_frame_params(const FrameArgs &a, int NS, void *ws) {
     p.Hb = (float *)(base + L.Hb);
     p.PGz = (float *)(base + L.PGz);
     p.Gzf = (E *)(base + L.Gzf);
+    p.fqt = (float *)(base + L.FQT);
+    p.fqh = (float *)(base + L.FQH);
+    p.fkt = (float *)(base + L.FKT);
+    p.fkh = (float *)(base + L.FKH);
+    p.ybuf = (float *)(base + L.Y);
+    p.sum_mode = 0;
     p.gate = (const E *)a.gate;
     p.w_o = (const E *)a.w_o;
     p.gain_q = a.gain_q;
@@ -678,6 +697,99 @@ hipError_t launch_frame(const gdn::FrameParams<E> &p, hipStream_t s, int reps, h
     return er;
 }
 
+// The fused operator in fp32: features, then the summaries on the rotated keys
+// (G, A) and on the unrotated ones (the normalizer's Gram matrix and K~^T beta),
+// the fused reduction and scan, and the fp32 output and projection.  The four
+// profiled stages are: features and summaries, reduction, scan, output and
+// projection.
+template <int DK, int DV, bool BIDIR>
+hipError_t launch_frame_fused32(const gdn::FrameParams<float> &p, hipStream_t s, int reps, hipEvent_t *ev) {
+    using E = float;
+    using LS = gdn::FrameSumLds<E, DK, DV, false>;
+    using LO = gdn::FrameOutLds<E, DK, DV, true>;
+    using LP = gdn::ProjectLds<DV>;
+    static std::once_flag attr_once;
+    static hipError_t attr_err = hipSuccess;
+    std::call_once(attr_once, [&] {
+        hipError_t e = hipFuncSetAttribute((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, true, false>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)LS::bytes);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)gdn::gdn_frame_output_f32_fused_kernel<DK, DV>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)LO::bytes);
+        if (e == hipSuccess)
+            e = hipFuncSetAttribute((const void *)gdn::gdn_frame_project_f32_kernel<DV>,
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, (int)LP::bytes);
+        attr_err = e;
+    });
+    if (attr_err != hipSuccess) return attr_err;
+    const long long BH = (long long)p.B * p.H, units = BH * p.F;
+    constexpr int NJ = DV / 16 + 1;
+    constexpr int NI = (DK / 16) * (DK / 32) * 2 + (DK / 16) * NJ;
+    const size_t rows = 2 * (size_t)BH * p.F * p.N;                 // q and k rows
+    const size_t feat_blocks = (rows + 4 * (128 / DK) - 1) / (4 * (128 / DK));
+    auto stage = [&](int i) -> hipError_t {
+        switch (i) {
+        case 0: {
+            hipError_t e = launch((const void *)gdn::gdn_frame_features_kernel<DK>, dim3((unsigned)feat_blocks),
+                                  dim3(256), 0, s, p);
+            // rotated keys: G and the A tiles
+            gdn::FrameParams<E> pr = p;
+            pr.k = p.fkh;
+            pr.sum_mode = 1;
+            if (e == hipSuccess)
+                e = launch((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, true, false>,
+                           dim3((unsigned)(units * p.NS)), dim3(gdn::sum_threads<false>()), LS::bytes, s, pr);
+            // unrotated keys: their Gram matrix into the unrotated-key regions, the normalizer tile
+            gdn::FrameParams<E> pu = p;
+            pu.k = p.fkt;
+            pu.sum_mode = 2;
+            pu.PG = p.PGz;
+            pu.Gf = p.Gzf;
+            if (e == hipSuccess)
+                e = launch((const void *)gdn::gdn_frame_summary_kernel<E, DK, DV, true, false>,
+                           dim3((unsigned)(units * p.NS)), dim3(gdn::sum_threads<false>()), LS::bytes, s, pu);
+            return e;
+        }
+        case 1:
+            if (p.NS > 1)
+                return launch((const void *)gdn::gdn_frame_reduce_kernel<E, DK, DV, true, true>,
+                              dim3((unsigned)units, (NI + 3) / 4), dim3(256), 0, s, p);
+            return hipSuccess;
+        case 2:
+            return launch((const void *)gdn::gdn_frame_scan_kernel<E, DK, DV, true, BIDIR, true>,
+                          dim3(gdn::xcd_blocks(BH, NJ)), dim3(64), 0, s, p);
+        default: {
+            hipError_t e = launch((const void *)gdn::gdn_frame_output_f32_fused_kernel<DK, DV>,
+                                  dim3(gdn::xcd_blocks(units, p.OB)), dim3(LO::WAVES * 64), LO::bytes, s, p);
+            if (e == hipSuccess)
+                e = launch((const void *)gdn::gdn_frame_project_f32_kernel<DV>,
+                           dim3((unsigned)(((size_t)p.F * p.N + 63) / 64), (unsigned)BH), dim3(256), LP::bytes, s, p);
+            return e;
+        }
+        }
+    };
+    hipError_t er = hipSuccess;
+    for (int i = 0; i < kFrameStages && er == hipSuccess; ++i) {
+        if (!ev) {
+            er = stage(i);
+            continue;
+        }
+        er = hipEventRecord(ev[2 * i], s);
+        for (int r = 0; r < reps && er == hipSuccess; ++r) er = stage(i);
+        if (er == hipSuccess) er = hipEventRecord(ev[2 * i + 1], s);
+    }
+    return er;
+}
+
+template <bool BIDIR>
+hipError_t frame_dispatch_fused32(const gdn::FrameParams<float> &p, int Dk, int Dv, hipStream_t s, int reps,
+                                  hipEvent_t *ev) {
+    if (Dk == 128 && Dv == 128) return launch_frame_fused32<128, 128, BIDIR>(p, s, reps, ev);
+    if (Dk == 64 && Dv == 64) return launch_frame_fused32<64, 64, BIDIR>(p, s, reps, ev);
+    if (Dk == 128 && Dv == 64) return launch_frame_fused32<128, 64, BIDIR>(p, s, reps, ev);
+    return launch_frame_fused32<64, 128, BIDIR>(p, s, reps, ev);
+}
+
 template <class E, bool NORM, bool BIDIR, bool FUSED = false>
 hipError_t frame_dispatch_n(const gdn::FrameParams<E> &p, int Dk, int Dv, hipStream_t s, int reps, hipEvent_t *ev) {
     if (Dk == 128 && Dv == 128) return launch_frame<E, 128, 128, NORM, BIDIR, FUSED>(p, s, reps, ev);
@@ -693,6 +805,10 @@ hipError_t frame_dispatch(const FrameArgs &a, int NS, void *ws, hipStream_t s, i
         if (a.fused)
             return a.bidir ? frame_dispatch_n<E, true, true, true>(p, a.Dk, a.Dv, s, reps, ev)
                            : frame_dispatch_n<E, true, false, true>(p, a.Dk, a.Dv, s, reps, ev);
+    } else {
+        if (a.fused)
+            return a.bidir ? frame_dispatch_fused32<true>(p, a.Dk, a.Dv, s, reps, ev)
+                           : frame_dispatch_fused32<false>(p, a.Dk, a.Dv, s, reps, ev);
     }
     if (a.bidir)
         return a.norm ? frame_dispatch_n<E, true, true>(p, a.Dk, a.Dv, s, reps, ev)
@@ -707,7 +823,9 @@ int frame_run(const FrameArgs &a, int token_splits, void *ws, size_t ws_bytes, v
     if (st != GDN_OK) return st;
     const int NS = frame_splits((long long)a.B * a.H * a.F, a.N, token_splits);
     if (!ws || ((uintptr_t)ws & 255u) ||
-        ws_bytes < frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, a.bf16 ? 2 : 4, NS).total)
+        ws_bytes < frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, a.bf16 ? 2 : 4, NS,
+                                   frame_feat_rows(a.fused, a.bf16, a.B, a.H, a.F, a.N))
+                       .total)
         return GDN_ERR_WORKSPACE;
     hipStream_t s = (hipStream_t)stream;
     const hipError_t e = a.bf16 ? frame_dispatch<uint16_t>(a, NS, ws, s, reps, ev)
@@ -719,7 +837,8 @@ int frame_run_cached(const FrameArgs &a, void *stream) {
     int st = frame_validate(a);
     if (st != GDN_OK) return st;
     const size_t need = frame_ws_layout(a.B, a.H, a.F, a.Dk, a.Dv, a.bf16 ? 2 : 4,
-                                        frame_splits((long long)a.B * a.H * a.F, a.N, 0))
+                                        frame_splits((long long)a.B * a.H * a.F, a.N, 0),
+                                        frame_feat_rows(a.fused, a.bf16, a.B, a.H, a.F, a.N))
                             .total;
     void *ws = nullptr;
     st = cached_workspace(need, &ws);
@@ -764,9 +883,10 @@ FrameArgs fused_args(const void *q_raw, const void *k_raw, const void *v, const 
                      const float *alpha, const float *beta, const float *gain_q, const float *gain_k,
                      const float *rope_freq, const int *rope_axis, const float *state_in, const float *z_in,
                      void *out, float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
-                     int lat_w, int t0, float key_scale, float rms_eps, float eps, int bidirectional) {
+                     int lat_w, int t0, float key_scale, float rms_eps, float eps, int bidirectional,
+                     bool bf16 = true) {
     FrameArgs a = frame_args(q_raw, k_raw, v, alpha, beta, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk,
-                             Dv, key_scale, eps, true, true, bidirectional != 0);
+                             Dv, key_scale, eps, bf16, true, bidirectional != 0);
     a.fused = true;
     a.gate = gate;
     a.w_o = w_o;
@@ -1033,6 +1153,52 @@ int gdn_frame_profile_stages_fused(const void *q_raw, const void *k_raw, const v
                                     rope_axis, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w, t0,
                                     key_scale, rms_eps, eps, bidirectional),
                          token_splits, ws, ws_bytes, reps, stage_ms, stream);
+}
+
+int gdn_frame_forward_fused_f32(const float *q_raw, const float *k_raw, const float *v, const float *gate,
+                                const float *w_o, const float *alpha, const float *beta, const float *gain_q,
+                                const float *gain_k, const float *rope_freq, const int *rope_axis,
+                                const float *state_in, const float *z_in, float *out, float *state_out,
+                                float *z_out, int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0,
+                                float key_scale, float rms_eps, float eps, int bidirectional, void *stream) {
+    return frame_run_cached(fused_args(q_raw, k_raw, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq,
+                                       rope_axis, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w,
+                                       t0, key_scale, rms_eps, eps, bidirectional, false),
+                            stream);
+}
+
+int gdn_frame_forward_fused_f32_ex(const float *q_raw, const float *k_raw, const float *v, const float *gate,
+                                   const float *w_o, const float *alpha, const float *beta, const float *gain_q,
+                                   const float *gain_k, const float *rope_freq, const int *rope_axis,
+                                   const float *state_in, const float *z_in, float *out, float *state_out,
+                                   float *z_out, int B, int H, int F, int N, int Dk, int Dv, int lat_w, int t0,
+                                   float key_scale, float rms_eps, float eps, int bidirectional, int token_splits,
+                                   void *ws, size_t ws_bytes, void *stream) {
+    return frame_run(fused_args(q_raw, k_raw, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq, rope_axis,
+                                state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w, t0, key_scale,
+                                rms_eps, eps, bidirectional, false),
+                     token_splits, ws, ws_bytes, stream, 1, nullptr);
+}
+
+int gdn_frame_profile_stages_fused_f32(const float *q_raw, const float *k_raw, const float *v, const float *gate,
+                                       const float *w_o, const float *alpha, const float *beta,
+                                       const float *gain_q, const float *gain_k, const float *rope_freq,
+                                       const int *rope_axis, const float *state_in, const float *z_in, float *out,
+                                       float *state_out, float *z_out, int B, int H, int F, int N, int Dk, int Dv,
+                                       int lat_w, int t0, float key_scale, float rms_eps, float eps,
+                                       int bidirectional, int token_splits, void *ws, size_t ws_bytes, int reps,
+                                       float *stage_ms, void *stream) {
+    return frame_profile(fused_args(q_raw, k_raw, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq,
+                                    rope_axis, state_in, z_in, out, state_out, z_out, B, H, F, N, Dk, Dv, lat_w, t0,
+                                    key_scale, rms_eps, eps, bidirectional, false),
+                         token_splits, ws, ws_bytes, reps, stage_ms, stream);
+}
+
+size_t gdn_frame_fused_workspace_bytes(int B, int H, int F, int N, int Dk, int Dv, int is_bf16, int token_splits) {
+    if (!frame_shape_ok(B, H, F, N) || !frame_dims_ok(Dk, Dv)) return 0;
+    return frame_ws_layout(B, H, F, Dk, Dv, is_bf16 ? 2 : 4, frame_splits((long long)B * H * F, N, token_splits),
+                           frame_feat_rows(true, is_bf16 != 0, B, H, F, N))
+        .total;
 }
 
 const char *gdn_status_string(int status) {

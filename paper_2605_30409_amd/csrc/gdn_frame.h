@@ -91,6 +91,11 @@ template <class E> struct FrameParams {
     const int *rope_axis;        // [Dk/2]         its coordinate: 0 time, 1 latent row, else latent column
     float rms_eps, feat_scale;   // RMSNorm epsilon; key scale applied to the key features
     int lat_w, t0;               // tokens per latent row; time coordinate of frame 0
+    // the fused operator in fp32: its feature maps and gated readout in the
+    // workspace, and which summaries a summary launch stores
+    float *fqt, *fqh, *fkt, *fkh;  // [B][T][H][Dk]  q~, q^, k~, k^
+    float *ybuf;                 // [B][T][H][Dv]  SiLU(gate) o y
+    int sum_mode;                // 0 all; 1 all but the normalizer tile; 2 all but the A tiles
 };
 
 // A fragment of ones: as the B operand, a 16-column tile whose every column is
@@ -579,14 +584,16 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
                     *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + NCA) * 256 + l * 4) = accz[a] * ks;
             }
         } else {
+            if (p.sum_mode != 2) {
 #pragma unroll
-            for (int j = 0; j < CPA; ++j) {
-                const int jt = c0 * CPA + j;
+                for (int j = 0; j < CPA; ++j) {
+                    const int jt = c0 * CPA + j;
 #pragma unroll
-                for (int a = 0; a < 2; ++a)
-                    *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + jt) * 256 + l * 4) = acc[a][j] * ks;
+                    for (int a = 0; a < 2; ++a)
+                        *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + jt) * 256 + l * 4) = acc[a][j] * ks;
+                }
             }
-            if (!FUSED && zw) {
+            if (!FUSED && zw && p.sum_mode != 1) {
 #pragma unroll
                 for (int a = 0; a < 2; ++a)
                     *(f32x4 *)(p.Af + ((fi * NR + 2 * kbw + a) * NJA + NCA) * 256 + l * 4) = accz[a] * ks;
@@ -595,13 +602,15 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
     } else {
         const int NC = gram ? NCG : NJA;
         float *dst = (gw ? p.PG : zgw ? p.PGz : p.PA) + (fi * p.NS + s) * (size_t)NR * NC * 256;
+        if (gram || p.sum_mode != 2) {
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int j = 0; j < CPW; ++j)
-                if (j < cpw)
-                    *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + c0 * cpw + j) * 64 + l) * 4) = acc[a][j];
-        if (zw) {
+                for (int j = 0; j < CPW; ++j)
+                    if (j < cpw)
+                        *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + c0 * cpw + j) * 64 + l) * 4) = acc[a][j];
+        }
+        if (zw && (FUSED || p.sum_mode != 1)) {
             // the A partials' normalizer tile (FUSED: written by the unrotated Gram waves)
             float *dz = p.PA + (fi * p.NS + s) * (size_t)NR * NJA * 256;
 #pragma unroll
@@ -1112,6 +1121,197 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
         if (i + SW >= tile_hi) break;
         load(clampi(i + 2 * SW), qa, ga);
         compute(i + SW, qb, gb);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The fused operator in fp32 (the paper's "ieee" precision mode, appendix "GDN
+// Kernel Details", "Precision modes"): every feature, product and readout in
+// fp32.  Phase A's feature maps are formed once per token by
+// gdn_frame_features_kernel into the workspace; the summaries then run as the
+// plain frame-wise summary kernel twice (rotated keys: G and A; unrotated
+// keys: the normalizer's Gram matrix and K~^T beta); the split reduction and
+// the scan are the fused variants; Phase C is gdn_frame_output_f32_fused_kernel
+// (numerator on q^, normalizer on q~, gate) and gdn_frame_project_f32_kernel
+// (the per-head projection).
+// ---------------------------------------------------------------------------
+
+// Features of every token row of q_raw and k_raw: with r(x) = gain o x /
+// sqrt(mean_i x_i^2 + rms_eps),
+//   q~ = ReLU(r_q(q)),  q^ = R q~,  k~ = feat_scale ReLU(r_k(k)),  k^ = R k~,
+// R rotating channel pair (2i, 2i + 1) by rope_freq[i] times the token's
+// coordinate on rope_axis[i] (0 time t0 + f, 1 latent row s / lat_w, else
+// latent column s % lat_w).  One lane per channel pair, Dk / 2 lanes per row
+// (the row's sum of squares reduced across them); the angle in fp64 and its
+// sine and cosine by the accurate fp64 routine, so that long time coordinates
+// cost no precision.
+template <int DK>
+__global__ __launch_bounds__(256) void gdn_frame_features_kernel(FrameParams<float> p) {
+    constexpr int P = DK / 2;                                   // lanes per row
+    const size_t nrow = (size_t)p.B * p.F * p.N * p.H;           // rows per tensor
+    const int l = threadIdx.x & 63;
+    const size_t r = ((size_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * (64 / P) + l / P;
+    if (r >= 2 * nrow) return;
+    const bool isk = r >= nrow;
+    const size_t row = isk ? r - nrow : r;                       // (b T + t) H + h
+    const int h = (int)(row % p.H);
+    const int t = (int)((row / p.H) % ((size_t)p.F * p.N));
+    const int f = t / p.N, sidx = t - f * p.N;
+    const int i = l % P;
+    const float2 x = *(const float2 *)((isk ? p.k : p.q) + row * DK + 2 * i);
+    float ss = x.x * x.x + x.y * x.y;
+#pragma unroll
+    for (int o = P / 2; o >= 1; o >>= 1) ss += __shfl_xor(ss, o);
+    const float inv = 1.f / sqrtf(ss * (1.f / DK) + p.rms_eps);
+    const float *gain = (isk ? p.gain_k : p.gain_q) + (size_t)h * DK + 2 * i;
+    const float sc = isk ? p.feat_scale : 1.f;
+    const float x0 = sc * fmaxf(gain[0] * x.x * inv, 0.f), x1 = sc * fmaxf(gain[1] * x.y * inv, 0.f);
+    const int ax = p.rope_axis[i];
+    const int yc = sidx / p.lat_w;
+    const double coord = ax == 0 ? (double)(p.t0 + f) : ax == 1 ? (double)yc : (double)(sidx - yc * p.lat_w);
+    double sn, cs;
+    sincos((double)p.rope_freq[i] * coord, &sn, &cs);
+    const float s1 = (float)sn, c1 = (float)cs;
+    float *ft = (isk ? p.fkt : p.fqt) + row * DK + 2 * i, *fh = (isk ? p.fkh : p.fqh) + row * DK + 2 * i;
+    *(float2 *)ft = make_float2(x0, x1);
+    *(float2 *)fh = make_float2(x0 * c1 - x1 * s1, x0 * s1 + x1 * c1);
+}
+
+// Phase C numerator, normalizer and gate in fp32: as gdn_frame_output_kernel
+// with the normalizer (one 16-token tile per wave at a time, H_f of the
+// (frame, head) in LDS), with the numerator tiles on q^, the normalizer tile
+// on q~, and y = SiLU(gate) o numerator / (z . q~ + eps) written to ybuf.
+template <int DK, int DV>
+__global__ __launch_bounds__(64 * frame_out_waves<true>()) void gdn_frame_output_f32_fused_kernel(
+    FrameParams<float> p) {
+    using E = float;
+    using TR = Tr<E>;
+    using frag = typename TR::frag;
+    using LO = FrameOutLds<E, DK, DV, true>;
+    constexpr int KB = DK / 32, NV = DV / 16, NJ = LO::NJ;
+    constexpr int HV = NJ * 16 * DK * (int)sizeof(E) / 16;    // 16-byte vectors of H_f
+    extern __shared__ __align__(16) unsigned char smem[];
+    int unit, blk;
+    xcd_unit(blockIdx.x, p.OB, unit, blk);
+    if (unit >= p.F * p.B * p.H) return;
+    const int bh = unit / p.F, f = unit - bh * p.F;
+    const int b = bh / p.H, h = bh - b * p.H;
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
+    const size_t fi = (size_t)bh * p.F + f;
+    {
+        constexpr int NTH = 64 * LO::WAVES, HIT = (HV + NTH - 1) / NTH;
+        const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
+        u32x4 hv[HIT];
+#pragma unroll
+        for (int it = 0; it < HIT; ++it)
+            if (HV % NTH == 0 || tid + NTH * it < HV) hv[it] = src[tid + NTH * it];
+#pragma unroll
+        for (int it = 0; it < HIT; ++it)
+            if (HV % NTH == 0 || tid + NTH * it < HV) ((u32x4 *)smem)[tid + NTH * it] = hv[it];
+    }
+    const size_t T = (size_t)p.F * p.N;
+    const int ntf = (p.N + 15) / 16;
+    const int tile_lo = blk * p.OTPW, tile_hi = min(ntf, tile_lo + p.OTPW);
+    const size_t row_f = (size_t)b * T + (size_t)f * p.N;
+    // query features of tile i (rotated and unrotated); rows past the frame
+    // read its last token
+    auto load_q = [&](int i, frag (&qh)[KB], frag (&qt)[KB]) {
+        const int n = min(16 * i + li, p.N - 1);
+        const size_t o = ((row_f + n) * p.H + h) * DK;
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            qh[kb] = load_frag<E>(p.fqh + o + 32 * kb, lg);
+            qt[kb] = load_frag<E>(p.fqt + o + 32 * kb, lg);
+        }
+    };
+    const E *sH = (const E *)smem + l * 8;
+    E *sO = (E *)(smem + LO::oO) + w * 16 * LO::LDO;
+    constexpr int RV = DV / 4;                                 // float4 per row
+    auto tile_product = [&](int jo, const frag (&qf)[KB]) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) acc = TR::mma(TR::load8(sH + (jo * KB + kb) * 512), qf[kb], acc);
+        return acc;
+    };
+    auto compute = [&](int tile, const frag (&qh)[KB], const frag (&qt)[KB]) {
+        f32x4 acc[NV];
+#pragma unroll
+        for (int jo = 0; jo < NV; ++jo) acc[jo] = tile_product(jo, qh);
+        const float inv = 1.f / (tile_product(NV, qt)[0] + p.eps);
+        // lane (li, lg) holds columns 16 jo + 4 lg + q of token li
+        const int n = min(16 * tile + li, p.N - 1);
+        const float *grow = p.gate + ((row_f + n) * p.H + h) * DV;
+#pragma unroll
+        for (int jo = 0; jo < NV; ++jo) {
+            const f32x4 g = *(const f32x4 *)(grow + 16 * jo + 4 * lg);
+            f32x4 y;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) y[q] = g[q] / (1.f + expf(-g[q])) * (acc[jo][q] * inv);
+            *(f32x4 *)(sO + li * LO::LDO + 16 * jo + 4 * lg) = y;
+        }
+#pragma unroll
+        for (int pass = 0; pass < 16 * RV / 64; ++pass) {
+            const int r = pass * (64 / RV) + l / RV, c = (l % RV) * 4;
+            const f32x4 val = *(const f32x4 *)(sO + r * LO::LDO + c);
+            const int nn = 16 * tile + r;
+            if (tile < tile_hi && nn < p.N) *(f32x4 *)(p.ybuf + ((row_f + nn) * p.H + h) * DV + c) = val;
+        }
+    };
+    auto clampi = [&](int i) { return min(i, tile_hi - 1); };
+    frag ha[KB], ta[KB], hb[KB], tb[KB];
+    const int i0 = tile_lo + w;
+    load_q(clampi(i0), ha, ta);
+    lds_barrier();
+    constexpr int SW = LO::WAVES;
+    for (int i = i0; i < tile_hi; i += 2 * SW) {
+        load_q(clampi(i + SW), hb, tb);
+        compute(i, ha, ta);
+        if (i + SW >= tile_hi) break;
+        load_q(clampi(i + 2 * SW), ha, ta);
+        compute(i + SW, hb, tb);
+    }
+}
+
+// The per-head projection in fp32: out_n = W_o[h] ybuf_n.  Workgroup (run of 64
+// tokens, b h): W_o[h] and the run's rows of ybuf staged in LDS with row
+// stride DV + 4 (the 16 rows x 4 k slots an operand read touches fall in 64
+// distinct banks); wave w takes tokens 16 w .. 16 w + 15 of the run and every
+// 16-channel output tile on 16x16x4 fp32 MFMA, lane (li, lg) supplying
+// W_o[16 it + li][4 kk + lg] and ybuf[token li][4 kk + lg]; the accumulator
+// lane (li, lg) then holds channels 16 it + 4 lg .. + 3 of token li.
+template <int DV> struct ProjectLds {
+    static constexpr int LD = DV + 4;
+    static constexpr size_t bytes = (size_t)4 * (DV + 64) * LD;
+};
+
+template <int DV>
+__global__ __launch_bounds__(256) void gdn_frame_project_f32_kernel(FrameParams<float> p) {
+    constexpr int LD = ProjectLds<DV>::LD, RV = DV / 4;
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *sW = (float *)smem, *sY = sW + DV * LD;
+    const size_t T = (size_t)p.F * p.N;
+    const int bh = blockIdx.y, b = bh / p.H, h = bh - b * p.H;
+    const int t0 = blockIdx.x * 64;
+    const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
+    for (int idx = tid; idx < DV * RV; idx += 256) {
+        const int r = idx / RV, c = idx - r * RV;
+        *(f32x4 *)(sW + r * LD + 4 * c) = *(const f32x4 *)(p.w_o + ((size_t)h * DV + r) * DV + 4 * c);
+    }
+    for (int idx = tid; idx < 64 * RV; idx += 256) {
+        const int r = idx / RV, c = idx - r * RV;
+        const size_t t = min((size_t)(t0 + r), T - 1);
+        *(f32x4 *)(sY + r * LD + 4 * c) = *(const f32x4 *)(p.ybuf + (((size_t)b * T + t) * p.H + h) * DV + 4 * c);
+    }
+    __syncthreads();
+    const float *yl = sY + (16 * w + li) * LD + lg;
+    const size_t tok = (size_t)t0 + 16 * w + li;
+#pragma unroll 2
+    for (int it = 0; it < DV / 16; ++it) {
+        const float *wl = sW + (16 * it + li) * LD + lg;
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < DV / 4; ++kk) acc = mma_f32_k4(wl[4 * kk], yl[4 * kk], acc);
+        if (tok < T) *(f32x4 *)(p.out + (((size_t)b * T + tok) * p.H + h) * DV + 16 * it + 4 * lg) = acc;
     }
 }
 

@@ -88,6 +88,14 @@ def lib():
         L.gdn_frame_forward_fused_ex.argtypes = ucore + [i, vp, sz, vp]
         L.gdn_frame_profile_stages_fused.restype = i
         L.gdn_frame_profile_stages_fused.argtypes = ucore + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        L.gdn_frame_forward_fused_f32.restype = i
+        L.gdn_frame_forward_fused_f32.argtypes = ucore + [vp]
+        L.gdn_frame_forward_fused_f32_ex.restype = i
+        L.gdn_frame_forward_fused_f32_ex.argtypes = ucore + [i, vp, sz, vp]
+        L.gdn_frame_profile_stages_fused_f32.restype = i
+        L.gdn_frame_profile_stages_fused_f32.argtypes = ucore + [i, vp, sz, i, ctypes.POINTER(ctypes.c_float), vp]
+        L.gdn_frame_fused_workspace_bytes.restype = sz
+        L.gdn_frame_fused_workspace_bytes.argtypes = [i, i, i, i, i, i, i, i]
         L.gdn_status_string.restype = ctypes.c_char_p
         L.gdn_status_string.argtypes = [i]
         _lib = L
@@ -291,6 +299,18 @@ def frame_workspace(q, v, frame_tokens, token_splits=0):
     return torch.empty(n, dtype=torch.uint8, device=q.device)
 
 
+def fused_workspace(q, v, frame_tokens, token_splits=0):
+    """Workspace tensor for gdn_frame_forward_fused_ex / _f32_ex on inputs shaped like q and v
+    (the fp32 operator also keeps its feature maps and gated readout there)."""
+    B, T, H, Dk = q.shape
+    N = int(frame_tokens)
+    n = lib().gdn_frame_fused_workspace_bytes(B, H, T // N, N, Dk, v.shape[-1], 1 if q.dtype == torch.bfloat16
+                                              else 0, int(token_splits))
+    if n == 0:
+        raise ValueError("unsupported shape for the fused frame-wise GDN operator")
+    return torch.empty(n, dtype=torch.uint8, device=q.device)
+
+
 def _frame_call(name, q, k, v, alpha, beta, state_in, out, state_out, frame_tokens, key_scale,
                 extra, stream):
     B, H, T, Dk, Dv, _ = _check(q, k, v, alpha, beta, state_in, out, state_out, frame_tokens)
@@ -477,11 +497,12 @@ def _fused_call(name, q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_freq
                 out, state_out, z_out, frame_tokens, lat_w, t0, key_scale, rms_eps, eps, bidirectional, extra,
                 stream):
     B, H, T, Dk, Dv, is_bf16 = _check(q, k, v, alpha, beta, state_in, out, state_out, frame_tokens)
-    if not is_bf16:
-        raise ValueError("the fused operator takes bf16 q, k, v, gate and w_o")
     dev = q.device
-    _check_param(gate, v.shape, torch.bfloat16, dev, "gate")
-    _check_param(w_o, (H, Dv, Dv), torch.bfloat16, dev, "w_o")
+    dt = torch.bfloat16 if is_bf16 else torch.float32
+    _check_param(gate, v.shape, dt, dev, "gate")
+    _check_param(w_o, (H, Dv, Dv), dt, dev, "w_o")
+    if not is_bf16:
+        name = name.replace("fused", "fused_f32")
     _check_param(gain_q, (H, Dk), torch.float32, dev, "gain_q")
     _check_param(gain_k, (H, Dk), torch.float32, dev, "gain_k")
     _check_param(rope_freq, (Dk // 2,), torch.float32, dev, "rope_freq")
@@ -516,13 +537,14 @@ def frame_forward_fused(q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_fr
                         z_in=None, *, frame_tokens, lat_w, t0=0, key_scale=None, rms_eps=1e-6, eps=1e-6,
                         bidirectional=False, out=None, state_out=None, z_out=None, want_state=True, ws=None,
                         token_splits=None, stream=None):
-    """The fused frame-wise GDN operator (bf16).  q, k: the raw projections
+    """The fused frame-wise GDN operator, bf16 or fp32 (all of q, k, v, gate,
+    w_o one type; fp32 runs the fp32 mode).  q, k: the raw projections
     [B, T, H, Dk]; v, gate (pre-SiLU) [B, T, H, Dv]; w_o [H, Dv, Dv] (row = output
     channel); alpha [B, F, H], beta [B, T, H] fp32; gain_q, gain_k [H, Dk] fp32
     RMSNorm gains; rope_freq [Dk/2] fp32 and rope_axis [Dk/2] int32 (0 time, 1
     latent row, 2 latent column) of the 3D RoPE, with lat_w tokens per latent row
     and t0 the time coordinate of the first frame; state_in [B, H, Dk, Dv] and
-    z_in [B, H, Dk] fp32 or None.  Returns (out [B, T, H, Dv] bf16, state_out,
+    z_in [B, H, Dk] fp32 or None.  Returns (out [B, T, H, Dv] like q, state_out,
     z_out)."""
     B, T, H, Dk = q.shape
     Dv = v.shape[-1]
@@ -538,7 +560,7 @@ def frame_forward_fused(q, k, v, gate, w_o, alpha, beta, gain_q, gain_k, rope_fr
     if ws is not None or token_splits is not None:
         ts = 0 if token_splits is None else int(token_splits)
         if ws is None:
-            ws = frame_workspace(q, v, frame_tokens, ts)
+            ws = fused_workspace(q, v, frame_tokens, ts)
         _fused_call("gdn_frame_forward_fused_ex", *args, (ts, _ptr(ws), ws.numel()), stream)
     else:
         _fused_call("gdn_frame_forward_fused", *args, (), stream)

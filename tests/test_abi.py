@@ -22,7 +22,7 @@ def declared_functions():
 
 def test_library_exports_every_declared_symbol():
     names = declared_functions()
-    assert len(names) == 27 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
+    assert len(names) == 31 and "gdn_workspace_bytes" in names and "gdn_frame_forward" in names, names
     lib = ctypes.CDLL(gdn.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -207,6 +207,15 @@ def test_frame_token_splits_and_workspace():
     assert wb(1, 16, 3, 3520, 128, 128, False, 1) > n
     assert wb(1, 16, 3, 0, 128, 128, True, 0) == 0
     assert wb(1, 16, 3, 3520, 128, 32, True, 0) == 0
+    # the fused operator: bf16 as above; fp32 also keeps q~, q^, k~, k^ and the
+    # gated readout for every token row
+    fb = gdn.lib().gdn_frame_fused_workspace_bytes
+    assert fb(1, 16, 3, 3520, 128, 128, 1, 1) == n
+    base32 = wb(1, 16, 3, 3520, 128, 128, False, 1)
+    rows = 16 * 3 * 3520
+    assert base32 + rows * (4 * 128 + 128) * 4 <= fb(1, 16, 3, 3520, 128, 128, 0, 1) < \
+        base32 + rows * (4 * 128 + 128) * 4 + 5 * 256
+    assert fb(1, 16, 3, 3520, 96, 128, 0, 1) == 0
 
 
 def fcall(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, a=BASE + 192 * MB, b=BASE + 200 * MB,
@@ -325,7 +334,8 @@ def ucall(fn, q=BASE, k=BASE + 64 * MB, v=BASE + 128 * MB, g=BASE + 160 * MB, w=
     return getattr(L, fn)(*args, None)
 
 
-@pytest.mark.parametrize("fn", ["gdn_frame_forward_fused", "gdn_frame_forward_fused_ex"])
+@pytest.mark.parametrize("fn", ["gdn_frame_forward_fused", "gdn_frame_forward_fused_ex",
+                                "gdn_frame_forward_fused_f32", "gdn_frame_forward_fused_f32_ex"])
 def test_frame_fused_validation_errors(fn):
     assert ucall(fn, g=None) == -1
     assert ucall(fn, w=None) == -1
@@ -339,12 +349,16 @@ def test_frame_fused_validation_errors(fn):
         assert ucall(fn) == -4
 
 
-def test_frame_fused_binding_rejects_fp32_on_cpu():
+def test_frame_fused_binding_rejects_mixed_types_and_host_tensors():
     import torch
     q = torch.zeros(1, 100, 2, 64)
-    with pytest.raises(ValueError):
-        gdn.frame_forward_fused(q, q, q, q, torch.zeros(2, 64, 64), torch.zeros(1, 2, 2), torch.zeros(1, 100, 2),
-                                torch.ones(2, 64), torch.ones(2, 64), torch.ones(32), torch.zeros(32, dtype=torch.int32),
+    args = (torch.zeros(1, 2, 2), torch.zeros(1, 100, 2), torch.ones(2, 64), torch.ones(2, 64), torch.ones(32),
+            torch.zeros(32, dtype=torch.int32))
+    with pytest.raises(ValueError):       # host tensors
+        gdn.frame_forward_fused(q, q, q, q, torch.zeros(2, 64, 64), *args, frame_tokens=50, lat_w=10)
+    qb = q.to(torch.bfloat16)
+    with pytest.raises(ValueError):       # bf16 q with an fp32 gate
+        gdn.frame_forward_fused(qb, qb, qb, q, torch.zeros(2, 64, 64, dtype=torch.bfloat16), *args,
                                 frame_tokens=50, lat_w=10)
 
 

@@ -502,29 +502,40 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
         struct Ops {
             frag a[2], b[NC];
         };
-        auto read = [&](int i, int kb, Ops &o) {
+        // the K^T fragments of k block kb of block i, multiplied by beta
+        auto read_a = [&](int i, int kb, frag (&fa)[2]) {
             const unsigned char *sl = slot(i);
-            const E *sK = (const E *)(sl + oKey), *sV = (const E *)(sl + L::oV);
+            const E *sK = (const E *)(sl + oKey);
             const float *sB = (const float *)(sl + L::oB);
             // betas of this lane's 8 k-slots: tokens 32 kb + 8 lg + q'
             const f32x4 be0 = *(const f32x4 *)(sB + 32 * kb + 8 * lg);
             const f32x4 be1 = *(const f32x4 *)(sB + 32 * kb + 8 * lg + 4);
 #pragma unroll
-            for (int a = 0; a < 2; ++a) o.a[a] = tr_frag_gm<E, RK>(sK, 32 * kb, 32 * kbw, true, a, li, lg);
-#pragma unroll
-            for (int j = 0; j < NC; ++j) {
-                const int c = c0 * NC + j;
-                if constexpr (GB)
-                    o.b[j] = tr_frag_gm<E, RK>(sK, 32 * kb, 32 * (c >> 1), true, c & 1, li, lg);
-                else
-                    o.b[j] = tr_frag_gm<E, RV>(sV, 32 * kb, 16 * c, false, 0, li, lg);
-            }
+            for (int a = 0; a < 2; ++a) fa[a] = tr_frag_gm<E, RK>(sK, 32 * kb, 32 * kbw, true, a, li, lg);
             const int nvalid = t_hi - (t_lo + 64 * i + 32 * kb + 8 * lg);
             float bt[8];
 #pragma unroll
             for (int q = 0; q < 8; ++q) bt[q] = q < nvalid ? (q < 4 ? be0[q] : be1[q - 4]) : 0.f;
 #pragma unroll
-            for (int a = 0; a < 2; ++a) o.a[a] = scale_frag(o.a[a], bt);
+            for (int a = 0; a < 2; ++a) fa[a] = scale_frag(fa[a], bt);
+        };
+        // the B fragments of column tiles J0 .. J0 + NB - 1 of the wave's share
+        auto read_b = [&](int i, int kb, int J0, auto nb_, frag *fb) {
+            constexpr int NB = decltype(nb_)::value;
+            const unsigned char *sl = slot(i);
+            const E *sK = (const E *)(sl + oKey), *sV = (const E *)(sl + L::oV);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) {
+                const int c = c0 * NC + J0 + j;
+                if constexpr (GB)
+                    fb[j] = tr_frag_gm<E, RK>(sK, 32 * kb, 32 * (c >> 1), true, c & 1, li, lg);
+                else
+                    fb[j] = tr_frag_gm<E, RV>(sV, 32 * kb, 16 * c, false, 0, li, lg);
+            }
+        };
+        auto read = [&](int i, int kb, Ops &o) {
+            read_a(i, kb, o.a);
+            read_b(i, kb, 0, std::integral_constant<int, NC>{}, o.b);
         };
         auto mul = [&](const Ops &o) {
 #pragma unroll
@@ -544,11 +555,31 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
             // loaders may refill that block's slot
             lds_only_barrier();                  // block i has landed (FUSED: its features formed)
             if constexpr (FUSED) {
-                // one operand set at a time: 16 waves leave 128 registers each
-                read(i, 0, o0);
-                mul(o0);
-                read(i, 1, o0);
-                mul(o0);
+                // 16 waves leave 128 registers each: per k block the K^T
+                // fragments, then the B fragments half the column tiles at a
+                // time, each half multiplied as it arrives
+                constexpr int NH = NC / 2;
+                static_assert(NC % 2 == 0, "two halves of the column tiles");
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb) {
+                    frag fa[2], fb[NH];
+#pragma unroll
+                    for (int hf = 0; hf < 2; ++hf) {
+                        if (hf == 0) read_a(i, kb, fa);
+                        read_b(i, kb, hf * NH, std::integral_constant<int, NH>{}, fb);
+#pragma unroll
+                        for (int a = 0; a < 2; ++a)
+#pragma unroll
+                            for (int j = 0; j < NH; ++j)
+                                acc[a][hf * NH + j] = TR::mma(fa[a], fb[j], acc[a][hf * NH + j]);
+                    }
+                    if constexpr (NORM && RO == 2) {
+                        if (zw) {
+#pragma unroll
+                            for (int a = 0; a < 2; ++a) accz[a] = TR::mma(fa[a], ones, accz[a]);
+                        }
+                    }
+                }
             } else {
                 read(i, 0, o0);
                 read(i, 1, o1);

@@ -975,21 +975,30 @@ __global__ __launch_bounds__(64 * frame_out_waves<NORM>()) void gdn_frame_output
 //   q~ = ReLU(gain_q o q / rms(q))   (the sum of squares reduced over the 4
 //                                     lanes of the token),  q^ = R q~ (RoPE);
 //   numerator tiles H_f^T q^, normalizer tile z . q~ (every column holds z);
-//   y = SiLU(gate) o numerator / (z . q~ + eps), staged in LDS as bf16;
-//   out^T = W_o y^T with W_o staged in LDS as operand fragments, then the
-//   result tile goes back through LDS for whole-row stores.
+//   y = SiLU(gate) o numerator / (z . q~ + eps);   out^T = W_o y^T.
+// The value channels are dealt to the numerator tiles, and the output
+// channels to the projection tiles, in the order of fused_out_chan: row
+// 4 m + q of tile 2 kb + e is channel 32 kb + 8 m + 4 e + q.  Lane (li, lg)
+// then holds channels 32 kb + 8 lg .. 32 kb + 8 lg + 7 of tiles 2 kb and
+// 2 kb + 1, which are at once a 16-byte piece of the token's gate row, the
+// projection's B operand fragment over k block kb (y never leaves the
+// registers) and a 16-byte piece of its output row.  The H_f and W_o
+// fragments take that order as they are staged into LDS.
 constexpr int kFusedOutWaves = 12;
+
+// Channel of row i (0 .. 15) of numerator or projection tile jo.
+__device__ __forceinline__ int fused_out_chan(int jo, int i) {
+    return 32 * (jo >> 1) + 8 * (i >> 2) + 4 * (jo & 1) + (i & 3);
+}
 
 template <int DK, int DV> struct FusedOutLds {
     static constexpr int NJ = DV / 16 + 1;
-    static constexpr int LDO = DV + 8;                          // staged row stride (bf16)
     static constexpr size_t oW = (size_t)2 * DK * 16 * NJ;      // after H_f: W_o fragments
     // gain_q[DK], then per channel pair the turns per unit of time, latent
     // row and latent column (the pair's frequency / 2 pi on its axis, zero on
     // the other two)
     static constexpr size_t oP = oW + (size_t)2 * DV * DV;
-    static constexpr size_t oO = oP + (size_t)4 * (DK + 3 * (DK / 2));   // one 16-row staging tile per wave
-    static constexpr size_t bytes = oO + (size_t)2 * kFusedOutWaves * 16 * LDO;
+    static constexpr size_t bytes = oP + (size_t)4 * (DK + 3 * (DK / 2));
 };
 
 template <int DK, int DV>
@@ -1009,20 +1018,34 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
     const int tid = threadIdx.x, w = tid >> 6, l = tid & 63, li = l & 15, lg = l >> 4;
     const size_t fi = (size_t)bh * p.F + f;
 
-    // H_f fragments, W_o fragments (jo, kb): lane l holds
-    // W_o[h][16 jo + l % 16][32 kb + 8 (l / 16) ..], and the prologue constants
+    // H_f fragments (jo, kb): lane l holds row l % 16 of tile jo (channel
+    // fused_out_chan(jo, l % 16); the normalizer tile as written) over
+    // k slots 32 kb + 8 (l / 16) ..; W_o fragments (jo, kb): lane l holds
+    // W_o[h][fused_out_chan(jo, l % 16)][32 kb + 8 (l / 16) ..]; the prologue
+    // constants
     {
         constexpr int HV = NJ * 16 * DK * 2 / 16, HIT = (HV + NTH - 1) / NTH;
         constexpr int WV = DV * DV * 2 / 16, WIT = (WV + NTH - 1) / NTH;
         const u32x4 *src = (const u32x4 *)(p.Hf + fi * (size_t)NJ * 16 * DK);
         u32x4 hv[HIT], wv[WIT];
 #pragma unroll
-        for (int it = 0; it < HIT; ++it)
-            if (HV % NTH == 0 || tid + NTH * it < HV) hv[it] = src[tid + NTH * it];
+        for (int it = 0; it < HIT; ++it) {
+            const int d = tid + NTH * it;
+            if (HV % NTH == 0 || d < HV) {
+                const int rec = d >> 6, ll = d & 63, jo = rec / KB, kb = rec - jo * KB;
+                int sd = d;
+                if (jo < NV) {
+                    const int c = fused_out_chan(jo, ll & 15);
+                    sd = (((c >> 4) * KB + kb) << 6) + (c & 15) + (ll & 48);
+                }
+                hv[it] = src[sd];
+            }
+        }
 #pragma unroll
         for (int it = 0; it < WIT; ++it) {
             const int j = min(tid + NTH * it, WV - 1), fr = j >> 6, ll = j & 63, jo = fr / KBV, kb = fr - jo * KBV;
-            wv[it] = *(const u32x4 *)(p.w_o + ((size_t)h * DV + 16 * jo + (ll & 15)) * DV + 32 * kb + 8 * (ll >> 4));
+            wv[it] = *(const u32x4 *)(p.w_o + ((size_t)h * DV + fused_out_chan(jo, ll & 15)) * DV + 32 * kb +
+                                      8 * (ll >> 4));
         }
         float *cp = (float *)(smem + LO::oP);
         for (int j = tid; j < DK + 3 * (DK / 2); j += NTH) {
@@ -1045,21 +1068,26 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
     const int ntf = (p.N + 15) / 16;
     const int tile_lo = blk * p.OTPW, tile_hi = min(ntf, tile_lo + p.OTPW);
     const size_t row_f = (size_t)b * T + (size_t)f * p.N;
-    // query fragments and gate quads of tile i; rows past the frame read its last token
-    auto load = [&](int i, frag (&qf)[KB], u32x2 (&gt)[NV]) {
+    // query fragments and gate pieces (channels 32 kb + 8 lg ..) of tile i;
+    // rows past the frame read its last token
+    auto load = [&](int i, frag (&qf)[KB], u32x4 (&gt)[KBV]) {
         const int n = min(16 * i + li, p.N - 1);
         const size_t row = (row_f + n) * p.H + h;
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) qf[kb] = load_frag<E>(p.q + row * DK + 32 * kb, lg);
 #pragma unroll
-        for (int jo = 0; jo < NV; ++jo) gt[jo] = *(const u32x2 *)(p.gate + row * DV + 16 * jo + 4 * lg);
+        for (int kb = 0; kb < KBV; ++kb) gt[kb] = *(const u32x4 *)(p.gate + row * DV + 32 * kb + 8 * lg);
     };
     const E *sH = (const E *)smem + l * 8;
     const E *sW = (const E *)(smem + LO::oW) + l * 8;
     const float *cgain = (const float *)(smem + LO::oP), *cang = cgain + DK;
-    E *sO = (E *)(smem + LO::oO) + w * 16 * LO::LDO;
-    constexpr int VE = 8, RV = DV / VE;                        // bf16 per 16 bytes, vectors per row
-    auto compute = [&](int tile, const frag (&qf)[KB], const u32x2 (&gt)[NV]) {
+    auto compute = [&](int tile, const frag (&qf)[KB], const u32x4 (&gt)[KBV]) {
+        // an offset the compiler cannot see through, so that the H_f and W_o
+        // fragments are read from LDS where they are used rather than held in
+        // registers across the tile loop
+        int lo = 0;
+        asm volatile("" : "+v"(lo));
+        const E *tH = sH + lo, *tW = sW + lo;
         // prologue: features of token li
         float x[KB][8];
         float ss = 0.f;
@@ -1102,39 +1130,48 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
         // the denominator of token li (every column of the normalizer tile is z)
         f32x4 dz = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) dz = TR::mma(TR::load8(sH + (NV * KB + kb) * 512), qt[kb], dz);
+        for (int kb = 0; kb < KB; ++kb) dz = TR::mma(TR::load8(tH + (NV * KB + kb) * 512), qt[kb], dz);
         const float invd = 1.f / (dz[0] + p.eps);
-        // gated, normalized readout into the staging tile
-#pragma unroll
-        for (int jo = 0; jo < NV; ++jo) {
-            f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb) acc = TR::mma(TR::load8(sH + (jo * KB + kb) * 512), qh[kb], acc);
-            const f32x4 g = TR::to_f32(gt[jo]);
-            f32x4 y;
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                y[q] = g[q] * __builtin_amdgcn_rcpf(1.f + __expf(-g[q])) * (acc[q] * invd);
-            TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(y));
-        }
-        // projection: out^T = W_o y^T, y^T as the B operand read back by rows
+        // gated, normalized readout: numerator tiles 2 kb and 2 kb + 1 give
+        // channels 32 kb + 8 lg .. + 7 of token li, the projection's B operand
+        // over k block kb
         frag yb[KBV];
 #pragma unroll
-        for (int kb = 0; kb < KBV; ++kb) yb[kb] = TR::load8(sO + li * LO::LDO + 32 * kb + 8 * lg);
+        for (int kv = 0; kv < KBV; ++kv) {
+            float y[8];
 #pragma unroll
-        for (int jo = 0; jo < NV; ++jo) {
-            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+            for (int e = 0; e < 2; ++e) {
+                f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kb = 0; kb < KBV; ++kb) o = TR::mma(TR::load8(sW + (jo * KBV + kb) * 512), yb[kb], o);
-            TR::store(sO + li * LO::LDO + 16 * jo + 4 * lg, TR::from_f32(o));
+                for (int kb = 0; kb < KB; ++kb)
+                    acc = TR::mma(TR::load8(tH + ((2 * kv + e) * KB + kb) * 512), qh[kb], acc);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t gw = gt[kv][2 * e + (q >> 1)];
+                    const float g = __uint_as_float((q & 1) ? (gw & 0xffff0000u) : (gw << 16));
+                    y[4 * e + q] = g * __builtin_amdgcn_rcpf(1.f + __expf(-g)) * (acc[q] * invd);
+                }
+            }
+            yb[kv] = frag{pack_bf16x2(y[0], y[1]), pack_bf16x2(y[2], y[3]), pack_bf16x2(y[4], y[5]),
+                          pack_bf16x2(y[6], y[7])};
         }
-        // rows r of the tile, RV lanes per row, 64 / RV rows per pass
+        // projection: out^T = W_o y^T; tiles 2 kv and 2 kv + 1 give output
+        // channels 32 kv + 8 lg .. + 7 of token li, stored as one 16-byte piece
+        const bool live = tile < tile_hi && 16 * tile + li < p.N;
+        E *orow = p.out + ((row_f + 16 * tile + li) * p.H + h) * DV + 8 * lg;
 #pragma unroll
-        for (int pass = 0; pass < 16 * RV / 64; ++pass) {
-            const int r = pass * (64 / RV) + l / RV, c = (l % RV) * VE;
-            const u32x4 val = *(const u32x4 *)(sO + r * LO::LDO + c);
-            const int nn = 16 * tile + r;
-            if (tile < tile_hi && nn < p.N) *(u32x4 *)(p.out + ((row_f + nn) * p.H + h) * DV + c) = val;
+        for (int kv = 0; kv < KBV; ++kv) {
+            f32x4 o[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                o[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kb = 0; kb < KBV; ++kb)
+                    o[e] = TR::mma(TR::load8(tW + ((2 * kv + e) * KBV + kb) * 512), yb[kb], o[e]);
+            }
+            const u32x4 val = {pack_bf16x2(o[0][0], o[0][1]), pack_bf16x2(o[0][2], o[0][3]),
+                               pack_bf16x2(o[1][0], o[1][1]), pack_bf16x2(o[1][2], o[1][3])};
+            if (live) *(u32x4 *)(orow + 32 * kv) = val;
         }
     };
     // the prefetch is unconditional (clamped to the workgroup's last tile) so
@@ -1142,7 +1179,7 @@ __global__ __launch_bounds__(kFusedOutWaves * 64) void gdn_frame_output_fused_ke
     constexpr int SW = kFusedOutWaves;
     auto clampi = [&](int i) { return min(i, tile_hi - 1); };
     frag qa[KB], qb[KB];
-    u32x2 ga[NV], gb[NV];
+    u32x4 ga[KBV], gb[KBV];
     const int i0 = tile_lo + w;
     load(clampi(i0), qa, ga);
     lds_barrier();                                // staging complete

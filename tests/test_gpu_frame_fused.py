@@ -186,6 +186,25 @@ def test_many_frames_fused(gdn, bidirectional):
     check(gdn, inp, f"{'bidir ' if bidirectional else ''}F33 N30", bidirectional)
 
 
+@pytest.mark.parametrize("bidirectional", [False, True])
+@pytest.mark.parametrize("Dk", [64, 128])
+def test_write_gates_outside_unit_interval_fused(gdn, Dk, bidirectional):
+    """Write gates outside [0, 1] (the interface takes any finite beta): about
+    a tenth of the tokens negative and a twentieth above one, with tokens
+    64 .. 191 of every frame kept non-negative so that whole 64-token blocks
+    have no negative gate and others have some."""
+    inp = gdn_inputs.make_fused_inputs(1, 3, frame_tokens=300, H=2, Dk=Dk, Dv=Dk, lat_w=20,
+                                       seed=39800 + Dk + bidirectional)
+    rng = np.random.default_rng(39850 + Dk + bidirectional)
+    b = inp["beta"]
+    neg = rng.random(b.shape) < 0.1
+    neg.reshape(b.shape[0], 3, 300, b.shape[2])[:, :, 64:192] = False
+    b = np.where(neg, -b, b)
+    b = np.where(rng.random(b.shape) < 0.05, 3.0 * b, b)
+    inp["beta"] = b.astype(np.float32)
+    check(gdn, inp, f"{'bidir ' if bidirectional else ''}Dk{Dk} beta in (-1, 3)", bidirectional)
+
+
 @pytest.mark.parametrize("t0", [5000, 20000])
 def test_long_time_coordinate_fused(gdn, t0):
     """Time coordinates whose angles run to thousands of turns (the first time

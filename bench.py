@@ -311,7 +311,10 @@ def _frame_counts(B, F, N, H, Dk, Dv, NS, esz, norm, bidir, fused):
     n = B * F * N * H                   # token-heads
     u = B * H * F                       # (frame, head) units
     st = B * H * Dk * Dv * 4 + (B * H * Dk * 4 if norm else 0)
-    part = u * NS * Dk * (Dk + Ds) * 4 if NS > 1 else 0
+    # a split's Gram partials: the 16 x 16 tiles on and above the diagonal
+    R = Dk // 16
+    gram = R * (R + 1) // 2 * 256 * 4
+    part = u * NS * (gram + Dk * Ds * 4) if NS > 1 else 0
     f = {"summaries": 2.0 * n * Dk * (Dk + Dv + Dz),
          "reduce": 0.0,
          "scan": u * (2.0 * Dk * Dk * (Dv + Dz) + 3.0 * Dk * (Dv + Dz)),
@@ -321,7 +324,7 @@ def _frame_counts(B, F, N, H, Dk, Dv, NS, esz, norm, bidir, fused):
           "scan": {"written": u * Dk * Ds * esz, "read": u * (Dk * Dk * esz + Dk * Ds * 4)},
           "output": {"written": 0, "read": u * Dk * Ds * esz}}
     if fused:
-        gpart = u * NS * Dk * Dk * 4 if NS > 1 else 0
+        gpart = u * NS * gram if NS > 1 else 0
         f["summaries"] += 2.0 * n * Dk * Dk
         ws["summaries"]["written"] += gpart if NS > 1 else u * Dk * Dk * esz
         ws["reduce"]["read"] += gpart

@@ -631,6 +631,8 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
             }
         }
     } else {
+        // the Gram matrices are symmetric: only the tiles on and above the
+        // diagonal (column tile >= row tile) go to the partials
         const int NC = gram ? NCG : NJA;
         float *dst = (gw ? p.PG : zgw ? p.PGz : p.PA) + (fi * p.NS + s) * (size_t)NR * NC * 256;
         if (gram || p.sum_mode != 2) {
@@ -638,7 +640,7 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
             for (int a = 0; a < 2; ++a)
 #pragma unroll
                 for (int j = 0; j < CPW; ++j)
-                    if (j < cpw)
+                    if (j < cpw && (!gram || c0 * cpw + j >= 2 * kbw + a))
                         *(f32x4 *)(dst + ((size_t)((2 * kbw + a) * NC + c0 * cpw + j) * 64 + l) * 4) = acc[a][j];
         }
         if (zw && (FUSED || p.sum_mode != 1)) {
@@ -653,7 +655,10 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
 
 // Sum over the splits.  Items per (frame, head): the Dk/16 x Dk/32 G operand
 // fragments, then the Dk/16 x Dv/16 A tiles, then (FUSED) the unrotated-key G
-// fragments; one wave per item.
+// fragments; one wave per item.  The splits store a Gram matrix's tiles on and
+// above the diagonal only; a tile below it is its mirror's sum transposed
+// through LDS: lane (li, lg) value q of tile (r, c) is lane
+// (4 lg + q) + 16 (li / 4) value li % 4 of tile (c, r) (both P32 ordered).
 template <class E, int DK, int DV, bool NORM, bool FUSED = false>
 __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p) {
     using TR = Tr<E>;
@@ -662,18 +667,28 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
     const int item = blockIdx.y * 4 + (threadIdx.x >> 6);
     const size_t fi = blockIdx.x;                                // (b*H + h) * F + f
     if (item >= NI) return;
-    const int l = threadIdx.x & 63;
+    const int l = threadIdx.x & 63, li = l & 15, lg = l >> 4;
     const bool gz = FUSED && item >= NGI + NAI;
     if (item < NGI || gz) {
+        __shared__ float tsm[4][256];                            // one transposition tile per wave
+        float *ts = tsm[threadIdx.x >> 6];
         const int gi = gz ? item - NGI - NAI : item;
         const int t = gi / KB, kb = gi - t * KB;
         const float *src = (gz ? p.PGz : p.PG) + fi * p.NS * (size_t)NR * NR * 256 + l * 4;
-        f32x4 lo = {0.f, 0.f, 0.f, 0.f}, hi = lo;
-        for (int s = 0; s < p.NS; ++s) {
-            const float *ps = src + (size_t)s * NR * NR * 256;
-            lo += *(const f32x4 *)(ps + (size_t)((2 * kb) * NR + t) * 256);
-            hi += *(const f32x4 *)(ps + (size_t)((2 * kb + 1) * NR + t) * 256);
-        }
+        // tile (r, t) of the sum: stored if t >= r, else the mirror (t, r) transposed
+        auto tile = [&](int r) {
+            const bool up = t >= r;
+            const size_t off = (size_t)(up ? r * NR + t : t * NR + r) * 256;
+            f32x4 x = {0.f, 0.f, 0.f, 0.f};
+            for (int s = 0; s < p.NS; ++s) x += *(const f32x4 *)(src + (size_t)s * NR * NR * 256 + off);
+            if (up) return x;
+            *(f32x4 *)(ts + 4 * l) = x;
+            f32x4 y;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) y[q] = ts[4 * ((4 * lg + q) + 16 * (li >> 2)) + (li & 3)];
+            return y;
+        };
+        const f32x4 lo = tile(2 * kb), hi = tile(2 * kb + 1);
         const float k2 = p.key_scale * p.key_scale;
         TR::store8((gz ? p.Gzf : p.Gf) + ((fi * NR + t) * KB + kb) * 512 + l * 8,
                    TR::cat(TR::from_f32(lo * k2), TR::from_f32(hi * k2)));

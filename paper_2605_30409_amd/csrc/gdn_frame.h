@@ -550,6 +550,10 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
             }
         };
         Ops o0, o1;
+        // split partials keep a Gram matrix's tiles on and above the diagonal
+        // only: a Gram wave whose first half of column tiles lies wholly below
+        // its row pair skips it
+        const bool skip0 = FUSED && GB && p.NS > 1 && c0 * NC + NC / 2 <= 2 * kbw;
         for (int i = 0; i < nb; ++i) {
             // the barrier also completes the previous block's reads, so the
             // loaders may refill that block's slot
@@ -565,7 +569,8 @@ __global__ __launch_bounds__(sum_threads<FUSED>()) void gdn_frame_summary_kernel
                     frag fa[2], fb[NH];
 #pragma unroll
                     for (int hf = 0; hf < 2; ++hf) {
-                        if (hf == 0) read_a(i, kb, fa);
+                        if (hf == 0 && skip0) continue;
+                        if (hf == 0 || skip0) read_a(i, kb, fa);
                         read_b(i, kb, hf * NH, std::integral_constant<int, NH>{}, fb);
 #pragma unroll
                         for (int a = 0; a < 2; ++a)

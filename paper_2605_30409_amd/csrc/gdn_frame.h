@@ -674,6 +674,24 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
     if (item >= NI) return;
     const int l = threadIdx.x & 63, li = l & 15, lg = l >> 4;
     const bool gz = FUSED && item >= NGI + NAI;
+    // the sum over the splits of the f32x4 at src + s * stride, in split
+    // order, four loads in flight at a time
+    auto split_sum = [&](const float *src, size_t stride) {
+        f32x4 x = {0.f, 0.f, 0.f, 0.f};
+        int s = 0;
+        for (; s + 4 <= p.NS; s += 4) {
+            const f32x4 a0 = *(const f32x4 *)(src + (size_t)s * stride);
+            const f32x4 a1 = *(const f32x4 *)(src + (size_t)(s + 1) * stride);
+            const f32x4 a2 = *(const f32x4 *)(src + (size_t)(s + 2) * stride);
+            const f32x4 a3 = *(const f32x4 *)(src + (size_t)(s + 3) * stride);
+            x += a0;
+            x += a1;
+            x += a2;
+            x += a3;
+        }
+        for (; s < p.NS; ++s) x += *(const f32x4 *)(src + (size_t)s * stride);
+        return x;
+    };
     if (item < NGI || gz) {
         __shared__ float tsm[4][256];                            // one transposition tile per wave
         float *ts = tsm[threadIdx.x >> 6];
@@ -684,8 +702,7 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
         auto tile = [&](int r) {
             const bool up = t >= r;
             const size_t off = (size_t)(up ? r * NR + t : t * NR + r) * 256;
-            f32x4 x = {0.f, 0.f, 0.f, 0.f};
-            for (int s = 0; s < p.NS; ++s) x += *(const f32x4 *)(src + (size_t)s * NR * NR * 256 + off);
+            const f32x4 x = split_sum(src + off, (size_t)NR * NR * 256);
             if (up) return x;
             *(f32x4 *)(ts + 4 * l) = x;
             f32x4 y;
@@ -700,8 +717,7 @@ __global__ __launch_bounds__(256) void gdn_frame_reduce_kernel(FrameParams<E> p)
     } else {
         const int a = item - NGI;                                // = t * NCV + jt
         const float *src = p.PA + fi * p.NS * (size_t)NR * NCV * 256 + (size_t)a * 256 + l * 4;
-        f32x4 sum = {0.f, 0.f, 0.f, 0.f};
-        for (int s = 0; s < p.NS; ++s) sum += *(const f32x4 *)(src + (size_t)s * NR * NCV * 256);
+        const f32x4 sum = split_sum(src, (size_t)NR * NCV * 256);
         *(f32x4 *)(p.Af + (fi * NR * NCV + a) * 256 + l * 4) = sum * p.key_scale;
     }
 }
